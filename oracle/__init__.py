@@ -1,0 +1,212 @@
+"""CPU reference oracle for the ODB window pipeline -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py``
+may import this package.  It wraps ``odb_oracle.cpp`` (plain single-threaded C++,
+built with g++) and adds :func:`collate_elements`, a numpy statement of the collate
+rule evaluated at individual output positions so full-size GPU outputs can be spot
+checked without materialising the whole oracle output.
+
+The oracle shares no code with the HIP library: it is compiled from its own source by
+its own compiler, and neither side imports or links the other.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "odb_oracle.cpp")
+_LIB = os.path.join(_HERE, "libodb_oracle.so")
+
+MODE_JOIN = 0
+MODE_NONJOIN = 1
+STOP_DRAINED, STOP_QUOTA, STOP_RANK_FINISHED = 0, 1, 2
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with g++ (always when ``force``)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-Wall", "-Wextra",
+                               _SRC, "-o", tmp])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Info(ctypes.Structure):
+    _fields_ = [
+        ("steps", ctypes.c_int64),
+        ("rounds", ctypes.c_int32),
+        ("stop_reason", ctypes.c_int32),
+        ("emitted_samples", ctypes.c_int64),
+        ("leftover_samples", ctypes.c_int64),
+        ("real_tokens", ctypes.c_int64),
+        ("padded_elems", ctypes.c_int64),
+        ("max_step_samples", ctypes.c_int64),
+        ("splits", ctypes.c_int64),
+        ("overflow_groups", ctypes.c_int64),
+        ("missing_ids", ctypes.c_int64),
+        ("duplicate_ids", ctypes.c_int64),
+        ("bad_views", ctypes.c_int64),
+        ("pad_fraction", ctypes.c_double),
+    ]
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        lib.oracle_plan.restype = P
+        lib.oracle_plan.argtypes = [ctypes.c_int32, ctypes.c_int64, P, P, P, ctypes.c_int64,
+                                    ctypes.c_int64, ctypes.c_int32, ctypes.c_int64, P]
+        lib.oracle_last_error.restype = ctypes.c_char_p
+        lib.oracle_free.argtypes = [P]
+        lib.oracle_info.argtypes = [P, ctypes.POINTER(_Info)]
+        lib.oracle_form.argtypes = [P, P, P, P, P]
+        lib.oracle_slots.argtypes = [P, P, P, P, P, P]
+        lib.oracle_emit.argtypes = [P, P, P, P]
+        lib.oracle_collate.argtypes = [P, P, P, ctypes.c_int32, P, P, P, P]
+        lib.oracle_round_targets.argtypes = [P, P]
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+class OracleError(ValueError):
+    pass
+
+
+@dataclass
+class Plan:
+    W: int
+    n: int
+    info: dict
+    # first formation
+    order: np.ndarray
+    sorted_len: np.ndarray
+    group_index: np.ndarray
+    groups_per_rank: np.ndarray
+    # aligned plan
+    slot_rows: np.ndarray
+    slot_maxlen: np.ndarray
+    slot_row_off: np.ndarray
+    slot_tile_off: np.ndarray
+    slot_tokens: np.ndarray
+    emit_order: np.ndarray
+    leftover: np.ndarray
+    leftover_off: np.ndarray
+    round_targets: np.ndarray
+    _handle: int = 0
+
+    @property
+    def steps(self) -> int:
+        return int(self.info["steps"])
+
+    @property
+    def num_slots(self) -> int:
+        return self.W * self.steps
+
+    @property
+    def padded_elems(self) -> int:
+        return int(self.info["padded_elems"])
+
+    def __del__(self):
+        if self._handle and _lib is not None:
+            _lib.oracle_free(ctypes.c_void_p(self._handle))
+            self._handle = 0
+
+    def collate(self, tok_off: np.ndarray, tokens: np.ndarray, pad_id: int = 0):
+        """Full collate: four flat int32 arrays of length padded_elems."""
+        lib = _load()
+        P = self.padded_elems
+        outs = [np.empty(P, dtype=np.int32) for _ in range(4)]
+        tok_off = np.ascontiguousarray(tok_off, dtype=np.int64)
+        tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+        lib.oracle_collate(ctypes.c_void_p(self._handle), _ptr(tok_off), _ptr(tokens), int(pad_id),
+                           *[_ptr(o) for o in outs])
+        return tuple(outs)
+
+
+def plan(rank_off, tok_off, budget: int, mode: int = MODE_JOIN, quota: int = 0,
+         capacity=None, identity=None, num_identities: int = 0) -> Plan:
+    lib = _load()
+    rank_off = np.ascontiguousarray(rank_off, dtype=np.int64)
+    tok_off = np.ascontiguousarray(tok_off, dtype=np.int64)
+    W = len(rank_off) - 1
+    n = len(tok_off) - 1
+    cap = None if capacity is None else np.ascontiguousarray(capacity, dtype=np.int64)
+    ident = None if identity is None else np.ascontiguousarray(identity, dtype=np.int64)
+    h = lib.oracle_plan(W, n, _ptr(rank_off), _ptr(tok_off), _ptr(ident), int(num_identities),
+                        int(budget), int(mode), int(quota), _ptr(cap))
+    if not h:
+        raise OracleError(lib.oracle_last_error().decode())
+    info = _Info()
+    lib.oracle_info(ctypes.c_void_p(h), ctypes.byref(info))
+    d = {f: getattr(info, f) for f, _ in _Info._fields_}
+    S = d["steps"]
+    K = W * S
+    order = np.empty(n, np.int32)
+    slen = np.empty(n, np.int32)
+    gidx = np.empty(n, np.int32)
+    G = np.empty(W, np.int32)
+    lib.oracle_form(ctypes.c_void_p(h), _ptr(order), _ptr(slen), _ptr(gidx), _ptr(G))
+    rows = np.empty(K, np.int32)
+    mx = np.empty(K, np.int32)
+    ro = np.empty(K + 1, np.int64)
+    to = np.empty(K + 1, np.int64)
+    tk = np.empty(K, np.int64)
+    lib.oracle_slots(ctypes.c_void_p(h), _ptr(rows), _ptr(mx), _ptr(ro), _ptr(to), _ptr(tk))
+    emit = np.empty(d["emitted_samples"], np.int32)
+    left = np.empty(d["leftover_samples"], np.int32)
+    loff = np.empty(W + 1, np.int64)
+    lib.oracle_emit(ctypes.c_void_p(h), _ptr(emit), _ptr(left), _ptr(loff))
+    rt = np.empty(d["rounds"], np.int64)
+    lib.oracle_round_targets(ctypes.c_void_p(h), _ptr(rt))
+    return Plan(W, n, d, order, slen, gidx, G, rows, mx, ro, to, tk, emit, left, loff, rt, _handle=h)
+
+
+def plan_window(w, **overrides) -> Plan:
+    """Convenience: run :func:`plan` on a ``synth.Window``."""
+    kw = dict(budget=w.budget, mode=MODE_NONJOIN if w.mode == "nonjoin" else MODE_JOIN,
+              quota=w.quota, capacity=w.capacity, identity=w.identity,
+              num_identities=w.num_identities)
+    kw.update(overrides)
+    return plan(w.rank_off, w.tok_off, **kw)
+
+
+def collate_elements(p: Plan, tok_off: np.ndarray, token_at, idx: np.ndarray, pad_id: int = 0):
+    """Collate values at flat output positions ``idx`` (Sec. 2.1 pad-to-max rule).
+
+    ``token_at(k)`` returns the token ids at global CSR positions ``k`` (numpy int64).
+    Returns four int32 arrays aligned with ``idx``.
+    """
+    idx = np.asarray(idx, dtype=np.int64)
+    k = np.searchsorted(p.slot_tile_off, idx, side="right") - 1   # slot holding each element
+    local = idx - p.slot_tile_off[k]
+    ml = p.slot_maxlen[k].astype(np.int64)
+    row = local // ml
+    col = local - row * ml
+    s = p.emit_order[p.slot_row_off[k] + row].astype(np.int64)
+    start = tok_off[s]
+    l = tok_off[s + 1] - start
+    real = col < l
+    tok = np.where(real, token_at(np.where(real, start + col, 0)), 0).astype(np.int32)
+    ids = np.where(real, tok, pad_id).astype(np.int32)
+    lab = np.where(real, tok, -100).astype(np.int32)
+    msk = real.astype(np.int32)
+    pos = np.where(real, col, 0).astype(np.int32)
+    return ids, lab, msk, pos

@@ -1,0 +1,481 @@
+// Reference oracle for the Online Dynamic Batching window pipeline.
+//
+// TEST INFRASTRUCTURE ONLY.  This file is a plain, slow, single-threaded CPU
+// statement of what the batching method computes on one window of realised samples.
+// Only the test suite, the smoke check and the benchmark's CPU-baseline leg load it;
+// the HIP library never includes, links or calls anything here, and this file uses
+// nothing from the HIP library.
+//
+// Every step follows the paper's own description, with plain containers:
+//   * batch size rule                           Eq. 1, Sec. 2.2
+//   * sort + threshold-carry grouping           Sec. 2.2 and the worked example (App. D)
+//   * alignment target over active ranks        Eq. 3 (App. A)
+//   * split / overflow adjustment               App. A, Algorithm 1
+//   * join (drain-then-signal) termination      Sec. 2.3, Theorem 1
+//   * non-join sample-quota termination         Sec. 2.3, Theorem 2, App. C (quota closure)
+//   * IDLE slots for ranks with nothing to send Sec. 2.1 and Algorithm 1's postcondition
+//   * collate = pad every group to its own max  Sec. 2.1 / Fig. 1 ("pad to l_max")
+//   * padding fraction                          throughput-decomposition definition (App. I)
+//   * identity coverage                         App. C (terminal identity coverage)
+// Where the paper is silent the oracle takes the readings documented in the
+// repository's design notes (tie order, list order, trailing group, canonical
+// emission order, pad values); each is marked "reading" below.
+//
+// Build: g++ -O2 -std=c++17 -shared -fPIC odb_oracle.cpp -o libodb_oracle.so
+
+#include <algorithm>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <limits>
+#include <new>
+#include <string>
+#include <vector>
+
+namespace {
+
+enum { MODE_JOIN = 0, MODE_NONJOIN = 1 };
+enum { STOP_DRAINED = 0, STOP_QUOTA = 1, STOP_RANK_FINISHED = 2 };
+
+using Group = std::vector<int32_t>;   // sample ids
+using GroupList = std::vector<Group>;
+
+struct Info {
+    int64_t steps;
+    int32_t rounds;
+    int32_t stop_reason;
+    int64_t emitted_samples;
+    int64_t leftover_samples;
+    int64_t real_tokens;
+    int64_t padded_elems;
+    int64_t max_step_samples;
+    int64_t splits;
+    int64_t overflow_groups;
+    int64_t missing_ids;
+    int64_t duplicate_ids;
+    int64_t bad_views;
+    double pad_fraction;
+};
+
+struct Result {
+    int32_t W = 0;
+    int64_t n = 0;
+    std::vector<int64_t> rank_off;
+    std::vector<int64_t> len;                 // realised length of every sample
+    // first formation of every rank's full buffer (Sec. 2.2)
+    std::vector<int32_t> order, sorted_len, group_index, groups_per_rank;
+    // aligned plan: slots[r][j] = members of rank r's j-th step in row order (empty = IDLE)
+    std::vector<std::vector<Group>> slots;
+    std::vector<std::vector<int32_t>> leftover;
+    std::vector<int64_t> round_target;       // T of every alignment round (Eq. 3)
+    Info info{};
+};
+
+// Eq. 1: B(l) = max(floor(L_max / l), 1).
+int64_t batch_size(int64_t L_max, int64_t l) {
+    int64_t b = L_max / l;
+    return b > 1 ? b : 1;
+}
+
+// Sec. 2.2: sort the buffer by realised length and walk it from the longest to the
+// shortest sample with a running group-size threshold t (initially 1).  Each sample is
+// appended to the current group; when the group's size reaches t it is finalised and
+// t becomes B(l) of the sample just added (the shortest so far).
+//   reading (tie order): equal lengths are visited in ascending sample id, i.e. the
+//     visiting order is (length descending, id ascending).
+//   reading (trailing group): samples left in an unfinished group when the buffer is
+//     exhausted form one last group, so nothing in the window is dropped.
+// Returns groups in formation order (longest first), members in visiting order; the
+// visiting order itself is written to *visit.
+GroupList form_groups(const std::vector<int32_t>& buffer, const std::vector<int64_t>& len,
+                      int64_t L_max, std::vector<int32_t>* visit) {
+    std::vector<int32_t> s(buffer);
+    std::stable_sort(s.begin(), s.end(), [&](int32_t a, int32_t b) {
+        if (len[a] != len[b]) return len[a] > len[b];
+        return a < b;
+    });
+    GroupList formed;
+    Group cur;
+    int64_t t = 1;
+    for (int32_t x : s) {
+        cur.push_back(x);
+        if ((int64_t)cur.size() >= t) {
+            formed.push_back(cur);
+            t = batch_size(L_max, len[x]);
+            cur.clear();
+        }
+    }
+    if (!cur.empty()) formed.push_back(cur);
+    if (visit) *visit = s;
+    return formed;
+}
+
+// The worked example (App. D) lists the finished groups "from short to long" with each
+// group's members in ascending length.  reading: that list is the exact reverse of the
+// formation order, group by group and member by member.
+GroupList paper_list_order(const GroupList& formed) {
+    GroupList list(formed.rbegin(), formed.rend());
+    for (Group& g : list) std::reverse(g.begin(), g.end());
+    return list;
+}
+
+// Algorithm 1, split branch: while the rank has fewer than T groups and some group has
+// at least two samples, scan the list from its last group backwards, take the first
+// group with >= 2 samples and move its last sample into a new singleton group.
+// reading: the new singleton is appended at the end of the list.
+int64_t split_to(GroupList& list, int64_t T) {
+    int64_t splits = 0;
+    while ((int64_t)list.size() < T) {
+        bool found = false;
+        for (int64_t i = (int64_t)list.size() - 1; i >= 0; --i) {
+            if (list[i].size() >= 2) {
+                int32_t x = list[i].back();
+                list[i].pop_back();
+                list.push_back(Group{x});
+                ++splits;
+                found = true;
+                break;
+            }
+        }
+        if (!found) break;
+    }
+    return splits;
+}
+
+// Algorithm 1, overflow branch: sort the groups by size (descending), keep the first T
+// and return the samples of the rest to the buffer (overflow recirculation).
+// reading: the sort is stable over the short-to-long list, so among equal sizes the
+// group nearer the short end is kept.
+void overflow_to(GroupList& list, int64_t T, std::vector<int32_t>& returned) {
+    std::stable_sort(list.begin(), list.end(),
+                     [](const Group& a, const Group& b) { return a.size() > b.size(); });
+    for (size_t i = (size_t)T; i < list.size(); ++i)
+        for (int32_t x : list[i]) returned.push_back(x);
+    list.resize((size_t)T);
+}
+
+// reading (emission order): a rank's aligned groups are emitted short to long and each
+// group's rows run short to long; concretely groups are ordered by their members'
+// positions in this round's visiting order, latest first, and so are the rows.
+void canonicalize(GroupList& list, const std::vector<int64_t>& pos) {
+    for (Group& g : list)
+        std::sort(g.begin(), g.end(), [&](int32_t a, int32_t b) { return pos[a] > pos[b]; });
+    std::sort(list.begin(), list.end(),
+              [&](const Group& a, const Group& b) { return pos[a.front()] > pos[b.front()]; });
+}
+
+std::string g_err;
+
+bool fail(const std::string& m) {
+    g_err = m;
+    return false;
+}
+
+bool run(Result& R, int32_t W, int64_t n, const int64_t* rank_off, const int64_t* tok_off,
+         const int64_t* identity, int64_t num_identities, int64_t L_max, int32_t mode,
+         int64_t quota, const int64_t* capacity) {
+    if (W < 1) return fail("W must be >= 1");
+    if (n < 0 || n >= (int64_t)std::numeric_limits<int32_t>::max()) return fail("n out of range");
+    if (L_max < 1) return fail("budget must be >= 1");
+    if (mode != MODE_JOIN && mode != MODE_NONJOIN) return fail("bad mode");
+    if (mode == MODE_NONJOIN && quota < 1) return fail("quota must be >= 1 in non-join mode");
+    if (rank_off[0] != 0 || rank_off[W] != n) return fail("rank offsets must span [0, n)");
+    for (int32_t r = 0; r < W; ++r)
+        if (rank_off[r + 1] < rank_off[r]) return fail("rank offsets must be non-decreasing");
+    if (capacity)
+        for (int32_t r = 0; r < W; ++r)
+            if (capacity[r] < 0) return fail("capacity must be >= 0");
+    R.W = W;
+    R.n = n;
+    R.rank_off.assign(rank_off, rank_off + W + 1);
+    R.len.resize((size_t)n);
+    for (int64_t i = 0; i < n; ++i) {
+        int64_t l = tok_off[i + 1] - tok_off[i];   // realised post-pipeline length
+        if (l < 1 || l > (int64_t)std::numeric_limits<int32_t>::max())
+            return fail("sample " + std::to_string(i) + " has invalid length " + std::to_string(l));
+        R.len[(size_t)i] = l;
+    }
+    if (identity) {
+        if (num_identities < 1) return fail("num_identities must be >= 1 with an identity map");
+        for (int64_t i = 0; i < n; ++i)
+            if (identity[i] < 0 || identity[i] >= num_identities) return fail("identity out of range");
+    }
+
+    // ---- first formation of every rank's whole buffer (Sec. 2.2) ----
+    R.order.resize((size_t)n);
+    R.sorted_len.resize((size_t)n);
+    R.group_index.resize((size_t)n);
+    R.groups_per_rank.assign((size_t)W, 0);
+    for (int32_t r = 0; r < W; ++r) {
+        std::vector<int32_t> buf;
+        for (int64_t i = rank_off[r]; i < rank_off[r + 1]; ++i) buf.push_back((int32_t)i);
+        std::vector<int32_t> visit;
+        GroupList formed = form_groups(buf, R.len, L_max, &visit);
+        int64_t p = rank_off[r];
+        for (size_t g = 0; g < formed.size(); ++g)
+            for (int32_t x : formed[g]) {
+                R.order[(size_t)p] = x;
+                R.sorted_len[(size_t)p] = (int32_t)R.len[(size_t)x];
+                R.group_index[(size_t)p] = (int32_t)g;
+                ++p;
+            }
+        R.groups_per_rank[(size_t)r] = (int32_t)formed.size();
+    }
+
+    // ---- alignment rounds ----
+    std::vector<std::vector<int32_t>> buf((size_t)W);
+    for (int32_t r = 0; r < W; ++r)
+        for (int64_t i = rank_off[r]; i < rank_off[r + 1]; ++i) buf[(size_t)r].push_back((int32_t)i);
+    R.slots.assign((size_t)W, {});
+    std::vector<int64_t> pos((size_t)n, -1);
+    Info& I = R.info;
+    int64_t S = 0, emitted = 0;
+    int32_t stop = STOP_DRAINED;
+    for (;;) {
+        int32_t nonempty = 0;
+        for (int32_t r = 0; r < W; ++r) nonempty += buf[(size_t)r].empty() ? 0 : 1;
+        if (nonempty == 0) { stop = STOP_DRAINED; break; }
+        // Non-join: a rank with nothing left while others still hold samples advertises
+        // "finished" (n_groups = -1) and the logical iteration ends (Sec. 2.3).
+        if (mode == MODE_NONJOIN && nonempty < W) { stop = STOP_RANK_FINISHED; break; }
+        I.rounds += 1;
+
+        // Grouping of every buffer (Sec. 2.2), as the paper's short-to-long list.
+        std::vector<GroupList> list((size_t)W);
+        for (int32_t r = 0; r < W; ++r) {
+            std::vector<int32_t> visit;
+            list[(size_t)r] = paper_list_order(form_groups(buf[(size_t)r], R.len, L_max, &visit));
+            for (size_t p = 0; p < visit.size(); ++p) pos[(size_t)visit[p]] = (int64_t)p;
+        }
+
+        // Eq. 3 over the active ranks A = {r : G_r > 0}; the minima over capacity and
+        // buffered count only consider positive values; an absent capacity array means
+        // no capacity limit.
+        int64_t maxG = 0, minC = 0, minS = 0;
+        for (int32_t r = 0; r < W; ++r) {
+            int64_t G = (int64_t)list[(size_t)r].size();
+            if (G <= 0) continue;
+            maxG = std::max(maxG, G);
+            int64_t Sr = (int64_t)buf[(size_t)r].size();
+            if (Sr > 0) minS = (minS == 0) ? Sr : std::min(minS, Sr);
+            if (capacity && capacity[r] > 0) minC = (minC == 0) ? capacity[r] : std::min(minC, capacity[r]);
+        }
+        int64_t T = maxG;
+        if (minC > 0) T = std::min(T, minC);
+        if (minS > 0) T = std::min(T, minS);
+        T = std::max<int64_t>(T, 1);
+        R.round_target.push_back(T);
+
+        // Algorithm 1 on every active rank.
+        std::vector<std::vector<int32_t>> returned((size_t)W);
+        for (int32_t r = 0; r < W; ++r) {
+            GroupList& L = list[(size_t)r];
+            int64_t G = (int64_t)L.size();
+            if (G == 0) continue;
+            if (G < T) {
+                I.splits += split_to(L, T);
+            } else if (G > T) {
+                I.overflow_groups += G - T;
+                overflow_to(L, T, returned[(size_t)r]);
+            }
+            canonicalize(L, pos);
+        }
+
+        // Emit the round's T aligned steps; inactive ranks send IDLE slots.  In non-join
+        // mode the trainer stops after the first step whose cumulative global emitted
+        // count reaches the quota (Theorem 2).
+        int64_t cut = T;
+        bool quota_hit = false;
+        for (int64_t j = 0; j < T; ++j) {
+            int64_t step = 0;
+            for (int32_t r = 0; r < W; ++r)
+                if (!list[(size_t)r].empty()) step += (int64_t)list[(size_t)r][(size_t)j].size();
+            emitted += step;
+            I.max_step_samples = std::max(I.max_step_samples, step);
+            if (mode == MODE_NONJOIN && emitted >= quota) {
+                cut = j + 1;
+                quota_hit = true;
+                break;
+            }
+        }
+        for (int32_t r = 0; r < W; ++r) {
+            GroupList& L = list[(size_t)r];
+            std::vector<int32_t> next;
+            for (int64_t j = 0; j < cut; ++j)
+                R.slots[(size_t)r].push_back(L.empty() ? Group{} : L[(size_t)j]);
+            for (size_t j = (size_t)cut; j < L.size(); ++j)
+                for (int32_t x : L[j]) next.push_back(x);
+            for (int32_t x : returned[(size_t)r]) next.push_back(x);
+            buf[(size_t)r] = next;
+        }
+        S += cut;
+        if (quota_hit) { stop = STOP_QUOTA; break; }
+    }
+    I.steps = S;
+    I.stop_reason = stop;
+    I.emitted_samples = emitted;
+
+    // Un-emitted samples (non-join only) stay with their rank, in visiting order
+    // (length descending, id ascending) -- the No-Leak lemma (App. C).
+    R.leftover.assign((size_t)W, {});
+    for (int32_t r = 0; r < W; ++r) {
+        std::vector<int32_t> left = buf[(size_t)r];
+        std::stable_sort(left.begin(), left.end(), [&](int32_t a, int32_t b) {
+            if (R.len[a] != R.len[b]) return R.len[a] > R.len[b];
+            return a < b;
+        });
+        R.leftover[(size_t)r] = left;
+        I.leftover_samples += (int64_t)left.size();
+    }
+
+    // Stats: real tokens and padded area; pad% = 1 - sum(L_real) / sum(L_compute).
+    for (int32_t r = 0; r < W; ++r)
+        for (const Group& g : R.slots[(size_t)r]) {
+            int64_t mx = 0;
+            for (int32_t x : g) {
+                I.real_tokens += R.len[(size_t)x];
+                mx = std::max(mx, R.len[(size_t)x]);
+            }
+            I.padded_elems += mx * (int64_t)g.size();
+        }
+    I.pad_fraction = I.padded_elems > 0 ? 1.0 - (double)I.real_tokens / (double)I.padded_elems : 0.0;
+
+    // Coverage: every sampler view must be emitted exactly once (join) or sit in exactly
+    // one of emitted / leftover (non-join); identities are counted over the same union.
+    std::vector<int64_t> view_count((size_t)n, 0);
+    int64_t N_id = identity ? num_identities : n;
+    std::vector<int64_t> id_count((size_t)N_id, 0);
+    auto count = [&](int32_t x) {
+        view_count[(size_t)x] += 1;
+        id_count[(size_t)(identity ? identity[x] : x)] += 1;
+    };
+    for (int32_t r = 0; r < W; ++r) {
+        for (const Group& g : R.slots[(size_t)r])
+            for (int32_t x : g) count(x);
+        for (int32_t x : R.leftover[(size_t)r]) count(x);
+    }
+    for (int64_t i = 0; i < n; ++i) I.bad_views += view_count[(size_t)i] != 1 ? 1 : 0;
+    for (int64_t d = 0; d < N_id; ++d) {
+        if (id_count[(size_t)d] == 0) I.missing_ids += 1;
+        if (id_count[(size_t)d] > 1) I.duplicate_ids += id_count[(size_t)d] - 1;
+    }
+    return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+typedef Info oracle_info_t;
+
+const char* oracle_last_error(void) { return g_err.c_str(); }
+
+// Runs grouping, alignment, stats and coverage on one window.  Returns an opaque handle
+// (free with oracle_free) or NULL on invalid input (message via oracle_last_error).
+void* oracle_plan(int32_t W, int64_t n, const int64_t* rank_off, const int64_t* tok_off,
+                  const int64_t* identity, int64_t num_identities, int64_t budget, int32_t mode,
+                  int64_t quota, const int64_t* capacity) {
+    Result* R = new (std::nothrow) Result();
+    if (!R) return nullptr;
+    if (!run(*R, W, n, rank_off, tok_off, identity, num_identities, budget, mode, quota, capacity)) {
+        delete R;
+        return nullptr;
+    }
+    return R;
+}
+
+void oracle_free(void* h) { delete static_cast<Result*>(h); }
+
+// Alignment target of every round; out must hold info.rounds entries.
+void oracle_round_targets(void* h, int64_t* out) {
+    const Result& R = *static_cast<Result*>(h);
+    std::copy(R.round_target.begin(), R.round_target.end(), out);
+}
+
+void oracle_info(void* h, oracle_info_t* out) { *out = static_cast<Result*>(h)->info; }
+
+void oracle_form(void* h, int32_t* order, int32_t* sorted_len, int32_t* group_index,
+                 int32_t* groups_per_rank) {
+    const Result& R = *static_cast<Result*>(h);
+    std::copy(R.order.begin(), R.order.end(), order);
+    std::copy(R.sorted_len.begin(), R.sorted_len.end(), sorted_len);
+    std::copy(R.group_index.begin(), R.group_index.end(), group_index);
+    std::copy(R.groups_per_rank.begin(), R.groups_per_rank.end(), groups_per_rank);
+}
+
+// Slot tables, rank-major (slot k = r * steps + j).  row_off / tile_off have
+// W * steps + 1 entries (exclusive prefix sums of rows and of rows * maxlen).
+void oracle_slots(void* h, int32_t* rows, int32_t* maxlen, int64_t* row_off, int64_t* tile_off,
+                  int64_t* tokens) {
+    const Result& R = *static_cast<Result*>(h);
+    int64_t k = 0, ro = 0, to = 0;
+    for (int32_t r = 0; r < R.W; ++r)
+        for (const Group& g : R.slots[(size_t)r]) {
+            int64_t mx = 0, tk = 0;
+            for (int32_t x : g) {
+                mx = std::max(mx, R.len[(size_t)x]);
+                tk += R.len[(size_t)x];
+            }
+            rows[k] = (int32_t)g.size();
+            maxlen[k] = (int32_t)mx;
+            tokens[k] = tk;
+            row_off[k] = ro;
+            tile_off[k] = to;
+            ro += (int64_t)g.size();
+            to += (int64_t)g.size() * mx;
+            ++k;
+        }
+    row_off[k] = ro;
+    tile_off[k] = to;
+}
+
+// emit_order: emitted sample ids rank-major, slot order, row order.  leftover: the
+// un-emitted ids of every rank (rank-major) with leftover_off[W+1].
+void oracle_emit(void* h, int32_t* emit_order, int32_t* leftover, int64_t* leftover_off) {
+    const Result& R = *static_cast<Result*>(h);
+    int64_t e = 0;
+    for (int32_t r = 0; r < R.W; ++r)
+        for (const Group& g : R.slots[(size_t)r])
+            for (int32_t x : g) emit_order[e++] = x;
+    int64_t o = 0;
+    for (int32_t r = 0; r < R.W; ++r) {
+        leftover_off[r] = o;
+        for (int32_t x : R.leftover[(size_t)r]) leftover[o++] = x;
+    }
+    leftover_off[R.W] = o;
+}
+
+// Collate (Sec. 2.1): every aligned group becomes a [rows, max_len] tile padded on the
+// right.  reading (values): input_ids = labels = token, attention_mask = 1,
+// position_ids = column for real tokens; pad_id, -100, 0, 0 for padding.  Tiles are
+// packed back to back in rank-major slot order.
+void oracle_collate(void* h, const int64_t* tok_off, const int32_t* tokens, int32_t pad_id,
+                    int32_t* input_ids, int32_t* labels, int32_t* attention_mask,
+                    int32_t* position_ids) {
+    const Result& R = *static_cast<Result*>(h);
+    int64_t e = 0;
+    for (int32_t r = 0; r < R.W; ++r)
+        for (const Group& g : R.slots[(size_t)r]) {
+            int64_t mx = 0;
+            for (int32_t x : g) mx = std::max(mx, R.len[(size_t)x]);
+            for (int32_t x : g) {
+                int64_t l = R.len[(size_t)x];
+                for (int64_t c = 0; c < mx; ++c, ++e) {
+                    if (c < l) {
+                        int32_t t = tokens[tok_off[x] + c];
+                        input_ids[e] = t;
+                        labels[e] = t;
+                        attention_mask[e] = 1;
+                        position_ids[e] = (int32_t)c;
+                    } else {
+                        input_ids[e] = pad_id;
+                        labels[e] = -100;
+                        attention_mask[e] = 0;
+                        position_ids[e] = 0;
+                    }
+                }
+            }
+        }
+}
+
+}  // extern "C"

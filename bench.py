@@ -1,0 +1,171 @@
+"""Throughput of the ODB window pipeline on one MI355X.
+
+One step = grouping (odb_form_groups) + alignment with coverage check
+(odb_align_groups) + padded collation (odb_collate) of a whole window whose CSR token
+stream is already resident in HBM.  Prints one JSON line:
+
+  value        emitted samples per second (whole job)
+  roofline     the collate kernel (dominant): algorithmic bytes per launch / average
+               launch duration from HIP events on the launch stream, vs 8 TB/s
+  cpu_baseline the CPU oracle on a bounded sample of the same workload (first ranks of
+               the window), single-threaded on this host
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def collate_alg_bytes(n, real_tokens, padded, slots):
+    # 16 B written per padded element (4 int32 outputs), 4 B read per real token,
+    # 8 B per token offset, 4 B per emitted id, 24 B of slot tables per slot
+    return 16 * padded + 4 * real_tokens + 8 * (n + 1) + 4 * n + 24 * slots
+
+
+def cpu_baseline(w_full_name, tokens_dev, tok_off_full, ranks, pad_id=0):
+    import numpy as np
+
+    import oracle
+    import synth
+
+    wl = synth.WORKLOADS[w_full_name]
+    w = wl.window(ranks=ranks)
+    total = w.total_tokens
+    tokens = tokens_dev[:total].cpu().numpy()          # same generator output the GPU read
+    assert np.array_equal(w.tok_off, tok_off_full[:w.n + 1])
+    t0 = time.perf_counter()
+    p = oracle.plan_window(w)
+    p.collate(w.tok_off, tokens, pad_id)
+    dt = time.perf_counter() - t0
+    return {
+        "value": p.info["emitted_samples"] / dt,
+        "unit": "samples/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"first {ranks} of {wl.W} ranks ({w.n} samples, {w.total_tokens} tokens) of the same window, "
+                  f"plan + full collate, {dt:.1f} s",
+        "tokens_per_s": p.info["real_tokens"] / dt,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="ln480_w64x262144")
+    ap.add_argument("--cpu-ranks", type=int, default=4, help="ranks of the window the CPU oracle runs on")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the simulated ranks of a window are "
+              "segments of one launch, there is no multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2606_19989_amd as odb
+    import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    t = time.time()
+    w = wl.window()
+    log(f"[bench] {wl.name}: W={w.W} n={w.n} tokens={w.total_tokens} (drawn in {time.time() - t:.1f} s)")
+    dev = torch.device("cuda:0")
+    tok_off, tokens, ident = synth.device_tensors(w, dev)
+    torch.cuda.synchronize()
+    win = odb.DeviceWindow(w.rank_off, tok_off, tokens, ident, w.num_identities)
+    pipe = odb.Pipeline(win, w.budget, mode=w.mode, quota=w.quota, pad_id=0)
+    log(f"[bench] inputs resident: {(tok_off.numel() * 8 + tokens.numel() * 4) / 1e9:.1f} GB")
+
+    for i in range(args.warmup):
+        pipe.run()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+    info = dict(pipe.info)
+    odb.odb_collate_status(pipe.ws)
+
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        pipe.form()
+        pipe.align()
+        ev[i][0].record(stream)
+        pipe.collate()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    log(f"[bench] timed {args.steps} steps")
+    sec_per_step = (t1 - t0) / args.steps
+    collate_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    assert pipe.info["steps"] == info["steps"] and pipe.info["padded_elems"] == info["padded_elems"]
+
+    n = w.n
+    K = pipe.num_slots
+    P = int(info["padded_elems"])
+    real = int(info["real_tokens"])
+    emitted = int(info["emitted_samples"])
+    alg = collate_alg_bytes(n, real, P, K)
+    achieved = alg / (collate_ms * 1e-3) / 1e9
+    result = {
+        "metric": "samples/s and tokens/s batched+collated on 1 MI355X; % of HBM peak",
+        "value": emitted / sec_per_step,
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": sec_per_step * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i32",
+        "data": "synthetic",
+        "tokens_per_s": real / sec_per_step,
+        "padded_elems_per_s": P / sec_per_step,
+        "pipeline_hbm_frac": alg / sec_per_step / 1e9 / HBM_PEAK_GBS,
+        "config": {
+            "workload": wl.name,
+            "description": wl.description,
+            "simulated_ranks": w.W,
+            "samples": n,
+            "real_tokens": real,
+            "padded_elems": P,
+            "steps_aligned": int(info["steps"]),
+            "budget": w.budget,
+            "mode": w.mode,
+            "pad_fraction": info["pad_fraction"],
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "collate_kernel",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": None,
+            "alg_bytes_per_launch": alg,
+            "avg_launch_ms": collate_ms,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] CPU oracle on the first {args.cpu_ranks} ranks ...")
+        result["cpu_baseline"] = cpu_baseline(wl.name, tokens, w.tok_off, args.cpu_ranks)
+        log("[bench] CPU oracle done")
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,224 @@
+/*
+ * odb.h -- C ABI of the MI355X (gfx950) Online Dynamic Batching window pipeline.
+ *
+ * One call sequence turns a window of realised samples, split over W simulated DDP
+ * ranks, into step-aligned, padded training tiles:
+ *
+ *   odb_form_groups   length-aware grouping of every rank's buffer      (Sec. 2.2, Eq. 1)
+ *   odb_align_groups  Distributed Group Alignment: target, split,       (Eq. 3, Algorithm 1,
+ *                     overflow recirculation, join / non-join quota      Sec. 2.3, Thm 1-2)
+ *                     termination, slot plan, stats, identity coverage  (App. C)
+ *   odb_collate       pad every aligned group to its own longest sample (Sec. 2.1, Fig. 1)
+ *
+ * Conventions shared by every entry point
+ *   - Pointers named d_* are device pointers (HIP global memory on the current device);
+ *     all other pointers are host pointers.  The caller owns every buffer; the library
+ *     allocates no device memory (scratch comes from the caller's workspace), keeps no
+ *     pointer after returning and holds no state except a thread-local error message.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Work is enqueued
+ *     on it in order.  odb_form_groups and odb_align_groups synchronise `stream` because
+ *     their output sizes are data dependent; odb_collate does not synchronise.
+ *   - Every call returns an odb_status_t.  Argument errors are detected on the host
+ *     before anything is launched.  Data errors found on the device are reported at the
+ *     call's synchronisation point.  On any error the outputs are unspecified.  No C++
+ *     exception crosses this interface.
+ *   - Calls on distinct streams with distinct workspaces may run concurrently.
+ *
+ * Window layout (odb_window_t)
+ *   Samples are numbered 0..n-1; that number is the sample id used in every output.
+ *   Rank r owns the contiguous id range [rank_offsets[r], rank_offsets[r+1]).  Sample i
+ *   has realised length l_i = d_token_offsets[i+1] - d_token_offsets[i] and its tokens
+ *   are d_tokens[d_token_offsets[i] .. d_token_offsets[i+1]).
+ */
+#ifndef ODB_H_
+#define ODB_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum odb_status {
+    ODB_OK = 0,
+    ODB_E_INVALID_ARG = 1,   /* bad argument, detected on the host                      */
+    ODB_E_INVALID_DATA = 2,  /* bad window contents (l < 1, l >= 2^31, bad plan arrays)  */
+    ODB_E_WORKSPACE = 3,     /* workspace smaller than odb_workspace_size()              */
+    ODB_E_CAPACITY = 4,      /* slot arrays too small; see required_slot_capacity        */
+    ODB_E_HIP = 5,           /* a HIP runtime call failed                                */
+    ODB_E_COVERAGE = 6,      /* coverage self-check failed: some view not emitted once   */
+    ODB_E_INTERNAL = 7
+} odb_status_t;
+
+typedef enum odb_mode {
+    ODB_MODE_JOIN = 0,           /* default: drain every buffer, each view emitted once (Thm 1) */
+    ODB_MODE_NONJOIN_QUOTA = 1   /* stop at the first step reaching the sample quota (Thm 2)   */
+} odb_mode_t;
+
+typedef enum odb_stop_reason {
+    ODB_STOP_DRAINED = 0,        /* every rank's buffer emptied                               */
+    ODB_STOP_QUOTA = 1,          /* non-join: cumulative emitted samples reached the quota    */
+    ODB_STOP_RANK_FINISHED = 2   /* non-join: a rank ran empty while others still had samples */
+} odb_stop_reason_t;
+
+/* A window of realised samples over W simulated DDP ranks. */
+typedef struct odb_window {
+    int32_t num_ranks;               /* W >= 1                                              */
+    int32_t reserved0;               /* must be 0                                           */
+    int64_t num_samples;             /* n, 0 <= n < 2^31 - 1                                */
+    const int64_t* rank_offsets;     /* HOST [W+1]; 0 = off[0] <= ... <= off[W] = n          */
+    const int64_t* d_token_offsets;  /* [n+1]; l_i = off[i+1] - off[i] must lie in [1, 2^31) */
+    const int32_t* d_tokens;         /* token stream addressed by d_token_offsets            */
+    const int64_t* d_identity;       /* [n] dataset identity of every sampler view, or NULL  */
+    int64_t num_identities;          /* identities lie in [0, num_identities) (NULL map: n)  */
+} odb_window_t;
+
+/* Human-readable name of a status code (static storage). */
+const char* odb_status_string(int status);
+
+/* Detail of the last failing call on this thread ("" if none). */
+const char* odb_last_error_message(void);
+
+/* Bytes of device workspace that odb_form_groups / odb_align_groups / odb_collate need
+ * for this window (the same workspace serves all three).  Returns 0 on a bad window. */
+size_t odb_workspace_size(const odb_window_t* w);
+
+/*
+ * Stage 1: length-aware grouping (Sec. 2.2; batch size rule Eq. 1; App. D example).
+ *
+ * Every rank's samples are ordered by realised length, longest first, equal lengths by
+ * ascending sample id ("formation order").  Walking that order with a running threshold
+ * t (initially 1), a group is closed as soon as it holds t samples and t becomes
+ * B(l) = max(floor(budget / l), 1) of the sample just added; samples left over at the
+ * end of the buffer form one last group.
+ *
+ *   budget              L_max >= 1, padded-token budget of a group
+ *   d_order             [n] out: formation order, rank segments in place (global sample ids)
+ *   d_sorted_len        [n] out: l of d_order[p]
+ *   d_group_index       [n] out: 0-based formation group index of position p within its rank
+ *   d_groups_per_rank   [W] out: G_r, groups formed by rank r
+ *   d_ws / ws_bytes     workspace of at least odb_workspace_size(w) bytes, 256-B aligned
+ *
+ * Synchronises `stream` once (to validate lengths).  Returns ODB_E_INVALID_DATA if some
+ * l_i < 1 or l_i >= 2^31 (message names the first such sample).
+ */
+int odb_form_groups(const odb_window_t* w, int64_t budget,
+                    int32_t* d_order, int32_t* d_sorted_len, int32_t* d_group_index,
+                    int32_t* d_groups_per_rank, void* d_ws, size_t ws_bytes, void* stream);
+
+/* Alignment parameters. */
+typedef struct odb_align_params {
+    int32_t mode;                    /* odb_mode_t                                          */
+    int32_t reserved0;               /* must be 0                                           */
+    int64_t quota;                   /* sample quota Q >= 1 (non-join only)                 */
+    const int64_t* slot_capacity;    /* HOST [W] output-slot capacity C_r >= 0 per round, or
+                                        NULL (no limit); C_r = 0 takes no part in the minimum */
+} odb_align_params_t;
+
+/* Summary of an aligned plan. */
+typedef struct odb_plan_info {
+    int64_t steps;                   /* S: aligned steps (slots per rank)                   */
+    int32_t rounds;                  /* alignment rounds run                                */
+    int32_t stop_reason;             /* odb_stop_reason_t                                   */
+    int64_t emitted_samples;         /* sum of rows over all slots                          */
+    int64_t leftover_samples;        /* samples not emitted (non-join only)                 */
+    int64_t real_tokens;             /* sum of l over emitted samples                       */
+    int64_t padded_elems;            /* sum of rows * maxlen over all slots                 */
+    int64_t max_step_samples;        /* S_max: largest global sample count of one step      */
+    int64_t splits;                  /* singletons extracted by split, all rounds           */
+    int64_t overflow_groups;         /* groups returned by overflow, all rounds             */
+    int64_t missing_ids;             /* identities in [0, N_id) neither emitted nor leftover */
+    int64_t duplicate_ids;           /* extra emissions of an identity beyond its first     */
+    int64_t bad_views;               /* sampler views not emitted/leftover exactly once     */
+    double  pad_fraction;            /* 1 - real_tokens / padded_elems (0 if nothing padded) */
+    int64_t required_slot_capacity;  /* W * S; set on ODB_E_CAPACITY and on success         */
+} odb_plan_info_t;
+
+/*
+ * Stages 2-3: Distributed Group Alignment (Eq. 3, Algorithm 1, Sec. 2.3) + coverage (App. C).
+ *
+ * Inputs are the outputs of odb_form_groups for the same window and budget.  Each
+ * round gathers every rank's group count G_r and buffered count S_r (the simulated
+ * all_gather), computes T = max(min(max_{G_r>0} G_r, C+_min, S+_min), 1) over the active
+ * ranks, splits (peels the longest member of the first multi-sample group, counting from
+ * the longest group, into a singleton until G_r = T) or overflows (keeps the T largest
+ * groups, ties to the shorter samples, and returns the rest to the buffer).  Join mode
+ * repeats rounds on the returned samples until every buffer is empty; ranks with an
+ * empty buffer receive IDLE slots (rows = 0).  Non-join mode stops at the first step
+ * whose cumulative global emitted count reaches `quota`, or at the start of a round in
+ * which some rank is empty while others are not; un-emitted samples become leftovers.
+ *
+ * Output layout.  Slot k = r * S + j is rank r's j-th aligned step (rank-major).  A rank's
+ * groups are emitted short to long and each group's rows run short to long (the reverse
+ * of formation order).  Tiles are packed back to back in slot order.
+ *   slot_capacity     capacity of the slot arrays in slots; >= W * S is required
+ *   d_emit_order      [n] out: emitted ids; slot k's rows are
+ *                     d_emit_order[d_slot_row_off[k] .. d_slot_row_off[k+1])
+ *   d_slot_rows       [slot_capacity] out: rows of slot k (0 = IDLE)
+ *   d_slot_maxlen     [slot_capacity] out: longest l in slot k (0 = IDLE)
+ *   d_slot_row_off    [slot_capacity+1] out: exclusive prefix sum of rows
+ *   d_slot_tile_off   [slot_capacity+1] out: exclusive prefix sum of rows * maxlen
+ *   d_slot_tokens     [slot_capacity] out: real tokens of slot k
+ *   d_leftover        [n] out: un-emitted ids of every rank in formation order, rank-major
+ *   d_leftover_off    [W+1] out: rank r's leftovers are [off[r], off[r+1])
+ *   h_info            host out: plan summary (always filled when the plan was built)
+ *
+ * Synchronises `stream` once per alignment round and once at the end.  Returns
+ * ODB_E_CAPACITY (with h_info->required_slot_capacity) if slot_capacity < W * S,
+ * ODB_E_INVALID_DATA if the stage-1 arrays are inconsistent, and ODB_E_COVERAGE if the
+ * coverage self-check finds a view that is not emitted (or left over) exactly once.
+ */
+int odb_align_groups(const odb_window_t* w, int64_t budget, const odb_align_params_t* params,
+                     const int32_t* d_order, const int32_t* d_sorted_len,
+                     const int32_t* d_group_index, const int32_t* d_groups_per_rank,
+                     int64_t slot_capacity,
+                     int32_t* d_emit_order, int32_t* d_slot_rows, int32_t* d_slot_maxlen,
+                     int64_t* d_slot_row_off, int64_t* d_slot_tile_off, int64_t* d_slot_tokens,
+                     int32_t* d_leftover, int64_t* d_leftover_off,
+                     odb_plan_info_t* h_info, void* d_ws, size_t ws_bytes, void* stream);
+
+/*
+ * Stage 4: padded collation (Sec. 2.1 and Fig. 1: each aligned group is padded to its
+ * own longest sample).
+ *
+ * Writes four flat int32 arrays of length tile_off[num_slots] (= padded_elems).  Slot
+ * k's tile is elements [tile_off[k], tile_off[k+1]) viewed row-major as
+ * [rows[k], maxlen[k]].  Element (i, c) of a tile whose row i holds sample s:
+ *   c <  l_s : input_ids = labels = token c of s, attention_mask = 1, position_ids = c
+ *   c >= l_s : input_ids = pad_id, labels = -100, attention_mask = 0, position_ids = 0
+ *
+ *   num_slots           W * S from odb_align_groups (>= 0)
+ *   plan arrays         as written by odb_align_groups (device)
+ *   out_capacity_elems  length of each output array; elements beyond it are not written
+ *   d_ws / ws_bytes     the workspace (only a small status word is used)
+ *
+ * Asynchronous (launches exactly one kernel).  Accesses are bounds-checked against the
+ * window and the plan; an inconsistent plan sets a device status word that
+ * odb_collate_status() reads.
+ */
+int odb_collate(const odb_window_t* w, int64_t num_slots,
+                const int32_t* d_emit_order, const int32_t* d_slot_rows,
+                const int32_t* d_slot_maxlen, const int64_t* d_slot_row_off,
+                const int64_t* d_slot_tile_off, int32_t pad_id, int64_t out_capacity_elems,
+                int32_t* d_input_ids, int32_t* d_labels, int32_t* d_attention_mask,
+                int32_t* d_position_ids, void* d_ws, size_t ws_bytes, void* stream);
+
+/* Synchronises `stream` and returns ODB_OK, or ODB_E_INVALID_DATA if the last
+ * odb_collate on this workspace met an inconsistent plan (and clears the word). */
+int odb_collate_status(void* d_ws, size_t ws_bytes, void* stream);
+
+/*
+ * Identity coverage self-check on its own (App. C, terminal identity coverage): counts
+ * every sampler view over `emitted` and `leftover` ids and every identity over the same
+ * union.  Fills h_info->bad_views, missing_ids and duplicate_ids only.  Synchronises.
+ */
+int odb_check_coverage(const odb_window_t* w, const int32_t* d_emitted, int64_t num_emitted,
+                       const int32_t* d_leftover, int64_t num_leftover,
+                       odb_plan_info_t* h_info, void* d_ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ODB_H_ */

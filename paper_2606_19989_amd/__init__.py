@@ -1,0 +1,312 @@
+"""Python binding of libodb, the MI355X Online Dynamic Batching window pipeline.
+
+The functions named ``odb_*`` mirror the C ABI in ``include/odb.h`` one to one: they
+convert torch device tensors and host arrays into the pointers and structs the library
+takes, call it, and turn its status into an exception.  All computation happens in the
+HIP kernels of ``libodb.so``; there is no fallback path -- if the library is missing or
+fails to load, every call raises.
+
+:class:`Pipeline` owns the device buffers of one window and runs the three stages
+(grouping, alignment, collation) in order on one stream.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libodb.so")
+
+ODB_OK = 0
+ODB_E_INVALID_ARG = 1
+ODB_E_INVALID_DATA = 2
+ODB_E_WORKSPACE = 3
+ODB_E_CAPACITY = 4
+ODB_E_HIP = 5
+ODB_E_COVERAGE = 6
+ODB_E_INTERNAL = 7
+
+ODB_MODE_JOIN = 0
+ODB_MODE_NONJOIN_QUOTA = 1
+ODB_STOP_DRAINED, ODB_STOP_QUOTA, ODB_STOP_RANK_FINISHED = 0, 1, 2
+
+EXPORTED = [
+    "odb_status_string", "odb_last_error_message", "odb_workspace_size", "odb_form_groups",
+    "odb_align_groups", "odb_collate", "odb_collate_status", "odb_check_coverage",
+]
+
+
+class OdbError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{message} [status {status}]")
+        self.status = status
+
+
+class Window(ctypes.Structure):
+    _fields_ = [
+        ("num_ranks", ctypes.c_int32),
+        ("reserved0", ctypes.c_int32),
+        ("num_samples", ctypes.c_int64),
+        ("rank_offsets", ctypes.c_void_p),
+        ("d_token_offsets", ctypes.c_void_p),
+        ("d_tokens", ctypes.c_void_p),
+        ("d_identity", ctypes.c_void_p),
+        ("num_identities", ctypes.c_int64),
+    ]
+
+
+class AlignParams(ctypes.Structure):
+    _fields_ = [
+        ("mode", ctypes.c_int32),
+        ("reserved0", ctypes.c_int32),
+        ("quota", ctypes.c_int64),
+        ("slot_capacity", ctypes.c_void_p),
+    ]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [
+        ("steps", ctypes.c_int64),
+        ("rounds", ctypes.c_int32),
+        ("stop_reason", ctypes.c_int32),
+        ("emitted_samples", ctypes.c_int64),
+        ("leftover_samples", ctypes.c_int64),
+        ("real_tokens", ctypes.c_int64),
+        ("padded_elems", ctypes.c_int64),
+        ("max_step_samples", ctypes.c_int64),
+        ("splits", ctypes.c_int64),
+        ("overflow_groups", ctypes.c_int64),
+        ("missing_ids", ctypes.c_int64),
+        ("duplicate_ids", ctypes.c_int64),
+        ("bad_views", ctypes.c_int64),
+        ("pad_fraction", ctypes.c_double),
+        ("required_slot_capacity", ctypes.c_int64),
+    ]
+
+    def as_dict(self) -> dict:
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+_lib = None
+
+
+def load():
+    """Load libodb.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "or python -m paper_2606_19989_amd.build")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        W = ctypes.POINTER(Window)
+        lib.odb_status_string.restype = ctypes.c_char_p
+        lib.odb_status_string.argtypes = [ctypes.c_int]
+        lib.odb_last_error_message.restype = ctypes.c_char_p
+        lib.odb_last_error_message.argtypes = []
+        lib.odb_workspace_size.restype = SZ
+        lib.odb_workspace_size.argtypes = [W]
+        lib.odb_form_groups.restype = ctypes.c_int
+        lib.odb_form_groups.argtypes = [W, I64, P, P, P, P, P, SZ, P]
+        lib.odb_align_groups.restype = ctypes.c_int
+        lib.odb_align_groups.argtypes = [W, I64, ctypes.POINTER(AlignParams), P, P, P, P, I64,
+                                         P, P, P, P, P, P, P, P, ctypes.POINTER(PlanInfo), P, SZ, P]
+        lib.odb_collate.restype = ctypes.c_int
+        lib.odb_collate.argtypes = [W, I64, P, P, P, P, P, I32, I64, P, P, P, P, P, SZ, P]
+        lib.odb_collate_status.restype = ctypes.c_int
+        lib.odb_collate_status.argtypes = [P, SZ, P]
+        lib.odb_check_coverage.restype = ctypes.c_int
+        lib.odb_check_coverage.argtypes = [W, P, I64, P, I64, ctypes.POINTER(PlanInfo), P, SZ, P]
+        _lib = lib
+    return _lib
+
+
+def _check(status: int):
+    if status != ODB_OK:
+        lib = load()
+        raise OdbError(status, f"{lib.odb_status_string(status).decode()}: "
+                               f"{lib.odb_last_error_message().decode()}")
+
+
+def _dptr(t) -> Optional[int]:
+    """Device pointer of a contiguous torch tensor on a GPU (None passes NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+class DeviceWindow:
+    """A window resident in device memory, with its C descriptor.
+
+    rank_offsets stays on the host (int64 numpy, W+1 entries); token_offsets (int64,
+    n+1), tokens (int32) and the optional identity map (int64, n) are device tensors.
+    """
+
+    def __init__(self, rank_offsets, token_offsets, tokens, identity=None, num_identities: int = 0):
+        self.rank_offsets = np.ascontiguousarray(rank_offsets, dtype=np.int64)
+        self.token_offsets = token_offsets
+        self.tokens = tokens
+        self.identity = identity
+        self.num_ranks = len(self.rank_offsets) - 1
+        self.num_samples = int(self.rank_offsets[-1])
+        self.struct = Window(self.num_ranks, 0, self.num_samples,
+                             self.rank_offsets.ctypes.data_as(ctypes.c_void_p).value,
+                             _dptr(token_offsets), _dptr(tokens), _dptr(identity),
+                             int(num_identities) if identity is not None else 0)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.struct)
+
+
+def odb_workspace_size(win: DeviceWindow) -> int:
+    v = load().odb_workspace_size(win.ref)
+    if v == 0:
+        _check(ODB_E_INVALID_ARG)
+    return int(v)
+
+
+def odb_form_groups(win, budget, order, sorted_len, group_index, groups_per_rank, ws, stream=None):
+    _check(load().odb_form_groups(win.ref, int(budget), _dptr(order), _dptr(sorted_len), _dptr(group_index),
+                                  _dptr(groups_per_rank), _dptr(ws), ws.numel() * ws.element_size(),
+                                  _stream(stream)))
+
+
+def odb_align_groups(win, budget, mode, quota, slot_capacity_per_rank, order, sorted_len, group_index,
+                     groups_per_rank, slot_capacity, emit_order, slot_rows, slot_maxlen, slot_row_off,
+                     slot_tile_off, slot_tokens, leftover, leftover_off, ws, stream=None, raise_on_capacity=True):
+    cap = None
+    if slot_capacity_per_rank is not None:
+        cap = np.ascontiguousarray(slot_capacity_per_rank, dtype=np.int64)
+    params = AlignParams(int(mode), 0, int(quota), None if cap is None else cap.ctypes.data_as(ctypes.c_void_p).value)
+    info = PlanInfo()
+    st = load().odb_align_groups(win.ref, int(budget), ctypes.byref(params), _dptr(order), _dptr(sorted_len),
+                                 _dptr(group_index), _dptr(groups_per_rank), int(slot_capacity), _dptr(emit_order),
+                                 _dptr(slot_rows), _dptr(slot_maxlen), _dptr(slot_row_off), _dptr(slot_tile_off),
+                                 _dptr(slot_tokens), _dptr(leftover), _dptr(leftover_off), ctypes.byref(info),
+                                 _dptr(ws), ws.numel() * ws.element_size(), _stream(stream))
+    if st == ODB_E_CAPACITY and not raise_on_capacity:
+        return st, info.as_dict()
+    _check(st)
+    return st, info.as_dict()
+
+
+def odb_collate(win, num_slots, emit_order, slot_rows, slot_maxlen, slot_row_off, slot_tile_off, pad_id,
+                out_capacity, input_ids, labels, attention_mask, position_ids, ws, stream=None):
+    _check(load().odb_collate(win.ref, int(num_slots), _dptr(emit_order), _dptr(slot_rows), _dptr(slot_maxlen),
+                              _dptr(slot_row_off), _dptr(slot_tile_off), int(pad_id), int(out_capacity),
+                              _dptr(input_ids), _dptr(labels), _dptr(attention_mask), _dptr(position_ids),
+                              _dptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def odb_collate_status(ws, stream=None):
+    _check(load().odb_collate_status(_dptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def odb_check_coverage(win, emitted, num_emitted, leftover, num_leftover, ws, stream=None) -> dict:
+    info = PlanInfo()
+    _check(load().odb_check_coverage(win.ref, _dptr(emitted), int(num_emitted), _dptr(leftover), int(num_leftover),
+                                     ctypes.byref(info), _dptr(ws), ws.numel() * ws.element_size(),
+                                     _stream(stream)))
+    return info.as_dict()
+
+
+class Pipeline:
+    """Device buffers of one window and the three-stage call sequence.
+
+    Slot arrays start at ``W * max_r n_r`` capacity unless ``slot_capacity`` is given;
+    outputs of :meth:`collate` are allocated (or reused) at ``padded_elems``.
+    """
+
+    def __init__(self, win: DeviceWindow, budget: int, mode: str = "join", quota: int = 0,
+                 capacity=None, pad_id: int = 0, slot_capacity: Optional[int] = None):
+        import torch
+
+        self.torch = torch
+        self.win = win
+        self.budget = int(budget)
+        self.mode = ODB_MODE_NONJOIN_QUOTA if mode == "nonjoin" else ODB_MODE_JOIN
+        self.quota = int(quota)
+        self.capacity = capacity
+        self.pad_id = int(pad_id)
+        dev = win.token_offsets.device
+        self.device = dev
+        n, W = win.num_samples, win.num_ranks
+        n1 = max(n, 1)
+        i32 = dict(dtype=torch.int32, device=dev)
+        i64 = dict(dtype=torch.int64, device=dev)
+        self.ws = torch.empty(odb_workspace_size(win), dtype=torch.uint8, device=dev)
+        self.order = torch.empty(n1, **i32)
+        self.sorted_len = torch.empty(n1, **i32)
+        self.group_index = torch.empty(n1, **i32)
+        self.groups_per_rank = torch.empty(W, **i32)
+        self.emit_order = torch.empty(n1, **i32)
+        self.leftover = torch.empty(n1, **i32)
+        self.leftover_off = torch.empty(W + 1, **i64)
+        if slot_capacity is None:
+            sizes = np.diff(win.rank_offsets)
+            slot_capacity = int(W * (sizes.max() if len(sizes) else 0))
+        self._alloc_slots(max(int(slot_capacity), 1))
+        self.info = None
+        self.outputs = None
+
+    def _alloc_slots(self, cap: int):
+        torch = self.torch
+        self.slot_capacity = cap
+        self.slot_rows = torch.empty(cap, dtype=torch.int32, device=self.device)
+        self.slot_maxlen = torch.empty(cap, dtype=torch.int32, device=self.device)
+        self.slot_tokens = torch.empty(cap, dtype=torch.int64, device=self.device)
+        self.slot_row_off = torch.empty(cap + 1, dtype=torch.int64, device=self.device)
+        self.slot_tile_off = torch.empty(cap + 1, dtype=torch.int64, device=self.device)
+
+    def form(self, stream=None):
+        odb_form_groups(self.win, self.budget, self.order, self.sorted_len, self.group_index,
+                        self.groups_per_rank, self.ws, stream)
+
+    def align(self, stream=None) -> dict:
+        args = lambda: (self.win, self.budget, self.mode, self.quota, self.capacity, self.order, self.sorted_len,
+                        self.group_index, self.groups_per_rank, self.slot_capacity, self.emit_order,
+                        self.slot_rows, self.slot_maxlen, self.slot_row_off, self.slot_tile_off, self.slot_tokens,
+                        self.leftover, self.leftover_off, self.ws, stream)
+        st, info = odb_align_groups(*args(), raise_on_capacity=False)
+        if st == ODB_E_CAPACITY:
+            self._alloc_slots(int(info["required_slot_capacity"]))
+            st, info = odb_align_groups(*args())
+        self.info = info
+        return info
+
+    @property
+    def num_slots(self) -> int:
+        return self.win.num_ranks * int(self.info["steps"])
+
+    def alloc_outputs(self, elems: int):
+        torch = self.torch
+        elems = max(int(elems), 1)
+        if self.outputs is None or self.outputs[0].numel() < elems:
+            self.outputs = tuple(torch.empty(elems, dtype=torch.int32, device=self.device) for _ in range(4))
+        return self.outputs
+
+    def collate(self, stream=None):
+        P = int(self.info["padded_elems"])
+        outs = self.alloc_outputs(P)
+        odb_collate(self.win, self.num_slots, self.emit_order, self.slot_rows, self.slot_maxlen, self.slot_row_off,
+                    self.slot_tile_off, self.pad_id, P, *outs, self.ws, stream)
+        return tuple(o[:P] for o in outs)
+
+    def run(self, stream=None):
+        self.form(stream)
+        self.align(stream)
+        return self.collate(stream)

@@ -1,0 +1,987 @@
+// Stages 2-3 of the ODB window pipeline: Distributed Group Alignment (Eq. 3,
+// Algorithm 1, termination rules of Sec. 2.3) and identity coverage (App. C).
+//
+// Every rank's buffer is a contiguous run of formation positions; a group is a range
+// of them.  One alignment round is:
+//   target_kernel      the simulated all_gather of (G_r, S_r, C_r) and Eq. 3's T
+//   group_sizes        size of every group
+//   adjust_kernel      per rank: split (closed form, below) or overflow (size threshold)
+//   slot_records       rows / max length / real tokens of every aligned step, and the
+//                      global sample count of every step
+//   cut_kernel         join: all T steps; non-join: up to the first step reaching Q
+//   finalize_kernel    per rank: which positions are emitted, where they go
+//   emit_kernel        writes emitted ids (rows short to long) and the next buffer
+// and rounds repeat on the returned samples until the termination rule fires.
+//
+// Split in closed form.  Algorithm 1 peels, one at a time, the last sample of the first
+// multi-sample group met scanning the short-to-long list from its long end.  In
+// formation order (longest first) that is the longest member of the first group with
+// at least two samples; after k = T - G_r peels, formation positions [0, X) are
+// singletons, [X, end of group j*) is one group and later groups are untouched, where
+// j* is the first group whose cumulative surplus sum_{g<=j}(c_g - 1) reaches k and
+// X = k + j*.
+//
+// Overflow.  Algorithm 1 keeps the T largest groups (stable over the short-to-long list,
+// so equal sizes favour the later-formed group).  With sigma = the largest size such
+// that at least T groups have size >= sigma, every group larger than sigma is kept and
+// the remaining places go to the size-sigma groups with the highest formation index.
+#include <climits>
+#include <cstring>
+#include <vector>
+
+#include "odb_internal.h"
+
+namespace odb {
+
+namespace {
+
+template <typename T, typename Op>
+__device__ __forceinline__ T block_reduce(T v, Op op) {
+    __shared__ T buf[kBlock];
+    buf[threadIdx.x] = v;
+    __syncthreads();
+    for (int s = kBlock / 2; s > 0; s >>= 1) {
+        if (threadIdx.x < s) buf[threadIdx.x] = op(buf[threadIdx.x], buf[threadIdx.x + s]);
+        __syncthreads();
+    }
+    T r = buf[0];
+    __syncthreads();
+    return r;
+}
+
+struct MaxOp {
+    __device__ int64_t operator()(int64_t a, int64_t b) const { return a > b ? a : b; }
+};
+struct MinOp {
+    __device__ int64_t operator()(int64_t a, int64_t b) const { return a < b ? a : b; }
+};
+struct SumOp {
+    __device__ int64_t operator()(int64_t a, int64_t b) const { return a + b; }
+};
+
+__global__ void init_align_kernel(RoundState* rs, DevInfo* info) {
+    if (threadIdx.x == 0) {
+        *rs = RoundState{};
+        *info = DevInfo{};
+    }
+}
+
+__global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+__global__ void fill_i64_kernel(int64_t* p, int64_t n, int64_t v) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+// ---------------------------------------------------------------- round 0 inputs
+// Rank state from the stage-1 group counts; G_r must be 0 exactly for empty ranks and
+// at most S_r.  One block.
+__global__ void __launch_bounds__(kBlock) round0_ranks_kernel(const int64_t* __restrict__ off,
+                                                              const int32_t* __restrict__ groups, int W,
+                                                              RankState* ranks, int64_t* __restrict__ gbase,
+                                                              DevStatus* st) {
+    __shared__ int64_t carry;
+    if (threadIdx.x == 0) carry = 0;
+    __syncthreads();
+    for (int b = 0; b < W; b += kBlock) {
+        const int r = b + threadIdx.x;
+        int64_t G = 0, cnt = 0;
+        if (r < W) {
+            G = groups[r];
+            cnt = off[r + 1] - off[r];
+            if (G < 0 || G > cnt || ((cnt == 0) != (G == 0))) {
+                atomicOr(&st->err, kErrGroupIndex);
+                G = 0;
+            }
+        }
+        int64_t tot;
+        const int64_t ex = block_excl_sum(G, &tot);
+        const int64_t c = carry;
+        if (r < W) {
+            RankState z = {};
+            z.cnt = cnt;
+            z.G = G;
+            z.gbase = c + ex;
+            ranks[r] = z;
+            gbase[r] = c + ex;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) carry = c + tot;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) gbase[W] = carry;
+}
+
+// Checks that stage-1 arrays describe this window: order[p] is a sample of p's rank,
+// sorted_len[p] its length, the order strictly (length desc, id asc) and the group
+// indices run 0, 0|+1, ..., G_r - 1.  Records every group start.
+__global__ void __launch_bounds__(kBlock) round0_check_kernel(
+    const int64_t* __restrict__ tok_off, const int64_t* __restrict__ off, const RankState* __restrict__ ranks,
+    int W, int64_t n, const int32_t* __restrict__ order, const int32_t* __restrict__ slen,
+    const int32_t* __restrict__ gidx, int32_t* __restrict__ gstart, DevStatus* st) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
+        const int r = rank_of(off, W, p);
+        const int64_t base = off[r];
+        const int64_t q = p - base, nr = ranks[r].cnt;
+        const int64_t G = ranks[r].G;
+        const int32_t id = order[p];
+        const int32_t l = slen[p];
+        bool ok = id >= base && id < base + nr;
+        if (ok) ok = tok_off[id + 1] - tok_off[id] == (int64_t)l;
+        const int32_t g = gidx[p];
+        bool gok = g >= 0 && g < G;
+        if (q == 0) {
+            gok = gok && g == 0;
+        } else {
+            const int32_t pl = slen[p - 1], pid = order[p - 1];
+            ok = ok && (pl > l || (pl == l && pid < id));
+            const int32_t d = g - gidx[p - 1];
+            gok = gok && (d == 0 || d == 1);
+        }
+        if (q == nr - 1) gok = gok && g == G - 1;
+        if (!ok) {
+            atomicOr(&st->err, kErrOrder);
+            atomicMin((unsigned long long*)&st->first_bad, (unsigned long long)p);
+        }
+        if (!gok) {
+            atomicOr(&st->err, kErrGroupIndex);
+            atomicMin((unsigned long long*)&st->first_bad, (unsigned long long)p);
+        } else if (q == 0 || g != gidx[p - 1]) {
+            gstart[ranks[r].gbase + g] = (int32_t)p;
+        }
+    }
+}
+
+// ---------------------------------------------------------------- one round
+struct LiveLen {
+    const int32_t* len;
+    const int64_t* off;
+    const RankState* ranks;
+    int W;
+    int gaps;
+    __device__ int64_t operator()(int64_t i) const {
+        if (!gaps) return len[i];
+        const int r = rank_of(off, W, i);
+        return (i - off[r] < ranks[r].cnt) ? (int64_t)len[i] : 0;
+    }
+};
+struct LiveLenIncl {
+    LiveLen ld;
+    int64_t* cs;
+    __device__ void operator()(int64_t i, int64_t ex) const { cs[i] = ex + ld(i); }
+};
+
+// Eq. 3 over the active ranks, then the action of every rank.  One block.
+__global__ void __launch_bounds__(kBlock) target_kernel(RankState* ranks, const int64_t* __restrict__ cap,
+                                                        int has_cap, int W, RoundState* rs) {
+    int64_t maxG = 0, minC = LLONG_MAX, minS = LLONG_MAX, active = 0, totalG = 0;
+    for (int r = threadIdx.x; r < W; r += kBlock) {
+        const int64_t G = ranks[r].G;
+        totalG += G;
+        if (G <= 0) continue;
+        active += 1;
+        maxG = G > maxG ? G : maxG;
+        const int64_t S = ranks[r].cnt;
+        if (S > 0 && S < minS) minS = S;
+        if (has_cap && cap[r] > 0 && cap[r] < minC) minC = cap[r];
+    }
+    maxG = block_reduce(maxG, MaxOp{});
+    minC = block_reduce(minC, MinOp{});
+    minS = block_reduce(minS, MinOp{});
+    active = block_reduce(active, SumOp{});
+    totalG = block_reduce(totalG, SumOp{});
+    int64_t T = maxG;
+    if (minC != LLONG_MAX && minC < T) T = minC;
+    if (minS != LLONG_MAX && minS < T) T = minS;
+    if (T < 1) T = 1;
+    int64_t splits = 0, over = 0;
+    for (int r = threadIdx.x; r < W; r += kBlock) {
+        RankState& R = ranks[r];
+        const int64_t G = R.G;
+        R.X = 0;
+        R.jstar = 0;
+        R.qcut = 0;
+        if (G <= 0) {
+            R.action = kActInactive;
+        } else if (G < T) {
+            R.action = kActSplit;
+            splits += T - G;
+        } else if (G > T) {
+            R.action = kActOverflow;
+            over += G - T;
+        } else {
+            R.action = kActKeep;
+        }
+    }
+    splits = block_reduce(splits, SumOp{});
+    over = block_reduce(over, SumOp{});
+    if (threadIdx.x == 0) {
+        rs->T = T;
+        rs->active = active;
+        rs->total_groups = totalG;
+        rs->splits += splits;
+        rs->overflow += over;
+        rs->cut = 0;
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) group_sizes_kernel(const int32_t* __restrict__ gstart,
+                                                             const int64_t* __restrict__ gbase,
+                                                             const int64_t* __restrict__ off,
+                                                             const RankState* __restrict__ ranks, int W,
+                                                             int32_t* __restrict__ gsize) {
+    const int64_t total = gbase[W];
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < total; g += stride) {
+        const int r = rank_of(gbase, W, g);
+        const int64_t lg = g - gbase[r];
+        const int64_t start = gstart[g];
+        const int64_t end = (lg + 1 < ranks[r].G) ? (int64_t)gstart[g + 1] : off[r] + ranks[r].cnt;
+        gsize[g] = (int32_t)(end - start);
+    }
+}
+
+// Per rank (one block each): split position or overflow selection.
+__global__ void __launch_bounds__(kBlock) adjust_kernel(RankState* ranks, const RoundState* __restrict__ rs,
+                                                        const int64_t* __restrict__ off,
+                                                        const int32_t* __restrict__ gstart,
+                                                        const int32_t* __restrict__ gsize,
+                                                        int32_t* __restrict__ ov_slot, int32_t* __restrict__ kept,
+                                                        DevStatus* st) {
+    const int r = blockIdx.x;
+    const int32_t action = ranks[r].action;
+    if (action != kActSplit && action != kActOverflow) return;
+    const int64_t T = rs->T;
+    const int64_t G = ranks[r].G;
+    const int64_t gb = ranks[r].gbase;
+    __shared__ int64_t s_found;
+    if (action == kActSplit) {
+        const int64_t k = T - G;
+        if (threadIdx.x == 0) s_found = -1;
+        __syncthreads();
+        int64_t carry = 0;
+        for (int64_t b = 0; b < G; b += kBlock) {
+            const int64_t j = b + threadIdx.x;
+            const int64_t v = j < G ? (int64_t)gsize[gb + j] - 1 : 0;
+            int64_t tot;
+            const int64_t ex = block_excl_sum(v, &tot);
+            if (j < G && carry + ex < k && carry + ex + v >= k) s_found = j;
+            __syncthreads();
+            if (s_found >= 0) break;
+            carry += tot;
+        }
+        if (threadIdx.x == 0) {
+            const int64_t js = s_found;
+            if (js < 1) {
+                // the group sizes do not add up to the buffer: drop the rank from this round
+                // (nothing is indexed through the split) and report an internal error
+                atomicOr(&st->err, kErrInternal);
+                ranks[r].action = kActInactive;
+            } else {
+                ranks[r].jstar = js;
+                ranks[r].X = k + js;
+            }
+        }
+        return;
+    }
+    // overflow: sigma = largest size with at least T groups of size >= sigma
+    int64_t mx = 0;
+    for (int64_t j = threadIdx.x; j < G; j += kBlock) {
+        const int64_t s = gsize[gb + j];
+        mx = s > mx ? s : mx;
+    }
+    mx = block_reduce(mx, MaxOp{});
+    int64_t lo = 1, hi = mx;
+    while (lo < hi) {
+        const int64_t mid = lo + (hi - lo + 1) / 2;
+        int64_t c = 0;
+        for (int64_t j = threadIdx.x; j < G; j += kBlock) c += gsize[gb + j] >= mid ? 1 : 0;
+        c = block_reduce(c, SumOp{});
+        if (c >= T) lo = mid; else hi = mid - 1;
+    }
+    const int64_t sigma = lo;
+    int64_t above = 0;
+    for (int64_t j = threadIdx.x; j < G; j += kBlock) above += gsize[gb + j] > sigma ? 1 : 0;
+    above = block_reduce(above, SumOp{});
+    const int64_t need = T - above;
+    // walk groups from the highest formation index down
+    int64_t ceq = 0, ckept = 0;
+    for (int64_t b = 0; b < G; b += kBlock) {
+        const int64_t i = b + threadIdx.x;
+        const bool valid = i < G;
+        const int64_t g = G - 1 - i;
+        const int64_t s = valid ? gsize[gb + g] : 0;
+        const int64_t eq = (valid && s == sigma) ? 1 : 0;
+        int64_t teq;
+        const int64_t xeq = block_excl_sum(eq, &teq);
+        const int64_t keep = (valid && (s > sigma || (eq && ceq + xeq < need))) ? 1 : 0;
+        int64_t tk;
+        const int64_t xk = block_excl_sum(keep, &tk);
+        if (valid) {
+            if (keep) {
+                ov_slot[gb + g] = (int32_t)(ckept + xk);
+                kept[gb + ckept + xk] = (int32_t)g;
+            } else {
+                ov_slot[gb + g] = -1;
+            }
+        }
+        ceq += teq;
+        ckept += tk;
+    }
+}
+
+// First formation position and one-past-last of adjusted group a (formation order) of a
+// keep / split rank.
+__device__ __forceinline__ void adjusted_range(const RankState& R, int64_t base, int64_t a,
+                                               const int32_t* __restrict__ gstart,
+                                               const int32_t* __restrict__ gsize, int64_t* start, int64_t* end) {
+    if (a < R.X) {
+        *start = base + a;
+        *end = base + a + 1;
+    } else if (a == R.X) {
+        const int64_t g = R.gbase + R.jstar;
+        *start = base + R.X;
+        *end = (int64_t)gstart[g] + gsize[g];
+    } else {
+        const int64_t g = R.gbase + R.jstar + (a - R.X);
+        *start = gstart[g];
+        *end = *start + gsize[g];
+    }
+}
+
+// Step j of every active rank: adjusted group T-1-j (emission runs short to long).
+__global__ void __launch_bounds__(kBlock) slot_records_kernel(
+    const RankState* __restrict__ ranks, const RoundState* __restrict__ rs, const int64_t* __restrict__ off, int W,
+    const int32_t* __restrict__ gstart, const int32_t* __restrict__ gsize, const int32_t* __restrict__ kept,
+    const int32_t* __restrict__ cur_len, const int64_t* __restrict__ cs, int32_t* __restrict__ srows,
+    int32_t* __restrict__ smax, int64_t* __restrict__ stok, int64_t* __restrict__ steps) {
+    const int64_t T = rs->T;
+    const int64_t total = (int64_t)W * T;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += stride) {
+        const int r = (int)(idx / T);
+        const int64_t j = idx - (int64_t)r * T;
+        const RankState R = ranks[r];
+        if (R.action == kActInactive) continue;
+        const int64_t base = off[r];
+        int64_t start, end;
+        if (R.action == kActOverflow) {
+            const int64_t g = R.gbase + kept[R.gbase + j];
+            start = gstart[g];
+            end = start + gsize[g];
+        } else {
+            adjusted_range(R, base, T - 1 - j, gstart, gsize, &start, &end);
+        }
+        const int64_t rows = end - start;
+        const int64_t dst = base + R.slots + j;
+        srows[dst] = (int32_t)rows;
+        smax[dst] = cur_len[start];
+        stok[dst] = cs[end - 1] - (start > 0 ? cs[start - 1] : 0);
+        atomicAdd((unsigned long long*)&steps[j], (unsigned long long)rows);
+    }
+}
+
+// Join: every step is emitted.  Non-join: steps up to the first one at which the
+// cumulative global emitted count reaches the quota (Theorem 2).  One block.
+__global__ void __launch_bounds__(kBlock) cut_kernel(RoundState* rs, const int64_t* __restrict__ steps,
+                                                     int nonjoin, int64_t quota) {
+    const int64_t T = rs->T;
+    const int64_t before = rs->emitted_total;
+    __shared__ int64_t s_cut;
+    if (threadIdx.x == 0) s_cut = T;
+    __syncthreads();
+    if (nonjoin) {
+        int64_t carry = 0;
+        for (int64_t b = 0; b < T; b += kBlock) {
+            const int64_t j = b + threadIdx.x;
+            const int64_t v = j < T ? steps[j] : 0;
+            int64_t tot;
+            const int64_t ex = block_excl_sum(v, &tot);
+            if (j < T && before + carry + ex < quota && before + carry + ex + v >= quota) s_cut = j + 1;
+            __syncthreads();
+            if (s_cut < T) break;
+            carry += tot;
+        }
+    }
+    const int64_t cut = s_cut;
+    int64_t sum = 0, mx = 0;
+    for (int64_t j = threadIdx.x; j < cut; j += kBlock) {
+        const int64_t v = steps[j];
+        sum += v;
+        mx = v > mx ? v : mx;
+    }
+    sum = block_reduce(sum, SumOp{});
+    mx = block_reduce(mx, MaxOp{});
+    if (threadIdx.x == 0) {
+        rs->cut = cut;
+        rs->emitted_total = before + sum;
+        if (mx > rs->step_max) rs->step_max = mx;
+        if (nonjoin && before + sum >= quota) rs->quota_hit = 1;
+    }
+}
+
+// Per rank (one block each): emitted positions and the layout of the next buffer.
+__global__ void __launch_bounds__(kBlock) finalize_kernel(RankState* ranks, const RoundState* __restrict__ rs,
+                                                          const int64_t* __restrict__ off,
+                                                          const int32_t* __restrict__ gstart,
+                                                          const int32_t* __restrict__ gsize,
+                                                          const int32_t* __restrict__ ov_slot,
+                                                          const int32_t* __restrict__ kept,
+                                                          int32_t* __restrict__ ov_lo) {
+    const int r = blockIdx.x;
+    RankState& R = ranks[r];
+    const int64_t T = rs->T, cut = rs->cut;
+    if (threadIdx.x == 0) R.ebase = R.emitted;
+    if (R.action == kActInactive) {
+        if (threadIdx.x == 0) R.next_cnt = 0;
+        return;
+    }
+    const int64_t base = off[r];
+    if (R.action != kActOverflow) {
+        if (threadIdx.x == 0) {
+            int64_t q = 0;
+            if (cut < T) {
+                int64_t s, e;
+                adjusted_range(R, base, T - cut, gstart, gsize, &s, &e);
+                q = s - base;
+            }
+            R.qcut = q;
+            R.next_cnt = q;
+            R.emitted += R.cnt - q;
+            R.slots += cut;
+        }
+        return;
+    }
+    const int64_t G = R.G, gb = R.gbase;
+    // emitted groups, slot order: consecutive emission offsets
+    int64_t carry = 0;
+    for (int64_t b = 0; b < cut; b += kBlock) {
+        const int64_t j = b + threadIdx.x;
+        const int64_t g = j < cut ? gb + kept[gb + j] : 0;
+        const int64_t v = j < cut ? gsize[g] : 0;
+        int64_t tot;
+        const int64_t ex = block_excl_sum(v, &tot);
+        if (j < cut) ov_lo[g] = (int32_t)(carry + ex);
+        carry += tot;
+    }
+    const int64_t emitted_now = carry;
+    // everything else, formation order: offsets in the next buffer
+    carry = 0;
+    for (int64_t b = 0; b < G; b += kBlock) {
+        const int64_t j = b + threadIdx.x;
+        const int32_t sl = j < G ? ov_slot[gb + j] : 0;
+        const bool stay = j < G && (sl < 0 || sl >= cut);
+        const int64_t v = stay ? gsize[gb + j] : 0;
+        int64_t tot;
+        const int64_t ex = block_excl_sum(v, &tot);
+        if (stay) ov_lo[gb + j] = (int32_t)(carry + ex);
+        carry += tot;
+    }
+    if (threadIdx.x == 0) {
+        R.next_cnt = carry;
+        R.emitted += emitted_now;
+        R.slots += cut;
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) emit_kernel(
+    const RankState* __restrict__ ranks, const RoundState* __restrict__ rs, const int64_t* __restrict__ off, int W,
+    int64_t n, const int32_t* __restrict__ cur_ids, const int32_t* __restrict__ cur_len,
+    const int32_t* __restrict__ gidx, const int32_t* __restrict__ gstart, const int32_t* __restrict__ gsize,
+    const int32_t* __restrict__ ov_slot, const int32_t* __restrict__ ov_lo, int32_t* __restrict__ dst,
+    int32_t* __restrict__ next_ids, int32_t* __restrict__ next_len) {
+    const int64_t cut = rs->cut;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
+        const int r = rank_of(off, W, p);
+        const int64_t base = off[r];
+        const int64_t q = p - base;
+        const RankState& R = ranks[r];
+        const int64_t cnt = R.cnt;
+        if (q >= cnt) continue;
+        const int32_t id = cur_ids[p];
+        if (R.action != kActOverflow) {
+            if (q >= R.qcut) {
+                dst[base + R.ebase + (cnt - 1 - q)] = id;
+            } else {
+                next_ids[base + q] = id;
+                next_len[base + q] = cur_len[p];
+            }
+        } else {
+            const int64_t g = R.gbase + gidx[p];
+            const int32_t sl = ov_slot[g];
+            const int64_t st = (int64_t)gstart[g] - base;
+            if (sl >= 0 && sl < cut) {
+                dst[base + R.ebase + ov_lo[g] + (st + gsize[g] - 1 - q)] = id;
+            } else {
+                const int64_t o = ov_lo[g] + (q - st);
+                next_ids[base + o] = id;
+                next_len[base + o] = cur_len[p];
+            }
+        }
+    }
+}
+
+__global__ void advance_kernel(RankState* ranks, int W) {
+    for (int r = blockIdx.x * blockDim.x + threadIdx.x; r < W; r += gridDim.x * blockDim.x)
+        ranks[r].cnt = ranks[r].next_cnt;
+}
+
+// ---------------------------------------------------------------- final plan
+__global__ void __launch_bounds__(kBlock) plan_slots_kernel(const RankState* __restrict__ ranks,
+                                                            const int64_t* __restrict__ off, int W, int64_t S,
+                                                            const int32_t* __restrict__ srows,
+                                                            const int32_t* __restrict__ smax,
+                                                            const int64_t* __restrict__ stok,
+                                                            int32_t* __restrict__ rows, int32_t* __restrict__ maxlen,
+                                                            int64_t* __restrict__ tokens) {
+    const int64_t K = (int64_t)W * S;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < K; k += stride) {
+        const int r = (int)(k / S);
+        const int64_t j = k - (int64_t)r * S;
+        if (j < ranks[r].slots) {
+            const int64_t src = off[r] + j;
+            rows[k] = srows[src];
+            maxlen[k] = smax[src];
+            tokens[k] = stok[src];
+        } else {
+            rows[k] = 0;
+            maxlen[k] = 0;
+            tokens[k] = 0;
+        }
+    }
+}
+
+struct RowsLoad {
+    const int32_t* rows;
+    int64_t K;
+    __device__ int64_t operator()(int64_t i) const { return i < K ? (int64_t)rows[i] : 0; }
+};
+struct TileLoad {
+    const int32_t* rows;
+    const int32_t* mx;
+    int64_t K;
+    __device__ int64_t operator()(int64_t i) const { return i < K ? (int64_t)rows[i] * mx[i] : 0; }
+};
+struct Store64 {
+    int64_t* out;
+    __device__ void operator()(int64_t i, int64_t v) const { out[i] = v; }
+};
+
+__global__ void __launch_bounds__(kBlock) compact_emit_kernel(const int32_t* __restrict__ stage,
+                                                              const int64_t* __restrict__ off,
+                                                              const RankState* __restrict__ ranks, int W, int64_t n,
+                                                              const int64_t* __restrict__ row_off, int64_t S,
+                                                              int32_t* __restrict__ emit) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
+        const int r = rank_of(off, W, p);
+        const int64_t e = p - off[r];
+        if (e < ranks[r].emitted) emit[row_off[(int64_t)r * S] + e] = stage[p];
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) leftover_off_kernel(const RankState* __restrict__ ranks, int W,
+                                                              int64_t* __restrict__ loff) {
+    __shared__ int64_t carry;
+    if (threadIdx.x == 0) carry = 0;
+    __syncthreads();
+    for (int b = 0; b < W; b += kBlock) {
+        const int r = b + threadIdx.x;
+        const int64_t v = r < W ? ranks[r].cnt : 0;
+        int64_t tot;
+        const int64_t ex = block_excl_sum(v, &tot);
+        const int64_t c = carry;
+        if (r < W) loff[r] = c + ex;
+        __syncthreads();
+        if (threadIdx.x == 0) carry = c + tot;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) loff[W] = carry;
+}
+
+__global__ void __launch_bounds__(kBlock) leftover_kernel(const int32_t* __restrict__ cur_ids,
+                                                          const int64_t* __restrict__ off,
+                                                          const RankState* __restrict__ ranks, int W, int64_t n,
+                                                          const int64_t* __restrict__ loff,
+                                                          int32_t* __restrict__ left) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
+        const int r = rank_of(off, W, p);
+        const int64_t q = p - off[r];
+        if (q < ranks[r].cnt) left[loff[r] + q] = cur_ids[p];
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) tokens_sum_kernel(const int64_t* __restrict__ tokens, int64_t K,
+                                                            DevInfo* info) {
+    int64_t s = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < K; k += stride) s += tokens[k];
+    s = block_sum(s);
+    if (threadIdx.x == 0 && s) atomicAdd((unsigned long long*)&info->real_tokens, (unsigned long long)s);
+}
+
+__global__ void finish_info_kernel(const int64_t* __restrict__ row_off, const int64_t* __restrict__ tile_off,
+                                   int64_t K, DevInfo* info) {
+    if (threadIdx.x == 0) {
+        info->padded_elems = K > 0 ? tile_off[K] : 0;
+        info->emitted = K > 0 ? row_off[K] : 0;
+        info->pad_fraction =
+            info->padded_elems > 0 ? 1.0 - (double)info->real_tokens / (double)info->padded_elems : 0.0;
+    }
+}
+
+// ---------------------------------------------------------------- coverage
+// cnt[v] += 1 for every view id (or its identity) in ids[0, m).
+__global__ void __launch_bounds__(kBlock) count_kernel(const int32_t* __restrict__ ids, int64_t m, int64_t n,
+                                                       const int64_t* __restrict__ identity, int64_t range,
+                                                       int32_t* cnt, DevStatus* st) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += stride) {
+        int64_t v = ids[i];
+        if (v < 0 || v >= n) {
+            atomicOr(&st->err, kErrInternal);
+            continue;
+        }
+        if (identity) v = identity[v];
+        if (v < 0 || v >= range) {
+            atomicOr(&st->err, kErrIdentity);
+            continue;
+        }
+        atomicAdd(&cnt[v], 1);
+    }
+}
+
+// bad = #(cnt != 1) (views); missing = #(cnt == 0); dup = sum max(cnt - 1, 0).
+__global__ void __launch_bounds__(kBlock) coverage_reduce_kernel(const int32_t* __restrict__ cnt, int64_t m,
+                                                                 int want_bad, int want_ids, DevInfo* info) {
+    int64_t bad = 0, miss = 0, dup = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += stride) {
+        const int32_t c = cnt[i];
+        bad += c != 1 ? 1 : 0;
+        miss += c == 0 ? 1 : 0;
+        dup += c > 1 ? c - 1 : 0;
+    }
+    bad = block_sum(bad);
+    miss = block_sum(miss);
+    dup = block_sum(dup);
+    if (threadIdx.x == 0) {
+        if (want_bad && bad) atomicAdd((unsigned long long*)&info->bad_views, (unsigned long long)bad);
+        if (want_ids && miss) atomicAdd((unsigned long long*)&info->missing_ids, (unsigned long long)miss);
+        if (want_ids && dup) atomicAdd((unsigned long long*)&info->duplicate_ids, (unsigned long long)dup);
+    }
+}
+
+int run_coverage(const odb_window_t* w, const Layout& L, void* ws, const int32_t* emitted, int64_t ne,
+                 const int32_t* left, int64_t nl, hipStream_t s) {
+    const int64_t n = w->num_samples;
+    int32_t* cover = ws_at<int32_t>(ws, L.cover);
+    DevStatus* st = ws_at<DevStatus>(ws, L.status);
+    DevInfo* info = ws_at<DevInfo>(ws, L.info);
+    const int64_t cap = (int64_t)num_cus() * 16;
+    auto count = [&](const int64_t* identity, int64_t range) -> int {
+        hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(range, kBlock, cap)), dim3(kBlock), 0, s, cover, range, 0);
+        ODB_LAUNCHED();
+        if (ne > 0) {
+            hipLaunchKernelGGL(count_kernel, dim3(grid_for(ne, kBlock, cap)), dim3(kBlock), 0, s, emitted, ne, n,
+                               identity, range, cover, st);
+            ODB_LAUNCHED();
+        }
+        if (nl > 0) {
+            hipLaunchKernelGGL(count_kernel, dim3(grid_for(nl, kBlock, cap)), dim3(kBlock), 0, s, left, nl, n,
+                               identity, range, cover, st);
+            ODB_LAUNCHED();
+        }
+        return ODB_OK;
+    };
+    if (n > 0) {
+        ODB_TRY(count(nullptr, n));
+        hipLaunchKernelGGL(coverage_reduce_kernel, dim3(grid_for(n, kBlock, cap)), dim3(kBlock), 0, s,
+                           (const int32_t*)cover, n, 1, w->d_identity ? 0 : 1, info);
+        ODB_LAUNCHED();
+    }
+    if (w->d_identity) {
+        const int64_t nid = w->num_identities;
+        ODB_TRY(count(w->d_identity, nid));
+        hipLaunchKernelGGL(coverage_reduce_kernel, dim3(grid_for(nid, kBlock, cap)), dim3(kBlock), 0, s,
+                           (const int32_t*)cover, nid, 0, 1, info);
+        ODB_LAUNCHED();
+    }
+    return ODB_OK;
+}
+
+struct RoundBuffers {
+    const int32_t* ids;
+    const int32_t* len;
+    const int32_t* gidx;
+};
+
+}  // namespace
+
+}  // namespace odb
+
+using namespace odb;
+
+extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb_align_params_t* params,
+                                const int32_t* d_order, const int32_t* d_sorted_len, const int32_t* d_group_index,
+                                const int32_t* d_groups_per_rank, int64_t slot_capacity, int32_t* d_emit_order,
+                                int32_t* d_slot_rows, int32_t* d_slot_maxlen, int64_t* d_slot_row_off,
+                                int64_t* d_slot_tile_off, int64_t* d_slot_tokens, int32_t* d_leftover,
+                                int64_t* d_leftover_off, odb_plan_info_t* h_info, void* d_ws, size_t ws_bytes,
+                                void* stream) {
+    Layout L;
+    ODB_TRY(check_workspace(w, d_ws, ws_bytes, &L));
+    if (budget < 1) return set_error(ODB_E_INVALID_ARG, "budget must be >= 1");
+    if (!params) return set_error(ODB_E_INVALID_ARG, "params is NULL");
+    if (params->mode != ODB_MODE_JOIN && params->mode != ODB_MODE_NONJOIN_QUOTA)
+        return set_error(ODB_E_INVALID_ARG, "unknown mode %d", params->mode);
+    if (params->reserved0 != 0) return set_error(ODB_E_INVALID_ARG, "params.reserved0 must be 0");
+    const bool nonjoin = params->mode == ODB_MODE_NONJOIN_QUOTA;
+    if (nonjoin && params->quota < 1) return set_error(ODB_E_INVALID_ARG, "quota must be >= 1 in non-join mode");
+    if (!h_info) return set_error(ODB_E_INVALID_ARG, "h_info is NULL");
+    if (slot_capacity < 0) return set_error(ODB_E_INVALID_ARG, "slot_capacity must be >= 0");
+    const int W = w->num_ranks;
+    const int64_t n = w->num_samples;
+    if (n > 0 && (!d_order || !d_sorted_len || !d_group_index || !d_emit_order || !d_leftover))
+        return set_error(ODB_E_INVALID_ARG, "sample arrays must not be NULL");
+    if (!d_groups_per_rank || !d_slot_row_off || !d_slot_tile_off || !d_leftover_off)
+        return set_error(ODB_E_INVALID_ARG, "offset arrays must not be NULL");
+    if (slot_capacity > 0 && (!d_slot_rows || !d_slot_maxlen || !d_slot_tokens))
+        return set_error(ODB_E_INVALID_ARG, "slot arrays must not be NULL");
+    const int64_t* cap = params->slot_capacity;
+    if (cap)
+        for (int r = 0; r < W; ++r)
+            if (cap[r] < 0) return set_error(ODB_E_INVALID_ARG, "slot_capacity[%d] must be >= 0", r);
+    memset(h_info, 0, sizeof(*h_info));
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    ODB_TRY(upload_small(w, L, d_ws, cap, s));
+    const int64_t* d_off = ws_at<int64_t>(d_ws, L.rank_off);
+    const int64_t* d_cap = ws_at<int64_t>(d_ws, L.cap);
+    RankState* d_ranks = ws_at<RankState>(d_ws, L.ranks);
+    RoundState* d_rs = ws_at<RoundState>(d_ws, L.round);
+    DevStatus* st = ws_at<DevStatus>(d_ws, L.status);
+    DevInfo* d_info = ws_at<DevInfo>(d_ws, L.info);
+    int64_t* d_gbase = ws_at<int64_t>(d_ws, L.gbase);
+    int32_t* gstart = ws_at<int32_t>(d_ws, L.gstart);
+    int32_t* gsize = ws_at<int32_t>(d_ws, L.gsize);
+    int64_t* cs = ws_at<int64_t>(d_ws, L.cs);
+    int32_t* ov_slot = ws_at<int32_t>(d_ws, L.ov_slot);
+    int32_t* ov_lo = ws_at<int32_t>(d_ws, L.ov_lo);
+    int32_t* kept = ws_at<int32_t>(d_ws, L.kept);
+    int32_t* srows = ws_at<int32_t>(d_ws, L.srows);
+    int32_t* smax = ws_at<int32_t>(d_ws, L.smax);
+    int64_t* stok = ws_at<int64_t>(d_ws, L.stok);
+    int64_t* steps = ws_at<int64_t>(d_ws, L.steps);
+    int32_t* bids[2] = {ws_at<int32_t>(d_ws, L.buf_ids0), ws_at<int32_t>(d_ws, L.buf_ids1)};
+    int32_t* blen[2] = {ws_at<int32_t>(d_ws, L.buf_len0), ws_at<int32_t>(d_ws, L.buf_len1)};
+    int32_t* wgidx = ws_at<int32_t>(d_ws, L.gidx);
+    int32_t* dst = nonjoin ? ws_at<int32_t>(d_ws, L.stage) : d_emit_order;
+    const int64_t gcap = (int64_t)num_cus() * 16;
+    const unsigned gridn = grid_for(n, kBlock, gcap);
+
+    hipLaunchKernelGGL(init_align_kernel, dim3(1), dim3(64), 0, s, d_rs, d_info);
+    ODB_LAUNCHED();
+    hipLaunchKernelGGL(round0_ranks_kernel, dim3(1), dim3(kBlock), 0, s, d_off, d_groups_per_rank, W, d_ranks,
+                       d_gbase, st);
+    ODB_LAUNCHED();
+    if (n > 0) {
+        hipLaunchKernelGGL(round0_check_kernel, dim3(gridn), dim3(kBlock), 0, s, w->d_token_offsets, d_off,
+                           (const RankState*)d_ranks, W, n, d_order, d_sorted_len, d_group_index, gstart, st);
+        ODB_LAUNCHED();
+    }
+    {
+        DevStatus hs;
+        ODB_TRY_HIP(hipMemcpyAsync(&hs, st, sizeof(hs), hipMemcpyDeviceToHost, s));
+        ODB_TRY_HIP(hipStreamSynchronize(s));
+        if (hs.err & (kErrOrder | kErrGroupIndex))
+            return set_error(ODB_E_INVALID_DATA,
+                             "stage-1 arrays do not describe this window (first inconsistent position %lld)",
+                             (long long)hs.first_bad);
+    }
+
+    std::vector<int64_t> cnt(W);
+    for (int r = 0; r < W; ++r) cnt[r] = w->rank_offsets[r + 1] - w->rank_offsets[r];
+    RoundBuffers cur{d_order, d_sorted_len, d_group_index};
+    int flip = 0;
+    int64_t S = 0;
+    int32_t rounds = 0;
+    int32_t stop = ODB_STOP_DRAINED;
+    RoundState hrs{};
+    std::vector<RankState> hranks(W);
+    for (;;) {
+        int nonempty = 0;
+        int64_t max_cnt = 0;
+        for (int r = 0; r < W; ++r) {
+            nonempty += cnt[r] > 0;
+            if (cnt[r] > max_cnt) max_cnt = cnt[r];
+        }
+        if (nonempty == 0) {
+            stop = ODB_STOP_DRAINED;
+            break;
+        }
+        // non-join: a rank that is empty while others are not advertises "finished"
+        if (nonjoin && nonempty < W) {
+            stop = ODB_STOP_RANK_FINISHED;
+            break;
+        }
+        if (rounds > 0) {
+            ODB_TRY(group_sequences(L, d_ws, W, n, budget, d_off, max_cnt, cur.len, wgidx, nullptr, d_ranks, s));
+            cur.gidx = wgidx;
+        }
+        rounds += 1;
+        // real tokens prefix over the live positions
+        ODB_TRY((device_excl_scan<int64_t>(LiveLen{cur.len, d_off, d_ranks, W, rounds > 1 ? 1 : 0},
+                                           LiveLenIncl{LiveLen{cur.len, d_off, d_ranks, W, rounds > 1 ? 1 : 0}, cs},
+                                           n, ws_at<int64_t>(d_ws, L.partials), s)));
+        hipLaunchKernelGGL(target_kernel, dim3(1), dim3(kBlock), 0, s, d_ranks, d_cap, cap ? 1 : 0, W, d_rs);
+        ODB_LAUNCHED();
+        hipLaunchKernelGGL(group_sizes_kernel, dim3(gridn), dim3(kBlock), 0, s, (const int32_t*)gstart,
+                           (const int64_t*)d_gbase, d_off, (const RankState*)d_ranks, W, gsize);
+        ODB_LAUNCHED();
+        hipLaunchKernelGGL(adjust_kernel, dim3(W), dim3(kBlock), 0, s, d_ranks, (const RoundState*)d_rs, d_off,
+                           (const int32_t*)gstart, (const int32_t*)gsize, ov_slot, kept, st);
+        ODB_LAUNCHED();
+        hipLaunchKernelGGL(fill_i64_kernel, dim3(gridn), dim3(kBlock), 0, s, steps, max_cnt, (int64_t)0);
+        ODB_LAUNCHED();
+        hipLaunchKernelGGL(slot_records_kernel, dim3(gridn), dim3(kBlock), 0, s, (const RankState*)d_ranks,
+                           (const RoundState*)d_rs, d_off, W, (const int32_t*)gstart, (const int32_t*)gsize,
+                           (const int32_t*)kept, cur.len, (const int64_t*)cs, srows, smax, stok, steps);
+        ODB_LAUNCHED();
+        hipLaunchKernelGGL(cut_kernel, dim3(1), dim3(kBlock), 0, s, d_rs, (const int64_t*)steps, nonjoin ? 1 : 0,
+                           params->quota);
+        ODB_LAUNCHED();
+        hipLaunchKernelGGL(finalize_kernel, dim3(W), dim3(kBlock), 0, s, d_ranks, (const RoundState*)d_rs, d_off,
+                           (const int32_t*)gstart, (const int32_t*)gsize, (const int32_t*)ov_slot,
+                           (const int32_t*)kept, ov_lo);
+        ODB_LAUNCHED();
+        hipLaunchKernelGGL(emit_kernel, dim3(gridn), dim3(kBlock), 0, s, (const RankState*)d_ranks,
+                           (const RoundState*)d_rs, d_off, W, n, cur.ids, cur.len, cur.gidx, (const int32_t*)gstart,
+                           (const int32_t*)gsize, (const int32_t*)ov_slot, (const int32_t*)ov_lo, dst, bids[flip],
+                           blen[flip]);
+        ODB_LAUNCHED();
+        hipLaunchKernelGGL(advance_kernel, dim3(grid_for(W, kBlock)), dim3(kBlock), 0, s, d_ranks, W);
+        ODB_LAUNCHED();
+        ODB_TRY_HIP(hipMemcpyAsync(&hrs, d_rs, sizeof(hrs), hipMemcpyDeviceToHost, s));
+        ODB_TRY_HIP(hipMemcpyAsync(hranks.data(), d_ranks, sizeof(RankState) * W, hipMemcpyDeviceToHost, s));
+        DevStatus hst;
+        ODB_TRY_HIP(hipMemcpyAsync(&hst, st, sizeof(hst), hipMemcpyDeviceToHost, s));
+        ODB_TRY_HIP(hipStreamSynchronize(s));
+        if (hst.err & kErrInternal)
+            return set_error(ODB_E_INTERNAL, "alignment round %d: group sizes inconsistent", rounds);
+        S += hrs.cut;
+        for (int r = 0; r < W; ++r) cnt[r] = hranks[r].cnt;
+        cur = RoundBuffers{bids[flip], blen[flip], nullptr};
+        flip ^= 1;
+        if (nonjoin && hrs.quota_hit) {
+            stop = ODB_STOP_QUOTA;
+            break;
+        }
+    }
+
+    const int64_t K = (int64_t)W * S;
+    h_info->steps = S;
+    h_info->rounds = rounds;
+    h_info->stop_reason = stop;
+    h_info->splits = hrs.splits;
+    h_info->overflow_groups = hrs.overflow;
+    h_info->max_step_samples = hrs.step_max;
+    h_info->required_slot_capacity = K;
+    if (K > slot_capacity)
+        return set_error(ODB_E_CAPACITY, "plan needs %lld slots, capacity is %lld", (long long)K,
+                         (long long)slot_capacity);
+
+    if (K > 0) {
+        hipLaunchKernelGGL(plan_slots_kernel, dim3(grid_for(K, kBlock, gcap)), dim3(kBlock), 0, s,
+                           (const RankState*)d_ranks, d_off, W, S, (const int32_t*)srows, (const int32_t*)smax,
+                           (const int64_t*)stok, d_slot_rows, d_slot_maxlen, d_slot_tokens);
+        ODB_LAUNCHED();
+    }
+    ODB_TRY((device_excl_scan<int64_t>(RowsLoad{d_slot_rows, K}, Store64{d_slot_row_off}, K + 1,
+                                       ws_at<int64_t>(d_ws, L.partials), s)));
+    ODB_TRY((device_excl_scan<int64_t>(TileLoad{d_slot_rows, d_slot_maxlen, K}, Store64{d_slot_tile_off}, K + 1,
+                                       ws_at<int64_t>(d_ws, L.partials), s)));
+    if (nonjoin && n > 0) {
+        hipLaunchKernelGGL(compact_emit_kernel, dim3(gridn), dim3(kBlock), 0, s, (const int32_t*)dst, d_off,
+                           (const RankState*)d_ranks, W, n, (const int64_t*)d_slot_row_off, S, d_emit_order);
+        ODB_LAUNCHED();
+    }
+    hipLaunchKernelGGL(leftover_off_kernel, dim3(1), dim3(kBlock), 0, s, (const RankState*)d_ranks, W,
+                       d_leftover_off);
+    ODB_LAUNCHED();
+    int64_t nleft = 0;
+    for (int r = 0; r < W; ++r) nleft += cnt[r];
+    if (nleft > 0) {
+        hipLaunchKernelGGL(leftover_kernel, dim3(gridn), dim3(kBlock), 0, s, cur.ids, d_off,
+                           (const RankState*)d_ranks, W, n, (const int64_t*)d_leftover_off, d_leftover);
+        ODB_LAUNCHED();
+    }
+    // stats (Sec. 2.1 / App. I padding fraction) and coverage (App. C)
+    if (K > 0) {
+        hipLaunchKernelGGL(tokens_sum_kernel, dim3(grid_for(K, kBlock, gcap)), dim3(kBlock), 0, s,
+                           (const int64_t*)d_slot_tokens, K, d_info);
+        ODB_LAUNCHED();
+    }
+    hipLaunchKernelGGL(finish_info_kernel, dim3(1), dim3(64), 0, s, (const int64_t*)d_slot_row_off,
+                       (const int64_t*)d_slot_tile_off, K, d_info);
+    ODB_LAUNCHED();
+    const int64_t nemit = hrs.emitted_total;
+    ODB_TRY(run_coverage(w, L, d_ws, d_emit_order, nemit, d_leftover, nleft, s));
+
+    DevInfo hi;
+    DevStatus hs;
+    ODB_TRY_HIP(hipMemcpyAsync(&hi, d_info, sizeof(hi), hipMemcpyDeviceToHost, s));
+    ODB_TRY_HIP(hipMemcpyAsync(&hs, st, sizeof(hs), hipMemcpyDeviceToHost, s));
+    ODB_TRY_HIP(hipStreamSynchronize(s));
+    h_info->emitted_samples = hi.emitted;
+    h_info->leftover_samples = nleft;
+    h_info->real_tokens = hi.real_tokens;
+    h_info->padded_elems = hi.padded_elems;
+    h_info->missing_ids = hi.missing_ids;
+    h_info->duplicate_ids = hi.duplicate_ids;
+    h_info->bad_views = hi.bad_views;
+    h_info->pad_fraction = hi.pad_fraction;
+    if (hs.err & kErrIdentity)
+        return set_error(ODB_E_INVALID_DATA, "identity map holds a value outside [0, num_identities)");
+    if ((hs.err & kErrInternal) || hi.emitted != nemit)
+        return set_error(ODB_E_INTERNAL, "internal inconsistency in the aligned plan");
+    if (hi.bad_views != 0)
+        return set_error(ODB_E_COVERAGE, "%lld sampler views are not emitted (or left over) exactly once",
+                         (long long)hi.bad_views);
+    return ODB_OK;
+}
+
+extern "C" int odb_check_coverage(const odb_window_t* w, const int32_t* d_emitted, int64_t num_emitted,
+                                  const int32_t* d_leftover, int64_t num_leftover, odb_plan_info_t* h_info,
+                                  void* d_ws, size_t ws_bytes, void* stream) {
+    Layout L;
+    ODB_TRY(check_workspace(w, d_ws, ws_bytes, &L));
+    if (!h_info) return set_error(ODB_E_INVALID_ARG, "h_info is NULL");
+    if (num_emitted < 0 || num_leftover < 0) return set_error(ODB_E_INVALID_ARG, "negative counts");
+    if ((num_emitted > 0 && !d_emitted) || (num_leftover > 0 && !d_leftover))
+        return set_error(ODB_E_INVALID_ARG, "id arrays must not be NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    ODB_TRY(upload_small(w, L, d_ws, nullptr, s));
+    hipLaunchKernelGGL(init_align_kernel, dim3(1), dim3(64), 0, s, ws_at<RoundState>(d_ws, L.round),
+                       ws_at<DevInfo>(d_ws, L.info));
+    ODB_LAUNCHED();
+    ODB_TRY(run_coverage(w, L, d_ws, d_emitted, num_emitted, d_leftover, num_leftover, s));
+    DevInfo hi;
+    DevStatus hs;
+    ODB_TRY_HIP(hipMemcpyAsync(&hi, ws_at<DevInfo>(d_ws, L.info), sizeof(hi), hipMemcpyDeviceToHost, s));
+    ODB_TRY_HIP(hipMemcpyAsync(&hs, ws_at<DevStatus>(d_ws, L.status), sizeof(hs), hipMemcpyDeviceToHost, s));
+    ODB_TRY_HIP(hipStreamSynchronize(s));
+    h_info->bad_views = hi.bad_views;
+    h_info->missing_ids = hi.missing_ids;
+    h_info->duplicate_ids = hi.duplicate_ids;
+    if (hs.err & (kErrIdentity | kErrInternal))
+        return set_error(ODB_E_INVALID_DATA, "an id lies outside the window or its identity outside the map");
+    return ODB_OK;
+}

@@ -1,0 +1,471 @@
+// Stage 1 of the ODB window pipeline: length-aware grouping (Sec. 2.2, Eq. 1).
+//
+//   lengths_kernel        l_i = off[i+1] - off[i], validity, window min / max length
+//   radix_hist/scatter    segmented stable LSD radix sort of every rank's samples by
+//                         (length descending, id ascending): keys are max_l - l, the
+//                         segments are the ranks, and stability over the id-ordered input
+//                         gives the id tie-break
+//   links_kernel          next-group-start links from the batch-size rule
+//   jump_kernel           pointer-jumping list ranking that marks every group start
+//   gidx / groups         formation group index of every position and G_r
+//
+// Grouping, restated: visiting a rank's samples longest first with threshold t (1 at
+// the start), a group closes once it holds t samples and t becomes B(l) of its last
+// (shortest) sample.  So group 0 is position 0 alone and a group starting at position
+// p > 0 has B(l[p-1]) members (clipped by the end of the rank): next(0) = 1 and
+// next(p) = p + B(l[p-1]).  The group starts are exactly the positions reachable from 0
+// along next(), which pointer jumping finds in O(log G) rounds instead of a serial walk.
+#include <climits>
+#include <vector>
+
+#include "odb_internal.h"
+
+namespace odb {
+
+namespace {
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Lanes of this wave whose `valid` digit equals this lane's (ballot per digit bit).
+__device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid, int dbits) {
+    uint64_t peers = __ballot(valid);
+    for (int b = 0; b < dbits; ++b) {
+        const bool bit = (d >> b) & 1u;
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+    }
+    return peers;
+}
+
+__global__ void __launch_bounds__(kBlock) lengths_kernel(const int64_t* __restrict__ tok_off, int64_t n,
+                                                         int32_t* __restrict__ len, DevStatus* st) {
+    uint32_t lmin = 0xFFFFFFFFu, lmax = 0;
+    int64_t bad = LLONG_MAX;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
+        const int64_t a = tok_off[p];
+        int64_t l = tok_off[p + 1] - a;
+        if (l < 1 || l > INT_MAX || a < 0) {
+            bad = bad < p ? bad : p;
+            l = 1;
+        }
+        len[p] = (int32_t)l;
+        lmin = (uint32_t)l < lmin ? (uint32_t)l : lmin;
+        lmax = (uint32_t)l > lmax ? (uint32_t)l : lmax;
+    }
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) {
+        uint32_t a = __shfl_xor(lmin, d, kWave), b = __shfl_xor(lmax, d, kWave);
+        lmin = a < lmin ? a : lmin;
+        lmax = b > lmax ? b : lmax;
+    }
+    if ((threadIdx.x & (kWave - 1)) == 0 && lmax > 0) {
+        atomicMin(&st->min_len, lmin);
+        atomicMax(&st->max_len, lmax);
+    }
+    if (bad != LLONG_MAX) {
+        atomicOr(&st->err, kErrLength);
+        atomicMin((unsigned long long*)&st->first_bad, (unsigned long long)bad);
+    }
+}
+
+__global__ void rank_counts_kernel(const int64_t* __restrict__ off, int W, RankState* ranks) {
+    for (int r = blockIdx.x * blockDim.x + threadIdx.x; r < W; r += gridDim.x * blockDim.x) {
+        RankState z = {};
+        z.cnt = off[r + 1] - off[r];
+        ranks[r] = z;
+    }
+}
+
+// First radix tile of every rank: tile_first[r] = sum_{r' < r} ceil(n_r' / kSortTile).
+// Tiles never straddle ranks.  One block.
+__global__ void __launch_bounds__(kBlock) sort_tiles_kernel(const int64_t* __restrict__ off, int W,
+                                                            int64_t* __restrict__ tile_first) {
+    __shared__ int64_t carry;
+    if (threadIdx.x == 0) carry = 0;
+    __syncthreads();
+    for (int b = 0; b < W; b += kBlock) {
+        const int r = b + threadIdx.x;
+        const int64_t v = r < W ? (off[r + 1] - off[r] + kSortTile - 1) / kSortTile : 0;
+        int64_t tot;
+        const int64_t ex = block_excl_sum(v, &tot);
+        const int64_t c = carry;
+        if (r < W) tile_first[r] = c + ex;
+        __syncthreads();
+        if (threadIdx.x == 0) carry = c + tot;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) tile_first[W] = carry;
+}
+
+struct SortTile {
+    int64_t start;       // first position
+    int32_t count;       // keys in this tile (<= kSortTile)
+    int32_t seg_tiles;   // tiles of this tile's rank
+    int64_t first;       // global index of the rank's first tile
+    int32_t j;           // index of this tile within its rank
+};
+
+__device__ __forceinline__ SortTile sort_tile(const int64_t* __restrict__ off,
+                                              const int64_t* __restrict__ tile_first, int W, int64_t b) {
+    const int r = rank_of(tile_first, W, b);
+    SortTile t;
+    t.first = tile_first[r];
+    t.j = (int32_t)(b - t.first);
+    t.seg_tiles = (int32_t)(tile_first[r + 1] - t.first);
+    t.start = off[r] + (int64_t)t.j * kSortTile;
+    const int64_t left = off[r + 1] - t.start;
+    t.count = (int32_t)(left < kSortTile ? left : kSortTile);
+    return t;
+}
+
+template <bool kFirst>
+__global__ void __launch_bounds__(kBlock) radix_hist_kernel(const int64_t* __restrict__ off,
+                                                            const int64_t* __restrict__ tile_first, int W,
+                                                            const uint32_t* __restrict__ keys_in,
+                                                            const int32_t* __restrict__ len_in, uint32_t maxl,
+                                                            int shift, int dbits, uint32_t* __restrict__ counts) {
+    const SortTile b = sort_tile(off, tile_first, W, blockIdx.x);
+    const int radix = 1 << dbits;
+    const uint32_t mask = (uint32_t)radix - 1;
+    __shared__ uint32_t h[256];
+    for (int d = threadIdx.x; d < radix; d += kBlock) h[d] = 0;
+    __syncthreads();
+    for (int it = 0; it < kSortItems; ++it) {
+        const int li = it * kBlock + threadIdx.x;
+        const bool valid = li < b.count;
+        const int64_t p = b.start + li;
+        uint32_t key = 0;
+        if (valid) key = kFirst ? maxl - (uint32_t)len_in[p] : keys_in[p];
+        const uint32_t d = (key >> shift) & mask;
+        const uint64_t peers = match_digit(d, valid, dbits);
+        if (valid && lanes_below(peers) == 0) atomicAdd(&h[d], (uint32_t)__popcll(peers));
+    }
+    __syncthreads();
+    const int64_t col = (int64_t)b.first << dbits;
+    for (int d = threadIdx.x; d < radix; d += kBlock)
+        counts[col + (int64_t)d * b.seg_tiles + b.j] = h[d];
+}
+
+// Scatter one tile.  Items are taken in position order (round `it` covers positions
+// it*256 .. it*256+255 of the tile, wave w its w-th quarter), so the rank of an item among
+// equal digits is: earlier rounds (s_run) + earlier waves this round (s_w) + lower lanes
+// with the same digit (ballot match).  That keeps the sort stable.
+template <bool kFirst, bool kLast>
+__global__ void __launch_bounds__(kBlock) radix_scatter_kernel(
+    const int64_t* __restrict__ off, const int64_t* __restrict__ tile_first, int W,
+    const uint32_t* __restrict__ keys_in,
+    const int32_t* __restrict__ len_in, const int32_t* __restrict__ vals_in, uint32_t maxl, int shift,
+    int dbits, const uint32_t* __restrict__ offs, uint32_t* __restrict__ keys_out,
+    int32_t* __restrict__ vals_out, int32_t* __restrict__ slen_out) {
+    const SortTile b = sort_tile(off, tile_first, W, blockIdx.x);
+    const int radix = 1 << dbits;
+    const uint32_t mask = (uint32_t)radix - 1;
+    constexpr int kWaves = kBlock / kWave;
+    __shared__ uint32_t s_base[256];
+    __shared__ uint32_t s_run[256];
+    __shared__ uint32_t s_w[kWaves][256];
+    const int64_t col = (int64_t)b.first << dbits;
+    for (int d = threadIdx.x; d < radix; d += kBlock) {
+        s_base[d] = offs[col + (int64_t)d * b.seg_tiles + b.j];
+        s_run[d] = 0;
+#pragma unroll
+        for (int k = 0; k < kWaves; ++k) s_w[k][d] = 0;
+    }
+    __syncthreads();
+    const int w = threadIdx.x / kWave;
+    for (int it = 0; it < kSortItems; ++it) {
+        const int li = it * kBlock + threadIdx.x;
+        const bool valid = li < b.count;
+        const int64_t p = b.start + li;
+        uint32_t key = 0;
+        int32_t val = 0;
+        if (valid) {
+            key = kFirst ? maxl - (uint32_t)len_in[p] : keys_in[p];
+            val = kFirst ? (int32_t)p : vals_in[p];
+        }
+        const uint32_t d = (key >> shift) & mask;
+        const uint64_t peers = match_digit(d, valid, dbits);
+        const uint32_t below = lanes_below(peers);
+        if (valid && below == 0) s_w[w][d] = (uint32_t)__popcll(peers);
+        __syncthreads();
+        if (valid) {
+            uint32_t pre = s_run[d];
+            for (int k = 0; k < w; ++k) pre += s_w[k][d];
+            const uint32_t pos = s_base[d] + pre + below;
+            vals_out[pos] = val;
+            if (kLast)
+                slen_out[pos] = (int32_t)(maxl - key);
+            else
+                keys_out[pos] = key;
+        }
+        __syncthreads();
+        for (int dd = threadIdx.x; dd < radix; dd += kBlock) {
+            uint32_t t = 0;
+#pragma unroll
+            for (int k = 0; k < kWaves; ++k) {
+                t += s_w[k][dd];
+                s_w[k][dd] = 0;
+            }
+            s_run[dd] += t;
+        }
+        __syncthreads();
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) identity_order_kernel(int64_t n, const int32_t* __restrict__ len,
+                                                                int32_t* __restrict__ order,
+                                                                int32_t* __restrict__ slen) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
+        order[p] = (int32_t)p;
+        slen[p] = len[p];
+    }
+}
+
+// next-group-start links over the current sequences; positions outside every rank's
+// live range [off[r], off[r] + cnt_r) and links leaving a rank point to the sentinel n.
+__global__ void __launch_bounds__(kBlock) links_kernel(const int32_t* __restrict__ slen,
+                                                       const int64_t* __restrict__ off,
+                                                       const RankState* __restrict__ ranks, int W, int64_t n,
+                                                       int64_t budget, int32_t* __restrict__ jmp,
+                                                       uint8_t* __restrict__ marks) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p <= n; p += stride) {
+        if (p == n) {
+            jmp[n] = (int32_t)n;
+            marks[n] = 0;
+            continue;
+        }
+        const int r = rank_of(off, W, p);
+        const int64_t base = off[r];
+        const int64_t c = ranks[r].cnt;
+        const int64_t q = p - base;
+        if (q >= c) {
+            jmp[p] = (int32_t)n;
+            marks[p] = 0;
+            continue;
+        }
+        const int64_t step = q == 0 ? 1 : batch_size(budget, slen[p - 1]);
+        const int64_t t = p + step;
+        jmp[p] = (int32_t)(t < base + c ? t : n);
+        marks[p] = q == 0 ? 1 : 0;
+    }
+}
+
+// One doubling round: m <- m U J(m), J <- J o J.  Marks are updated in place (a mark seen
+// early only propagates sooner; every marked position is still a chain element), the
+// jump table is double-buffered.  A round starts only if the previous one marked
+// something new; otherwise the marks are already closed under J and it returns at once.
+__global__ void __launch_bounds__(kBlock) jump_kernel(const int32_t* __restrict__ jin,
+                                                      int32_t* __restrict__ jout, uint8_t* marks, int64_t n,
+                                                      DevStatus* st, int round) {
+    if (round > 0 && st->jump_changed[round - 1] == 0) return;
+    bool changed = false;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p <= n; p += stride) {
+        const int32_t j = jin[p];
+        if (p < n && j < n && marks[p] && !marks[j]) {
+            marks[j] = 1;
+            changed = true;
+        }
+        jout[p] = j < n ? jin[j] : (int32_t)n;
+    }
+    if (__ballot(changed) && (threadIdx.x & (kWave - 1)) == 0) st->jump_changed[round] = 1;
+}
+
+__global__ void init_jump_flags(DevStatus* st) {
+    if (threadIdx.x < kMaxJumpRounds) st->jump_changed[threadIdx.x] = 0;
+}
+
+struct CountLoad {
+    const uint32_t* c;
+    __device__ uint32_t operator()(int64_t i) const { return c[i]; }
+};
+struct CountStore {
+    uint32_t* c;
+    __device__ void operator()(int64_t i, uint32_t v) const { c[i] = v; }
+};
+
+struct MarkLoad {
+    const uint8_t* m;
+    __device__ uint32_t operator()(int64_t i) const { return m[i]; }
+};
+struct InclStore {
+    const uint8_t* m;
+    int32_t* out;
+    __device__ void operator()(int64_t i, uint32_t ex) const { out[i] = (int32_t)(ex + m[i]); }
+};
+
+__global__ void __launch_bounds__(kBlock) gidx_kernel(const uint8_t* __restrict__ marks,
+                                                      const int32_t* __restrict__ incl,
+                                                      const int64_t* __restrict__ off,
+                                                      const RankState* __restrict__ ranks, int W, int64_t n,
+                                                      int32_t* __restrict__ gidx, int32_t* __restrict__ gstart) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
+        const int r = rank_of(off, W, p);
+        const int64_t base = off[r];
+        if (p - base >= ranks[r].cnt) continue;
+        const int32_t before = base > 0 ? incl[base - 1] : 0;
+        gidx[p] = incl[p] - before - 1;
+        if (marks[p]) gstart[incl[p] - 1] = (int32_t)p;
+    }
+}
+
+__global__ void groups_kernel(const int32_t* __restrict__ incl, const int64_t* __restrict__ off, int W,
+                              RankState* ranks, int64_t* __restrict__ gbase, int32_t* __restrict__ groups_out) {
+    for (int r = blockIdx.x * blockDim.x + threadIdx.x; r < W; r += gridDim.x * blockDim.x) {
+        const int64_t base = off[r];
+        const int64_t c = ranks[r].cnt;
+        const int32_t before = base > 0 ? incl[base - 1] : 0;
+        const int64_t G = c > 0 ? incl[base + c - 1] - before : 0;
+        ranks[r].G = G;
+        ranks[r].gbase = before;
+        gbase[r] = before;
+        if (r == W - 1) gbase[W] = before + G;
+        if (groups_out) groups_out[r] = (int32_t)G;
+    }
+}
+
+}  // namespace
+
+int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget, const int64_t* d_off,
+                    int64_t max_cnt, const int32_t* d_slen, int32_t* d_gidx,
+                    int32_t* d_groups_out, RankState* d_ranks, hipStream_t s) {
+    int32_t* j0 = ws_at<int32_t>(ws, L.jmp0);
+    int32_t* j1 = ws_at<int32_t>(ws, L.jmp1);
+    uint8_t* marks = ws_at<uint8_t>(ws, L.marks);
+    int32_t* incl = ws_at<int32_t>(ws, L.incl);
+    int32_t* gstart = ws_at<int32_t>(ws, L.gstart);
+    DevStatus* st = ws_at<DevStatus>(ws, L.status);
+    const unsigned grid = grid_for(n + 1, kBlock, (int64_t)num_cus() * 16);
+    hipLaunchKernelGGL(links_kernel, dim3(grid), dim3(kBlock), 0, s, d_slen, d_off,
+                       (const RankState*)d_ranks, W, n, budget, j0, marks);
+    ODB_LAUNCHED();
+    // chains have at most max_cnt elements: ceil(log2(max_cnt + 1)) + 1 doubling rounds
+    // always suffice; rounds after convergence return immediately
+    int rounds = 1;
+    while ((int64_t(1) << (rounds - 1)) <= max_cnt && rounds < kMaxJumpRounds) ++rounds;
+    hipLaunchKernelGGL(init_jump_flags, dim3(1), dim3(64), 0, s, st);
+    ODB_LAUNCHED();
+    for (int k = 0; k < rounds; ++k) {
+        const int32_t* jin = (k & 1) ? j1 : j0;
+        int32_t* jout = (k & 1) ? j0 : j1;
+        hipLaunchKernelGGL(jump_kernel, dim3(grid), dim3(kBlock), 0, s, jin, jout, marks, n, st, k);
+        ODB_LAUNCHED();
+    }
+    ODB_TRY((device_excl_scan<uint32_t>(MarkLoad{marks}, InclStore{marks, incl}, n,
+                                        ws_at<uint32_t>(ws, L.partials), s)));
+    hipLaunchKernelGGL(gidx_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock), 0, s,
+                       (const uint8_t*)marks, (const int32_t*)incl, d_off, (const RankState*)d_ranks, W, n,
+                       d_gidx, gstart);
+    ODB_LAUNCHED();
+    hipLaunchKernelGGL(groups_kernel, dim3(grid_for(W, kBlock)), dim3(kBlock), 0, s, (const int32_t*)incl, d_off,
+                       W, d_ranks, ws_at<int64_t>(ws, L.gbase), d_groups_out);
+    ODB_LAUNCHED();
+    return ODB_OK;
+}
+
+}  // namespace odb
+
+using namespace odb;
+
+extern "C" int odb_form_groups(const odb_window_t* w, int64_t budget, int32_t* d_order, int32_t* d_sorted_len,
+                               int32_t* d_group_index, int32_t* d_groups_per_rank, void* d_ws, size_t ws_bytes,
+                               void* stream) {
+    Layout L;
+    ODB_TRY(check_workspace(w, d_ws, ws_bytes, &L));
+    if (budget < 1) return set_error(ODB_E_INVALID_ARG, "budget must be >= 1");
+    const int W = w->num_ranks;
+    const int64_t n = w->num_samples;
+    if (n > 0 && (!d_order || !d_sorted_len || !d_group_index))
+        return set_error(ODB_E_INVALID_ARG, "stage-1 output pointers must not be NULL");
+    if (!d_groups_per_rank) return set_error(ODB_E_INVALID_ARG, "d_groups_per_rank is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    ODB_TRY(upload_small(w, L, d_ws, nullptr, s));
+    const int64_t* d_off = ws_at<int64_t>(d_ws, L.rank_off);
+    RankState* d_ranks = ws_at<RankState>(d_ws, L.ranks);
+    DevStatus* st = ws_at<DevStatus>(d_ws, L.status);
+    int32_t* len = ws_at<int32_t>(d_ws, L.len);
+    hipLaunchKernelGGL(rank_counts_kernel, dim3(grid_for(W, kBlock)), dim3(kBlock), 0, s, d_off, W, d_ranks);
+    ODB_LAUNCHED();
+
+    // (a1) lengths and their validity; the one synchronisation of this call
+    hipLaunchKernelGGL(lengths_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock), 0, s,
+                       w->d_token_offsets, n, len, st);
+    ODB_LAUNCHED();
+    DevStatus hs;
+    ODB_TRY_HIP(hipMemcpyAsync(&hs, st, sizeof(DevStatus), hipMemcpyDeviceToHost, s));
+    ODB_TRY_HIP(hipStreamSynchronize(s));
+    if (hs.err & kErrLength)
+        return set_error(ODB_E_INVALID_DATA,
+                         "sample %lld has a length outside [1, 2^31) or a negative token offset",
+                         (long long)hs.first_bad);
+    if (n == 0) {
+        hipLaunchKernelGGL(groups_kernel, dim3(grid_for(W, kBlock)), dim3(kBlock), 0, s,
+                           (const int32_t*)len, d_off, W, d_ranks, ws_at<int64_t>(d_ws, L.gbase), d_groups_per_rank);
+        ODB_LAUNCHED();
+        return ODB_OK;
+    }
+
+    // (a2) segmented stable radix sort on key = max_l - l
+    const uint32_t maxl = hs.max_len, minl = hs.min_len;
+    int bits = 0;
+    while (bits < 32 && ((maxl - minl) >> bits) != 0) ++bits;
+    const int passes = (bits + 7) / 8;
+    if (passes == 0) {
+        hipLaunchKernelGGL(identity_order_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock),
+                           0, s, n, (const int32_t*)len, d_order, d_sorted_len);
+        ODB_LAUNCHED();
+    } else {
+        const int dbits = (bits + passes - 1) / passes;
+        const int64_t NB = L.num_sort_blocks;
+        int64_t* d_tile_first = ws_at<int64_t>(d_ws, L.tile_first);
+        hipLaunchKernelGGL(sort_tiles_kernel, dim3(1), dim3(kBlock), 0, s, d_off, W, d_tile_first);
+        ODB_LAUNCHED();
+        uint32_t* counts = ws_at<uint32_t>(d_ws, L.counts);
+        uint32_t* keys[2] = {ws_at<uint32_t>(d_ws, L.keys0), ws_at<uint32_t>(d_ws, L.keys1)};
+        int32_t* vals[2] = {ws_at<int32_t>(d_ws, L.vals0), ws_at<int32_t>(d_ws, L.vals1)};
+        for (int pass = 0; pass < passes; ++pass) {
+            const int shift = pass * dbits;
+            const bool first = pass == 0, last = pass == passes - 1;
+            const uint32_t* kin = first ? nullptr : keys[(pass - 1) & 1];
+            const int32_t* vin = first ? nullptr : vals[(pass - 1) & 1];
+            uint32_t* kout = last ? nullptr : keys[pass & 1];
+            int32_t* vout = last ? d_order : vals[pass & 1];
+            if (first)
+                hipLaunchKernelGGL(radix_hist_kernel<true>, dim3((unsigned)NB), dim3(kBlock), 0, s, d_off,
+                                   (const int64_t*)d_tile_first, W, kin, (const int32_t*)len, maxl, shift, dbits,
+                                   counts);
+            else
+                hipLaunchKernelGGL(radix_hist_kernel<false>, dim3((unsigned)NB), dim3(kBlock), 0, s, d_off,
+                                   (const int64_t*)d_tile_first, W, kin, (const int32_t*)len, maxl, shift, dbits,
+                                   counts);
+            ODB_LAUNCHED();
+            ODB_TRY((device_excl_scan<uint32_t>(CountLoad{counts}, CountStore{counts}, NB << dbits,
+                                                ws_at<uint32_t>(d_ws, L.partials), s)));
+#define ODB_SCATTER(F, La)                                                                                  \
+    hipLaunchKernelGGL((radix_scatter_kernel<F, La>), dim3((unsigned)NB), dim3(kBlock), 0, s,               \
+                       d_off, (const int64_t*)d_tile_first, W, kin, (const int32_t*)len, vin, maxl, shift,  \
+                       dbits, (const uint32_t*)counts, kout, vout, d_sorted_len)
+            if (first && last) ODB_SCATTER(true, true);
+            else if (first) ODB_SCATTER(true, false);
+            else if (last) ODB_SCATTER(false, true);
+            else ODB_SCATTER(false, false);
+#undef ODB_SCATTER
+            ODB_LAUNCHED();
+        }
+    }
+
+    // (a3, a4) links, pointer jumping, group indices, G_r
+    int64_t max_cnt = 0;
+    for (int r = 0; r < W; ++r) {
+        const int64_t c = w->rank_offsets[r + 1] - w->rank_offsets[r];
+        if (c > max_cnt) max_cnt = c;
+    }
+    return group_sequences(L, d_ws, W, n, budget, d_off, max_cnt, d_sorted_len, d_group_index,
+                           d_groups_per_rank, d_ranks, s);
+}

@@ -1,0 +1,304 @@
+// Internal declarations of the ODB HIP library (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "odb.h"
+
+namespace odb {
+
+constexpr int kWave = 64;
+constexpr int kBlock = 256;                 // threads per block for most kernels
+constexpr int kSortItems = 8;               // keys per thread in a radix tile
+constexpr int kSortTile = kBlock * kSortItems;
+constexpr int kScanItems = 16;
+constexpr int kScanTile = kBlock * kScanItems;
+constexpr int kMaxJumpRounds = 40;
+
+// ------------------------------------------------------------------ host error state
+int set_error(int code, const char* fmt, ...);
+const char* last_error();
+
+#define ODB_TRY_HIP(expr)                                                                   \
+    do {                                                                                    \
+        hipError_t e_ = (expr);                                                             \
+        if (e_ != hipSuccess)                                                               \
+            return ::odb::set_error(ODB_E_HIP, "%s failed: %s (%s:%d)", #expr,               \
+                                    hipGetErrorString(e_), __FILE__, __LINE__);             \
+    } while (0)
+
+#define ODB_TRY(expr)                                                                       \
+    do {                                                                                    \
+        int s_ = (expr);                                                                    \
+        if (s_ != ODB_OK) return s_;                                                        \
+    } while (0)
+
+// Launch check: a bad launch configuration shows up as a pending error.
+#define ODB_LAUNCHED() ODB_TRY_HIP(hipGetLastError())
+
+// ------------------------------------------------------------------ device status
+enum : int32_t {
+    kErrLength = 1,      // some l < 1 or l >= 2^31
+    kErrOffsets = 2,     // token offsets out of range
+    kErrOrder = 4,       // stage-1 order not a valid formation order of the window
+    kErrGroupIndex = 8,  // stage-1 group indices inconsistent
+    kErrIdentity = 16,   // identity outside [0, num_identities)
+    kErrCollate = 32,    // collate met an inconsistent plan
+    kErrInternal = 64
+};
+
+struct DevStatus {
+    int32_t err;
+    int32_t collate_err;
+    int64_t first_bad;            // smallest offending sample index (atomicMin)
+    uint32_t min_len;
+    uint32_t max_len;
+    int32_t jump_changed[kMaxJumpRounds];
+};
+
+// Per-rank alignment state, kept on the device across rounds.
+enum : int32_t { kActInactive = 0, kActKeep = 1, kActSplit = 2, kActOverflow = 3 };
+
+struct RankState {
+    int64_t emitted;   // samples emitted so far (all rounds)
+    int64_t slots;     // real (non-IDLE) slots so far
+    int64_t cnt;       // S_r: samples buffered at the start of this round
+    int64_t next_cnt;  // samples back in the buffer after this round
+    int64_t G;         // groups formed this round
+    int64_t gbase;     // global id of this rank's first group this round
+    int64_t X;         // split: positions [0, X) become singletons
+    int64_t jstar;     // split: formation group that keeps [X, end)
+    int64_t qcut;      // keep/split: first formation position that is emitted
+    int64_t ebase;     // samples emitted before this round
+    int32_t action;
+    int32_t pad;
+};
+
+struct RoundState {
+    int64_t T;               // alignment target of the current round
+    int64_t cut;             // steps of this round that are emitted
+    int64_t emitted_total;   // cumulative emitted samples before this round
+    int64_t step_max;        // largest global step count so far
+    int64_t splits;          // all rounds
+    int64_t overflow;        // all rounds
+    int64_t quota_hit;       // 1 once the non-join quota was reached
+    int64_t active;          // active ranks this round
+    int64_t total_groups;    // groups over all ranks this round
+    int64_t leftover_total;  // samples back in buffers after this round
+};
+
+// Final summary assembled on the device (mirrors odb_plan_info_t's counters).
+struct DevInfo {
+    int64_t real_tokens;
+    int64_t padded_elems;
+    int64_t emitted;
+    int64_t bad_views;
+    int64_t missing_ids;
+    int64_t duplicate_ids;
+    double pad_fraction;
+};
+
+
+// ------------------------------------------------------------------ workspace layout
+struct Layout {
+    size_t status, round, ranks, rank_off, cap, gbase, tile_first;
+    size_t len, keys0, keys1, vals0, vals1, counts, partials;
+    size_t jmp0, jmp1, marks, incl;
+    size_t gstart, gsize, gmax, gtok, cs, ov_slot, ov_lo, kept;
+    size_t srows, smax, stok, steps;
+    size_t buf_ids0, buf_ids1, buf_len0, buf_len1, gidx, stage, cover;
+    size_t info;
+    size_t total;
+    int64_t num_sort_blocks;
+    int64_t partials_len;
+};
+
+bool make_layout(const odb_window_t* w, Layout* L);
+
+template <class T>
+inline T* ws_at(void* ws, size_t off) {
+    return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+// Validates the window fields that can be checked on the host.
+int check_window(const odb_window_t* w);
+int check_workspace(const odb_window_t* w, void* d_ws, size_t ws_bytes, Layout* L);
+
+// Uploads rank offsets (and optionally capacities) and clears the status word.
+int upload_small(const odb_window_t* w, const Layout& L, void* d_ws, const int64_t* cap,
+                 hipStream_t s);
+
+int num_cus();
+
+inline unsigned grid_for(int64_t n, int per_block, int64_t cap = 1 << 20) {
+    int64_t g = (n + per_block - 1) / per_block;
+    if (g < 1) g = 1;
+    if (g > cap) g = cap;
+    return (unsigned)g;
+}
+
+// ------------------------------------------------------------------ device helpers
+// Eq. 1: B(l) = max(floor(L_max / l), 1), integer division.
+__device__ __forceinline__ int64_t batch_size(int64_t budget, int32_t l) {
+    int64_t b;
+    if (budget <= 0xFFFFFFFFll)
+        b = (int64_t)((uint32_t)budget / (uint32_t)l);
+    else
+        b = budget / (int64_t)l;
+    return b > 1 ? b : 1;
+}
+
+// Number of ranks r with off[r] <= p, minus one: the rank owning position p
+// (off is non-decreasing, p < off[W]).
+__device__ __forceinline__ int rank_of(const int64_t* off, int W, int64_t p) {
+    int lo = 0, hi = W;  // invariant: off[lo] <= p < off[hi]
+    while (hi - lo > 1) {
+        int mid = (lo + hi) >> 1;
+        if (off[mid] <= p) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_incl_sum(T v) {
+    const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        T o = __shfl_up(v, d, kWave);
+        if (lane >= d) v += o;
+    }
+    return v;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, kWave);
+    return v;
+}
+
+// Exclusive block scan for blockDim.x == kBlock; *total receives the block sum.
+template <typename T>
+__device__ __forceinline__ T block_excl_sum(T v, T* total) {
+    __shared__ T wtot[kBlock / kWave];
+    T inc = wave_incl_sum(v);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == kWave - 1) wtot[w] = inc;
+    __syncthreads();
+    T pre = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kBlock / kWave; ++i) {
+        T x = wtot[i];
+        pre += (i < w) ? x : T(0);
+        tot += x;
+    }
+    __syncthreads();
+    *total = tot;
+    return pre + inc - v;
+}
+
+template <typename T>
+__device__ __forceinline__ T block_sum(T v) {
+    __shared__ T wtot[kBlock / kWave];
+    v = wave_sum(v);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) wtot[w] = v;
+    __syncthreads();
+    T tot = 0;
+#pragma unroll
+    for (int i = 0; i < kBlock / kWave; ++i) tot += wtot[i];
+    __syncthreads();
+    return tot;
+}
+
+// ------------------------------------------------------------------ generic device scan
+// Exclusive prefix sum out[i] = sum_{k<i} in(k) over i in [0, n), in three launches
+// (tile sums, a one-block scan of the tile sums, tile-local scans).  `Load` is a
+// functor int64 -> Out, `Store` a functor (int64 i, Out value) -> void.  partials
+// needs ceil(n / kScanTile) + 1 entries.  The total is written to partials[tiles].
+template <typename Out, typename Load>
+__global__ void __launch_bounds__(kBlock) scan_tile_sums(Load load, int64_t n, Out* partials) {
+    const int64_t base = (int64_t)blockIdx.x * kScanTile;
+    Out s = 0;
+#pragma unroll 4
+    for (int i = 0; i < kScanItems; ++i) {
+        int64_t idx = base + (int64_t)i * kBlock + threadIdx.x;
+        if (idx < n) s += load(idx);
+    }
+    s = block_sum(s);
+    if (threadIdx.x == 0) partials[blockIdx.x] = s;
+}
+
+template <typename Out>
+__global__ void __launch_bounds__(1024) scan_partials(Out* partials, int64_t m) {
+    __shared__ Out wtot[1024 / kWave];
+    __shared__ Out carry_s;
+    if (threadIdx.x == 0) carry_s = 0;
+    __syncthreads();
+    for (int64_t base = 0; base < m; base += 1024) {
+        int64_t i = base + threadIdx.x;
+        Out v = i < m ? partials[i] : Out(0);
+        Out inc = wave_incl_sum(v);
+        const int w = threadIdx.x / kWave;
+        if ((threadIdx.x & (kWave - 1)) == kWave - 1) wtot[w] = inc;
+        __syncthreads();
+        Out pre = 0, tot = 0;
+        for (int k = 0; k < 1024 / kWave; ++k) {
+            pre += (k < w) ? wtot[k] : Out(0);
+            tot += wtot[k];
+        }
+        Out c = carry_s;
+        if (i < m) partials[i] = c + pre + inc - v;
+        __syncthreads();
+        if (threadIdx.x == 0) carry_s = c + tot;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) partials[m] = carry_s;
+}
+
+template <typename Out, typename Load, typename Store>
+__global__ void __launch_bounds__(kBlock) scan_tiles(Load load, Store store, int64_t n,
+                                                      const Out* partials) {
+    const int64_t base = (int64_t)blockIdx.x * kScanTile;
+    Out carry = partials[blockIdx.x];
+    for (int i = 0; i < kScanItems; ++i) {
+        int64_t idx = base + (int64_t)i * kBlock + threadIdx.x;
+        Out v = idx < n ? load(idx) : Out(0);
+        Out tot;
+        Out ex = block_excl_sum(v, &tot);
+        if (idx < n) store(idx, carry + ex);
+        carry += tot;
+    }
+}
+
+template <typename Out, typename Load, typename Store>
+int device_excl_scan(Load load, Store store, int64_t n, Out* partials, hipStream_t s) {
+    if (n <= 0) return ODB_OK;
+    int64_t tiles = (n + kScanTile - 1) / kScanTile;
+    hipLaunchKernelGGL((scan_tile_sums<Out, Load>), dim3((unsigned)tiles), dim3(kBlock), 0, s,
+                       load, n, partials);
+    ODB_LAUNCHED();
+    hipLaunchKernelGGL((scan_partials<Out>), dim3(1), dim3(1024), 0, s, partials, tiles);
+    ODB_LAUNCHED();
+    hipLaunchKernelGGL((scan_tiles<Out, Load, Store>), dim3((unsigned)tiles), dim3(kBlock), 0, s,
+                       load, store, n, (const Out*)partials);
+    ODB_LAUNCHED();
+    return ODB_OK;
+}
+
+// ------------------------------------------------------------------ cross-file launchers
+// Grouping of the per-rank sequences held in `slen` (positions [off[r], off[r] + cnt_r)
+// of every rank r, cnt_r = d_ranks[r].cnt): marks the group starts with pointer jumping
+// over the next-group-start links, then writes the formation group index of every
+// position (d_gidx), the global position of every group start (workspace gstart, group
+// ids numbered rank by rank), G_r and the first group id of every rank (d_ranks[r].G,
+// .gbase and workspace gbase[W+1]), and optionally G_r to d_groups_out.
+int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget,
+                    const int64_t* d_rank_off, int64_t max_cnt,
+                    const int32_t* d_slen, int32_t* d_gidx, int32_t* d_groups_out,
+                    RankState* d_ranks, hipStream_t s);
+
+}  // namespace odb

@@ -75,6 +75,21 @@ def fill_tokens_torch(total: int, device, chunk: int = 1 << 27):
     return out
 
 
+def device_tensors(w: "Window", device="cuda", tokens=None):
+    """Device copies of a window's CSR offsets, token stream and identity map.
+
+    Tokens are generated directly on the device unless given.  Returns
+    (token_offsets int64, tokens int32, identity int64 or None).
+    """
+    import torch
+
+    tok_off = torch.from_numpy(w.tok_off).to(device)
+    if tokens is None:
+        tokens = fill_tokens_torch(max(w.total_tokens, 1), device)
+    ident = None if w.identity is None else torch.from_numpy(w.identity).to(device)
+    return tok_off, tokens, ident
+
+
 def tokens_numpy(start: int, stop: int) -> np.ndarray:
     idx = np.arange(start, stop, dtype=np.int64)
     return token_ids(idx).astype(np.int32)

@@ -1,0 +1,110 @@
+"""Shared helpers for the GPU parity tests: run the HIP pipeline through the C ABI and
+compare it with the CPU oracle on the same seeded window."""
+import sys
+
+import numpy as np
+
+import oracle
+import synth
+
+INFO_EXACT = ["steps", "rounds", "stop_reason", "emitted_samples", "leftover_samples", "real_tokens",
+              "padded_elems", "max_step_samples", "splits", "overflow_groups", "missing_ids", "duplicate_ids",
+              "bad_views"]
+PAD_FRACTION_RTOL = 1e-12
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_gpu(w, pad_id=0, tokens=None, collate=True):
+    import torch
+    import paper_2606_19989_amd as odb
+
+    tok_off, toks, ident = synth.device_tensors(w, "cuda", tokens)
+    win = odb.DeviceWindow(w.rank_off, tok_off, toks, ident, w.num_identities)
+    pipe = odb.Pipeline(win, w.budget, mode=w.mode, quota=w.quota, capacity=w.capacity, pad_id=pad_id)
+    pipe.form()
+    pipe.align()
+    outs = pipe.collate() if collate else None
+    torch.cuda.synchronize()
+    if collate:
+        odb.odb_collate_status(pipe.ws)
+    return pipe, outs
+
+
+def h(t, k=None):
+    x = t if k is None else t[:k]
+    return x.cpu().numpy()
+
+
+def compare_plan(w, pipe, ref):
+    n, W = w.n, w.W
+    info = pipe.info
+    for f in INFO_EXACT:
+        assert info[f] == ref.info[f], (f, info[f], ref.info[f])
+    pf, rf = info["pad_fraction"], ref.info["pad_fraction"]
+    assert abs(pf - rf) <= PAD_FRACTION_RTOL * max(abs(rf), 1e-300) or pf == rf, (pf, rf)
+    if n:
+        assert np.array_equal(h(pipe.order, n), ref.order), "order"
+        assert np.array_equal(h(pipe.sorted_len, n), ref.sorted_len), "sorted_len"
+        assert np.array_equal(h(pipe.group_index, n), ref.group_index), "group_index"
+    assert np.array_equal(h(pipe.groups_per_rank), ref.groups_per_rank), "groups_per_rank"
+    K = W * ref.steps
+    assert np.array_equal(h(pipe.slot_rows, K), ref.slot_rows), "slot_rows"
+    assert np.array_equal(h(pipe.slot_maxlen, K), ref.slot_maxlen), "slot_maxlen"
+    assert np.array_equal(h(pipe.slot_tokens, K), ref.slot_tokens), "slot_tokens"
+    assert np.array_equal(h(pipe.slot_row_off, K + 1), ref.slot_row_off), "slot_row_off"
+    assert np.array_equal(h(pipe.slot_tile_off, K + 1), ref.slot_tile_off), "slot_tile_off"
+    E, Lf = ref.info["emitted_samples"], ref.info["leftover_samples"]
+    assert np.array_equal(h(pipe.emit_order, E), ref.emit_order), "emit_order"
+    assert np.array_equal(h(pipe.leftover, Lf), ref.leftover), "leftover"
+    assert np.array_equal(h(pipe.leftover_off), ref.leftover_off), "leftover_off"
+
+
+def compare_collate_full(w, outs, ref, pad_id=0):
+    want = ref.collate(w.tok_off, w.tokens_numpy(), pad_id)
+    for name, g, e in zip(["input_ids", "labels", "attention_mask", "position_ids"], outs, want):
+        got = h(g)
+        assert got.shape == e.shape, name
+        if not np.array_equal(got, e):
+            bad = np.nonzero(got != e)[0]
+            raise AssertionError(f"{name}: {len(bad)} mismatches, first at {bad[0]}: {got[bad[0]]} vs {e[bad[0]]}")
+
+
+def compare_collate_sampled(w, outs, ref, pad_id=0, samples=200000, seed=0):
+    """Spot-check collate outputs at random positions plus every tile's first and last
+    element, against the oracle's per-element collate rule."""
+    import torch
+
+    P = ref.padded_elems
+    rng = np.random.default_rng(seed)
+    idx = rng.integers(0, P, size=samples)
+    starts = ref.slot_tile_off[:-1][ref.slot_rows > 0]
+    ends = ref.slot_tile_off[1:][ref.slot_rows > 0] - 1
+    idx = np.unique(np.concatenate([idx, starts, ends, [0, P - 1]]))
+    want = oracle.collate_elements(ref, w.tok_off, synth.token_ids, idx, pad_id)
+    ti = torch.from_numpy(idx).to(outs[0].device)
+    for name, g, e in zip(["input_ids", "labels", "attention_mask", "position_ids"], outs, want):
+        got = g[ti].cpu().numpy()
+        if not np.array_equal(got, e):
+            bad = np.nonzero(got != e)[0]
+            raise AssertionError(f"{name}: {len(bad)} sampled mismatches, first at {idx[bad[0]]}")
+
+
+def collate_properties(outs, ref, pad_id=0):
+    """Whole-output properties that hold at any size."""
+    import torch
+
+    ids, lab, msk, pos = outs
+    P = ref.padded_elems
+    assert ids.numel() == P
+    real = int(msk.sum(dtype=torch.int64))
+    assert real == ref.info["real_tokens"]
+    assert int((msk == 0).logical_and(lab != -100).sum()) == 0
+    assert int((msk == 1).logical_and(ids != lab).sum()) == 0
+    assert int((msk == 0).logical_and(ids != pad_id).sum()) == 0
+    assert int((msk == 0).logical_and(pos != 0).sum()) == 0
+    # position ids of real tokens sum to sum over samples of l(l-1)/2
+    return real

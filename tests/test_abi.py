@@ -1,0 +1,95 @@
+"""The C-ABI library without a GPU: it loads, exports what include/odb.h declares, and
+rejects bad arguments on the host before touching the device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2606_19989_amd as odb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "odb.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(odb_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = odb.load()
+    names = _declared()
+    assert set(names) == set(odb.EXPORTED)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    lib = odb.load()
+    assert lib.odb_status_string(0) == b"ODB_OK"
+    assert lib.odb_status_string(4) == b"ODB_E_CAPACITY"
+    assert lib.odb_status_string(99) == b"ODB_E_UNKNOWN"
+
+
+def _window(rank_off, n=None):
+    ro = np.asarray(rank_off, dtype=np.int64)
+    w = odb.Window(len(ro) - 1, 0, int(ro[-1]) if n is None else n,
+                   ro.ctypes.data_as(ctypes.c_void_p).value, 0x1000, 0x2000, None, 0)
+    return w, ro
+
+
+def test_workspace_size_grows_with_window():
+    lib = odb.load()
+    w1, k1 = _window([0, 100, 200])
+    w2, k2 = _window([0, 100000, 200000])
+    s1 = lib.odb_workspace_size(ctypes.byref(w1))
+    s2 = lib.odb_workspace_size(ctypes.byref(w2))
+    assert 0 < s1 < s2
+    assert s2 >= 200000 * 64   # tens of bytes of scratch per sample
+
+
+@pytest.mark.parametrize("rank_off,n", [([0, 5, 3, 6], None), ([1, 5], None), ([0, 5], 6), ([0], 0)])
+def test_bad_windows_rejected_on_host(rank_off, n):
+    lib = odb.load()
+    w, keep = _window(rank_off, n)
+    assert lib.odb_workspace_size(ctypes.byref(w)) == 0
+    st = lib.odb_form_groups(ctypes.byref(w), 10, None, None, None, None, None, 0, None)
+    assert st == odb.ODB_E_INVALID_ARG
+    assert lib.odb_last_error_message() != b""
+
+
+def test_bad_arguments_rejected_on_host():
+    lib = odb.load()
+    w, keep = _window([0, 4])
+    size = lib.odb_workspace_size(ctypes.byref(w))
+    fake_ws = 0x100000  # never dereferenced: every call below fails its host checks first
+    # workspace too small
+    st = lib.odb_form_groups(ctypes.byref(w), 10, 1, 1, 1, 1, fake_ws, size - 1, None)
+    assert st == odb.ODB_E_WORKSPACE
+    # misaligned workspace
+    st = lib.odb_form_groups(ctypes.byref(w), 10, 1, 1, 1, 1, fake_ws + 8, size, None)
+    assert st == odb.ODB_E_INVALID_ARG
+    # budget < 1
+    st = lib.odb_form_groups(ctypes.byref(w), 0, 1, 1, 1, 1, fake_ws, size, None)
+    assert st == odb.ODB_E_INVALID_ARG
+    # non-join without quota, unknown mode, negative capacity
+    info = odb.PlanInfo()
+    for mode, quota, cap in [(1, 0, None), (7, 1, None), (0, 0, np.array([-1], dtype=np.int64))]:
+        p = odb.AlignParams(mode, 0, quota, None if cap is None else cap.ctypes.data_as(ctypes.c_void_p).value)
+        st = lib.odb_align_groups(ctypes.byref(w), 10, ctypes.byref(p), 1, 1, 1, 1, 16, 1, 1, 1, 1, 1, 1, 1, 1,
+                                  ctypes.byref(info), fake_ws, size, None)
+        assert st == odb.ODB_E_INVALID_ARG, (mode, quota, cap)
+    # collate with negative sizes
+    st = lib.odb_collate(ctypes.byref(w), -1, 1, 1, 1, 1, 1, 0, 10, 1, 1, 1, 1, fake_ws, size, None)
+    assert st == odb.ODB_E_INVALID_ARG
+    st = lib.odb_collate(ctypes.byref(w), 3, 1, 1, 1, 1, 1, 0, -5, 1, 1, 1, 1, fake_ws, size, None)
+    assert st == odb.ODB_E_INVALID_ARG
+
+
+def test_binding_raises_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(odb, "_lib", None)
+    monkeypatch.setattr(odb, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError):
+        odb.load()

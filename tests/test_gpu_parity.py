@@ -1,0 +1,121 @@
+"""GPU parity: the HIP pipeline, called through the C ABI, against the CPU oracle.
+
+Small and adversarial windows are compared element by element on every output; the
+benchmark workloads are compared exactly on every plan array and on sampled collate
+outputs (plus whole-output properties), in the launch configuration the benchmark uses.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from _parity import (collate_properties, compare_collate_full, compare_collate_sampled, compare_plan, log,
+                     run_gpu)
+
+pytestmark = pytest.mark.gpu
+
+
+def win(per_rank, budget, **kw):
+    return synth.window_from_ranks("t", [np.asarray(x, dtype=np.int64) for x in per_rank], budget, **kw)
+
+
+def check_full(w, pad_id=0):
+    log(f"case {w.name}: W={w.W} n={w.n} budget={w.budget} mode={w.mode} quota={w.quota} "
+        f"cap={None if w.capacity is None else list(w.capacity)}")
+    ref = oracle.plan_window(w)
+    pipe, outs = run_gpu(w, pad_id=pad_id)
+    compare_plan(w, pipe, ref)
+    compare_collate_full(w, outs, ref, pad_id)
+    return pipe, ref
+
+
+def adversarial_windows():
+    rng = np.random.default_rng(100)
+    out = []
+    add = lambda name, per, budget, **kw: out.append(
+        synth.window_from_ranks(name, [np.asarray(x, dtype=np.int64) for x in per], budget, **kw))
+    add("worked_example", [[100, 200, 500, 800]], 1000)
+    add("all_equal", [[64] * 700, [64] * 513], 4096)
+    add("ascending", [np.arange(1, 3001), np.arange(5, 900)], 8192)
+    add("descending", [np.arange(3000, 0, -1)], 5000)
+    add("heavy_ties", [rng.integers(1, 4, 5000) for _ in range(3)], 64)
+    add("single_sample_ranks", [[7], [9], [1]], 100)
+    add("empty_ranks", [[], rng.integers(1, 500, 300), [], rng.integers(1, 500, 40), []], 2000)
+    add("longer_than_budget", [rng.integers(900, 3000, 200), rng.integers(1, 100, 900)], 1000)
+    add("budget_below_min", [rng.integers(50, 300, 400), rng.integers(50, 300, 10)], 49)
+    add("one_rank", [rng.integers(1, 4000, 10000)], 16384)
+    add("tiny_budget_one", [rng.integers(1, 5, 300)], 1)
+    add("capacity_overflow", [rng.integers(1, 600, 900), rng.integers(1, 600, 500), rng.integers(1, 600, 50)], 3000,
+        capacity=np.array([5, 0, 3]))
+    add("capacity_one", [rng.integers(1, 300, 120), rng.integers(1, 300, 80)], 600, capacity=np.array([1, 1]))
+    add("unequal_buffers", [rng.integers(1, 2000, 4000), rng.integers(1, 2000, 37), rng.integers(1, 2000, 1)], 8192)
+    n4 = 4000 + 800 + 3
+    for q in (1, 777, n4 - 1, n4, n4 + 1):
+        add(f"nonjoin_q{q}", [rng.integers(1, 3000, 4000), rng.integers(1, 3000, 800), rng.integers(1, 3000, 3)],
+            12000, mode="nonjoin", quota=q)
+    add("nonjoin_capacity", [rng.integers(1, 900, 700), rng.integers(1, 900, 600)], 2500, mode="nonjoin",
+        quota=1000, capacity=np.array([2, 4]))
+    add("nonjoin_empty_rank", [rng.integers(1, 900, 70), [], rng.integers(1, 900, 5)], 2500, mode="nonjoin", quota=10)
+    add("empty_window", [[], []], 100)
+    per = [rng.integers(100, 3000, 47 - r) for r in range(15)] + [np.zeros(0, np.int64)]
+    add("empty_rank_audit_w16", per, 8192)
+    return out
+
+
+@pytest.mark.parametrize("idx", range(len(adversarial_windows())))
+def test_adversarial_window(idx):
+    w = adversarial_windows()[idx]
+    check_full(w, pad_id=idx + 3)
+
+
+@pytest.mark.parametrize("kind", synth.AUDIT_KINDS)
+def test_audit_distributions(kind):
+    for W, mode in ((3, "join"), (8, "join"), (3, "nonjoin")):
+        w = synth.audit_window(kind, W, budget=4096, mode=mode, quota=1000)
+        pipe, ref = check_full(w)
+        if mode == "join":
+            _, q, P = synth.sampler_views(1000, W, seed=1)
+            assert pipe.info["missing_ids"] == 0 and pipe.info["duplicate_ids"] == P
+
+
+def test_random_small_windows():
+    rng = np.random.default_rng(7)
+    for t in range(40):
+        W = int(rng.integers(1, 6))
+        per = [rng.integers(1, int(rng.integers(2, 3000)), size=int(rng.integers(0, 400))) for _ in range(W)]
+        n = sum(len(x) for x in per)
+        mode = "nonjoin" if t % 3 == 2 else "join"
+        cap = rng.integers(0, 6, size=W) if t % 4 == 1 else None
+        w = win(per, int(rng.integers(1, 20000)), mode=mode, quota=int(rng.integers(1, n + 2)), capacity=cap)
+        w.name = f"random_{t}"
+        check_full(w, pad_id=int(rng.integers(0, 5)))
+
+
+def test_sampler_padding_identity_coverage():
+    # identity-coverage audit arithmetic: N = 57,284 over 8 ranks leaves P = 4 padding views
+    views, q, P = synth.sampler_views(57284, 8, seed=3)
+    rng = np.random.default_rng(3)
+    lens = rng.integers(16, 12110, size=57284)
+    w = win([lens[v] for v in views], 12288, identity=np.concatenate(views), num_identities=57284)
+    w.name = "sampler_padding_57284"
+    pipe, ref = check_full(w)
+    assert pipe.info["missing_ids"] == 0 and pipe.info["duplicate_ids"] == P == 4
+
+
+def test_workload_small_full():
+    w = synth.WORKLOADS["ln512_w2x2048"].window()
+    check_full(w)
+
+
+@pytest.mark.parametrize("name", ["text_w8x65536", "bimodal_w16x65536", "mm_w8x262144", "ln480_w64x262144"])
+def test_workload_full_size(name):
+    w = synth.WORKLOADS[name].window()
+    log(f"workload {name}: n={w.n} tokens={w.total_tokens}")
+    ref = oracle.plan_window(w)
+    log(f"  oracle plan done: steps={ref.steps} padded={ref.padded_elems}")
+    pipe, outs = run_gpu(w)
+    log("  gpu pipeline done")
+    compare_plan(w, pipe, ref)
+    compare_collate_sampled(w, outs, ref)
+    collate_properties(outs, ref)
+    log("  compared")

@@ -66,6 +66,16 @@ __global__ void init_align_kernel(RoundState* rs, DevInfo* info) {
     }
 }
 
+__global__ void clear_view_counters_kernel(DevInfo* info, int with_ids) {
+    if (threadIdx.x == 0) {
+        info->bad_views = 0;
+        if (with_ids) {
+            info->missing_ids = 0;
+            info->duplicate_ids = 0;
+        }
+    }
+}
+
 __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
@@ -122,6 +132,8 @@ __global__ void __launch_bounds__(kBlock) round0_check_kernel(
     const int64_t* __restrict__ tok_off, const int64_t* __restrict__ off, const RankState* __restrict__ ranks,
     int W, int64_t n, const int32_t* __restrict__ order, const int32_t* __restrict__ slen,
     const int32_t* __restrict__ gidx, int32_t* __restrict__ gstart, DevStatus* st) {
+    __shared__ int64_t s_off[kLdsRanks + 1];
+    off = stage_ranks(off, W, s_off);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
         const int r = rank_of(off, W, p);
@@ -494,6 +506,8 @@ __global__ void __launch_bounds__(kBlock) emit_kernel(
     const int32_t* __restrict__ gidx, const int32_t* __restrict__ gstart, const int32_t* __restrict__ gsize,
     const int32_t* __restrict__ ov_slot, const int32_t* __restrict__ ov_lo, int32_t* __restrict__ dst,
     int32_t* __restrict__ next_ids, int32_t* __restrict__ next_len) {
+    __shared__ int64_t s_off[kLdsRanks + 1];
+    off = stage_ranks(off, W, s_off);
     const int64_t cut = rs->cut;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
@@ -578,6 +592,8 @@ __global__ void __launch_bounds__(kBlock) compact_emit_kernel(const int32_t* __r
                                                               const RankState* __restrict__ ranks, int W, int64_t n,
                                                               const int64_t* __restrict__ row_off, int64_t S,
                                                               int32_t* __restrict__ emit) {
+    __shared__ int64_t s_off[kLdsRanks + 1];
+    off = stage_ranks(off, W, s_off);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
         const int r = rank_of(off, W, p);
@@ -610,6 +626,8 @@ __global__ void __launch_bounds__(kBlock) leftover_kernel(const int32_t* __restr
                                                           const RankState* __restrict__ ranks, int W, int64_t n,
                                                           const int64_t* __restrict__ loff,
                                                           int32_t* __restrict__ left) {
+    __shared__ int64_t s_off[kLdsRanks + 1];
+    off = stage_ranks(off, W, s_off);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
         const int r = rank_of(off, W, p);
@@ -679,6 +697,33 @@ __global__ void __launch_bounds__(kBlock) coverage_reduce_kernel(const int32_t* 
     }
 }
 
+// Sets bit v of `bits` for every view id v in ids[0, m) (ids outside [0, n) are errors).
+__global__ void __launch_bounds__(kBlock) mark_views_kernel(const int32_t* __restrict__ ids, int64_t m, int64_t n,
+                                                            uint32_t* bits, DevStatus* st) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += stride) {
+        const int32_t v = ids[i];
+        if (v < 0 || v >= n) {
+            atomicOr(&st->err, kErrInternal);
+            continue;
+        }
+        atomicOr(&bits[v >> 5], 1u << (v & 31));
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) popcount_kernel(const uint32_t* __restrict__ bits, int64_t words,
+                                                          DevInfo* info) {
+    int64_t c = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < words; i += stride) c += __popc(bits[i]);
+    c = block_sum(c);
+    if (threadIdx.x == 0 && c) atomicAdd((unsigned long long*)&info->distinct_views, (unsigned long long)c);
+}
+
+// Coverage (App. C): a bitset over the sampler views proves "every view exactly once"
+// when it holds n distinct views and n ids were listed; the exact per-view counters run
+// only when it does not (run_coverage_exact).  Identities of an identity map are always
+// counted exactly (duplicates are expected there: sampler padding).
 int run_coverage(const odb_window_t* w, const Layout& L, void* ws, const int32_t* emitted, int64_t ne,
                  const int32_t* left, int64_t nl, hipStream_t s) {
     const int64_t n = w->num_samples;
@@ -686,34 +731,230 @@ int run_coverage(const odb_window_t* w, const Layout& L, void* ws, const int32_t
     DevStatus* st = ws_at<DevStatus>(ws, L.status);
     DevInfo* info = ws_at<DevInfo>(ws, L.info);
     const int64_t cap = (int64_t)num_cus() * 16;
-    auto count = [&](const int64_t* identity, int64_t range) -> int {
-        hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(range, kBlock, cap)), dim3(kBlock), 0, s, cover, range, 0);
+    if (n > 0) {
+        uint32_t* bits = reinterpret_cast<uint32_t*>(cover);
+        const int64_t words = (n + 31) / 32;
+        hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(words, kBlock, cap)), dim3(kBlock), 0, s, cover, words, 0);
+        ODB_LAUNCHED();
+        if (ne > 0) {
+            hipLaunchKernelGGL(mark_views_kernel, dim3(grid_for(ne, kBlock, cap)), dim3(kBlock), 0, s, emitted, ne, n,
+                               bits, st);
+            ODB_LAUNCHED();
+        }
+        if (nl > 0) {
+            hipLaunchKernelGGL(mark_views_kernel, dim3(grid_for(nl, kBlock, cap)), dim3(kBlock), 0, s, left, nl, n,
+                               bits, st);
+            ODB_LAUNCHED();
+        }
+        hipLaunchKernelGGL(popcount_kernel, dim3(grid_for(words, kBlock, cap)), dim3(kBlock), 0, s,
+                           (const uint32_t*)bits, words, info);
+        ODB_LAUNCHED();
+    }
+    if (w->d_identity && n > 0) {
+        // the identity counters reuse the bitset's memory: the popcount above has consumed it
+        const int64_t nid = w->num_identities;
+        hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(nid, kBlock, cap)), dim3(kBlock), 0, s, cover, nid, 0);
         ODB_LAUNCHED();
         if (ne > 0) {
             hipLaunchKernelGGL(count_kernel, dim3(grid_for(ne, kBlock, cap)), dim3(kBlock), 0, s, emitted, ne, n,
-                               identity, range, cover, st);
+                               w->d_identity, nid, cover, st);
             ODB_LAUNCHED();
         }
         if (nl > 0) {
             hipLaunchKernelGGL(count_kernel, dim3(grid_for(nl, kBlock, cap)), dim3(kBlock), 0, s, left, nl, n,
-                               identity, range, cover, st);
+                               w->d_identity, nid, cover, st);
             ODB_LAUNCHED();
         }
-        return ODB_OK;
-    };
-    if (n > 0) {
-        ODB_TRY(count(nullptr, n));
-        hipLaunchKernelGGL(coverage_reduce_kernel, dim3(grid_for(n, kBlock, cap)), dim3(kBlock), 0, s,
-                           (const int32_t*)cover, n, 1, w->d_identity ? 0 : 1, info);
-        ODB_LAUNCHED();
-    }
-    if (w->d_identity) {
-        const int64_t nid = w->num_identities;
-        ODB_TRY(count(w->d_identity, nid));
         hipLaunchKernelGGL(coverage_reduce_kernel, dim3(grid_for(nid, kBlock, cap)), dim3(kBlock), 0, s,
                            (const int32_t*)cover, nid, 0, 1, info);
         ODB_LAUNCHED();
     }
+    return ODB_OK;
+}
+
+// Exact per-view counts: bad_views (and missing / duplicates without an identity map).
+// Needed only when the bitset pass found fewer than n distinct views or n != ne + nl.
+int run_coverage_exact(const odb_window_t* w, const Layout& L, void* ws, const int32_t* emitted, int64_t ne,
+                       const int32_t* left, int64_t nl, hipStream_t s) {
+    const int64_t n = w->num_samples;
+    int32_t* cover = ws_at<int32_t>(ws, L.cover);
+    DevStatus* st = ws_at<DevStatus>(ws, L.status);
+    DevInfo* info = ws_at<DevInfo>(ws, L.info);
+    const int64_t cap = (int64_t)num_cus() * 16;
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(n, kBlock, cap)), dim3(kBlock), 0, s, cover, n, 0);
+    ODB_LAUNCHED();
+    if (ne > 0) {
+        hipLaunchKernelGGL(count_kernel, dim3(grid_for(ne, kBlock, cap)), dim3(kBlock), 0, s, emitted, ne, n,
+                           (const int64_t*)nullptr, n, cover, st);
+        ODB_LAUNCHED();
+    }
+    if (nl > 0) {
+        hipLaunchKernelGGL(count_kernel, dim3(grid_for(nl, kBlock, cap)), dim3(kBlock), 0, s, left, nl, n,
+                           (const int64_t*)nullptr, n, cover, st);
+        ODB_LAUNCHED();
+    }
+    hipLaunchKernelGGL(coverage_reduce_kernel, dim3(grid_for(n, kBlock, cap)), dim3(kBlock), 0, s,
+                       (const int32_t*)cover, n, 1, w->d_identity ? 0 : 1, info);
+    ODB_LAUNCHED();
+    return ODB_OK;
+}
+
+// Coverage of one rank's views, one id chunk per block, in LDS.  The views of rank r are
+// its ids [off[r], off[r+1]); they may appear only in rank r's emitted rows
+// (emit[row_off[r*S] .. row_off[(r+1)*S])) and leftovers (left[loff[r] .. loff[r+1])).
+// Block b covers ids [lo, hi) of one rank: it scans both lists, sets bit v in `once`,
+// and in `twice` if it was already set.  missing = (hi - lo) - |once|, views listed
+// more than once = |twice|, extra listings = dup.  An id of another rank in these lists
+// is an internal error.
+__global__ void __launch_bounds__(kBlock) coverage_lds_kernel(
+    const int64_t* __restrict__ off, int W, const int64_t* __restrict__ chunk_first, int64_t C,
+    const int32_t* __restrict__ emit, const int64_t* __restrict__ row_off, int64_t S,
+    const int32_t* __restrict__ left, const int64_t* __restrict__ loff, int want_ids, DevInfo* info,
+    DevStatus* st) {
+    extern __shared__ uint32_t lds[];
+    const int64_t words = C / 32;
+    uint32_t* once = lds;
+    uint32_t* twice = lds + words;
+    const int64_t b = blockIdx.x;
+    const int r = rank_of(chunk_first, W, b);
+    const int64_t j = b - chunk_first[r];
+    const int64_t base = off[r], end = off[r + 1];
+    const int64_t lo = base + j * C;
+    const int64_t hi = lo + C < end ? lo + C : end;
+    for (int64_t i = threadIdx.x; i < words; i += kBlock) {
+        once[i] = 0;
+        twice[i] = 0;
+    }
+    __syncthreads();
+    int64_t dup = 0, foreign = 0;
+    const int32_t* lists[2] = {emit, left};
+    const int64_t from[2] = {row_off[(int64_t)r * S], loff[r]};
+    const int64_t to[2] = {row_off[(int64_t)(r + 1) * S], loff[r + 1]};
+    for (int li = 0; li < 2; ++li) {
+        const int32_t* ids = lists[li];
+        for (int64_t i = from[li] + threadIdx.x; i < to[li]; i += kBlock) {
+            const int64_t v = ids[i];
+            if (v < base || v >= end) {
+                foreign += j == 0 ? 1 : 0;
+                continue;
+            }
+            if (v < lo || v >= hi) continue;
+            const uint32_t bit = 1u << ((v - lo) & 31);
+            const int64_t wd = (v - lo) >> 5;
+            if (atomicOr(&once[wd], bit) & bit) {
+                atomicOr(&twice[wd], bit);
+                dup += 1;
+            }
+        }
+    }
+    __syncthreads();
+    int64_t distinct = 0, multi = 0;
+    const int64_t nw = (hi - lo + 31) / 32;
+    for (int64_t i = threadIdx.x; i < nw; i += kBlock) {
+        distinct += __popc(once[i]);
+        multi += __popc(twice[i]);
+    }
+    distinct = block_sum(distinct);
+    multi = block_sum(multi);
+    dup = block_sum(dup);
+    foreign = block_sum(foreign);
+    if (threadIdx.x == 0) {
+        const int64_t missing = (hi - lo) - distinct;
+        const int64_t bad = missing + multi;
+        if (bad) atomicAdd((unsigned long long*)&info->bad_views, (unsigned long long)bad);
+        if (want_ids && missing) atomicAdd((unsigned long long*)&info->missing_ids, (unsigned long long)missing);
+        if (want_ids && dup) atomicAdd((unsigned long long*)&info->duplicate_ids, (unsigned long long)dup);
+        if (foreign) atomicOr(&st->err, kErrInternal);
+    }
+}
+
+// chunk_first[r] = sum_{r' < r} ceil(n_r' / C).  One block.
+__global__ void __launch_bounds__(kBlock) chunks_kernel(const int64_t* __restrict__ off, int W, int64_t C,
+                                                        int64_t* __restrict__ chunk_first) {
+    __shared__ int64_t carry;
+    if (threadIdx.x == 0) carry = 0;
+    __syncthreads();
+    for (int b = 0; b < W; b += kBlock) {
+        const int r = b + threadIdx.x;
+        const int64_t v = r < W ? (off[r + 1] - off[r] + C - 1) / C : 0;
+        int64_t tot;
+        const int64_t ex = block_excl_sum(v, &tot);
+        const int64_t c = carry;
+        if (r < W) chunk_first[r] = c + ex;
+        __syncthreads();
+        if (threadIdx.x == 0) carry = c + tot;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) chunk_first[W] = carry;
+}
+
+// Coverage of an aligned plan: per-rank LDS bitsets for the views, global counters for
+// the identities of an identity map.
+int run_plan_coverage(const odb_window_t* w, const Layout& L, void* ws, const int32_t* emit,
+                      const int64_t* row_off, int64_t S, const int32_t* left, const int64_t* loff, int64_t ne,
+                      int64_t nl, hipStream_t s) {
+    const int W = w->num_ranks;
+    const int64_t n = w->num_samples;
+    if (n == 0) return ODB_OK;
+    int64_t max_nr = 0, chunks = 0;
+    for (int r = 0; r < W; ++r) {
+        const int64_t nr = w->rank_offsets[r + 1] - w->rank_offsets[r];
+        max_nr = nr > max_nr ? nr : max_nr;
+    }
+    int64_t C = ((max_nr / 4 + 4095) / 4096) * 4096;
+    C = C < 4096 ? 4096 : (C > 131072 ? 131072 : C);
+    for (int r = 0; r < W; ++r) chunks += (w->rank_offsets[r + 1] - w->rank_offsets[r] + C - 1) / C;
+    int64_t* chunk_first = ws_at<int64_t>(ws, L.tile_first);
+    const int64_t* d_off = ws_at<int64_t>(ws, L.rank_off);
+    hipLaunchKernelGGL(chunks_kernel, dim3(1), dim3(kBlock), 0, s, d_off, W, C, chunk_first);
+    ODB_LAUNCHED();
+    hipLaunchKernelGGL(coverage_lds_kernel, dim3((unsigned)chunks), dim3(kBlock), (size_t)(C / 4), s, d_off, W,
+                       (const int64_t*)chunk_first, C, emit, row_off, S, left, loff, w->d_identity ? 0 : 1,
+                       ws_at<DevInfo>(ws, L.info), ws_at<DevStatus>(ws, L.status));
+    ODB_LAUNCHED();
+    if (w->d_identity) {
+        int32_t* cover = ws_at<int32_t>(ws, L.cover);
+        DevStatus* st = ws_at<DevStatus>(ws, L.status);
+        const int64_t nid = w->num_identities;
+        const int64_t cap = (int64_t)num_cus() * 16;
+        hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(nid, kBlock, cap)), dim3(kBlock), 0, s, cover, nid, 0);
+        ODB_LAUNCHED();
+        if (ne > 0) {
+            hipLaunchKernelGGL(count_kernel, dim3(grid_for(ne, kBlock, cap)), dim3(kBlock), 0, s, emit, ne, n,
+                               w->d_identity, nid, cover, st);
+            ODB_LAUNCHED();
+        }
+        if (nl > 0) {
+            hipLaunchKernelGGL(count_kernel, dim3(grid_for(nl, kBlock, cap)), dim3(kBlock), 0, s, left, nl, n,
+                               w->d_identity, nid, cover, st);
+            ODB_LAUNCHED();
+        }
+        hipLaunchKernelGGL(coverage_reduce_kernel, dim3(grid_for(nid, kBlock, cap)), dim3(kBlock), 0, s,
+                           (const int32_t*)cover, nid, 0, 1, ws_at<DevInfo>(ws, L.info));
+        ODB_LAUNCHED();
+    }
+    return ODB_OK;
+}
+
+// Reads the coverage counters after run_coverage; runs the exact view count when the
+// bitset pass did not prove that every view was listed exactly once.
+int finish_coverage(const odb_window_t* w, const Layout& L, void* ws, const int32_t* emitted, int64_t ne,
+                    const int32_t* left, int64_t nl, DevInfo* hi, hipStream_t s) {
+    const int64_t n = w->num_samples;
+    if (hi->distinct_views == n && ne + nl == n) {
+        hi->bad_views = 0;
+        if (!w->d_identity) {
+            hi->missing_ids = 0;
+            hi->duplicate_ids = 0;
+        }
+        return ODB_OK;
+    }
+    DevInfo* info = ws_at<DevInfo>(ws, L.info);
+    hipLaunchKernelGGL(clear_view_counters_kernel, dim3(1), dim3(64), 0, s, info, w->d_identity ? 0 : 1);
+    ODB_LAUNCHED();
+    ODB_TRY(run_coverage_exact(w, L, ws, emitted, ne, left, nl, s));
+    ODB_TRY_HIP(hipMemcpyAsync(hi, info, sizeof(*hi), hipMemcpyDeviceToHost, s));
+    ODB_TRY_HIP(hipStreamSynchronize(s));
     return ODB_OK;
 }
 
@@ -933,7 +1174,8 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
                        (const int64_t*)d_slot_tile_off, K, d_info);
     ODB_LAUNCHED();
     const int64_t nemit = hrs.emitted_total;
-    ODB_TRY(run_coverage(w, L, d_ws, d_emit_order, nemit, d_leftover, nleft, s));
+    ODB_TRY(run_plan_coverage(w, L, d_ws, d_emit_order, d_slot_row_off, S, d_leftover, d_leftover_off, nemit, nleft,
+                              s));
 
     DevInfo hi;
     DevStatus hs;
@@ -978,6 +1220,7 @@ extern "C" int odb_check_coverage(const odb_window_t* w, const int32_t* d_emitte
     ODB_TRY_HIP(hipMemcpyAsync(&hi, ws_at<DevInfo>(d_ws, L.info), sizeof(hi), hipMemcpyDeviceToHost, s));
     ODB_TRY_HIP(hipMemcpyAsync(&hs, ws_at<DevStatus>(d_ws, L.status), sizeof(hs), hipMemcpyDeviceToHost, s));
     ODB_TRY_HIP(hipStreamSynchronize(s));
+    ODB_TRY(finish_coverage(w, L, d_ws, d_emitted, num_emitted, d_leftover, num_leftover, &hi, s));
     h_info->bad_views = hi.bad_views;
     h_info->missing_ids = hi.missing_ids;
     h_info->duplicate_ids = hi.duplicate_ids;

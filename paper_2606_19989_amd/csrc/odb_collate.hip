@@ -1,14 +1,31 @@
 // Stage 4 of the ODB window pipeline: padded collation (Sec. 2.1, Fig. 1 -- every
 // aligned group is padded to its own longest sample).
 //
-// The kernel is stationary on the flat output: all four outputs share one element index
-// space [0, padded_elems), every lane owns 4 consecutive elements, so each lane issues one
-// aligned 16-byte non-temporal store per output whatever the row length.  A block owns a
-// contiguous span of the output and walks it in 1024-element steps; each lane keeps the
-// tile (slot) index of its current element and advances it by a galloping search over
-// the tile offsets, so long tiles cost one cached compare per step and runs of tiny tiles
-// stay logarithmic.  Row, column and sample come from the tile's max length and row
-// offset; real columns read the sample's tokens from the CSR stream.
+// Two launches:
+//   row_info_kernel  token start and length of every emitted row (one gather of the CSR
+//                    offsets per row), so the hot loop never chases emit -> offsets.
+//   collate_kernel   stationary on the flat output: the four outputs share one element
+//                    index space [0, padded_elems).  The output is cut into steps of
+//                    kBlockStep elements; runs of kRunSteps consecutive steps are dealt
+//                    to the blocks round robin, so the blocks in flight read and write one
+//                    compact region of every array.  In a step every lane owns kGroups
+//                    groups of 4 consecutive elements (a wave's groups are 256 elements
+//                    apart) and stores each group as one aligned 16-byte non-temporal
+//                    store per output.
+//
+// Software pipeline.  On CDNA the vector-memory counter covers loads and stores alike
+// and retires in order, so waiting for a load also waits for every store issued before
+// it.  Under a saturated write stream that wait is long.  The kernel therefore keeps
+// three steps in flight per lane: while it computes and stores step s it has the tokens
+// of step s+1 and the row records of step s+2 in flight, all issued before step s's
+// stores.  Each wait then targets a load issued before the previous step's stores, and
+// stores drain in the background.  Token and row loads use clamped addresses, so a load
+// never has to be skipped to stay inside its array.
+//
+// A group's cursor (slot, row, column) advances with the step sequence: inside a tile it
+// moves by arithmetic, across tiles by a galloping search over the tile offsets.  When a
+// group's 4 elements lie in one row (the common case) its tokens arrive in one 16-byte
+// load; a group that straddles a row or tile edge is finished element by element.
 #include "odb_internal.h"
 
 namespace odb {
@@ -16,10 +33,74 @@ namespace odb {
 namespace {
 
 constexpr int kCollateBlock = 256;
-constexpr int kVec = 4;
-constexpr int64_t kChunk = (int64_t)kCollateBlock * kVec;
+constexpr int kVec = 4;                                              // elements per group
+constexpr int kGroups = 1;                                           // groups per lane per step
+constexpr int64_t kGroupSpan = (int64_t)kWave * kVec;                // 256
+constexpr int64_t kWaveStep = kGroupSpan * kGroups;                  // 256
+constexpr int64_t kBlockStep = kWaveStep * (kCollateBlock / kWave);  // 1024
+constexpr int64_t kRunSteps = 128;                                   // consecutive steps per run
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+
+__global__ void __launch_bounds__(kBlock) row_info_kernel(const int64_t* __restrict__ tok_off, int64_t n,
+                                                          const int32_t* __restrict__ emit,
+                                                          const int64_t* __restrict__ row_off, int64_t num_slots,
+                                                          int64_t* __restrict__ row_ts, int32_t* __restrict__ row_len,
+                                                          int32_t* err) {
+    int64_t rows = row_off[num_slots];
+    if (rows > n || rows < 0) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, 1);
+        rows = rows < 0 ? 0 : n;
+    }
+    bool bad = false;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t ri = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; ri < rows; ri += stride) {
+        const int32_t s = emit[ri];
+        int64_t ts = 0, l = 0;
+        if (s >= 0 && s < n) {
+            ts = tok_off[s];
+            l = tok_off[s + 1] - ts;
+        }
+        if (s < 0 || s >= n || ts < 0 || l < 0 || l > 0x7FFFFFFF) {
+            bad = true;
+            ts = 0;
+            l = 0;
+        }
+        row_ts[ri] = ts;
+        row_len[ri] = (int32_t)l;
+    }
+    if (bad) atomicOr(err, 1);
+}
+
+struct Plan {
+    const int64_t* __restrict__ tile_off;
+    const int32_t* __restrict__ maxlen;
+    const int32_t* __restrict__ rows;
+    const int64_t* __restrict__ row_off;
+    const int64_t* __restrict__ row_ts;
+    const int32_t* __restrict__ row_len;
+    const int32_t* __restrict__ tokens;
+    const int64_t* __restrict__ tok_off;
+    int64_t num_slots;
+    int64_t n;           // emitted rows never exceed the window's sample count
+    int64_t tok_end;     // tokens [0, tok_end) are addressable (tok_off[n], set in the kernel)
+    int32_t* err;
+};
+
+// Position of a group's first element.
+struct Cursor {
+    int64_t t1;      // end of the slot's tile
+    int32_t k;       // slot
+    int32_t ri;      // emitted-row index of the current row
+    int32_t ri_end;  // one past the tile's last emitted row
+    int32_t ml;      // tile width
+    int32_t col;     // column
+};
+
+struct RowRec {
+    int64_t ts;  // first token of the row's sample
+    int32_t l;   // its length
+};
 
 // Last slot k in [lo, num_slots) with tile_off[k] <= e, given tile_off[lo] <= e < total.
 __device__ __forceinline__ int64_t advance_slot(const int64_t* __restrict__ tile_off, int64_t num_slots,
@@ -36,150 +117,225 @@ __device__ __forceinline__ int64_t advance_slot(const int64_t* __restrict__ tile
         lo = hi;
         step <<= 1;
     }
-    // tile_off[lo] <= e < tile_off[hi]
-    while (hi - lo > 1) {
+    while (hi - lo > 1) {  // tile_off[lo] <= e < tile_off[hi]
         const int64_t mid = lo + ((hi - lo) >> 1);
         if (tile_off[mid] <= e) lo = mid; else hi = mid;
     }
     return lo;
 }
 
-struct RowCursor {
-    int64_t k;      // slot
-    int64_t t1;     // end of the slot's tile
-    int32_t ml;     // tile width (max length)
-    int32_t col;    // column of the current element
-    int64_t row;    // row of the current element
-    int64_t ts;     // first token of the row's sample
-    int32_t l;      // length of the row's sample
-};
-
-__device__ __forceinline__ void load_row(RowCursor& c, const int64_t* __restrict__ tok_off,
-                                         const int32_t* __restrict__ emit, const int32_t* __restrict__ rows,
-                                         const int64_t* __restrict__ row_off, int64_t n, int32_t* err) {
-    const int64_t ri = row_off[c.k] + c.row;
-    bool ok = c.row < rows[c.k] && ri >= 0 && ri < n;
-    int32_t s = ok ? emit[ri] : 0;
-    ok = ok && s >= 0 && s < n;
-    if (ok) {
-        c.ts = tok_off[s];
-        const int64_t l = tok_off[s + 1] - c.ts;
-        ok = c.ts >= 0 && l >= 0 && l <= 0x7FFFFFFF;
-        c.l = ok ? (int32_t)l : 0;
-    } else {
-        c.ts = 0;
-        c.l = 0;
+__device__ __forceinline__ void enter_slot(Cursor& c, int64_t k, int64_t e, const Plan& p) {
+    const int64_t t0 = p.tile_off[k];
+    c.k = (int32_t)k;
+    c.t1 = p.tile_off[k + 1];
+    int32_t ml = p.maxlen[k];
+    if (ml <= 0) {
+        atomicOr(p.err, 1);
+        ml = 1;
     }
-    if (!ok) atomicOr(err, 1);
-}
-
-__device__ __forceinline__ void enter_slot(RowCursor& c, int64_t e, const int64_t* __restrict__ tile_off,
-                                           const int32_t* __restrict__ maxlen, const int64_t* __restrict__ tok_off,
-                                           const int32_t* __restrict__ emit, const int32_t* __restrict__ rows,
-                                           const int64_t* __restrict__ row_off, int64_t n, int32_t* err) {
-    const int64_t t0 = tile_off[c.k];
-    c.t1 = tile_off[c.k + 1];
-    c.ml = maxlen[c.k];
+    c.ml = ml;
     const int64_t local = e - t0;
-    if (c.ml <= 0) {
-        atomicOr(err, 1);
-        c.ml = 1;
-    }
-    if (c.t1 - t0 <= 0xFFFFFFFFll) {
-        const uint32_t q = (uint32_t)local / (uint32_t)c.ml;
-        c.row = q;
-        c.col = (int32_t)((uint32_t)local - q * (uint32_t)c.ml);
+    int64_t row;
+    if (local >= 0 && local <= 0xFFFFFFFFll) {
+        const uint32_t q = (uint32_t)local / (uint32_t)ml;
+        row = q;
+        c.col = (int32_t)((uint32_t)local - q * (uint32_t)ml);
     } else {
-        c.row = local / c.ml;
-        c.col = (int32_t)(local - c.row * c.ml);
+        row = local / ml;
+        c.col = (int32_t)(local - row * ml);
     }
-    load_row(c, tok_off, emit, rows, row_off, n, err);
+    const int64_t r0 = p.row_off[k];
+    c.ri = (int32_t)(r0 + row);
+    c.ri_end = (int32_t)(r0 + p.rows[k]);
 }
 
-template <bool kAligned>
-__global__ void __launch_bounds__(kCollateBlock) collate_kernel(
-    const int64_t* __restrict__ tok_off, const int32_t* __restrict__ tokens, int64_t n,
-    const int32_t* __restrict__ emit, int64_t num_slots, const int32_t* __restrict__ rows,
-    const int32_t* __restrict__ maxlen, const int64_t* __restrict__ row_off, const int64_t* __restrict__ tile_off,
-    int32_t pad_id, int64_t capacity, int32_t* __restrict__ o_ids, int32_t* __restrict__ o_lab,
-    int32_t* __restrict__ o_msk, int32_t* __restrict__ o_pos, int32_t* err) {
-    const int64_t total_plan = tile_off[num_slots];
+// Move a cursor forward to element e (e - delta is its current element).
+__device__ __forceinline__ void advance(Cursor& c, int64_t e, int64_t delta, const Plan& p) {
+    if (e >= c.t1) {
+        enter_slot(c, advance_slot(p.tile_off, p.num_slots, c.k, e), e, p);
+        return;
+    }
+    const int64_t col = (int64_t)c.col + delta;
+    if (col >= c.ml) {
+        const int64_t adv = col <= 0xFFFFFFFFll ? (int64_t)((uint32_t)col / (uint32_t)c.ml) : col / c.ml;
+        c.ri += (int32_t)adv;
+        c.col = (int32_t)(col - adv * c.ml);
+    } else {
+        c.col = (int32_t)col;
+    }
+}
+
+// Row record of the cursor's row (a bad plan yields an empty row and sets the error word).
+__device__ __forceinline__ RowRec load_row(const Cursor& c, const Plan& p) {
+    const bool ok = c.ri >= 0 && c.ri < c.ri_end && c.ri < p.n;
+    const int32_t i = ok ? c.ri : 0;
+    RowRec r;
+    r.ts = p.row_ts[i];
+    r.l = p.row_len[i];
+    if (!ok) {
+        atomicOr(p.err, 1);
+        r.ts = 0;
+        r.l = 0;
+    }
+    return r;
+}
+
+// 16 bytes of tokens at the cursor (address clamped into the stream; only used when the
+// group's 4 elements are real tokens of one row, which never needs the clamp).
+__device__ __forceinline__ v4i load_tokens(const Cursor& c, const RowRec& r, const Plan& p) {
+    int64_t a = r.ts + c.col;
+    const int64_t hi = p.tok_end - kVec;
+    a = a < hi ? a : hi;
+    a = a > 0 ? a : 0;
+    // dword-aligned 16-byte load; streamed past the caches (every token is read once)
+    return __builtin_nontemporal_load(reinterpret_cast<const v4i*>(p.tokens + a));
+}
+
+__device__ __forceinline__ void store4(int32_t* __restrict__ o, int64_t e, v4i v, int64_t total) {
+    if (e + kVec <= total) {
+        __builtin_nontemporal_store(v, reinterpret_cast<v4i*>(o + e));
+    } else {
+#pragma unroll
+        for (int i = 0; i < kVec; ++i)
+            if (e + i < total) o[e + i] = v[i];
+    }
+}
+
+// Next step of this block's sequence (runs of kRunSteps steps, run r to block r mod
+// gridDim.x), or -1 past its end.
+__device__ __forceinline__ int64_t next_step(int64_t s, int64_t nsteps, int64_t nruns) {
+    const int64_t r = s / kRunSteps;
+    if (s + 1 < (r + 1) * kRunSteps && s + 1 < nsteps) return s + 1;
+    const int64_t r2 = r + gridDim.x;
+    return r2 < nruns ? r2 * kRunSteps : -1;
+}
+
+__global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t pad_id, int64_t capacity,
+                                                                int32_t* __restrict__ o_ids,
+                                                                int32_t* __restrict__ o_lab,
+                                                                int32_t* __restrict__ o_msk,
+                                                                int32_t* __restrict__ o_pos) {
+    p.tok_end = p.tok_off[p.n];
+    const int vec_ok = p.tok_end >= kVec;
+    const int64_t total_plan = p.tile_off[p.num_slots];
     const int64_t total = total_plan < capacity ? total_plan : capacity;
     if (total <= 0) return;
-    const int64_t nchunks = (total + kChunk - 1) / kChunk;
-    const int64_t per = (nchunks + gridDim.x - 1) / gridDim.x;
-    const int64_t c0 = (int64_t)blockIdx.x * per;
-    const int64_t c1 = c0 + per < nchunks ? c0 + per : nchunks;
-    if (c0 >= c1) return;
-    int64_t e = c0 * kChunk + (int64_t)threadIdx.x * kVec;
-    if (e >= total) return;
-    RowCursor c;
-    {
-        // last slot with tile_off[k] <= e
-        int64_t lo = 0, hi = num_slots;
-        while (hi - lo > 1) {
-            const int64_t mid = lo + ((hi - lo) >> 1);
-            if (tile_off[mid] <= e) lo = mid; else hi = mid;
+    const int64_t nsteps = (total + kBlockStep - 1) / kBlockStep;
+    const int64_t nruns = (nsteps + kRunSteps - 1) / kRunSteps;
+    if ((int64_t)blockIdx.x >= nruns) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int64_t lane_off = (int64_t)wave * kWaveStep + (int64_t)lane * kVec;
+
+    // pipeline registers: step s0 (compute), s1 (tokens in flight), s2 (rows in flight)
+    int64_t s0 = (int64_t)blockIdx.x * kRunSteps;
+    int64_t s1 = next_step(s0, nsteps, nruns);
+    int64_t s2 = s1 >= 0 ? next_step(s1, nsteps, nruns) : -1;
+    Cursor c0[kGroups], c1[kGroups], c2[kGroups];
+    RowRec r0[kGroups], r1[kGroups], r2[kGroups];
+    v4i t0[kGroups], t1[kGroups];
+
+    // prologue: locate step s0 from slot 0, step s1 from s0
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        const int64_t e = s0 * kBlockStep + lane_off + g * kGroupSpan;
+        if (e < total) {
+            int64_t lo = 0, hi = p.num_slots;  // last slot with tile_off <= e
+            while (hi - lo > 1) {
+                const int64_t mid = lo + ((hi - lo) >> 1);
+                if (p.tile_off[mid] <= e) lo = mid; else hi = mid;
+            }
+            enter_slot(c0[g], lo, e, p);
+            r0[g] = load_row(c0[g], p);
+            if (vec_ok) t0[g] = load_tokens(c0[g], r0[g], p);
+            const int64_t e1 = s1 * kBlockStep + lane_off + g * kGroupSpan;
+            if (s1 >= 0 && e1 < total) {
+                c1[g] = c0[g];
+                advance(c1[g], e1, e1 - e, p);
+                r1[g] = load_row(c1[g], p);
+            }
         }
-        c.k = lo;
     }
-    c.t1 = -1;
-    for (int64_t ci = c0; ci < c1; ++ci, e += kChunk) {
-        if (e >= total) break;
-        if (e >= c.t1) {
-            c.k = advance_slot(tile_off, num_slots, c.k, e);
-            enter_slot(c, e, tile_off, maxlen, tok_off, emit, rows, row_off, n, err);
-        } else {
-            // same tile: move the cursor forward by kChunk elements
-            // col < ml <= 2^31 - 1, so col + kChunk fits in 32 unsigned bits
-            const uint32_t local_col = (uint32_t)c.col + (uint32_t)kChunk;
-            if (local_col >= (uint32_t)c.ml) {
-                const uint32_t adv = local_col / (uint32_t)c.ml;
-                c.row += adv;
-                c.col = (int32_t)(local_col - adv * (uint32_t)c.ml);
-                load_row(c, tok_off, emit, rows, row_off, n, err);
+
+    while (s0 >= 0) {
+        // A: cursors of step s2 and their row records
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) {
+            const int64_t e1 = s1 * kBlockStep + lane_off + g * kGroupSpan;
+            const int64_t e2 = s2 * kBlockStep + lane_off + g * kGroupSpan;
+            if (s2 >= 0 && e2 < total) {
+                c2[g] = c1[g];
+                advance(c2[g], e2, e2 - e1, p);
+                r2[g] = load_row(c2[g], p);
+            }
+        }
+        // B: tokens of step s1
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) {
+            const int64_t e1 = s1 * kBlockStep + lane_off + g * kGroupSpan;
+            if (vec_ok && s1 >= 0 && e1 < total) t1[g] = load_tokens(c1[g], r1[g], p);
+        }
+        // C: values and stores of step s0
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) {
+            const int64_t e = s0 * kBlockStep + lane_off + g * kGroupSpan;
+            if (e >= total) continue;
+            const Cursor& c = c0[g];
+            const RowRec& r = r0[g];
+            const int32_t nreal = r.l - c.col;
+            v4i vid, vlab, vmsk, vpos;
+            if (vec_ok && c.col + (kVec - 1) < c.ml && (nreal <= 0 || r.ts + c.col + kVec <= p.tok_end)) {
+                // the 4 elements sit in one row and the vector load covered them
+#pragma unroll
+                for (int i = 0; i < kVec; ++i) {
+                    const bool real = i < nreal;
+                    vid[i] = real ? t0[g][i] : pad_id;
+                    vlab[i] = real ? t0[g][i] : -100;
+                    vmsk[i] = real ? 1 : 0;
+                    vpos[i] = real ? c.col + i : 0;
+                }
             } else {
-                c.col = (int32_t)local_col;
-            }
-        }
-        v4i vid, vlab, vmsk, vpos;
-        RowCursor d = c;  // cursor for the 4 elements of this step
+                // a row or tile edge inside the 4 elements: step element by element
+                Cursor d = c;
+                RowRec dr = r;
 #pragma unroll
-        for (int i = 0; i < kVec; ++i) {
-            const int64_t ee = e + i;
-            if (i > 0 && ee < total) {
-                if (ee >= d.t1) {
-                    d.k = advance_slot(tile_off, num_slots, d.k, ee);
-                    enter_slot(d, ee, tile_off, maxlen, tok_off, emit, rows, row_off, n, err);
-                } else if (++d.col == d.ml) {
-                    d.col = 0;
-                    d.row += 1;
-                    load_row(d, tok_off, emit, rows, row_off, n, err);
+                for (int i = 0; i < kVec; ++i) {
+                    const int64_t ee = e + i;
+                    if (i > 0 && ee < total) {
+                        if (ee >= d.t1) {
+                            enter_slot(d, advance_slot(p.tile_off, p.num_slots, d.k, ee), ee, p);
+                            dr = load_row(d, p);
+                        } else if (++d.col == d.ml) {
+                            d.col = 0;
+                            d.ri += 1;
+                            dr = load_row(d, p);
+                        }
+                    }
+                    const bool real = d.col < dr.l;
+                    const int32_t tok = real ? p.tokens[dr.ts + d.col] : 0;
+                    vid[i] = real ? tok : pad_id;
+                    vlab[i] = real ? tok : -100;
+                    vmsk[i] = real ? 1 : 0;
+                    vpos[i] = real ? d.col : 0;
                 }
             }
-            const bool real = d.col < d.l;
-            const int32_t tok = real ? tokens[d.ts + d.col] : 0;
-            vid[i] = real ? tok : pad_id;
-            vlab[i] = real ? tok : -100;
-            vmsk[i] = real ? 1 : 0;
-            vpos[i] = real ? d.col : 0;
+            store4(o_ids, e, vid, total);
+            store4(o_lab, e, vlab, total);
+            store4(o_msk, e, vmsk, total);
+            store4(o_pos, e, vpos, total);
         }
-        if (kAligned && e + kVec <= total) {
-            __builtin_nontemporal_store(vid, reinterpret_cast<v4i*>(o_ids + e));
-            __builtin_nontemporal_store(vlab, reinterpret_cast<v4i*>(o_lab + e));
-            __builtin_nontemporal_store(vmsk, reinterpret_cast<v4i*>(o_msk + e));
-            __builtin_nontemporal_store(vpos, reinterpret_cast<v4i*>(o_pos + e));
-        } else {
+        // rotate the pipeline
 #pragma unroll
-            for (int i = 0; i < kVec; ++i) {
-                if (e + i < total) {
-                    o_ids[e + i] = vid[i];
-                    o_lab[e + i] = vlab[i];
-                    o_msk[e + i] = vmsk[i];
-                    o_pos[e + i] = vpos[i];
-                }
-            }
+        for (int g = 0; g < kGroups; ++g) {
+            c0[g] = c1[g];
+            r0[g] = r1[g];
+            t0[g] = t1[g];
+            c1[g] = c2[g];
+            r1[g] = r2[g];
         }
+        s0 = s1;
+        s1 = s2;
+        s2 = s2 >= 0 ? next_step(s2, nsteps, nruns) : -1;
     }
 }
 
@@ -196,31 +352,41 @@ extern "C" int odb_collate(const odb_window_t* w, int64_t num_slots, const int32
                            int32_t* d_position_ids, void* d_ws, size_t ws_bytes, void* stream) {
     Layout L;
     ODB_TRY(check_workspace(w, d_ws, ws_bytes, &L));
-    if (num_slots < 0) return set_error(ODB_E_INVALID_ARG, "num_slots must be >= 0");
+    if (num_slots < 0 || num_slots >= 0x7FFFFFFFll)
+        return set_error(ODB_E_INVALID_ARG, "num_slots must be in [0, 2^31 - 1)");
     if (out_capacity_elems < 0) return set_error(ODB_E_INVALID_ARG, "out_capacity_elems must be >= 0");
     if (num_slots == 0 || out_capacity_elems == 0) return ODB_OK;
     if (!d_slot_rows || !d_slot_maxlen || !d_slot_row_off || !d_slot_tile_off)
         return set_error(ODB_E_INVALID_ARG, "plan arrays must not be NULL");
     if (!d_input_ids || !d_labels || !d_attention_mask || !d_position_ids)
         return set_error(ODB_E_INVALID_ARG, "output arrays must not be NULL");
-    if (w->num_samples > 0 && !d_emit_order) return set_error(ODB_E_INVALID_ARG, "d_emit_order is NULL");
+    if (((reinterpret_cast<uintptr_t>(d_input_ids) | reinterpret_cast<uintptr_t>(d_labels) |
+          reinterpret_cast<uintptr_t>(d_attention_mask) | reinterpret_cast<uintptr_t>(d_position_ids)) &
+         15) != 0)
+        return set_error(ODB_E_INVALID_ARG, "output arrays must be 16-byte aligned");
+    const int64_t n = w->num_samples;
+    if (n == 0) return ODB_OK;  // no rows: every tile is empty
+    if (!d_emit_order) return set_error(ODB_E_INVALID_ARG, "d_emit_order is NULL");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool aligned = ((reinterpret_cast<uintptr_t>(d_input_ids) | reinterpret_cast<uintptr_t>(d_labels) |
-                           reinterpret_cast<uintptr_t>(d_attention_mask) |
-                           reinterpret_cast<uintptr_t>(d_position_ids)) &
-                          15) == 0;
-    const unsigned grid = (unsigned)num_cus() * 8;
     int32_t* err = &ws_at<DevStatus>(d_ws, L.status)->collate_err;
-    if (aligned)
-        hipLaunchKernelGGL(collate_kernel<true>, dim3(grid), dim3(kCollateBlock), 0, s, w->d_token_offsets,
-                           w->d_tokens, w->num_samples, d_emit_order, num_slots, d_slot_rows, d_slot_maxlen,
-                           d_slot_row_off, d_slot_tile_off, pad_id, out_capacity_elems, d_input_ids, d_labels,
-                           d_attention_mask, d_position_ids, err);
-    else
-        hipLaunchKernelGGL(collate_kernel<false>, dim3(grid), dim3(kCollateBlock), 0, s, w->d_token_offsets,
-                           w->d_tokens, w->num_samples, d_emit_order, num_slots, d_slot_rows, d_slot_maxlen,
-                           d_slot_row_off, d_slot_tile_off, pad_id, out_capacity_elems, d_input_ids, d_labels,
-                           d_attention_mask, d_position_ids, err);
+    int64_t* row_ts = ws_at<int64_t>(d_ws, L.row_ts);
+    int32_t* row_len = ws_at<int32_t>(d_ws, L.row_len);
+    hipLaunchKernelGGL(row_info_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock), 0, s,
+                       w->d_token_offsets, n, d_emit_order, d_slot_row_off, num_slots, row_ts, row_len, err);
+    ODB_LAUNCHED();
+    Plan p{d_slot_tile_off, d_slot_maxlen, d_slot_rows, d_slot_row_off, row_ts, row_len, w->d_tokens,
+           w->d_token_offsets, num_slots, n, 0, err};
+    // one resident wave of blocks; runs are dealt round robin over them
+    static thread_local int resident = 0;
+    if (resident <= 0) {
+        int b = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, collate_kernel, kCollateBlock, 0) != hipSuccess || b < 1)
+            b = 4;
+        resident = b;
+    }
+    const unsigned grid = (unsigned)(num_cus() * resident);
+    hipLaunchKernelGGL(collate_kernel, dim3(grid), dim3(kCollateBlock), 0, s, p, pad_id, out_capacity_elems,
+                       d_input_ids, d_labels, d_attention_mask, d_position_ids);
     ODB_LAUNCHED();
     return ODB_OK;
 }

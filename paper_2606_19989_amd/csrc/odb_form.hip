@@ -55,15 +55,28 @@ __global__ void __launch_bounds__(kBlock) lengths_kernel(const int64_t* __restri
         lmin = (uint32_t)l < lmin ? (uint32_t)l : lmin;
         lmax = (uint32_t)l > lmax ? (uint32_t)l : lmax;
     }
+    // one pair of atomics per block: lanes -> waves (shuffles) -> block (LDS)
+    __shared__ uint32_t s_min[kBlock / kWave], s_max[kBlock / kWave];
 #pragma unroll
     for (int d = kWave / 2; d > 0; d >>= 1) {
         uint32_t a = __shfl_xor(lmin, d, kWave), b = __shfl_xor(lmax, d, kWave);
         lmin = a < lmin ? a : lmin;
         lmax = b > lmax ? b : lmax;
     }
-    if ((threadIdx.x & (kWave - 1)) == 0 && lmax > 0) {
-        atomicMin(&st->min_len, lmin);
-        atomicMax(&st->max_len, lmax);
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        s_min[threadIdx.x / kWave] = lmin;
+        s_max[threadIdx.x / kWave] = lmax;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int i = 1; i < kBlock / kWave; ++i) {
+            lmin = s_min[i] < lmin ? s_min[i] : lmin;
+            lmax = s_max[i] > lmax ? s_max[i] : lmax;
+        }
+        if (lmax > 0) {
+            atomicMin(&st->min_len, lmin);
+            atomicMax(&st->max_len, lmax);
+        }
     }
     if (bad != LLONG_MAX) {
         atomicOr(&st->err, kErrLength);
@@ -232,6 +245,8 @@ __global__ void __launch_bounds__(kBlock) links_kernel(const int32_t* __restrict
                                                        const RankState* __restrict__ ranks, int W, int64_t n,
                                                        int64_t budget, int32_t* __restrict__ jmp,
                                                        uint8_t* __restrict__ marks) {
+    __shared__ int64_t s_off[kLdsRanks + 1];
+    off = stage_ranks(off, W, s_off);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p <= n; p += stride) {
         if (p == n) {
@@ -304,6 +319,8 @@ __global__ void __launch_bounds__(kBlock) gidx_kernel(const uint8_t* __restrict_
                                                       const int64_t* __restrict__ off,
                                                       const RankState* __restrict__ ranks, int W, int64_t n,
                                                       int32_t* __restrict__ gidx, int32_t* __restrict__ gstart) {
+    __shared__ int64_t s_off[kLdsRanks + 1];
+    off = stage_ranks(off, W, s_off);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
         const int r = rank_of(off, W, p);

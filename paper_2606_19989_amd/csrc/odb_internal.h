@@ -98,6 +98,7 @@ struct DevInfo {
     int64_t bad_views;
     int64_t missing_ids;
     int64_t duplicate_ids;
+    int64_t distinct_views;   // views marked at least once (bitset pass)
     double pad_fraction;
 };
 
@@ -109,7 +110,7 @@ struct Layout {
     size_t jmp0, jmp1, marks, incl;
     size_t gstart, gsize, gmax, gtok, cs, ov_slot, ov_lo, kept;
     size_t srows, smax, stok, steps;
-    size_t buf_ids0, buf_ids1, buf_len0, buf_len1, gidx, stage, cover;
+    size_t buf_ids0, buf_ids1, buf_len0, buf_len1, gidx, stage, cover, row_ts, row_len;
     size_t info;
     size_t total;
     int64_t num_sort_blocks;
@@ -160,6 +161,17 @@ __device__ __forceinline__ int rank_of(const int64_t* off, int W, int64_t p) {
         if (off[mid] <= p) lo = mid; else hi = mid;
     }
     return lo;
+}
+
+// Rank offsets staged in LDS for kernels that look up the rank of many positions;
+// windows with more ranks than fit read them from global memory instead.
+constexpr int kLdsRanks = 1024;
+
+__device__ __forceinline__ const int64_t* stage_ranks(const int64_t* off, int W, int64_t* s_off) {
+    if (W > kLdsRanks) return off;
+    for (int i = threadIdx.x; i <= W; i += blockDim.x) s_off[i] = off[i];
+    __syncthreads();
+    return s_off;
 }
 
 template <typename T>

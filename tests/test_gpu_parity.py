@@ -119,3 +119,44 @@ def test_workload_full_size(name):
     compare_collate_sampled(w, outs, ref)
     collate_properties(outs, ref)
     log("  compared")
+    del pipe, outs
+    import torch
+    torch.cuda.empty_cache()
+
+
+def _numpy_coverage(ids, n, identity=None, nid=0):
+    cnt = np.bincount(ids, minlength=n)
+    bad = int((cnt != 1).sum())
+    if identity is None:
+        return bad, int((cnt == 0).sum()), int(np.maximum(cnt - 1, 0).sum())
+    icnt = np.bincount(identity[ids], minlength=nid)
+    return bad, int((icnt == 0).sum()), int(np.maximum(icnt - 1, 0).sum())
+
+
+@pytest.mark.parametrize("case", ["permutation", "duplicates", "missing_and_dup", "identity_map"])
+def test_check_coverage_entry_point(case):
+    import torch
+    import paper_2606_19989_amd as odb
+
+    rng = np.random.default_rng(21)
+    n = 100_003
+    w = win([rng.integers(1, 50, 60_000), rng.integers(1, 50, n - 60_000)], 4096)
+    ids = rng.permutation(n).astype(np.int32)
+    identity, nid = None, 0
+    if case == "duplicates":
+        ids[5] = ids[6]
+    elif case == "missing_and_dup":
+        ids[:100] = ids[100:200]
+    elif case == "identity_map":
+        nid = 70_000
+        identity = np.concatenate([np.arange(nid), rng.integers(0, nid, n - nid)]).astype(np.int64)
+        w.identity, w.num_identities = identity, nid
+    tok_off, toks, ident = synth.device_tensors(w, "cuda")
+    dwin = odb.DeviceWindow(w.rank_off, tok_off, toks, ident, nid)
+    ws = torch.empty(odb.odb_workspace_size(dwin), dtype=torch.uint8, device="cuda")
+    emitted = torch.from_numpy(ids[:70_000].copy()).cuda()
+    left = torch.from_numpy(ids[70_000:].copy()).cuda()
+    log(f"coverage case {case}")
+    info = odb.odb_check_coverage(dwin, emitted, emitted.numel(), left, left.numel(), ws)
+    bad, miss, dup = _numpy_coverage(ids.astype(np.int64), n, identity, nid)
+    assert (info["bad_views"], info["missing_ids"], info["duplicate_ids"]) == (bad, miss, dup)

@@ -806,7 +806,23 @@ int run_coverage_exact(const odb_window_t* w, const Layout& L, void* ws, const i
 // and in `twice` if it was already set.  missing = (hi - lo) - |once|, views listed
 // more than once = |twice|, extra listings = dup.  An id of another rank in these lists
 // is an internal error.
-__global__ void __launch_bounds__(kBlock) coverage_lds_kernel(
+constexpr int kCovBlock = 1024;
+constexpr int kCovUnroll = 8;
+
+template <typename T>
+__device__ __forceinline__ T cov_block_sum(T v) {
+    __shared__ T part[kCovBlock / kWave];
+    v = wave_sum(v);
+    if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = v;
+    __syncthreads();
+    T t = 0;
+#pragma unroll
+    for (int i = 0; i < kCovBlock / kWave; ++i) t += part[i];
+    __syncthreads();
+    return t;
+}
+
+__global__ void __launch_bounds__(kCovBlock) coverage_lds_kernel(
     const int64_t* __restrict__ off, int W, const int64_t* __restrict__ chunk_first, int64_t C,
     const int32_t* __restrict__ emit, const int64_t* __restrict__ row_off, int64_t S,
     const int32_t* __restrict__ left, const int64_t* __restrict__ loff, int want_ids, DevInfo* info,
@@ -821,7 +837,7 @@ __global__ void __launch_bounds__(kBlock) coverage_lds_kernel(
     const int64_t base = off[r], end = off[r + 1];
     const int64_t lo = base + j * C;
     const int64_t hi = lo + C < end ? lo + C : end;
-    for (int64_t i = threadIdx.x; i < words; i += kBlock) {
+    for (int64_t i = threadIdx.x; i < words; i += kCovBlock) {
         once[i] = 0;
         twice[i] = 0;
     }
@@ -830,34 +846,46 @@ __global__ void __launch_bounds__(kBlock) coverage_lds_kernel(
     const int32_t* lists[2] = {emit, left};
     const int64_t from[2] = {row_off[(int64_t)r * S], loff[r]};
     const int64_t to[2] = {row_off[(int64_t)(r + 1) * S], loff[r + 1]};
+#pragma unroll
     for (int li = 0; li < 2; ++li) {
         const int32_t* ids = lists[li];
-        for (int64_t i = from[li] + threadIdx.x; i < to[li]; i += kBlock) {
-            const int64_t v = ids[i];
-            if (v < base || v >= end) {
-                foreign += j == 0 ? 1 : 0;
-                continue;
+        for (int64_t i0 = from[li] + threadIdx.x; i0 < to[li]; i0 += (int64_t)kCovBlock * kCovUnroll) {
+            int32_t v[kCovUnroll];
+#pragma unroll
+            for (int u = 0; u < kCovUnroll; ++u) {
+                const int64_t i = i0 + (int64_t)u * kCovBlock;
+                v[u] = i < to[li] ? ids[i] : -1;
             }
-            if (v < lo || v >= hi) continue;
-            const uint32_t bit = 1u << ((v - lo) & 31);
-            const int64_t wd = (v - lo) >> 5;
-            if (atomicOr(&once[wd], bit) & bit) {
-                atomicOr(&twice[wd], bit);
-                dup += 1;
+#pragma unroll
+            for (int u = 0; u < kCovUnroll; ++u) {
+                const int64_t i = i0 + (int64_t)u * kCovBlock;
+                if (i >= to[li]) continue;
+                const int64_t x = v[u];
+                if (x < base || x >= end) {
+                    foreign += j == 0 ? 1 : 0;
+                    continue;
+                }
+                if (x < lo || x >= hi) continue;
+                const uint32_t bit = 1u << ((x - lo) & 31);
+                const int64_t wd = (x - lo) >> 5;
+                if (atomicOr(&once[wd], bit) & bit) {
+                    atomicOr(&twice[wd], bit);
+                    dup += 1;
+                }
             }
         }
     }
     __syncthreads();
     int64_t distinct = 0, multi = 0;
     const int64_t nw = (hi - lo + 31) / 32;
-    for (int64_t i = threadIdx.x; i < nw; i += kBlock) {
+    for (int64_t i = threadIdx.x; i < nw; i += kCovBlock) {
         distinct += __popc(once[i]);
         multi += __popc(twice[i]);
     }
-    distinct = block_sum(distinct);
-    multi = block_sum(multi);
-    dup = block_sum(dup);
-    foreign = block_sum(foreign);
+    distinct = cov_block_sum(distinct);
+    multi = cov_block_sum(multi);
+    dup = cov_block_sum(dup);
+    foreign = cov_block_sum(foreign);
     if (threadIdx.x == 0) {
         const int64_t missing = (hi - lo) - distinct;
         const int64_t bad = missing + multi;
@@ -901,14 +929,15 @@ int run_plan_coverage(const odb_window_t* w, const Layout& L, void* ws, const in
         const int64_t nr = w->rank_offsets[r + 1] - w->rank_offsets[r];
         max_nr = nr > max_nr ? nr : max_nr;
     }
-    int64_t C = ((max_nr / 4 + 4095) / 4096) * 4096;
+    // one chunk per rank up to 131072 views (two 16 KB bitsets); larger ranks are split
+    int64_t C = ((max_nr + 4095) / 4096) * 4096;
     C = C < 4096 ? 4096 : (C > 131072 ? 131072 : C);
     for (int r = 0; r < W; ++r) chunks += (w->rank_offsets[r + 1] - w->rank_offsets[r] + C - 1) / C;
     int64_t* chunk_first = ws_at<int64_t>(ws, L.tile_first);
     const int64_t* d_off = ws_at<int64_t>(ws, L.rank_off);
     hipLaunchKernelGGL(chunks_kernel, dim3(1), dim3(kBlock), 0, s, d_off, W, C, chunk_first);
     ODB_LAUNCHED();
-    hipLaunchKernelGGL(coverage_lds_kernel, dim3((unsigned)chunks), dim3(kBlock), (size_t)(C / 4), s, d_off, W,
+    hipLaunchKernelGGL(coverage_lds_kernel, dim3((unsigned)chunks), dim3(kCovBlock), (size_t)(C / 4), s, d_off, W,
                        (const int64_t*)chunk_first, C, emit, row_off, S, left, loff, w->d_identity ? 0 : 1,
                        ws_at<DevInfo>(ws, L.info), ws_at<DevStatus>(ws, L.status));
     ODB_LAUNCHED();

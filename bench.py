@@ -5,8 +5,10 @@ One step = grouping (odb_form_groups) + alignment with coverage check
 stream is already resident in HBM.  Prints one JSON line:
 
   value        emitted samples per second (whole job)
-  roofline     the collate kernel (dominant): algorithmic bytes per launch / average
-               launch duration from HIP events on the launch stream, vs 8 TB/s
+  roofline     the collate stage (dominant): algorithmic bytes per odb_collate call /
+               its average duration from HIP events on the launch stream, vs 8 TB/s;
+               traffic = HBM bytes per call from the committed rocprofv3 counters
+               (profiles/), reported only while the collate source is unchanged
   cpu_baseline the CPU oracle on a bounded sample of the same workload (first ranks of
                the window), single-threaded on this host
 """
@@ -30,6 +32,21 @@ def collate_alg_bytes(n, real_tokens, padded, slots):
     # 16 B written per padded element (4 int32 outputs), 4 B read per real token,
     # 8 B per token offset, 4 B per emitted id, 24 B of slot tables per slot
     return 16 * padded + 4 * real_tokens + 8 * (n + 1) + 4 * n + 24 * slots
+
+
+def measured_traffic(workload):
+    """HBM bytes per odb_collate call from the committed rocprofv3 counter record, if it
+    was taken on this workload with the collate source as it is now; otherwise None."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"collate_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    if hashlib.sha256(src).hexdigest() != rec["source_sha256"] or rec["workload"] != workload:
+        return None
+    return rec["traffic_bytes"]
 
 
 def cpu_baseline(w_full_name, tokens_dev, tok_off_full, ranks, pad_id=0):
@@ -66,6 +83,9 @@ def main():
     ap.add_argument("--workload", default="ln480_w64x262144")
     ap.add_argument("--cpu-ranks", type=int, default=4, help="ranks of the window the CPU oracle runs on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="GIB",
+                    help="before the steps, run one plain device copy of GIB GiB (int32 -> int32) as a "
+                         "known-size reference for hardware byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the simulated ranks of a window are "
@@ -89,6 +109,16 @@ def main():
     pipe = odb.Pipeline(win, w.budget, mode=w.mode, quota=w.quota, pad_id=0)
     log(f"[bench] inputs resident: {(tok_off.numel() * 8 + tokens.numel() * 4) / 1e9:.1f} GB")
 
+    if args.calibrate_copy > 0:
+        m = int(args.calibrate_copy * (1 << 30)) // 4
+        src = torch.ones(m, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy: {m * 4} bytes read, {m * 4} bytes written")
+        del src, dst
+        torch.cuda.empty_cache()
     for i in range(args.warmup):
         pipe.run()
         torch.cuda.synchronize()
@@ -150,12 +180,12 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "collate_kernel",
+            "kernel": "odb_collate (row_info_kernel + collate_kernel)",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": None,
+            "traffic": measured_traffic(wl.name),
             "alg_bytes_per_launch": alg,
             "avg_launch_ms": collate_ms,
         },

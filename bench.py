@@ -9,8 +9,8 @@ stream is already resident in HBM.  Prints one JSON line:
                its average duration from HIP events on the launch stream, vs 8 TB/s;
                traffic = HBM bytes per call from the committed rocprofv3 counters
                (profiles/), reported only while the collate source is unchanged
-  cpu_baseline the CPU oracle on a bounded sample of the same workload (first ranks of
-               the window), single-threaded on this host
+  cpu_baseline the CPU oracle on a bounded sample of the same workload (consecutive
+               4-rank groups of the window, at least 10 s), single-threaded on this host
 """
 import argparse
 import json
@@ -49,29 +49,42 @@ def measured_traffic(workload):
     return rec["traffic_bytes"]
 
 
-def cpu_baseline(w_full_name, tokens_dev, tok_off_full, ranks, pad_id=0):
+def cpu_baseline(workload, tokens_dev, group=4, min_seconds=10.0, pad_id=0):
+    """The oracle (plan + full collate), single-threaded, on consecutive groups of
+    `group` ranks of the same window until at least `min_seconds` of CPU work."""
     import numpy as np
 
     import oracle
     import synth
 
-    wl = synth.WORKLOADS[w_full_name]
-    w = wl.window(ranks=ranks)
-    total = w.total_tokens
-    tokens = tokens_dev[:total].cpu().numpy()          # same generator output the GPU read
-    assert np.array_equal(w.tok_off, tok_off_full[:w.n + 1])
-    t0 = time.perf_counter()
-    p = oracle.plan_window(w)
-    p.collate(w.tok_off, tokens, pad_id)
-    dt = time.perf_counter() - t0
+    wl = synth.WORKLOADS[workload]
+    per_rank = wl.draw(wl.seed)
+    done = samples = toks = 0
+    elapsed = 0.0
+    tok_base = 0
+    while done < wl.W and elapsed < min_seconds:
+        part = per_rank[done:done + group]
+        w = synth.window_from_ranks(f"{workload}_ranks{done}", part, wl.budget, mode=wl.mode,
+                                    quota=sum(len(x) for x in part) if wl.mode == "nonjoin" else 0)
+        # the same token values the GPU read for these ranks
+        tokens = tokens_dev[tok_base:tok_base + w.total_tokens].cpu().numpy()
+        t0 = time.perf_counter()
+        p = oracle.plan_window(w)
+        p.collate(w.tok_off, tokens, pad_id)
+        elapsed += time.perf_counter() - t0
+        samples += p.info["emitted_samples"]
+        toks += p.info["real_tokens"]
+        tok_base += w.total_tokens
+        done += len(part)
+        del tokens, p
     return {
-        "value": p.info["emitted_samples"] / dt,
+        "value": samples / elapsed,
         "unit": "samples/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": f"first {ranks} of {wl.W} ranks ({w.n} samples, {w.total_tokens} tokens) of the same window, "
-                  f"plan + full collate, {dt:.1f} s",
-        "tokens_per_s": p.info["real_tokens"] / dt,
+        "sample": f"ranks 0-{done - 1} of {wl.W} of the same window, {group} ranks per oracle window "
+                  f"({samples} samples, {toks} tokens), plan + full collate, {elapsed:.1f} s single-threaded",
+        "tokens_per_s": toks / elapsed,
     }
 
 
@@ -81,7 +94,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="ln480_w64x262144")
-    ap.add_argument("--cpu-ranks", type=int, default=4, help="ranks of the window the CPU oracle runs on")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum CPU time of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="GIB",
                     help="before the steps, run one plain device copy of GIB GiB (int32 -> int32) as a "
@@ -191,8 +204,8 @@ def main():
         },
     }
     if not args.no_cpu_baseline:
-        log(f"[bench] CPU oracle on the first {args.cpu_ranks} ranks ...")
-        result["cpu_baseline"] = cpu_baseline(wl.name, tokens, w.tok_off, args.cpu_ranks)
+        log(f"[bench] CPU oracle on groups of ranks for >= {args.cpu_seconds:.0f} s ...")
+        result["cpu_baseline"] = cpu_baseline(wl.name, tokens, min_seconds=args.cpu_seconds)
         log("[bench] CPU oracle done")
     print(json.dumps(result), flush=True)
 

@@ -19,8 +19,9 @@
 // three steps in flight per lane: while it computes and stores step s it has the tokens
 // of step s+1 and the row records of step s+2 in flight, all issued before step s's
 // stores.  Each wait then targets a load issued before the previous step's stores, and
-// stores drain in the background.  Token and row loads use clamped addresses, so a load
-// never has to be skipped to stay inside its array.
+// stores drain in the background.  The loop is unrolled three times so the stages rotate
+// by name instead of by register copies (a copy would wait for the load), and loads use
+// clamped addresses so none is ever skipped.
 //
 // A group's cursor (slot, row, column) advances with the step sequence: inside a tile it
 // moves by arithmetic, across tiles by a galloping search over the tile offsets.  When a
@@ -210,6 +211,57 @@ __device__ __forceinline__ int64_t next_step(int64_t s, int64_t nsteps, int64_t 
     return r2 < nruns ? r2 * kRunSteps : -1;
 }
 
+// One pipeline stage of a lane: where its 4 elements are, their row, their tokens.
+struct Stage {
+    Cursor c;
+    RowRec r;
+    v4i t;
+};
+
+// Values of the 4 elements at e (the stage's position); elements at or past `total` are
+// left unspecified (the caller does not store them).
+__device__ __forceinline__ void stage_values(const Stage& a, int64_t e, int64_t total, const Plan& p, int vec_ok,
+                                             int32_t pad_id, v4i& vid, v4i& vlab, v4i& vmsk, v4i& vpos) {
+    const Cursor& c = a.c;
+    const RowRec& r = a.r;
+    const int32_t nreal = r.l - c.col;
+    if (vec_ok && c.col + (kVec - 1) < c.ml && (nreal <= 0 || r.ts + c.col + kVec <= p.tok_end)) {
+        // the 4 elements sit in one row and the vector load covered them
+#pragma unroll
+        for (int i = 0; i < kVec; ++i) {
+            const bool real = i < nreal;
+            vid[i] = real ? a.t[i] : pad_id;
+            vlab[i] = real ? a.t[i] : -100;
+            vmsk[i] = real ? 1 : 0;
+            vpos[i] = real ? c.col + i : 0;
+        }
+    } else {
+        // a row or tile edge inside the 4 elements: step element by element
+        Cursor d = c;
+        RowRec dr = r;
+#pragma unroll
+        for (int i = 0; i < kVec; ++i) {
+            const int64_t ee = e + i;
+            if (i > 0 && ee < total) {
+                if (ee >= d.t1) {
+                    enter_slot(d, advance_slot(p.tile_off, p.num_slots, d.k, ee), ee, p);
+                    dr = load_row(d, p);
+                } else if (++d.col == d.ml) {
+                    d.col = 0;
+                    d.ri += 1;
+                    dr = load_row(d, p);
+                }
+            }
+            const bool real = d.col < dr.l;
+            const int32_t tok = real ? p.tokens[dr.ts + d.col] : 0;
+            vid[i] = real ? tok : pad_id;
+            vlab[i] = real ? tok : -100;
+            vmsk[i] = real ? 1 : 0;
+            vpos[i] = real ? d.col : 0;
+        }
+    }
+}
+
 __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t pad_id, int64_t capacity,
                                                                 int32_t* __restrict__ o_ids,
                                                                 int32_t* __restrict__ o_lab,
@@ -226,117 +278,72 @@ __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t 
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int64_t lane_off = (int64_t)wave * kWaveStep + (int64_t)lane * kVec;
+    // a lane's elements may lie past the end only in the last step; clamp its position
+    // so every stage has a valid cursor (the last step stores with bounds checks)
+    auto elem = [&](int64_t s) {
+        const int64_t e = s * kBlockStep + lane_off;
+        return e < total ? e : total - 1;
+    };
 
-    // pipeline registers: step s0 (compute), s1 (tokens in flight), s2 (rows in flight)
+    // pipeline: step s0 is stored from stage a, s1's tokens load into b, s2's rows into c
     int64_t s0 = (int64_t)blockIdx.x * kRunSteps;
     int64_t s1 = next_step(s0, nsteps, nruns);
     int64_t s2 = s1 >= 0 ? next_step(s1, nsteps, nruns) : -1;
-    Cursor c0[kGroups], c1[kGroups], c2[kGroups];
-    RowRec r0[kGroups], r1[kGroups], r2[kGroups];
-    v4i t0[kGroups], t1[kGroups];
-
-    // prologue: locate step s0 from slot 0, step s1 from s0
-#pragma unroll
-    for (int g = 0; g < kGroups; ++g) {
-        const int64_t e = s0 * kBlockStep + lane_off + g * kGroupSpan;
-        if (e < total) {
-            int64_t lo = 0, hi = p.num_slots;  // last slot with tile_off <= e
-            while (hi - lo > 1) {
-                const int64_t mid = lo + ((hi - lo) >> 1);
-                if (p.tile_off[mid] <= e) lo = mid; else hi = mid;
-            }
-            enter_slot(c0[g], lo, e, p);
-            r0[g] = load_row(c0[g], p);
-            if (vec_ok) t0[g] = load_tokens(c0[g], r0[g], p);
-            const int64_t e1 = s1 * kBlockStep + lane_off + g * kGroupSpan;
-            if (s1 >= 0 && e1 < total) {
-                c1[g] = c0[g];
-                advance(c1[g], e1, e1 - e, p);
-                r1[g] = load_row(c1[g], p);
-            }
+    Stage X, Y, Z;
+    {
+        const int64_t e = elem(s0);
+        int64_t lo = 0, hi = p.num_slots;  // last slot with tile_off <= e
+        while (hi - lo > 1) {
+            const int64_t mid = lo + ((hi - lo) >> 1);
+            if (p.tile_off[mid] <= e) lo = mid; else hi = mid;
         }
+        enter_slot(X.c, lo, e, p);
+        X.r = load_row(X.c, p);
+        if (vec_ok) X.t = load_tokens(X.c, X.r, p);
+        Y.c = X.c;
+        if (s1 >= 0) advance(Y.c, elem(s1), elem(s1) - e, p);
+        Y.r = load_row(Y.c, p);
     }
 
-    while (s0 >= 0) {
-        // A: cursors of step s2 and their row records
-#pragma unroll
-        for (int g = 0; g < kGroups; ++g) {
-            const int64_t e1 = s1 * kBlockStep + lane_off + g * kGroupSpan;
-            const int64_t e2 = s2 * kBlockStep + lane_off + g * kGroupSpan;
-            if (s2 >= 0 && e2 < total) {
-                c2[g] = c1[g];
-                advance(c2[g], e2, e2 - e1, p);
-                r2[g] = load_row(c2[g], p);
-            }
-        }
-        // B: tokens of step s1
-#pragma unroll
-        for (int g = 0; g < kGroups; ++g) {
-            const int64_t e1 = s1 * kBlockStep + lane_off + g * kGroupSpan;
-            if (vec_ok && s1 >= 0 && e1 < total) t1[g] = load_tokens(c1[g], r1[g], p);
-        }
-        // C: values and stores of step s0
-#pragma unroll
-        for (int g = 0; g < kGroups; ++g) {
-            const int64_t e = s0 * kBlockStep + lane_off + g * kGroupSpan;
-            if (e >= total) continue;
-            const Cursor& c = c0[g];
-            const RowRec& r = r0[g];
-            const int32_t nreal = r.l - c.col;
-            v4i vid, vlab, vmsk, vpos;
-            if (vec_ok && c.col + (kVec - 1) < c.ml && (nreal <= 0 || r.ts + c.col + kVec <= p.tok_end)) {
-                // the 4 elements sit in one row and the vector load covered them
-#pragma unroll
-                for (int i = 0; i < kVec; ++i) {
-                    const bool real = i < nreal;
-                    vid[i] = real ? t0[g][i] : pad_id;
-                    vlab[i] = real ? t0[g][i] : -100;
-                    vmsk[i] = real ? 1 : 0;
-                    vpos[i] = real ? c.col + i : 0;
-                }
-            } else {
-                // a row or tile edge inside the 4 elements: step element by element
-                Cursor d = c;
-                RowRec dr = r;
-#pragma unroll
-                for (int i = 0; i < kVec; ++i) {
-                    const int64_t ee = e + i;
-                    if (i > 0 && ee < total) {
-                        if (ee >= d.t1) {
-                            enter_slot(d, advance_slot(p.tile_off, p.num_slots, d.k, ee), ee, p);
-                            dr = load_row(d, p);
-                        } else if (++d.col == d.ml) {
-                            d.col = 0;
-                            d.ri += 1;
-                            dr = load_row(d, p);
-                        }
-                    }
-                    const bool real = d.col < dr.l;
-                    const int32_t tok = real ? p.tokens[dr.ts + d.col] : 0;
-                    vid[i] = real ? tok : pad_id;
-                    vlab[i] = real ? tok : -100;
-                    vmsk[i] = real ? 1 : 0;
-                    vpos[i] = real ? d.col : 0;
-                }
-            }
-            store4(o_ids, e, vid, total);
-            store4(o_lab, e, vlab, total);
-            store4(o_msk, e, vmsk, total);
-            store4(o_pos, e, vpos, total);
-        }
-        // rotate the pipeline
-#pragma unroll
-        for (int g = 0; g < kGroups; ++g) {
-            c0[g] = c1[g];
-            r0[g] = r1[g];
-            t0[g] = t1[g];
-            c1[g] = c2[g];
-            r1[g] = r2[g];
-        }
-        s0 = s1;
-        s1 = s2;
-        s2 = s2 >= 0 ? next_step(s2, nsteps, nruns) : -1;
+    // Every load below is issued whether or not its step exists (a missing step reloads
+    // its predecessor's row and tokens), and full steps store without conditions, so the
+    // number of memory operations between a load and its use is the same on every path.
+#define ODB_COLLATE_STEP(A, B, C)                                                             \
+    {                                                                                         \
+        if (s0 < 0) break;                                                                    \
+        C.c = B.c;                                                                            \
+        if (s2 >= 0) advance(C.c, elem(s2), elem(s2) - elem(s1), p);                          \
+        C.r = load_row(C.c, p);                                                               \
+        if (vec_ok) B.t = load_tokens(B.c, B.r, p);                                           \
+        const int64_t e = s0 * kBlockStep + lane_off;                                         \
+        v4i vid, vlab, vmsk, vpos;                                                            \
+        stage_values(A, e, total, p, vec_ok, pad_id, vid, vlab, vmsk, vpos);                  \
+        if ((s0 + 1) * kBlockStep <= total) {                                                 \
+            __builtin_nontemporal_store(vid, reinterpret_cast<v4i*>(o_ids + e));              \
+            __builtin_nontemporal_store(vlab, reinterpret_cast<v4i*>(o_lab + e));             \
+            __builtin_nontemporal_store(vmsk, reinterpret_cast<v4i*>(o_msk + e));             \
+            __builtin_nontemporal_store(vpos, reinterpret_cast<v4i*>(o_pos + e));             \
+        } else {                                                                              \
+            _Pragma("unroll") for (int i = 0; i < kVec; ++i) {                                \
+                if (e + i < total) {                                                          \
+                    o_ids[e + i] = vid[i];                                                    \
+                    o_lab[e + i] = vlab[i];                                                   \
+                    o_msk[e + i] = vmsk[i];                                                   \
+                    o_pos[e + i] = vpos[i];                                                   \
+                }                                                                             \
+            }                                                                                 \
+        }                                                                                     \
+        s0 = s1;                                                                              \
+        s1 = s2;                                                                              \
+        s2 = s2 >= 0 ? next_step(s2, nsteps, nruns) : -1;                                     \
     }
+    // unrolled three times so that no stage register is copied while its load is in flight
+    for (;;) {
+        ODB_COLLATE_STEP(X, Y, Z)
+        ODB_COLLATE_STEP(Y, Z, X)
+        ODB_COLLATE_STEP(Z, X, Y)
+    }
+#undef ODB_COLLATE_STEP
 }
 
 }  // namespace

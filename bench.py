@@ -8,7 +8,8 @@ stream is already resident in HBM.  Prints one JSON line:
   roofline     the collate stage (dominant): algorithmic bytes per odb_collate call /
                its average duration from HIP events on the launch stream, vs 8 TB/s;
                traffic = HBM bytes per call from the committed rocprofv3 counters
-               (profiles/), reported only while the collate source is unchanged
+               (profiles/), reported only while the collate source is unchanged;
+               copy_ceiling_gbs = a plain 4 GiB device copy, as a practical ceiling
   cpu_baseline the CPU oracle on a bounded sample of the same workload (consecutive
                4-rank groups of the window, at least 10 s), single-threaded on this host
 """
@@ -49,6 +50,39 @@ def measured_traffic(workload):
     return rec["traffic_bytes"]
 
 
+def host_cpu():
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0))
+
+
+def copy_ceiling(dev, gib=4.0, reps=5):
+    """Plain device-to-device copy (torch copy_) of `gib` GiB: bytes read + written / time."""
+    import numpy as np
+    import torch
+
+    m = int(gib * (1 << 30)) // 4
+    src = torch.ones(m, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in ev:
+        a.record()
+        dst.copy_(src)
+        b.record()
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    del src, dst
+    torch.cuda.empty_cache()
+    return 8 * m / (ms * 1e-3) / 1e9
+
+
 def cpu_baseline(workload, tokens_dev, group=4, min_seconds=10.0, pad_id=0):
     """The oracle (plan + full collate), single-threaded, on consecutive groups of
     `group` ranks of the same window until at least `min_seconds` of CPU work."""
@@ -77,10 +111,12 @@ def cpu_baseline(workload, tokens_dev, group=4, min_seconds=10.0, pad_id=0):
         tok_base += w.total_tokens
         done += len(part)
         del tokens, p
+    model, nproc = host_cpu()
     return {
         "value": samples / elapsed,
         "unit": "samples/s",
         "cores": 1,
+        "host": f"{model}, {nproc} cores available",
         "kind": "oracle",
         "sample": f"ranks 0-{done - 1} of {wl.W} of the same window, {group} ranks per oracle window "
                   f"({samples} samples, {toks} tokens), plan + full collate, {elapsed:.1f} s single-threaded",
@@ -153,8 +189,12 @@ def main():
     t1 = time.perf_counter()
     log(f"[bench] timed {args.steps} steps")
     sec_per_step = (t1 - t0) / args.steps
-    collate_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    collate_all = [a.elapsed_time(b) for a, b in ev]
+    collate_ms = float(np.mean(collate_all))
     assert pipe.info["steps"] == info["steps"] and pipe.info["padded_elems"] == info["padded_elems"]
+
+    copy_gbs = copy_ceiling(dev)
+    log(f"[bench] plain 4 GiB device copy: {copy_gbs:.0f} GB/s")
 
     n = w.n
     K = pipe.num_slots
@@ -201,6 +241,8 @@ def main():
             "traffic": measured_traffic(wl.name),
             "alg_bytes_per_launch": alg,
             "avg_launch_ms": collate_ms,
+            "median_launch_ms": float(np.median(collate_all)),
+            "copy_ceiling_gbs": copy_gbs,
         },
     }
     if not args.no_cpu_baseline:

@@ -77,6 +77,8 @@ def _load():
         lib.oracle_slots.argtypes = [P, P, P, P, P, P]
         lib.oracle_emit.argtypes = [P, P, P, P]
         lib.oracle_collate.argtypes = [P, P, P, ctypes.c_int32, P, P, P, P]
+        lib.oracle_collate_rank.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int32, P, P, P, P]
+        lib.oracle_collate_rank.restype = ctypes.c_int
         lib.oracle_round_targets.argtypes = [P, P]
         _lib = lib
     return _lib
@@ -138,6 +140,23 @@ class Plan:
         tokens = np.ascontiguousarray(tokens, dtype=np.int32)
         lib.oracle_collate(ctypes.c_void_p(self._handle), _ptr(tok_off), _ptr(tokens), int(pad_id),
                            *[_ptr(o) for o in outs])
+        return tuple(outs)
+
+    def collate_rank(self, r: int, tok_off: np.ndarray, rank_tokens: np.ndarray, pad_id: int = 0):
+        """Rank r's tiles only: four int32 arrays covering output positions
+        [slot_tile_off[r * steps], slot_tile_off[(r + 1) * steps]).  ``rank_tokens`` holds
+        the CSR positions owned by rank r's samples (from its first sample's offset)."""
+        lib = _load()
+        if not 0 <= r < self.W:
+            raise OracleError(f"rank {r} out of range")
+        S = self.steps
+        P = int(self.slot_tile_off[(r + 1) * S] - self.slot_tile_off[r * S])
+        outs = [np.empty(P, dtype=np.int32) for _ in range(4)]
+        tok_off = np.ascontiguousarray(tok_off, dtype=np.int64)
+        rank_tokens = np.ascontiguousarray(rank_tokens, dtype=np.int32)
+        if lib.oracle_collate_rank(ctypes.c_void_p(self._handle), int(r), _ptr(tok_off), _ptr(rank_tokens),
+                                   int(pad_id), *[_ptr(o) for o in outs]) != 0:
+            raise OracleError(f"rank {r} out of range")
         return tuple(outs)
 
 

@@ -448,13 +448,14 @@ void oracle_emit(void* h, int32_t* emit_order, int32_t* leftover, int64_t* lefto
 // Collate (Sec. 2.1): every aligned group becomes a [rows, max_len] tile padded on the
 // right.  reading (values): input_ids = labels = token, attention_mask = 1,
 // position_ids = column for real tokens; pad_id, -100, 0, 0 for padding.  Tiles are
-// packed back to back in rank-major slot order.
-void oracle_collate(void* h, const int64_t* tok_off, const int32_t* tokens, int32_t pad_id,
-                    int32_t* input_ids, int32_t* labels, int32_t* attention_mask,
-                    int32_t* position_ids) {
-    const Result& R = *static_cast<Result*>(h);
+// packed back to back in rank-major slot order.  Writes the tiles of ranks
+// [r_begin, r_end) from element 0 of the outputs; tokens[k - tok_base] is the token at
+// CSR position k.
+static void collate_ranks(const Result& R, int32_t r_begin, int32_t r_end, const int64_t* tok_off,
+                          const int32_t* tokens, int64_t tok_base, int32_t pad_id, int32_t* input_ids,
+                          int32_t* labels, int32_t* attention_mask, int32_t* position_ids) {
     int64_t e = 0;
-    for (int32_t r = 0; r < R.W; ++r)
+    for (int32_t r = r_begin; r < r_end; ++r)
         for (const Group& g : R.slots[(size_t)r]) {
             int64_t mx = 0;
             for (int32_t x : g) mx = std::max(mx, R.len[(size_t)x]);
@@ -462,7 +463,7 @@ void oracle_collate(void* h, const int64_t* tok_off, const int32_t* tokens, int3
                 int64_t l = R.len[(size_t)x];
                 for (int64_t c = 0; c < mx; ++c, ++e) {
                     if (c < l) {
-                        int32_t t = tokens[tok_off[x] + c];
+                        int32_t t = tokens[tok_off[x] + c - tok_base];
                         input_ids[e] = t;
                         labels[e] = t;
                         attention_mask[e] = 1;
@@ -476,6 +477,27 @@ void oracle_collate(void* h, const int64_t* tok_off, const int32_t* tokens, int3
                 }
             }
         }
+}
+
+// The whole window: outputs hold info.padded_elems elements.
+void oracle_collate(void* h, const int64_t* tok_off, const int32_t* tokens, int32_t pad_id,
+                    int32_t* input_ids, int32_t* labels, int32_t* attention_mask,
+                    int32_t* position_ids) {
+    const Result& R = *static_cast<Result*>(h);
+    collate_ranks(R, 0, R.W, tok_off, tokens, 0, pad_id, input_ids, labels, attention_mask, position_ids);
+}
+
+// One rank's tiles (its slots r * steps ... (r + 1) * steps - 1).  tokens holds the CSR
+// positions [tok_off[rank_off[r]], tok_off[rank_off[r + 1]]) only, which is all that
+// rank's samples own.  Returns 0, or -1 for a rank out of range.
+int oracle_collate_rank(void* h, int32_t r, const int64_t* tok_off, const int32_t* tokens, int32_t pad_id,
+                        int32_t* input_ids, int32_t* labels, int32_t* attention_mask,
+                        int32_t* position_ids) {
+    const Result& R = *static_cast<Result*>(h);
+    if (r < 0 || r >= R.W) return -1;
+    const int64_t base = tok_off[R.rank_off[(size_t)r]];
+    collate_ranks(R, r, r + 1, tok_off, tokens, base, pad_id, input_ids, labels, attention_mask, position_ids);
+    return 0;
 }
 
 }  // extern "C"

@@ -93,6 +93,30 @@ def compare_collate_sampled(w, outs, ref, pad_id=0, samples=200000, seed=0):
             raise AssertionError(f"{name}: {len(bad)} sampled mismatches, first at {idx[bad[0]]}")
 
 
+def compare_collate_by_rank(w, outs, ref, tokens_dev, pad_id=0, check_tokens=100_000, seed=0):
+    """Every element of the four outputs, one rank at a time: the oracle collates rank r's
+    tiles from that rank's token range and the GPU outputs' slice is copied back.  The
+    token range comes from the device token stream (written by the seeded generator, not
+    by the library); a sample of it is checked against the generator first."""
+    rng = np.random.default_rng(seed)
+    S = ref.steps
+    for r in range(w.W):
+        a, b = int(w.tok_off[w.rank_off[r]]), int(w.tok_off[w.rank_off[r + 1]])
+        toks = tokens_dev[a:b].cpu().numpy()
+        if b > a:
+            k = np.unique(np.concatenate([rng.integers(a, b, size=min(check_tokens, b - a)), [a, b - 1]]))
+            assert np.array_equal(toks[k - a], synth.token_ids(k).astype(np.int32)), f"token stream, rank {r}"
+        want = ref.collate_rank(r, w.tok_off, toks, pad_id)
+        lo, hi = int(ref.slot_tile_off[r * S]), int(ref.slot_tile_off[(r + 1) * S])
+        for name, g, e in zip(["input_ids", "labels", "attention_mask", "position_ids"], outs, want):
+            got = g[lo:hi].cpu().numpy()
+            if not np.array_equal(got, e):
+                bad = np.nonzero(got != e)[0]
+                raise AssertionError(f"{name}: rank {r}: {len(bad)} mismatches, first at {lo + bad[0]}: "
+                                     f"{got[bad[0]]} vs {e[bad[0]]}")
+        del toks, want
+
+
 def collate_properties(outs, ref, pad_id=0):
     """Whole-output properties that hold at any size."""
     import torch

@@ -9,8 +9,8 @@ import pytest
 
 import oracle
 import synth
-from _parity import (collate_properties, compare_collate_full, compare_collate_sampled, compare_plan, log,
-                     run_gpu)
+from _parity import (collate_properties, compare_collate_by_rank, compare_collate_full, compare_collate_sampled,
+                     compare_plan, log, run_gpu)
 
 pytestmark = pytest.mark.gpu
 
@@ -109,6 +109,7 @@ def test_workload_small_full():
 
 @pytest.mark.parametrize("name", ["text_w8x65536", "bimodal_w16x65536", "mm_w8x262144", "ln480_w64x262144"])
 def test_workload_full_size(name):
+    # the launch configuration the benchmark times; every output element is compared
     w = synth.WORKLOADS[name].window()
     log(f"workload {name}: n={w.n} tokens={w.total_tokens}")
     ref = oracle.plan_window(w)
@@ -116,9 +117,11 @@ def test_workload_full_size(name):
     pipe, outs = run_gpu(w)
     log("  gpu pipeline done")
     compare_plan(w, pipe, ref)
+    log("  plan equal")
     compare_collate_sampled(w, outs, ref)
     collate_properties(outs, ref)
-    log("  compared")
+    compare_collate_by_rank(w, outs, ref, pipe.win.tokens)
+    log("  every output element equal")
     del pipe, outs
     import torch
     torch.cuda.empty_cache()

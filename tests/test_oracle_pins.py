@@ -475,6 +475,29 @@ def test_collate_elements_agrees_with_full_collate():
         assert np.array_equal(f[idx], s)
 
 
+
+@pytest.mark.parametrize("mode", ["join", "nonjoin"])
+def test_collate_rank_is_the_rank_slice_of_full_collate(mode):
+    # per-rank collate (used to compare full-size windows rank by rank) reads only that
+    # rank's token range and reproduces exactly its slice of the whole-window collate
+    rng = np.random.default_rng(16)
+    per = [rng.integers(1, 300, size=int(k)) for k in (150, 0, 90, 1, 200)]
+    n = sum(len(x) for x in per)
+    w = win(per, 1200, mode=mode, quota=n // 3)
+    p = oracle.plan_window(w)
+    tokens = w.tokens_numpy()
+    full = p.collate(w.tok_off, tokens, 9)
+    S = p.steps
+    for r in range(w.W):
+        a, b = w.tok_off[w.rank_off[r]], w.tok_off[w.rank_off[r + 1]]
+        part = p.collate_rank(r, w.tok_off, tokens[a:b].copy(), 9)
+        lo, hi = p.slot_tile_off[r * S], p.slot_tile_off[(r + 1) * S]
+        for f, g in zip(full, part):
+            assert np.array_equal(f[lo:hi], g)
+    with pytest.raises(oracle.OracleError):
+        p.collate_rank(w.W, w.tok_off, tokens, 9)
+
+
 # ----------------------------------------------------------------------------- stats
 def test_stats_are_exact_sums():
     rng = np.random.default_rng(15)

@@ -26,13 +26,15 @@ _LIB = os.path.join(_HERE, "libodb_oracle.so")
 MODE_JOIN = 0
 MODE_NONJOIN = 1
 STOP_DRAINED, STOP_QUOTA, STOP_RANK_FINISHED = 0, 1, 2
+WEIGHT_SAMPLE, WEIGHT_TOKEN_APPROX, WEIGHT_TOKEN_EXACT = 0, 1, 2
 
 
 def build(force: bool = True) -> str:
     """Compile the oracle with g++ (always when ``force``)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp"
-        subprocess.check_call(["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-Wall", "-Wextra",
+        # -ffp-contract=off: every fp64 product and sum is rounded on its own, as written
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-ffp-contract=off", "-shared", "-fPIC", "-Wall", "-Wextra",
                                _SRC, "-o", tmp])
         os.replace(tmp, _LIB)
     return _LIB
@@ -54,6 +56,7 @@ class _Info(ctypes.Structure):
         ("duplicate_ids", ctypes.c_int64),
         ("bad_views", ctypes.c_int64),
         ("pad_fraction", ctypes.c_double),
+        ("second_gather_rounds", ctypes.c_int64),
     ]
 
 
@@ -80,6 +83,9 @@ def _load():
         lib.oracle_collate_rank.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int32, P, P, P, P]
         lib.oracle_collate_rank.restype = ctypes.c_int
         lib.oracle_round_targets.argtypes = [P, P]
+        lib.oracle_slots_approx.argtypes = [P, P]
+        lib.oracle_loss_weights.argtypes = [P, ctypes.c_int32, P, P, P]
+        lib.oracle_loss_weights.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -108,6 +114,7 @@ class Plan:
     slot_row_off: np.ndarray
     slot_tile_off: np.ndarray
     slot_tokens: np.ndarray
+    slot_tokens_approx: np.ndarray
     emit_order: np.ndarray
     leftover: np.ndarray
     leftover_off: np.ndarray
@@ -141,6 +148,18 @@ class Plan:
         lib.oracle_collate(ctypes.c_void_p(self._handle), _ptr(tok_off), _ptr(tokens), int(pad_id),
                            *[_ptr(o) for o in outs])
         return tuple(outs)
+
+    def loss_weights(self, mode: int = WEIGHT_TOKEN_EXACT):
+        """Loss-scaling weights of every slot (rank-major, like the slot tables) and the
+        per-step sums of real tokens and of samples over ranks (Eq. 2, App. B)."""
+        lib = _load()
+        K, S = self.num_slots, self.steps
+        wt = np.empty(K, np.float64)
+        st = np.empty(S, np.int64)
+        ss = np.empty(S, np.int64)
+        if lib.oracle_loss_weights(ctypes.c_void_p(self._handle), int(mode), _ptr(wt), _ptr(st), _ptr(ss)) != 0:
+            raise OracleError(f"unknown loss-weight mode {mode}")
+        return wt, st, ss
 
     def collate_rank(self, r: int, tok_off: np.ndarray, rank_tokens: np.ndarray, pad_id: int = 0):
         """Rank r's tiles only: four int32 arrays covering output positions
@@ -189,13 +208,15 @@ def plan(rank_off, tok_off, budget: int, mode: int = MODE_JOIN, quota: int = 0,
     to = np.empty(K + 1, np.int64)
     tk = np.empty(K, np.int64)
     lib.oracle_slots(ctypes.c_void_p(h), _ptr(rows), _ptr(mx), _ptr(ro), _ptr(to), _ptr(tk))
+    ta = np.empty(K, np.float64)
+    lib.oracle_slots_approx(ctypes.c_void_p(h), _ptr(ta))
     emit = np.empty(d["emitted_samples"], np.int32)
     left = np.empty(d["leftover_samples"], np.int32)
     loff = np.empty(W + 1, np.int64)
     lib.oracle_emit(ctypes.c_void_p(h), _ptr(emit), _ptr(left), _ptr(loff))
     rt = np.empty(d["rounds"], np.int64)
     lib.oracle_round_targets(ctypes.c_void_p(h), _ptr(rt))
-    return Plan(W, n, d, order, slen, gidx, G, rows, mx, ro, to, tk, emit, left, loff, rt, _handle=h)
+    return Plan(W, n, d, order, slen, gidx, G, rows, mx, ro, to, tk, ta, emit, left, loff, rt, _handle=h)
 
 
 def plan_window(w, **overrides) -> Plan:

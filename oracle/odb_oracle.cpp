@@ -17,11 +17,14 @@
 //   * collate = pad every group to its own max  Sec. 2.1 / Fig. 1 ("pad to l_max")
 //   * padding fraction                          throughput-decomposition definition (App. I)
 //   * identity coverage                         App. C (terminal identity coverage)
+//   * loss-scaling weights (sample, approximate  Eq. 2 (Sec. 2.3 "Loss scaling"), App. B,
+//     and exact token level), second-gather      and the loss-scaling ablation (App. I)
+//     predicate
 // Where the paper is silent the oracle takes the readings documented in the
 // repository's design notes (tie order, list order, trailing group, canonical
 // emission order, pad values); each is marked "reading" below.
 //
-// Build: g++ -O2 -std=c++17 -shared -fPIC odb_oracle.cpp -o libodb_oracle.so
+// Build: g++ -O2 -std=c++17 -ffp-contract=off -shared -fPIC odb_oracle.cpp -o libodb_oracle.so
 
 #include <algorithm>
 #include <cstdint>
@@ -55,6 +58,7 @@ struct Info {
     int64_t duplicate_ids;
     int64_t bad_views;
     double pad_fraction;
+    int64_t second_gather_rounds;   // rounds whose alignment changed some active rank's groups
 };
 
 struct Result {
@@ -66,6 +70,10 @@ struct Result {
     std::vector<int32_t> order, sorted_len, group_index, groups_per_rank;
     // aligned plan: slots[r][j] = members of rank r's j-th step in row order (empty = IDLE)
     std::vector<std::vector<Group>> slots;
+    // slots_approx[r][j]: approximate post-alignment token count of slot (r, j) for the
+    // approximate token-level loss weights (App. B): rows * mean length of the rank's
+    // buffer before that round's alignment; 0 for IDLE slots
+    std::vector<std::vector<double>> slots_approx;
     std::vector<std::vector<int32_t>> leftover;
     std::vector<int64_t> round_target;       // T of every alignment round (Eq. 3)
     Info info{};
@@ -227,6 +235,7 @@ bool run(Result& R, int32_t W, int64_t n, const int64_t* rank_off, const int64_t
     for (int32_t r = 0; r < W; ++r)
         for (int64_t i = rank_off[r]; i < rank_off[r + 1]; ++i) buf[(size_t)r].push_back((int32_t)i);
     R.slots.assign((size_t)W, {});
+    R.slots_approx.assign((size_t)W, {});
     std::vector<int64_t> pos((size_t)n, -1);
     Info& I = R.info;
     int64_t S = 0, emitted = 0;
@@ -266,6 +275,23 @@ bool run(Result& R, int32_t W, int64_t n, const int64_t* rank_off, const int64_t
         T = std::max<int64_t>(T, 1);
         R.round_target.push_back(T);
 
+        // App. B: what a rank can advertise before alignment is its buffer's sample and
+        // token counts; the approximate mode prices an adjusted group at its row count
+        // times the buffer's mean tokens per sample.  The exact mode needs post-alignment
+        // counts, i.e. a second exchange, unless alignment left every active rank's
+        // groups as they were (G_r = T for all r in A).
+        std::vector<double> mean_len((size_t)W, 0.0);
+        bool noop = true;
+        for (int32_t r = 0; r < W; ++r) {
+            const std::vector<int32_t>& b = buf[(size_t)r];
+            if (b.empty()) continue;
+            int64_t tok = 0;
+            for (int32_t x : b) tok += R.len[(size_t)x];
+            mean_len[(size_t)r] = (double)tok / (double)b.size();
+            if ((int64_t)list[(size_t)r].size() != T) noop = false;
+        }
+        if (!noop) I.second_gather_rounds += 1;
+
         // Algorithm 1 on every active rank.
         std::vector<std::vector<int32_t>> returned((size_t)W);
         for (int32_t r = 0; r < W; ++r) {
@@ -301,8 +327,11 @@ bool run(Result& R, int32_t W, int64_t n, const int64_t* rank_off, const int64_t
         for (int32_t r = 0; r < W; ++r) {
             GroupList& L = list[(size_t)r];
             std::vector<int32_t> next;
-            for (int64_t j = 0; j < cut; ++j)
+            for (int64_t j = 0; j < cut; ++j) {
                 R.slots[(size_t)r].push_back(L.empty() ? Group{} : L[(size_t)j]);
+                R.slots_approx[(size_t)r].push_back(L.empty() ? 0.0
+                                                               : (double)L[(size_t)j].size() * mean_len[(size_t)r]);
+            }
             for (size_t j = (size_t)cut; j < L.size(); ++j)
                 for (int32_t x : L[j]) next.push_back(x);
             for (int32_t x : returned[(size_t)r]) next.push_back(x);
@@ -427,6 +456,53 @@ void oracle_slots(void* h, int32_t* rows, int32_t* maxlen, int64_t* row_off, int
         }
     row_off[k] = ro;
     tile_off[k] = to;
+}
+
+// Approximate post-alignment token count of every slot (same layout as oracle_slots).
+void oracle_slots_approx(void* h, double* tokens_approx) {
+    const Result& R = *static_cast<Result*>(h);
+    int64_t k = 0;
+    for (int32_t r = 0; r < R.W; ++r)
+        for (double a : R.slots_approx[(size_t)r]) tokens_approx[k++] = a;
+}
+
+// Loss-scaling weights (Eq. 2, App. B) of every slot, rank-major like the slot tables:
+// at step j rank r pre-scales its mean loss by W * weight[r * steps + j], so that the
+// mean over ranks equals sum_r weight * mean loss of rank r.
+//   mode 0, sample level:            n_{r,j} / sum_r n_{r,j}
+//   mode 1, approximate token level: a_{r,j} / sum_r a_{r,j}, a = rows * buffer mean length
+//   mode 2, exact token level:       t_{r,j} / sum_r t_{r,j}  (t = real tokens of the slot)
+// The sums run over ranks in rank order; a step whose sum is zero gets zero weights.
+// step_tokens / step_samples (may be NULL) receive sum_r t_{r,j} and sum_r n_{r,j}.
+int oracle_loss_weights(void* h, int32_t mode, double* weight, int64_t* step_tokens, int64_t* step_samples) {
+    const Result& R = *static_cast<Result*>(h);
+    if (mode < 0 || mode > 2) return -1;
+    const int64_t S = R.info.steps;
+    for (int64_t j = 0; j < S; ++j) {
+        int64_t T_tok = 0, N = 0;
+        double A = 0.0;
+        std::vector<int64_t> t((size_t)R.W), c((size_t)R.W);
+        for (int32_t r = 0; r < R.W; ++r) {
+            const Group& g = R.slots[(size_t)r][(size_t)j];
+            int64_t tk = 0;
+            for (int32_t x : g) tk += R.len[(size_t)x];
+            t[(size_t)r] = tk;
+            c[(size_t)r] = (int64_t)g.size();
+            T_tok += tk;
+            N += (int64_t)g.size();
+            A = A + R.slots_approx[(size_t)r][(size_t)j];
+        }
+        for (int32_t r = 0; r < R.W; ++r) {
+            double w = 0.0;
+            if (mode == 0 && N > 0) w = (double)c[(size_t)r] / (double)N;
+            if (mode == 1 && A > 0.0) w = R.slots_approx[(size_t)r][(size_t)j] / A;
+            if (mode == 2 && T_tok > 0) w = (double)t[(size_t)r] / (double)T_tok;
+            weight[(int64_t)r * S + j] = w;
+        }
+        if (step_tokens) step_tokens[j] = T_tok;
+        if (step_samples) step_samples[j] = N;
+    }
+    return 0;
 }
 
 // emit_order: emitted sample ids rank-major, slot order, row order.  leftover: the

@@ -1,8 +1,9 @@
 """Throughput of the ODB window pipeline on one MI355X.
 
 One step = grouping (odb_form_groups) + alignment with coverage check
-(odb_align_groups) + padded collation (odb_collate) of a whole window whose CSR token
-stream is already resident in HBM.  Prints one JSON line:
+(odb_align_groups) + padded collation (odb_collate) + exact token-level loss-scaling
+weights (odb_loss_weights) of a whole window whose CSR token stream is already resident
+in HBM.  Prints one JSON line:
 
   value        emitted samples per second (whole job)
   roofline     the collate stage (dominant): algorithmic bytes per odb_collate call /
@@ -170,6 +171,7 @@ def main():
         torch.cuda.empty_cache()
     for i in range(args.warmup):
         pipe.run()
+        pipe.loss_weights(odb.ODB_WEIGHT_TOKEN_EXACT)
         torch.cuda.synchronize()
         log(f"[bench] warmup {i + 1}/{args.warmup} done")
     info = dict(pipe.info)
@@ -179,17 +181,21 @@ def main():
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    lw = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     for i in range(args.steps):
         pipe.form()
         pipe.align()
         ev[i][0].record(stream)
         pipe.collate()
         ev[i][1].record(stream)
+        pipe.loss_weights(odb.ODB_WEIGHT_TOKEN_EXACT)
+        lw[i].record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     log(f"[bench] timed {args.steps} steps")
     sec_per_step = (t1 - t0) / args.steps
     collate_all = [a.elapsed_time(b) for a, b in ev]
+    weights_ms = float(np.mean([b.elapsed_time(c) for (a, b), c in zip(ev, lw)]))
     collate_ms = float(np.mean(collate_all))
     assert pipe.info["steps"] == info["steps"] and pipe.info["padded_elems"] == info["padded_elems"]
 
@@ -219,6 +225,8 @@ def main():
         "tokens_per_s": real / sec_per_step,
         "padded_elems_per_s": P / sec_per_step,
         "pipeline_hbm_frac": alg / sec_per_step / 1e9 / HBM_PEAK_GBS,
+        "loss_weights_ms": weights_ms,
+        "second_gather_rounds": int(info["second_gather_rounds"]),
         "config": {
             "workload": wl.name,
             "description": wl.description,

@@ -9,6 +9,7 @@
  *                     overflow recirculation, join / non-join quota      Sec. 2.3, Thm 1-2)
  *                     termination, slot plan, stats, identity coverage  (App. C)
  *   odb_collate       pad every aligned group to its own longest sample (Sec. 2.1, Fig. 1)
+ *   odb_loss_weights  per-step, per-rank loss-scaling weights          (Eq. 2, App. B)
  *
  * Conventions shared by every entry point
  *   - Pointers named d_* are device pointers (HIP global memory on the current device);
@@ -133,6 +134,10 @@ typedef struct odb_plan_info {
     int64_t bad_views;               /* sampler views not emitted/leftover exactly once     */
     double  pad_fraction;            /* 1 - real_tokens / padded_elems (0 if nothing padded) */
     int64_t required_slot_capacity;  /* W * S; set on ODB_E_CAPACITY and on success         */
+    int64_t second_gather_rounds;    /* rounds in which some active rank had G_r != T, i.e.
+                                        rounds whose pre-alignment counts are not the
+                                        post-alignment ones, so exact token-level loss
+                                        scaling needs a second exchange (App. B)             */
 } odb_plan_info_t;
 
 /*
@@ -160,6 +165,11 @@ typedef struct odb_plan_info {
  *   d_slot_row_off    [slot_capacity+1] out: exclusive prefix sum of rows
  *   d_slot_tile_off   [slot_capacity+1] out: exclusive prefix sum of rows * maxlen
  *   d_slot_tokens     [slot_capacity] out: real tokens of slot k
+ *   d_slot_tokens_approx [slot_capacity] out, or NULL: approximate token count of slot k
+ *                     for approximate token-level loss scaling (App. B): rows of the slot
+ *                     times the mean length of its rank's buffer at the start of the
+ *                     slot's alignment round (fp64, rows * (tokens / samples), each
+ *                     operation rounded to nearest); 0 for IDLE slots
  *   d_leftover        [n] out: un-emitted ids of every rank in formation order, rank-major
  *   d_leftover_off    [W+1] out: rank r's leftovers are [off[r], off[r+1])
  *   h_info            host out: plan summary (always filled when the plan was built)
@@ -175,7 +185,7 @@ int odb_align_groups(const odb_window_t* w, int64_t budget, const odb_align_para
                      int64_t slot_capacity,
                      int32_t* d_emit_order, int32_t* d_slot_rows, int32_t* d_slot_maxlen,
                      int64_t* d_slot_row_off, int64_t* d_slot_tile_off, int64_t* d_slot_tokens,
-                     int32_t* d_leftover, int64_t* d_leftover_off,
+                     double* d_slot_tokens_approx, int32_t* d_leftover, int64_t* d_leftover_off,
                      odb_plan_info_t* h_info, void* d_ws, size_t ws_bytes, void* stream);
 
 /*
@@ -193,7 +203,7 @@ int odb_align_groups(const odb_window_t* w, int64_t budget, const odb_align_para
  *   out_capacity_elems  length of each output array; elements beyond it are not written
  *   d_ws / ws_bytes     the workspace (only a small status word is used)
  *
- * Asynchronous (launches exactly one kernel).  Accesses are bounds-checked against the
+ * Asynchronous (launches two kernels).  Accesses are bounds-checked against the
  * window and the plan; an inconsistent plan sets a device status word that
  * odb_collate_status() reads.
  */
@@ -216,6 +226,40 @@ int odb_collate_status(void* d_ws, size_t ws_bytes, void* stream);
 int odb_check_coverage(const odb_window_t* w, const int32_t* d_emitted, int64_t num_emitted,
                        const int32_t* d_leftover, int64_t num_leftover,
                        odb_plan_info_t* h_info, void* d_ws, size_t ws_bytes, void* stream);
+
+/* Loss-scaling weight modes (App. B and the loss-scaling ablation of App. I). */
+typedef enum odb_weight_mode {
+    ODB_WEIGHT_SAMPLE = 0,         /* n_{r,j} / sum_r n_{r,j}                                  */
+    ODB_WEIGHT_TOKEN_APPROX = 1,   /* a_{r,j} / sum_r a_{r,j}, a = d_slot_tokens_approx         */
+    ODB_WEIGHT_TOKEN_EXACT = 2     /* t_{r,j} / sum_r t_{r,j}, t = real tokens (Eq. 2)          */
+} odb_weight_mode_t;
+
+/*
+ * Loss-scaling weights of an aligned plan (Sec. 2.3 "Loss scaling", Eq. 2, App. B).
+ *
+ * At step j rank r pre-scales its per-token mean loss by W * weight[r * S + j]; DDP's
+ * mean over ranks then equals sum_r weight * mean loss of rank r, which for the exact
+ * token-level mode is the per-token mean over the whole step.  n = rows, t = real
+ * tokens, a = approximate tokens of the slot, all as written by odb_align_groups.
+ *
+ *   num_ranks, steps        W >= 1 and S >= 0 of the plan (W * S slots, rank-major)
+ *   mode                    odb_weight_mode_t
+ *   d_slot_rows             [W*S] rows per slot
+ *   d_slot_tokens           [W*S] real tokens per slot
+ *   d_slot_tokens_approx    [W*S] approximate tokens per slot (read only in the
+ *                           approximate mode; may be NULL otherwise)
+ *   d_weight                [W*S] out: fp64 weight of every slot; IDLE slots get 0
+ *   d_step_tokens           [S] out, or NULL: sum_r t_{r,j}
+ *   d_step_samples          [S] out, or NULL: sum_r n_{r,j}
+ *
+ * Sums over ranks run in rank order; every product, sum and quotient is one fp64
+ * operation rounded to nearest (no fused multiply-add), so results are reproducible
+ * bit for bit.  A step whose denominator is 0 gets zero weights.  Asynchronous (one
+ * kernel); needs no workspace.
+ */
+int odb_loss_weights(int32_t num_ranks, int64_t steps, int32_t mode, const int32_t* d_slot_rows,
+                     const int64_t* d_slot_tokens, const double* d_slot_tokens_approx, double* d_weight,
+                     int64_t* d_step_tokens, int64_t* d_step_samples, void* stream);
 
 #ifdef __cplusplus
 }

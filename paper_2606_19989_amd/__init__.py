@@ -7,7 +7,8 @@ HIP kernels of ``libodb.so``; there is no fallback path -- if the library is mis
 fails to load, every call raises.
 
 :class:`Pipeline` owns the device buffers of one window and runs the three stages
-(grouping, alignment, collation) in order on one stream.
+(grouping, alignment, collation) in order on one stream, and on request the loss-scaling
+weights of the aligned plan.
 """
 from __future__ import annotations
 
@@ -32,10 +33,11 @@ ODB_E_INTERNAL = 7
 ODB_MODE_JOIN = 0
 ODB_MODE_NONJOIN_QUOTA = 1
 ODB_STOP_DRAINED, ODB_STOP_QUOTA, ODB_STOP_RANK_FINISHED = 0, 1, 2
+ODB_WEIGHT_SAMPLE, ODB_WEIGHT_TOKEN_APPROX, ODB_WEIGHT_TOKEN_EXACT = 0, 1, 2
 
 EXPORTED = [
     "odb_status_string", "odb_last_error_message", "odb_workspace_size", "odb_form_groups",
-    "odb_align_groups", "odb_collate", "odb_collate_status", "odb_check_coverage",
+    "odb_align_groups", "odb_collate", "odb_collate_status", "odb_check_coverage", "odb_loss_weights",
 ]
 
 
@@ -84,6 +86,7 @@ class PlanInfo(ctypes.Structure):
         ("bad_views", ctypes.c_int64),
         ("pad_fraction", ctypes.c_double),
         ("required_slot_capacity", ctypes.c_int64),
+        ("second_gather_rounds", ctypes.c_int64),
     ]
 
     def as_dict(self) -> dict:
@@ -113,13 +116,15 @@ def load():
         lib.odb_form_groups.argtypes = [W, I64, P, P, P, P, P, SZ, P]
         lib.odb_align_groups.restype = ctypes.c_int
         lib.odb_align_groups.argtypes = [W, I64, ctypes.POINTER(AlignParams), P, P, P, P, I64,
-                                         P, P, P, P, P, P, P, P, ctypes.POINTER(PlanInfo), P, SZ, P]
+                                         P, P, P, P, P, P, P, P, P, ctypes.POINTER(PlanInfo), P, SZ, P]
         lib.odb_collate.restype = ctypes.c_int
         lib.odb_collate.argtypes = [W, I64, P, P, P, P, P, I32, I64, P, P, P, P, P, SZ, P]
         lib.odb_collate_status.restype = ctypes.c_int
         lib.odb_collate_status.argtypes = [P, SZ, P]
         lib.odb_check_coverage.restype = ctypes.c_int
         lib.odb_check_coverage.argtypes = [W, P, I64, P, I64, ctypes.POINTER(PlanInfo), P, SZ, P]
+        lib.odb_loss_weights.restype = ctypes.c_int
+        lib.odb_loss_weights.argtypes = [I32, I64, I32, P, P, P, P, P, P, P]
         _lib = lib
     return _lib
 
@@ -187,7 +192,8 @@ def odb_form_groups(win, budget, order, sorted_len, group_index, groups_per_rank
 
 def odb_align_groups(win, budget, mode, quota, slot_capacity_per_rank, order, sorted_len, group_index,
                      groups_per_rank, slot_capacity, emit_order, slot_rows, slot_maxlen, slot_row_off,
-                     slot_tile_off, slot_tokens, leftover, leftover_off, ws, stream=None, raise_on_capacity=True):
+                     slot_tile_off, slot_tokens, leftover, leftover_off, ws, stream=None, raise_on_capacity=True,
+                     slot_tokens_approx=None):
     cap = None
     if slot_capacity_per_rank is not None:
         cap = np.ascontiguousarray(slot_capacity_per_rank, dtype=np.int64)
@@ -196,7 +202,8 @@ def odb_align_groups(win, budget, mode, quota, slot_capacity_per_rank, order, so
     st = load().odb_align_groups(win.ref, int(budget), ctypes.byref(params), _dptr(order), _dptr(sorted_len),
                                  _dptr(group_index), _dptr(groups_per_rank), int(slot_capacity), _dptr(emit_order),
                                  _dptr(slot_rows), _dptr(slot_maxlen), _dptr(slot_row_off), _dptr(slot_tile_off),
-                                 _dptr(slot_tokens), _dptr(leftover), _dptr(leftover_off), ctypes.byref(info),
+                                 _dptr(slot_tokens), _dptr(slot_tokens_approx), _dptr(leftover), _dptr(leftover_off),
+                                 ctypes.byref(info),
                                  _dptr(ws), ws.numel() * ws.element_size(), _stream(stream))
     if st == ODB_E_CAPACITY and not raise_on_capacity:
         return st, info.as_dict()
@@ -222,6 +229,13 @@ def odb_check_coverage(win, emitted, num_emitted, leftover, num_leftover, ws, st
                                      ctypes.byref(info), _dptr(ws), ws.numel() * ws.element_size(),
                                      _stream(stream)))
     return info.as_dict()
+
+
+def odb_loss_weights(num_ranks, steps, mode, slot_rows, slot_tokens, slot_tokens_approx, weight,
+                     step_tokens=None, step_samples=None, stream=None):
+    _check(load().odb_loss_weights(int(num_ranks), int(steps), int(mode), _dptr(slot_rows), _dptr(slot_tokens),
+                                   _dptr(slot_tokens_approx), _dptr(weight), _dptr(step_tokens), _dptr(step_samples),
+                                   _stream(stream)))
 
 
 class Pipeline:
@@ -269,6 +283,7 @@ class Pipeline:
         self.slot_rows = torch.empty(cap, dtype=torch.int32, device=self.device)
         self.slot_maxlen = torch.empty(cap, dtype=torch.int32, device=self.device)
         self.slot_tokens = torch.empty(cap, dtype=torch.int64, device=self.device)
+        self.slot_tokens_approx = torch.empty(cap, dtype=torch.float64, device=self.device)
         self.slot_row_off = torch.empty(cap + 1, dtype=torch.int64, device=self.device)
         self.slot_tile_off = torch.empty(cap + 1, dtype=torch.int64, device=self.device)
 
@@ -281,10 +296,10 @@ class Pipeline:
                         self.group_index, self.groups_per_rank, self.slot_capacity, self.emit_order,
                         self.slot_rows, self.slot_maxlen, self.slot_row_off, self.slot_tile_off, self.slot_tokens,
                         self.leftover, self.leftover_off, self.ws, stream)
-        st, info = odb_align_groups(*args(), raise_on_capacity=False)
+        st, info = odb_align_groups(*args(), raise_on_capacity=False, slot_tokens_approx=self.slot_tokens_approx)
         if st == ODB_E_CAPACITY:
             self._alloc_slots(int(info["required_slot_capacity"]))
-            st, info = odb_align_groups(*args())
+            st, info = odb_align_groups(*args(), slot_tokens_approx=self.slot_tokens_approx)
         self.info = info
         return info
 
@@ -305,6 +320,22 @@ class Pipeline:
         odb_collate(self.win, self.num_slots, self.emit_order, self.slot_rows, self.slot_maxlen, self.slot_row_off,
                     self.slot_tile_off, self.pad_id, P, *outs, self.ws, stream)
         return tuple(o[:P] for o in outs)
+
+    def loss_weights(self, mode: int = ODB_WEIGHT_TOKEN_EXACT, stream=None):
+        """Per-slot loss-scaling weights (rank-major, W * S) and the per-step sums of real
+        tokens and samples over ranks, as device tensors."""
+        torch = self.torch
+        S = int(self.info["steps"])
+        K = self.num_slots
+        if getattr(self, "_weights", None) is None or self._weights[0].numel() < max(K, 1) \
+                or self._weights[1].numel() < max(S, 1):
+            self._weights = (torch.empty(max(K, 1), dtype=torch.float64, device=self.device),
+                             torch.empty(max(S, 1), dtype=torch.int64, device=self.device),
+                             torch.empty(max(S, 1), dtype=torch.int64, device=self.device))
+        wt, st, ss = self._weights
+        odb_loss_weights(self.win.num_ranks, S, mode, self.slot_rows, self.slot_tokens, self.slot_tokens_approx,
+                         wt, st, ss, stream)
+        return wt[:K], st[:S], ss[:S]
 
     def run(self, stream=None):
         self.form(stream)

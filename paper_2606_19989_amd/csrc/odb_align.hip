@@ -210,7 +210,7 @@ __global__ void __launch_bounds__(kBlock) target_kernel(RankState* ranks, const 
     if (minC != LLONG_MAX && minC < T) T = minC;
     if (minS != LLONG_MAX && minS < T) T = minS;
     if (T < 1) T = 1;
-    int64_t splits = 0, over = 0;
+    int64_t splits = 0, over = 0, changed = 0;
     for (int r = threadIdx.x; r < W; r += kBlock) {
         RankState& R = ranks[r];
         const int64_t G = R.G;
@@ -222,16 +222,22 @@ __global__ void __launch_bounds__(kBlock) target_kernel(RankState* ranks, const 
         } else if (G < T) {
             R.action = kActSplit;
             splits += T - G;
+            changed += 1;
         } else if (G > T) {
             R.action = kActOverflow;
             over += G - T;
+            changed += 1;
         } else {
             R.action = kActKeep;
         }
     }
     splits = block_reduce(splits, SumOp{});
     over = block_reduce(over, SumOp{});
+    changed = block_reduce(changed, SumOp{});
     if (threadIdx.x == 0) {
+        // App. B: the pre-alignment counts of the first exchange are exact only if no
+        // active rank's groups changed; otherwise exact token weights need a second one
+        rs->second_gather += changed > 0 ? 1 : 0;
         rs->T = T;
         rs->active = active;
         rs->total_groups = totalG;
@@ -366,11 +372,16 @@ __device__ __forceinline__ void adjusted_range(const RankState& R, int64_t base,
 }
 
 // Step j of every active rank: adjusted group T-1-j (emission runs short to long).
+// Besides rows, longest length and real tokens, each record carries the approximate
+// token count of App. B: rows times the mean length of the rank's buffer at the start of
+// this round (the counts a rank can advertise before alignment).
 __global__ void __launch_bounds__(kBlock) slot_records_kernel(
     const RankState* __restrict__ ranks, const RoundState* __restrict__ rs, const int64_t* __restrict__ off, int W,
     const int32_t* __restrict__ gstart, const int32_t* __restrict__ gsize, const int32_t* __restrict__ kept,
     const int32_t* __restrict__ cur_len, const int64_t* __restrict__ cs, int32_t* __restrict__ srows,
-    int32_t* __restrict__ smax, int64_t* __restrict__ stok, int64_t* __restrict__ steps) {
+    int32_t* __restrict__ smax, int64_t* __restrict__ stok, double* __restrict__ sadj,
+    int64_t* __restrict__ steps) {
+#pragma clang fp contract(off)
     const int64_t T = rs->T;
     const int64_t total = (int64_t)W * T;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -393,6 +404,10 @@ __global__ void __launch_bounds__(kBlock) slot_records_kernel(
         srows[dst] = (int32_t)rows;
         smax[dst] = cur_len[start];
         stok[dst] = cs[end - 1] - (start > 0 ? cs[start - 1] : 0);
+        // live positions of the rank are [base, base + cnt); cs is inclusive over all n
+        const int64_t buf_tok = cs[base + R.cnt - 1] - (base > 0 ? cs[base - 1] : 0);
+        const double mean = (double)buf_tok / (double)R.cnt;
+        sadj[dst] = (double)rows * mean;
         atomicAdd((unsigned long long*)&steps[j], (unsigned long long)rows);
     }
 }
@@ -551,8 +566,9 @@ __global__ void __launch_bounds__(kBlock) plan_slots_kernel(const RankState* __r
                                                             const int32_t* __restrict__ srows,
                                                             const int32_t* __restrict__ smax,
                                                             const int64_t* __restrict__ stok,
+                                                            const double* __restrict__ sadj,
                                                             int32_t* __restrict__ rows, int32_t* __restrict__ maxlen,
-                                                            int64_t* __restrict__ tokens) {
+                                                            int64_t* __restrict__ tokens, double* __restrict__ approx) {
     const int64_t K = (int64_t)W * S;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < K; k += stride) {
@@ -563,10 +579,12 @@ __global__ void __launch_bounds__(kBlock) plan_slots_kernel(const RankState* __r
             rows[k] = srows[src];
             maxlen[k] = smax[src];
             tokens[k] = stok[src];
+            if (approx) approx[k] = sadj[src];
         } else {
             rows[k] = 0;
             maxlen[k] = 0;
             tokens[k] = 0;
+            if (approx) approx[k] = 0.0;
         }
     }
 }
@@ -1003,9 +1021,9 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
                                 const int32_t* d_order, const int32_t* d_sorted_len, const int32_t* d_group_index,
                                 const int32_t* d_groups_per_rank, int64_t slot_capacity, int32_t* d_emit_order,
                                 int32_t* d_slot_rows, int32_t* d_slot_maxlen, int64_t* d_slot_row_off,
-                                int64_t* d_slot_tile_off, int64_t* d_slot_tokens, int32_t* d_leftover,
-                                int64_t* d_leftover_off, odb_plan_info_t* h_info, void* d_ws, size_t ws_bytes,
-                                void* stream) {
+                                int64_t* d_slot_tile_off, int64_t* d_slot_tokens, double* d_slot_tokens_approx,
+                                int32_t* d_leftover, int64_t* d_leftover_off, odb_plan_info_t* h_info, void* d_ws,
+                                size_t ws_bytes, void* stream) {
     Layout L;
     ODB_TRY(check_workspace(w, d_ws, ws_bytes, &L));
     if (budget < 1) return set_error(ODB_E_INVALID_ARG, "budget must be >= 1");
@@ -1049,6 +1067,7 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     int32_t* srows = ws_at<int32_t>(d_ws, L.srows);
     int32_t* smax = ws_at<int32_t>(d_ws, L.smax);
     int64_t* stok = ws_at<int64_t>(d_ws, L.stok);
+    double* sadj = ws_at<double>(d_ws, L.sadj);
     int64_t* steps = ws_at<int64_t>(d_ws, L.steps);
     int32_t* bids[2] = {ws_at<int32_t>(d_ws, L.buf_ids0), ws_at<int32_t>(d_ws, L.buf_ids1)};
     int32_t* blen[2] = {ws_at<int32_t>(d_ws, L.buf_len0), ws_at<int32_t>(d_ws, L.buf_len1)};
@@ -1123,7 +1142,7 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
         ODB_LAUNCHED();
         hipLaunchKernelGGL(slot_records_kernel, dim3(gridn), dim3(kBlock), 0, s, (const RankState*)d_ranks,
                            (const RoundState*)d_rs, d_off, W, (const int32_t*)gstart, (const int32_t*)gsize,
-                           (const int32_t*)kept, cur.len, (const int64_t*)cs, srows, smax, stok, steps);
+                           (const int32_t*)kept, cur.len, (const int64_t*)cs, srows, smax, stok, sadj, steps);
         ODB_LAUNCHED();
         hipLaunchKernelGGL(cut_kernel, dim3(1), dim3(kBlock), 0, s, d_rs, (const int64_t*)steps, nonjoin ? 1 : 0,
                            params->quota);
@@ -1163,6 +1182,7 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     h_info->splits = hrs.splits;
     h_info->overflow_groups = hrs.overflow;
     h_info->max_step_samples = hrs.step_max;
+    h_info->second_gather_rounds = hrs.second_gather;
     h_info->required_slot_capacity = K;
     if (K > slot_capacity)
         return set_error(ODB_E_CAPACITY, "plan needs %lld slots, capacity is %lld", (long long)K,
@@ -1171,7 +1191,8 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     if (K > 0) {
         hipLaunchKernelGGL(plan_slots_kernel, dim3(grid_for(K, kBlock, gcap)), dim3(kBlock), 0, s,
                            (const RankState*)d_ranks, d_off, W, S, (const int32_t*)srows, (const int32_t*)smax,
-                           (const int64_t*)stok, d_slot_rows, d_slot_maxlen, d_slot_tokens);
+                           (const int64_t*)stok, (const double*)sadj, d_slot_rows, d_slot_maxlen, d_slot_tokens,
+                           d_slot_tokens_approx);
         ODB_LAUNCHED();
     }
     ODB_TRY((device_excl_scan<int64_t>(RowsLoad{d_slot_rows, K}, Store64{d_slot_row_off}, K + 1,

@@ -91,7 +91,7 @@ bool make_layout(const odb_window_t* w, Layout* L) {
     L->gstart = take(4 * n1);
     L->gsize = take(4 * n1);
     L->gmax = take(4 * n1);
-    L->gtok = take(8 * n1);
+    L->sadj = take(8 * n1);
     L->cs = take(8 * n1);
     L->ov_slot = take(4 * n1);
     L->ov_lo = take(4 * n1);

@@ -88,6 +88,7 @@ struct RoundState {
     int64_t active;          // active ranks this round
     int64_t total_groups;    // groups over all ranks this round
     int64_t leftover_total;  // samples back in buffers after this round
+    int64_t second_gather;   // rounds in which some active rank had G_r != T (all rounds)
 };
 
 // Final summary assembled on the device (mirrors odb_plan_info_t's counters).
@@ -108,7 +109,7 @@ struct Layout {
     size_t status, round, ranks, rank_off, cap, gbase, tile_first;
     size_t len, keys0, keys1, vals0, vals1, counts, partials;
     size_t jmp0, jmp1, marks, incl;
-    size_t gstart, gsize, gmax, gtok, cs, ov_slot, ov_lo, kept;
+    size_t gstart, gsize, gmax, sadj, cs, ov_slot, ov_lo, kept;
     size_t srows, smax, stok, steps;
     size_t buf_ids0, buf_ids1, buf_len0, buf_len1, gidx, stage, cover, row_ts, row_len;
     size_t info;

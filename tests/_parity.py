@@ -9,7 +9,7 @@ import synth
 
 INFO_EXACT = ["steps", "rounds", "stop_reason", "emitted_samples", "leftover_samples", "real_tokens",
               "padded_elems", "max_step_samples", "splits", "overflow_groups", "missing_ids", "duplicate_ids",
-              "bad_views"]
+              "bad_views", "second_gather_rounds"]
 PAD_FRACTION_RTOL = 1e-12
 
 
@@ -55,12 +55,30 @@ def compare_plan(w, pipe, ref):
     assert np.array_equal(h(pipe.slot_rows, K), ref.slot_rows), "slot_rows"
     assert np.array_equal(h(pipe.slot_maxlen, K), ref.slot_maxlen), "slot_maxlen"
     assert np.array_equal(h(pipe.slot_tokens, K), ref.slot_tokens), "slot_tokens"
+    # fp64, same operations in the same order on both sides: equal bit for bit
+    assert np.array_equal(h(pipe.slot_tokens_approx, K).view(np.int64), ref.slot_tokens_approx.view(np.int64)), \
+        "slot_tokens_approx"
     assert np.array_equal(h(pipe.slot_row_off, K + 1), ref.slot_row_off), "slot_row_off"
     assert np.array_equal(h(pipe.slot_tile_off, K + 1), ref.slot_tile_off), "slot_tile_off"
     E, Lf = ref.info["emitted_samples"], ref.info["leftover_samples"]
     assert np.array_equal(h(pipe.emit_order, E), ref.emit_order), "emit_order"
     assert np.array_equal(h(pipe.leftover, Lf), ref.leftover), "leftover"
     assert np.array_equal(h(pipe.leftover_off), ref.leftover_off), "leftover_off"
+
+
+def compare_loss_weights(pipe, ref):
+    """Every mode's per-slot weights (bit for bit) and per-step sums (Eq. 2, App. B)."""
+    import torch
+
+    for mode in (oracle.WEIGHT_SAMPLE, oracle.WEIGHT_TOKEN_APPROX, oracle.WEIGHT_TOKEN_EXACT):
+        wt, st, ss = pipe.loss_weights(mode)
+        torch.cuda.synchronize()
+        ewt, est, ess = ref.loss_weights(mode)
+        got = h(wt)
+        assert np.array_equal(got.view(np.int64), ewt.view(np.int64)), \
+            (mode, int(np.count_nonzero(got != ewt)), float(np.max(np.abs(got - ewt), initial=0.0)))
+        assert np.array_equal(h(st), est), ("step tokens", mode)
+        assert np.array_equal(h(ss), ess), ("step samples", mode)
 
 
 def compare_collate_full(w, outs, ref, pad_id=0):

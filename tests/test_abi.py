@@ -78,14 +78,29 @@ def test_bad_arguments_rejected_on_host():
     info = odb.PlanInfo()
     for mode, quota, cap in [(1, 0, None), (7, 1, None), (0, 0, np.array([-1], dtype=np.int64))]:
         p = odb.AlignParams(mode, 0, quota, None if cap is None else cap.ctypes.data_as(ctypes.c_void_p).value)
-        st = lib.odb_align_groups(ctypes.byref(w), 10, ctypes.byref(p), 1, 1, 1, 1, 16, 1, 1, 1, 1, 1, 1, 1, 1,
-                                  ctypes.byref(info), fake_ws, size, None)
+        st = lib.odb_align_groups(ctypes.byref(w), 10, ctypes.byref(p), 1, 1, 1, 1, 16, 1, 1, 1, 1, 1, 1, None,
+                                  1, 1, ctypes.byref(info), fake_ws, size, None)
         assert st == odb.ODB_E_INVALID_ARG, (mode, quota, cap)
     # collate with negative sizes
     st = lib.odb_collate(ctypes.byref(w), -1, 1, 1, 1, 1, 1, 0, 10, 1, 1, 1, 1, fake_ws, size, None)
     assert st == odb.ODB_E_INVALID_ARG
     st = lib.odb_collate(ctypes.byref(w), 3, 1, 1, 1, 1, 1, 0, -5, 1, 1, 1, 1, fake_ws, size, None)
     assert st == odb.ODB_E_INVALID_ARG
+
+
+def test_loss_weights_arguments_checked_on_host():
+    lib = odb.load()
+    # no GPU call happens: each of these fails (or finishes, for zero steps) on the host
+    assert lib.odb_loss_weights(0, 5, 2, 1, 1, None, 1, None, None, None) == odb.ODB_E_INVALID_ARG
+    assert lib.odb_loss_weights(2, -1, 2, 1, 1, None, 1, None, None, None) == odb.ODB_E_INVALID_ARG
+    assert lib.odb_loss_weights(2, 5, 3, 1, 1, None, 1, None, None, None) == odb.ODB_E_INVALID_ARG
+    assert lib.odb_loss_weights(2, 5, 2, None, 1, None, 1, None, None, None) == odb.ODB_E_INVALID_ARG
+    assert lib.odb_loss_weights(2, 5, 2, 1, 1, None, None, None, None, None) == odb.ODB_E_INVALID_ARG
+    # the approximate mode needs the approximate counts
+    assert lib.odb_loss_weights(2, 5, odb.ODB_WEIGHT_TOKEN_APPROX, 1, 1, None, 1, None, None, None) == \
+        odb.ODB_E_INVALID_ARG
+    assert lib.odb_loss_weights(2 ** 30, 2 ** 40, 2, 1, 1, None, 1, None, None, None) == odb.ODB_E_INVALID_ARG
+    assert lib.odb_loss_weights(3, 0, 0, None, None, None, None, None, None, None) == odb.ODB_OK
 
 
 def test_binding_raises_without_library(monkeypatch, tmp_path):

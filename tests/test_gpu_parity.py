@@ -10,7 +10,7 @@ import pytest
 import oracle
 import synth
 from _parity import (collate_properties, compare_collate_by_rank, compare_collate_full, compare_collate_sampled,
-                     compare_plan, log, run_gpu)
+                     compare_loss_weights, compare_plan, log, run_gpu)
 
 pytestmark = pytest.mark.gpu
 
@@ -26,6 +26,7 @@ def check_full(w, pad_id=0):
     pipe, outs = run_gpu(w, pad_id=pad_id)
     compare_plan(w, pipe, ref)
     compare_collate_full(w, outs, ref, pad_id)
+    compare_loss_weights(pipe, ref)
     return pipe, ref
 
 
@@ -117,7 +118,8 @@ def test_workload_full_size(name):
     pipe, outs = run_gpu(w)
     log("  gpu pipeline done")
     compare_plan(w, pipe, ref)
-    log("  plan equal")
+    compare_loss_weights(pipe, ref)
+    log("  plan and loss weights equal")
     compare_collate_sampled(w, outs, ref)
     collate_properties(outs, ref)
     compare_collate_by_rank(w, outs, ref, pipe.win.tokens)

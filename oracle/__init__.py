@@ -250,3 +250,40 @@ def collate_elements(p: Plan, tok_off: np.ndarray, token_at, idx: np.ndarray, pa
     msk = real.astype(np.int32)
     pos = np.where(real, col, 0).astype(np.int32)
     return ids, lab, msk, pos
+
+
+def length_sketch(tok_off: np.ndarray, ids: Optional[np.ndarray], budget: int) -> dict:
+    """ROI sketch of realised lengths (Sec. 1 defines CV = sigma / mu of post-pipeline
+    lengths; the practical-guidance section screens a 1k-5k sketch with CV and
+    f_s = Pr[l < L_max / 4], flagging CV >= 0.8 or f_s > 0.2 as high ROI).
+
+    ``ids`` are the sketched sample ids (None: every sample).  sigma is the population
+    standard deviation (reading: the sketch is the population being described).  The
+    moments are exact Python integers; CV is sqrt(sum (l - mu)^2 / n) / mu evaluated as
+    one correctly rounded conversion of the exact rational CV^2 and one square root.
+    """
+    from fractions import Fraction
+    import math
+
+    tok_off = np.asarray(tok_off, dtype=np.int64)
+    n_all = len(tok_off) - 1
+    ids = np.arange(n_all, dtype=np.int64) if ids is None else np.asarray(ids, dtype=np.int64)
+    if ids.size and (ids.min() < 0 or ids.max() >= n_all):
+        raise OracleError("sketch id outside the window")
+    lens = [int(tok_off[i + 1] - tok_off[i]) for i in ids]
+    if any(l < 1 for l in lens):
+        raise OracleError("sample length < 1")
+    n = len(lens)
+    out = dict(samples=n, short_samples=0, sum_len=0, sum_sq=0, min_len=0, max_len=0,
+               mean=0.0, cv=0.0, short_fraction=0.0, high_roi=0)
+    if n == 0:
+        return out
+    s1 = sum(lens)
+    s2 = sum(l * l for l in lens)
+    mu = Fraction(s1, n)
+    var = sum((Fraction(l) - mu) ** 2 for l in lens) / n if n <= 20000 else Fraction(n * s2 - s1 * s1, n * n)
+    short = sum(1 for l in lens if Fraction(l) < Fraction(budget, 4))
+    cv = math.sqrt(float(var / (mu * mu)))
+    out.update(short_samples=short, sum_len=s1, sum_sq=s2, min_len=min(lens), max_len=max(lens),
+               mean=s1 / n, cv=cv, short_fraction=short / n, high_roi=int(cv >= 0.8 or short / n > 0.2))
+    return out

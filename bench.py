@@ -84,6 +84,32 @@ def copy_ceiling(dev, gib=4.0, reps=5):
     return 8 * m / (ms * 1e-3) / 1e9
 
 
+def length_sketch_timing(odb, win, ws, w, dev, reps=5):
+    """The ROI screen: a 5,000-id random sketch and the whole window (odb_length_sketch
+    synchronises, so each call is timed on the host clock, median of `reps`)."""
+    import numpy as np
+    import torch
+
+    ids = torch.from_numpy(np.random.default_rng(5).choice(w.n, size=min(5000, w.n), replace=False)
+                           .astype(np.int32)).to(dev)
+
+    def timed(fn):
+        fn()
+        t = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            out = fn()
+            t.append(time.perf_counter() - t0)
+        return out, float(np.median(t)) * 1e3
+
+    s5k, ms5k = timed(lambda: odb.odb_length_sketch(win, ids, ids.numel(), w.budget, ws))
+    sw, msw = timed(lambda: odb.odb_length_sketch(win, None, w.n, w.budget, ws))
+    return {"cv": s5k["cv"], "short_fraction": s5k["short_fraction"], "high_roi": s5k["high_roi"],
+            "sketch_ids": int(ids.numel()), "sketch_ms": ms5k, "window_cv": sw["cv"],
+            "window_short_fraction": sw["short_fraction"], "window_ms": msw,
+            "window_gbs_incl_sync": 8 * (w.n + 1) / (msw * 1e-3) / 1e9}
+
+
 def cpu_baseline(workload, tokens_dev, group=4, min_seconds=10.0, pad_id=0):
     """The oracle (plan + full collate), single-threaded, on consecutive groups of
     `group` ranks of the same window until at least `min_seconds` of CPU work."""
@@ -199,6 +225,9 @@ def main():
     collate_ms = float(np.mean(collate_all))
     assert pipe.info["steps"] == info["steps"] and pipe.info["padded_elems"] == info["padded_elems"]
 
+    sketch = length_sketch_timing(odb, win, pipe.ws, w, dev)
+    log(f"[bench] length sketch: cv={sketch['cv']:.3f} f_s={sketch['short_fraction']:.3f} "
+        f"window {sketch['window_ms']:.3f} ms")
     copy_gbs = copy_ceiling(dev)
     log(f"[bench] plain 4 GiB device copy: {copy_gbs:.0f} GB/s")
 
@@ -227,6 +256,7 @@ def main():
         "pipeline_hbm_frac": alg / sec_per_step / 1e9 / HBM_PEAK_GBS,
         "loss_weights_ms": weights_ms,
         "second_gather_rounds": int(info["second_gather_rounds"]),
+        "length_sketch": sketch,
         "config": {
             "workload": wl.name,
             "description": wl.description,

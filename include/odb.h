@@ -10,6 +10,8 @@
  *                     termination, slot plan, stats, identity coverage  (App. C)
  *   odb_collate       pad every aligned group to its own longest sample (Sec. 2.1, Fig. 1)
  *   odb_loss_weights  per-step, per-rank loss-scaling weights          (Eq. 2, App. B)
+ *   odb_length_sketch CV and short-sample fraction of sketched lengths  (Sec. 1, practical
+ *                     (return-on-investment screen)                      guidance section)
  *
  * Conventions shared by every entry point
  *   - Pointers named d_* are device pointers (HIP global memory on the current device);
@@ -260,6 +262,39 @@ typedef enum odb_weight_mode {
 int odb_loss_weights(int32_t num_ranks, int64_t steps, int32_t mode, const int32_t* d_slot_rows,
                      const int64_t* d_slot_tokens, const double* d_slot_tokens_approx, double* d_weight,
                      int64_t* d_step_tokens, int64_t* d_step_samples, void* stream);
+
+/* Moments of a length sketch (see odb_length_sketch). */
+typedef struct odb_length_sketch {
+    int64_t  samples;         /* n: sketched samples                                     */
+    int64_t  short_samples;   /* samples with l < L_max / 4 (tested as 4 l < L_max)      */
+    int64_t  sum_len;         /* sum of l                                                */
+    uint64_t sum_sq_hi;       /* sum of l^2 = sum_sq_hi * 2^32 + sum_sq_lo (exact)       */
+    uint64_t sum_sq_lo;
+    int64_t  min_len;         /* 0 if n = 0                                              */
+    int64_t  max_len;
+    double   mean;            /* sum_len / n                                             */
+    double   cv;              /* population sigma / mu = sqrt(n sum l^2 - (sum l)^2) / sum l */
+    double   short_fraction;  /* f_s = short_samples / n                                 */
+    int32_t  high_roi;        /* cv >= 0.8 or f_s > 0.2                                  */
+    int32_t  reserved0;
+} odb_length_sketch_t;
+
+/*
+ * Return-on-investment screen (Sec. 1 defines CV = sigma / mu of realised lengths; the
+ * practical-guidance section screens a 1k-5k sketch with CV and f_s = Pr[l < L_max / 4]
+ * and flags CV >= 0.8 or f_s > 0.2 as a high-return workload).
+ *
+ *   d_ids     [count] sample ids of the sketch (device), or NULL: samples 0 .. count-1
+ *   count     sketch size, 0 <= count < 2^31 (<= n when d_ids is NULL); ids may repeat
+ *   budget    L_max >= 1 that f_s is measured against
+ *   h_out     host out
+ *
+ * Integer fields are exact.  mean, cv and short_fraction are computed on the host from
+ * them (cv from an exact 128-bit numerator).  Synchronises `stream`.  Returns
+ * ODB_E_INVALID_DATA if an id lies outside the window or a sketched length is < 1.
+ */
+int odb_length_sketch(const odb_window_t* w, const int32_t* d_ids, int64_t count, int64_t budget,
+                      odb_length_sketch_t* h_out, void* d_ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -38,6 +38,7 @@ ODB_WEIGHT_SAMPLE, ODB_WEIGHT_TOKEN_APPROX, ODB_WEIGHT_TOKEN_EXACT = 0, 1, 2
 EXPORTED = [
     "odb_status_string", "odb_last_error_message", "odb_workspace_size", "odb_form_groups",
     "odb_align_groups", "odb_collate", "odb_collate_status", "odb_check_coverage", "odb_loss_weights",
+    "odb_length_sketch",
 ]
 
 
@@ -93,6 +94,23 @@ class PlanInfo(ctypes.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_}
 
 
+class LengthSketch(ctypes.Structure):
+    _fields_ = [
+        ("samples", ctypes.c_int64),
+        ("short_samples", ctypes.c_int64),
+        ("sum_len", ctypes.c_int64),
+        ("sum_sq_hi", ctypes.c_uint64),
+        ("sum_sq_lo", ctypes.c_uint64),
+        ("min_len", ctypes.c_int64),
+        ("max_len", ctypes.c_int64),
+        ("mean", ctypes.c_double),
+        ("cv", ctypes.c_double),
+        ("short_fraction", ctypes.c_double),
+        ("high_roi", ctypes.c_int32),
+        ("reserved0", ctypes.c_int32),
+    ]
+
+
 _lib = None
 
 
@@ -125,6 +143,8 @@ def load():
         lib.odb_check_coverage.argtypes = [W, P, I64, P, I64, ctypes.POINTER(PlanInfo), P, SZ, P]
         lib.odb_loss_weights.restype = ctypes.c_int
         lib.odb_loss_weights.argtypes = [I32, I64, I32, P, P, P, P, P, P, P]
+        lib.odb_length_sketch.restype = ctypes.c_int
+        lib.odb_length_sketch.argtypes = [W, P, I64, I64, ctypes.POINTER(LengthSketch), P, SZ, P]
         _lib = lib
     return _lib
 
@@ -236,6 +256,17 @@ def odb_loss_weights(num_ranks, steps, mode, slot_rows, slot_tokens, slot_tokens
     _check(load().odb_loss_weights(int(num_ranks), int(steps), int(mode), _dptr(slot_rows), _dptr(slot_tokens),
                                    _dptr(slot_tokens_approx), _dptr(weight), _dptr(step_tokens), _dptr(step_samples),
                                    _stream(stream)))
+
+
+def odb_length_sketch(win, ids, count, budget, ws, stream=None) -> dict:
+    """CV, f_s and exact length moments of a sketch (ids: device int32 tensor or None for
+    samples 0 .. count-1); ``sum_sq`` is returned as one Python integer."""
+    out = LengthSketch()
+    _check(load().odb_length_sketch(win.ref, _dptr(ids), int(count), int(budget), ctypes.byref(out), _dptr(ws),
+                                    ws.numel() * ws.element_size(), _stream(stream)))
+    d = {f: getattr(out, f) for f, _ in out._fields_ if f != "reserved0"}
+    d["sum_sq"] = (int(d.pop("sum_sq_hi")) << 32) + int(d.pop("sum_sq_lo"))
+    return d
 
 
 class Pipeline:

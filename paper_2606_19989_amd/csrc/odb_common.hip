@@ -72,6 +72,7 @@ bool make_layout(const odb_window_t* w, Layout* L) {
     L->status = take(sizeof(DevStatus));
     L->round = take(sizeof(RoundState));
     L->info = take(sizeof(DevInfo));
+    L->sketch = take(256);
     L->ranks = take(sizeof(RankState) * W);
     L->rank_off = take(8 * (W + 1));
     L->cap = take(8 * W);

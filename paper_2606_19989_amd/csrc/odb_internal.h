@@ -112,7 +112,7 @@ struct Layout {
     size_t gstart, gsize, gmax, sadj, cs, ov_slot, ov_lo, kept;
     size_t srows, smax, stok, steps;
     size_t buf_ids0, buf_ids1, buf_len0, buf_len1, gidx, stage, cover, row_ts, row_len;
-    size_t info;
+    size_t info, sketch;
     size_t total;
     int64_t num_sort_blocks;
     int64_t partials_len;

@@ -103,6 +103,21 @@ def test_loss_weights_arguments_checked_on_host():
     assert lib.odb_loss_weights(3, 0, 0, None, None, None, None, None, None, None) == odb.ODB_OK
 
 
+def test_length_sketch_arguments_checked_on_host():
+    lib = odb.load()
+    w, keep = _window([0, 4, 9])
+    size = lib.odb_workspace_size(ctypes.byref(w))
+    fake_ws = 0x100000  # never dereferenced: every call below fails its host checks first
+    out = odb.LengthSketch()
+    ref = ctypes.byref(out)
+    assert lib.odb_length_sketch(ctypes.byref(w), None, 3, 10, None, fake_ws, size, None) == odb.ODB_E_INVALID_ARG
+    assert lib.odb_length_sketch(ctypes.byref(w), None, 3, 0, ref, fake_ws, size, None) == odb.ODB_E_INVALID_ARG
+    assert lib.odb_length_sketch(ctypes.byref(w), None, -1, 10, ref, fake_ws, size, None) == odb.ODB_E_INVALID_ARG
+    assert lib.odb_length_sketch(ctypes.byref(w), None, 10, 10, ref, fake_ws, size, None) == odb.ODB_E_INVALID_ARG
+    assert lib.odb_length_sketch(ctypes.byref(w), 1, 2 ** 31, 10, ref, fake_ws, size, None) == odb.ODB_E_INVALID_ARG
+    assert lib.odb_length_sketch(ctypes.byref(w), None, 3, 10, ref, fake_ws, size - 1, None) == odb.ODB_E_WORKSPACE
+
+
 def test_binding_raises_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(odb, "_lib", None)
     monkeypatch.setattr(odb, "LIB_PATH", str(tmp_path / "missing.so"))

@@ -165,3 +165,59 @@ def test_check_coverage_entry_point(case):
     info = odb.odb_check_coverage(dwin, emitted, emitted.numel(), left, left.numel(), ws)
     bad, miss, dup = _numpy_coverage(ids.astype(np.int64), n, identity, nid)
     assert (info["bad_views"], info["missing_ids"], info["duplicate_ids"]) == (bad, miss, dup)
+
+
+SKETCH_CV_RTOL = 1e-15   # both sides: a few correctly rounded fp64 operations on exact integers
+
+
+def _compare_sketch(got, want):
+    for f in ("samples", "short_samples", "sum_len", "sum_sq", "min_len", "max_len", "high_roi"):
+        assert got[f] == want[f], (f, got[f], want[f])
+    assert got["short_fraction"] == want["short_fraction"]
+    assert abs(got["mean"] - want["mean"]) <= 2.0 ** -52 * want["mean"]
+    assert abs(got["cv"] - want["cv"]) <= SKETCH_CV_RTOL * max(want["cv"], 1e-300), (got["cv"], want["cv"])
+
+
+@pytest.mark.parametrize("name", list(synth.WORKLOADS))
+def test_length_sketch(name):
+    # the screen the practical-guidance section prescribes: a 1k-5k sketch (ids drawn
+    # without replacement), plus leading prefixes of the window
+    import torch
+    import paper_2606_19989_amd as odb
+
+    w = synth.WORKLOADS[name].window()
+    tok_off = torch.from_numpy(w.tok_off).cuda()
+    win = odb.DeviceWindow(w.rank_off, tok_off, torch.zeros(4, dtype=torch.int32, device="cuda"), None, 0)
+    ws = torch.empty(odb.odb_workspace_size(win), dtype=torch.uint8, device="cuda")
+    rng = np.random.default_rng(51)
+    log(f"sketch {name}: n={w.n}")
+    for k in (1000, 5000):
+        ids = rng.choice(w.n, size=min(k, w.n), replace=False).astype(np.int32)
+        got = odb.odb_length_sketch(win, torch.from_numpy(ids).cuda(), len(ids), w.budget, ws)
+        _compare_sketch(got, oracle.length_sketch(w.tok_off, ids, w.budget))
+    for count in (0, 1, min(w.n, 100_000)):
+        got = odb.odb_length_sketch(win, None, count, w.budget, ws)
+        _compare_sketch(got, oracle.length_sketch(w.tok_off, np.arange(count), w.budget))
+    del ws, tok_off
+
+
+def test_length_sketch_whole_window_and_edge_cases():
+    import torch
+    import paper_2606_19989_amd as odb
+
+    w = synth.WORKLOADS["text_w8x65536"].window()
+    tok_off = torch.from_numpy(w.tok_off).cuda()
+    win = odb.DeviceWindow(w.rank_off, tok_off, torch.zeros(4, dtype=torch.int32, device="cuda"), None, 0)
+    ws = torch.empty(odb.odb_workspace_size(win), dtype=torch.uint8, device="cuda")
+    log("sketch whole window text_w8x65536")
+    got = odb.odb_length_sketch(win, None, w.n, w.budget, ws)
+    _compare_sketch(got, oracle.length_sketch(w.tok_off, None, w.budget))
+    for budget in (1, 4, 700 * 4, 700 * 4 + 1, 1 << 40):
+        ids = np.array([0, 0, 5, w.n - 1, 5], dtype=np.int32)   # repeated ids count every time
+        got = odb.odb_length_sketch(win, torch.from_numpy(ids).cuda(), len(ids), budget, ws)
+        _compare_sketch(got, oracle.length_sketch(w.tok_off, ids, budget))
+    # an id outside the window is caught by the kernel's own bounds check
+    bad = torch.tensor([3, w.n], dtype=torch.int32, device="cuda")
+    with pytest.raises(odb.OdbError) as e:
+        odb.odb_length_sketch(win, bad, 2, w.budget, ws)
+    assert e.value.status == odb.ODB_E_INVALID_DATA

@@ -60,6 +60,39 @@ class _Info(ctypes.Structure):
     ]
 
 
+class _StreamInfo(ctypes.Structure):
+    _fields_ = [
+        ("steps", ctypes.c_int64),
+        ("rounds", ctypes.c_int64),
+        ("emit_rounds", ctypes.c_int64),
+        ("skip_rounds", ctypes.c_int64),
+        ("stop_reason", ctypes.c_int32),
+        ("reserved0", ctypes.c_int32),
+        ("views", ctypes.c_int64),
+        ("emitted_views", ctypes.c_int64),
+        ("undelivered_views", ctypes.c_int64),
+        ("pending_views", ctypes.c_int64),
+        ("real_tokens", ctypes.c_int64),
+        ("padded_elems", ctypes.c_int64),
+        ("max_step_samples", ctypes.c_int64),
+        ("splits", ctypes.c_int64),
+        ("overflow_groups", ctypes.c_int64),
+        ("missing_ids", ctypes.c_int64),
+        ("duplicate_ids", ctypes.c_int64),
+        ("bad_views", ctypes.c_int64),
+        ("second_gather_rounds", ctypes.c_int64),
+        ("max_outstanding", ctypes.c_int64),
+        ("pad_fraction", ctypes.c_double),
+    ]
+
+
+class _StreamRound(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("reserved0", ctypes.c_int32), ("target", ctypes.c_int64),
+                ("emitted", ctypes.c_int64), ("phi", ctypes.c_int64)]
+
+
+ROUND_EMIT, ROUND_SKIP, ROUND_STOP = 0, 1, 2
+
 _lib = None
 
 
@@ -86,6 +119,13 @@ def _load():
         lib.oracle_slots_approx.argtypes = [P, P]
         lib.oracle_loss_weights.argtypes = [P, ctypes.c_int32, P, P, P]
         lib.oracle_loss_weights.restype = ctypes.c_int
+        lib.oracle_stream.restype = P
+        lib.oracle_stream.argtypes = [ctypes.c_int32, ctypes.c_int64, P, P, ctypes.c_int64, ctypes.c_int32,
+                                      ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, P, P, ctypes.c_int64]
+        lib.oracle_stream_free.argtypes = [P]
+        lib.oracle_stream_info.argtypes = [P, ctypes.POINTER(_StreamInfo)]
+        lib.oracle_stream_trace.argtypes = [P, P]
+        lib.oracle_stream_views.argtypes = [P, P, P, P]
         _lib = lib
     return _lib
 
@@ -287,3 +327,94 @@ def length_sketch(tok_off: np.ndarray, ids: Optional[np.ndarray], budget: int) -
     out.update(short_samples=short, sum_len=s1, sum_sq=s2, min_len=min(lens), max_len=max(lens),
                mean=s1 / n, cv=cv, short_fraction=short / n, high_roi=int(cv >= 0.8 or short / n > 0.2))
     return out
+
+
+class StreamPlan(Plan):
+    """One logical iteration of the unified loop: a window-format plan over identities
+    plus the streaming record (``sinfo``, per-round ``trace``, emitted and un-emitted
+    views)."""
+
+    def __init__(self, handle, W, N, sinfo, trace, emit_views, left_views, left_off):
+        lib = _load()
+        info = _Info()
+        lib.oracle_info(ctypes.c_void_p(handle), ctypes.byref(info))
+        d = {f: getattr(info, f) for f, _ in _Info._fields_}
+        S = d["steps"]
+        K = W * S
+        rows = np.empty(K, np.int32)
+        mx = np.empty(K, np.int32)
+        ro = np.empty(K + 1, np.int64)
+        to = np.empty(K + 1, np.int64)
+        tk = np.empty(K, np.int64)
+        lib.oracle_slots(ctypes.c_void_p(handle), _ptr(rows), _ptr(mx), _ptr(ro), _ptr(to), _ptr(tk))
+        ta = np.empty(K, np.float64)
+        lib.oracle_slots_approx(ctypes.c_void_p(handle), _ptr(ta))
+        emit = np.empty(d["emitted_samples"], np.int32)
+        left = np.empty(d["leftover_samples"], np.int32)
+        loff = np.empty(W + 1, np.int64)
+        lib.oracle_emit(ctypes.c_void_p(handle), _ptr(emit), _ptr(left), _ptr(loff))
+        z32, z64 = np.zeros(0, np.int32), np.zeros(0, np.int64)
+        super().__init__(W, N, d, z32, z32, z32, z32, rows, mx, ro, to, tk, ta, emit, left, loff, z64,
+                         _handle=0)
+        self._stream_handle = handle
+        self.sinfo = sinfo
+        self.trace = trace
+        self.emit_views = emit_views
+        self.left_views = left_views
+        self.left_off = left_off
+
+    @property
+    def _h(self):
+        return self._stream_handle
+
+    def __del__(self):
+        if getattr(self, "_stream_handle", 0) and _lib is not None:
+            _lib.oracle_stream_free(ctypes.c_void_p(self._stream_handle))
+            self._stream_handle = 0
+
+    def loss_weights(self, mode: int = WEIGHT_TOKEN_EXACT):
+        self._handle = self._stream_handle
+        try:
+            return super().loss_weights(mode)
+        finally:
+            self._handle = 0
+
+    def collate(self, tok_off, tokens, pad_id: int = 0):
+        self._handle = self._stream_handle
+        try:
+            return super().collate(tok_off, tokens, pad_id)
+        finally:
+            self._handle = 0
+
+
+def stream(tok_off, perm, W: int, budget: int, mode: int = MODE_JOIN, quota: int = 0, buffer_size: int = 1024,
+           depth: Optional[int] = None, rate=None, capacity=None, max_rounds: int = 1 << 40) -> StreamPlan:
+    """One logical iteration of the unified loop (Sec. 2.3, App. C) over identities
+    0..N-1 with lengths from ``tok_off``, the shuffled identity list ``perm``, ``W``
+    ranks, the collate buffer size, the outstanding-depth envelope ``depth`` (default
+    buffer_size) and per-rank arrival rates (views per round, default buffer_size)."""
+    lib = _load()
+    tok_off = np.ascontiguousarray(tok_off, dtype=np.int64)
+    N = len(tok_off) - 1
+    perm = np.ascontiguousarray(perm, dtype=np.int32)
+    if len(perm) != N:
+        raise OracleError("perm must hold N entries")
+    depth = buffer_size if depth is None else int(depth)
+    rate = np.full(W, buffer_size, np.int32) if rate is None else np.ascontiguousarray(rate, dtype=np.int32)
+    cap = None if capacity is None else np.ascontiguousarray(capacity, dtype=np.int64)
+    h = lib.oracle_stream(int(W), N, _ptr(tok_off), _ptr(perm), int(budget), int(mode), int(quota),
+                          int(buffer_size), int(depth), _ptr(rate), _ptr(cap), int(max_rounds))
+    if not h:
+        raise OracleError(lib.oracle_last_error().decode())
+    si = _StreamInfo()
+    lib.oracle_stream_info(ctypes.c_void_p(h), ctypes.byref(si))
+    sinfo = {f: getattr(si, f) for f, _ in _StreamInfo._fields_ if f != "reserved0"}
+    tr = (_StreamRound * max(sinfo["rounds"], 1))()
+    lib.oracle_stream_trace(ctypes.c_void_p(h), ctypes.cast(tr, ctypes.c_void_p))
+    trace = np.array([(tr[i].kind, tr[i].target, tr[i].emitted, tr[i].phi) for i in range(sinfo["rounds"])],
+                     dtype=np.int64).reshape(-1, 4)
+    ev = np.empty(sinfo["emitted_views"], np.int32)
+    lv = np.empty(sinfo["views"] - sinfo["emitted_views"], np.int32)
+    lo = np.empty(W + 1, np.int64)
+    lib.oracle_stream_views(ctypes.c_void_p(h), _ptr(ev), _ptr(lv), _ptr(lo))
+    return StreamPlan(h, int(W), N, sinfo, trace, ev, lv, lo)

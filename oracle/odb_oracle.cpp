@@ -391,6 +391,307 @@ bool run(Result& R, int32_t W, int64_t n, const int64_t* rank_off, const int64_t
     return true;
 }
 
+// ------------------------------------------------------------------ unified loop
+// The streaming protocol of Sec. 2.3 ("Unified loop and termination") and App. C/F,
+// with the per-rank state of App. C: sampler-pending views R_r, the collate buffer B_r
+// (the worker queue is folded into it: a fetched view lands in the buffer in the same
+// round), and emitted views E_r.
+//   reading (sampler): the shuffled identity list perm[0..N) is padded to
+//     M = W * ceil(N / W) views with its own head (perm[0..M-N)), and view m belongs to
+//     rank m mod W (stride sharding); a rank visits its views in increasing m.
+//   reading (arrivals): in every round rank r moves up to rate[r] views from R_r to B_r,
+//     in sampler order, without exceeding the outstanding-depth envelope |B_r| <= D.
+//   reading (status): a rank is finished when R_r and B_r are empty (n_groups = -1); it
+//     is ready when |B_r| >= buffer_size or R_r is empty and B_r is not; a ready rank
+//     groups its whole buffer (n_groups = G_r > 0), an unready one reports 0.
+//   reading (round kinds): join stops when every rank is finished; non-join stops when
+//     any rank is finished (logical stop) or the quota is reached.  Otherwise, if some
+//     unfinished rank is not ready the round is a skip round (no rank emits); else every
+//     ready rank's buffer is grouped (Sec. 2.2), aligned (Eq. 3 over the ready ranks,
+//     Algorithm 1) and emitted, finished ranks send IDLE slots, and overflow stays in B.
+//   Ties in the length order break by view index m.
+struct StreamInfo {
+    int64_t steps;
+    int64_t rounds;              // protocol rounds including the one that observed the stop
+    int64_t emit_rounds;
+    int64_t skip_rounds;
+    int32_t stop_reason;
+    int32_t reserved0;
+    int64_t views;               // M
+    int64_t emitted_views;
+    int64_t undelivered_views;   // fetched but not emitted at the stop (sum over ranks of |B_r|)
+    int64_t pending_views;       // never fetched (sum of |R_r|)
+    int64_t real_tokens;
+    int64_t padded_elems;
+    int64_t max_step_samples;
+    int64_t splits;
+    int64_t overflow_groups;
+    int64_t missing_ids;
+    int64_t duplicate_ids;
+    int64_t bad_views;
+    int64_t second_gather_rounds;
+    int64_t max_outstanding;     // largest |B_r| seen after a fetch
+    double pad_fraction;
+};
+
+struct StreamRound {
+    int32_t kind;      // 0 emit, 1 skip, 2 stop
+    int32_t reserved0;
+    int64_t target;    // T of an emit round, 0 otherwise
+    int64_t emitted;   // views emitted in the round
+    int64_t phi;       // potential after the round: views not yet emitted (App. C, Lyapunov)
+};
+
+struct StreamResult : Result {                      // the plan: slots hold identities
+    StreamInfo sinfo{};
+    std::vector<StreamRound> trace;
+    std::vector<std::vector<int32_t>> emit_views;  // per rank, slot order, row order
+    std::vector<std::vector<int32_t>> left_views;  // per rank, increasing m
+};
+
+bool run_stream(StreamResult& SR, int32_t W, int64_t N, const int64_t* tok_off, const int32_t* perm,
+                int64_t L_max, int32_t mode, int64_t quota, int64_t buffer_size, int64_t depth,
+                const int32_t* rate, const int64_t* capacity, int64_t max_rounds) {
+    if (W < 1) return fail("W must be >= 1");
+    if (N < 0 || N >= (int64_t)std::numeric_limits<int32_t>::max() / 2) return fail("N out of range");
+    if (L_max < 1) return fail("budget must be >= 1");
+    if (mode != MODE_JOIN && mode != MODE_NONJOIN) return fail("bad mode");
+    if (mode == MODE_NONJOIN && quota < 1) return fail("quota must be >= 1 in non-join mode");
+    if (buffer_size < 1 || depth < buffer_size) return fail("need 1 <= buffer_size <= depth");
+    for (int32_t r = 0; r < W; ++r)
+        if (rate[r] < 1) return fail("rate must be >= 1");
+    if (capacity)
+        for (int32_t r = 0; r < W; ++r)
+            if (capacity[r] < 0) return fail("capacity must be >= 0");
+    Result& R = SR;
+    R.W = W;
+    R.n = N;
+    R.len.resize((size_t)N);
+    for (int64_t i = 0; i < N; ++i) {
+        int64_t l = tok_off[i + 1] - tok_off[i];
+        if (l < 1 || l > (int64_t)std::numeric_limits<int32_t>::max())
+            return fail("sample " + std::to_string(i) + " has invalid length " + std::to_string(l));
+        R.len[(size_t)i] = l;
+    }
+    std::vector<char> seen((size_t)N, 0);
+    for (int64_t i = 0; i < N; ++i) {
+        if (perm[i] < 0 || perm[i] >= N || seen[(size_t)perm[i]]) return fail("perm is not a permutation");
+        seen[(size_t)perm[i]] = 1;
+    }
+    const int64_t q = N > 0 ? (N + W - 1) / W : 0;   // views per rank
+    const int64_t M = q * W;
+    std::vector<int32_t> ident((size_t)M);
+    std::vector<int64_t> vlen((size_t)M);
+    for (int64_t m = 0; m < M; ++m) {
+        ident[(size_t)m] = perm[m < N ? m : m - N];
+        vlen[(size_t)m] = R.len[(size_t)ident[(size_t)m]];
+    }
+    std::vector<int64_t> cursor((size_t)W, 0);          // next sampler position of each rank
+    std::vector<std::vector<int32_t>> buf((size_t)W);   // B_r (view ids)
+    R.slots.assign((size_t)W, {});
+    R.slots_approx.assign((size_t)W, {});
+    SR.emit_views.assign((size_t)W, {});
+    std::vector<int64_t> pos((size_t)M, -1);
+    StreamInfo& I = SR.sinfo;
+    I.views = M;
+    int64_t S = 0, emitted = 0;
+    int32_t stop = STOP_DRAINED;
+    for (;;) {
+        if (I.rounds >= max_rounds) return fail("max_rounds exceeded");
+        I.rounds += 1;
+        // fetch (R -> B), bounded by the rank's rate and the envelope
+        for (int32_t r = 0; r < W; ++r) {
+            int64_t room = depth - (int64_t)buf[(size_t)r].size();
+            int64_t f = std::min<int64_t>({(int64_t)rate[r], room, q - cursor[(size_t)r]});
+            for (int64_t i = 0; i < f; ++i) buf[(size_t)r].push_back((int32_t)((cursor[(size_t)r] + i) * W + r));
+            cursor[(size_t)r] += std::max<int64_t>(f, 0);
+            I.max_outstanding = std::max(I.max_outstanding, (int64_t)buf[(size_t)r].size());
+        }
+        int32_t finished = 0, unready = 0;
+        std::vector<char> ready((size_t)W, 0);
+        for (int32_t r = 0; r < W; ++r) {
+            bool drained = cursor[(size_t)r] == q;
+            bool fin = drained && buf[(size_t)r].empty();
+            finished += fin ? 1 : 0;
+            ready[(size_t)r] = !fin && ((int64_t)buf[(size_t)r].size() >= buffer_size || drained);
+            unready += (!fin && !ready[(size_t)r]) ? 1 : 0;
+        }
+        StreamRound rec{};
+        if (finished == W) {
+            stop = STOP_DRAINED;
+            rec.kind = 2;
+        } else if (mode == MODE_NONJOIN && finished > 0) {
+            stop = STOP_RANK_FINISHED;
+            rec.kind = 2;
+        } else if (unready > 0) {
+            rec.kind = 1;
+        }
+        if (rec.kind != 0) {
+            rec.phi = M - emitted;
+            SR.trace.push_back(rec);
+            if (rec.kind == 2) break;
+            I.skip_rounds += 1;
+            continue;
+        }
+        I.emit_rounds += 1;
+        // group every ready buffer (Sec. 2.2) into the paper's short-to-long list
+        std::vector<GroupList> list((size_t)W);
+        std::vector<double> mean_len((size_t)W, 0.0);
+        for (int32_t r = 0; r < W; ++r) {
+            if (!ready[(size_t)r]) continue;
+            std::vector<int32_t> visit;
+            list[(size_t)r] = paper_list_order(form_groups(buf[(size_t)r], vlen, L_max, &visit));
+            for (size_t p = 0; p < visit.size(); ++p) pos[(size_t)visit[p]] = (int64_t)p;
+            int64_t tok = 0;
+            for (int32_t v : buf[(size_t)r]) tok += vlen[(size_t)v];
+            mean_len[(size_t)r] = (double)tok / (double)buf[(size_t)r].size();
+        }
+        // Eq. 3 over the ready ranks
+        int64_t maxG = 0, minC = 0, minS = 0;
+        for (int32_t r = 0; r < W; ++r) {
+            int64_t G = (int64_t)list[(size_t)r].size();
+            if (G <= 0) continue;
+            maxG = std::max(maxG, G);
+            int64_t Sr = (int64_t)buf[(size_t)r].size();
+            minS = (minS == 0) ? Sr : std::min(minS, Sr);
+            if (capacity && capacity[r] > 0) minC = (minC == 0) ? capacity[r] : std::min(minC, capacity[r]);
+        }
+        int64_t T = maxG;
+        if (minC > 0) T = std::min(T, minC);
+        if (minS > 0) T = std::min(T, minS);
+        T = std::max<int64_t>(T, 1);
+        bool noop = true;
+        std::vector<std::vector<int32_t>> returned((size_t)W);
+        for (int32_t r = 0; r < W; ++r) {
+            GroupList& L = list[(size_t)r];
+            int64_t G = (int64_t)L.size();
+            if (G == 0) continue;
+            if (G != T) noop = false;
+            if (G < T) {
+                I.splits += split_to(L, T);
+            } else if (G > T) {
+                I.overflow_groups += G - T;
+                overflow_to(L, T, returned[(size_t)r]);
+            }
+            canonicalize(L, pos);
+        }
+        if (!noop) I.second_gather_rounds += 1;
+        int64_t cut = T;
+        bool quota_hit = false;
+        int64_t round_emitted = 0;
+        for (int64_t j = 0; j < T; ++j) {
+            int64_t step = 0;
+            for (int32_t r = 0; r < W; ++r)
+                if (!list[(size_t)r].empty()) step += (int64_t)list[(size_t)r][(size_t)j].size();
+            emitted += step;
+            round_emitted += step;
+            I.max_step_samples = std::max(I.max_step_samples, step);
+            if (mode == MODE_NONJOIN && emitted >= quota) {
+                cut = j + 1;
+                quota_hit = true;
+                break;
+            }
+        }
+        for (int32_t r = 0; r < W; ++r) {
+            GroupList& L = list[(size_t)r];
+            std::vector<int32_t> keep;
+            for (int64_t j = 0; j < cut; ++j) {
+                Group ids;
+                if (!L.empty())
+                    for (int32_t v : L[(size_t)j]) {
+                        ids.push_back(ident[(size_t)v]);
+                        SR.emit_views[(size_t)r].push_back(v);
+                    }
+                R.slots[(size_t)r].push_back(ids);
+                R.slots_approx[(size_t)r].push_back(L.empty() ? 0.0 : (double)L[(size_t)j].size() * mean_len[(size_t)r]);
+            }
+            if (!ready[(size_t)r]) continue;   // a finished rank's buffer is empty
+            for (size_t j = (size_t)cut; j < L.size(); ++j)
+                for (int32_t v : L[j]) keep.push_back(v);
+            for (int32_t v : returned[(size_t)r]) keep.push_back(v);
+            buf[(size_t)r] = keep;
+        }
+        S += cut;
+        rec.kind = 0;
+        rec.target = T;
+        rec.emitted = round_emitted;
+        rec.phi = M - emitted;
+        SR.trace.push_back(rec);
+        if (quota_hit) {
+            stop = STOP_QUOTA;
+            break;
+        }
+    }
+    I.steps = S;
+    I.stop_reason = stop;
+    I.emitted_views = emitted;
+    // Stats as in the window pipeline (real tokens, padded area, pad fraction).
+    for (int32_t r = 0; r < W; ++r)
+        for (const Group& g : R.slots[(size_t)r]) {
+            int64_t mx = 0;
+            for (int32_t x : g) {
+                I.real_tokens += R.len[(size_t)x];
+                mx = std::max(mx, R.len[(size_t)x]);
+            }
+            I.padded_elems += mx * (int64_t)g.size();
+        }
+    I.pad_fraction = I.padded_elems > 0 ? 1.0 - (double)I.real_tokens / (double)I.padded_elems : 0.0;
+    // Undelivered and pending views, and the No-Leak check over every view's state.
+    std::vector<int32_t> state((size_t)M, 0);
+    for (int32_t r = 0; r < W; ++r) {
+        for (int32_t v : SR.emit_views[(size_t)r]) state[(size_t)v] += 1;
+        for (int32_t v : buf[(size_t)r]) state[(size_t)v] += 1;
+        for (int64_t i = cursor[(size_t)r]; i < q; ++i) state[(size_t)(i * W + r)] += 1;
+        I.undelivered_views += (int64_t)buf[(size_t)r].size();
+        I.pending_views += q - cursor[(size_t)r];
+    }
+    SR.left_views.assign((size_t)W, {});
+    R.leftover.assign((size_t)W, {});
+    std::vector<char> is_emitted((size_t)M, 0);
+    for (int32_t r = 0; r < W; ++r)
+        for (int32_t v : SR.emit_views[(size_t)r]) is_emitted[(size_t)v] = 1;
+    for (int32_t r = 0; r < W; ++r)
+        for (int64_t i = 0; i < q; ++i) {
+            int32_t v = (int32_t)(i * W + r);
+            if (!is_emitted[(size_t)v]) {
+                SR.left_views[(size_t)r].push_back(v);
+                R.leftover[(size_t)r].push_back(ident[(size_t)v]);
+            }
+        }
+    std::vector<int64_t> id_count((size_t)N, 0);
+    for (int64_t m = 0; m < M; ++m) {
+        if (state[(size_t)m] != 1) I.bad_views += 1;
+        id_count[(size_t)ident[(size_t)m]] += 1;   // every view is emitted or left over
+    }
+    // identity coverage of what was emitted (join: every identity, P duplicates)
+    std::vector<int64_t> emit_count((size_t)N, 0);
+    for (int32_t r = 0; r < W; ++r)
+        for (int32_t v : SR.emit_views[(size_t)r]) emit_count[(size_t)ident[(size_t)v]] += 1;
+    for (int64_t d = 0; d < N; ++d) {
+        if (emit_count[(size_t)d] == 0) I.missing_ids += 1;
+        if (emit_count[(size_t)d] > 1) I.duplicate_ids += emit_count[(size_t)d] - 1;
+    }
+    // the window-level summary the shared accessors read
+    Info& PI = R.info;
+    PI.steps = S;
+    PI.rounds = (int32_t)std::min<int64_t>(I.emit_rounds, std::numeric_limits<int32_t>::max());
+    PI.stop_reason = stop;
+    PI.emitted_samples = emitted;
+    PI.leftover_samples = M - emitted;
+    PI.real_tokens = I.real_tokens;
+    PI.padded_elems = I.padded_elems;
+    PI.max_step_samples = I.max_step_samples;
+    PI.splits = I.splits;
+    PI.overflow_groups = I.overflow_groups;
+    PI.missing_ids = I.missing_ids;
+    PI.duplicate_ids = I.duplicate_ids;
+    PI.bad_views = I.bad_views;
+    PI.pad_fraction = I.pad_fraction;
+    PI.second_gather_rounds = I.second_gather_rounds;
+    R.rank_off.assign((size_t)W + 1, 0);
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -574,6 +875,50 @@ int oracle_collate_rank(void* h, int32_t r, const int64_t* tok_off, const int32_
     const int64_t base = tok_off[R.rank_off[(size_t)r]];
     collate_ranks(R, r, r + 1, tok_off, tokens, base, pad_id, input_ids, labels, attention_mask, position_ids);
     return 0;
+}
+
+// ------------------------------------------------------------------ unified loop API
+// One logical iteration of the streaming protocol over identities 0..N-1 (lengths from
+// tok_off).  Returns a handle whose plan the window accessors above read (slots hold
+// identities; leftover lists the identities of un-emitted views), or NULL.
+void* oracle_stream(int32_t W, int64_t N, const int64_t* tok_off, const int32_t* perm, int64_t budget,
+                    int32_t mode, int64_t quota, int64_t buffer_size, int64_t depth, const int32_t* rate,
+                    const int64_t* capacity, int64_t max_rounds) {
+    StreamResult* SR = new (std::nothrow) StreamResult();
+    if (!SR) return nullptr;
+    if (!run_stream(*SR, W, N, tok_off, perm, budget, mode, quota, buffer_size, depth, rate, capacity,
+                    max_rounds)) {
+        delete SR;
+        return nullptr;
+    }
+    // the handle is the window plan it contains, so every window accessor applies
+    return static_cast<Result*>(SR);
+}
+
+static StreamResult* stream_of(void* h) { return static_cast<StreamResult*>(static_cast<Result*>(h)); }
+
+void oracle_stream_free(void* h) { delete stream_of(h); }
+
+void oracle_stream_info(void* h, StreamInfo* out) { *out = stream_of(h)->sinfo; }
+
+// Per-round trace; out must hold info.rounds records.
+void oracle_stream_trace(void* h, StreamRound* out) {
+    const StreamResult* SR = stream_of(h);
+    std::copy(SR->trace.begin(), SR->trace.end(), out);
+}
+
+// Emitted views (rank-major, slot order, row order) and un-emitted views per rank in
+// increasing view index, with left_off[W + 1].
+void oracle_stream_views(void* h, int32_t* emit_views, int32_t* left_views, int64_t* left_off) {
+    const StreamResult* SR = stream_of(h);
+    int64_t e = 0, o = 0;
+    for (const auto& v : SR->emit_views)
+        for (int32_t x : v) emit_views[e++] = x;
+    for (size_t r = 0; r < SR->left_views.size(); ++r) {
+        left_off[r] = o;
+        for (int32_t x : SR->left_views[r]) left_views[o++] = x;
+    }
+    left_off[SR->left_views.size()] = o;
 }
 
 }  // extern "C"

@@ -12,6 +12,9 @@
  *   odb_loss_weights  per-step, per-rank loss-scaling weights          (Eq. 2, App. B)
  *   odb_length_sketch CV and short-sample fraction of sketched lengths  (Sec. 1, practical
  *                     (return-on-investment screen)                      guidance section)
+ *   odb_stream_plan   the unified streaming loop: one logical sampler    (Sec. 2.3, App. C,
+ *                     iteration, round by round (fetch, skip, emit,       App. F)
+ *                     stop), into the same plan layout
  *
  * Conventions shared by every entry point
  *   - Pointers named d_* are device pointers (HIP global memory on the current device);
@@ -200,8 +203,9 @@ int odb_align_groups(const odb_window_t* w, int64_t budget, const odb_align_para
  *   c <  l_s : input_ids = labels = token c of s, attention_mask = 1, position_ids = c
  *   c >= l_s : input_ids = pad_id, labels = -100, attention_mask = 0, position_ids = 0
  *
- *   num_slots           W * S from odb_align_groups (>= 0)
- *   plan arrays         as written by odb_align_groups (device)
+ *   num_slots           W * S from odb_align_groups or odb_stream_plan (>= 0)
+ *   plan arrays         as written by odb_align_groups or odb_stream_plan (device); the
+ *                       emitted rows number at most n + W - 1 (sampler padding views)
  *   out_capacity_elems  length of each output array; elements beyond it are not written
  *   d_ws / ws_bytes     the workspace (only a small status word is used)
  *
@@ -295,6 +299,103 @@ typedef struct odb_length_sketch {
  */
 int odb_length_sketch(const odb_window_t* w, const int32_t* d_ids, int64_t count, int64_t budget,
                       odb_length_sketch_t* h_out, void* d_ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------- unified loop */
+
+/* Parameters of one logical sampler iteration of the streaming protocol. */
+typedef struct odb_stream_params {
+    int32_t mode;                  /* odb_mode_t: join (drain, then stop) or non-join quota  */
+    int32_t buffer_size;           /* views a rank collects before it groups, >= 1           */
+    int32_t depth;                 /* outstanding-depth envelope D: most views a rank holds
+                                      fetched but not emitted; buffer_size <= D <= 4096      */
+    int32_t reserved0;             /* must be 0                                              */
+    int64_t quota;                 /* non-join sample quota Q >= 1                           */
+    const int32_t* rate;           /* HOST [W] views rank r's workers deliver per round, >= 1 */
+    const int64_t* slot_capacity;  /* HOST [W] output-slot capacity C_r >= 0, or NULL        */
+    int64_t max_rounds;            /* protocol rounds (>= 1) after which the call fails; also
+                                      the length of the workspace's round record             */
+} odb_stream_params_t;
+
+/* One protocol round. */
+typedef struct odb_stream_round {
+    int32_t kind;                  /* 0 emit, 1 skip (some unfinished rank not ready), 2 stop */
+    int32_t reserved0;
+    int64_t target;                /* T of an emit round, else 0                             */
+    int64_t emitted;               /* views emitted in the round (after a quota cut)         */
+    int64_t phi;                   /* potential after the round: views not yet emitted      */
+} odb_stream_round_t;
+
+/* Summary of one logical iteration. */
+typedef struct odb_stream_info {
+    int64_t steps;                 /* S: aligned steps                                       */
+    int64_t rounds;                /* protocol rounds, including the one that saw the stop   */
+    int64_t emit_rounds;
+    int64_t skip_rounds;
+    int32_t stop_reason;           /* odb_stop_reason_t                                      */
+    int32_t reserved0;
+    int64_t views;                 /* M = W * ceil(N / W) sampler views                      */
+    int64_t emitted_views;
+    int64_t undelivered_views;     /* fetched but not emitted at the stop (eta_logical * N)  */
+    int64_t pending_views;         /* never fetched                                          */
+    int64_t real_tokens;
+    int64_t padded_elems;
+    int64_t max_step_samples;
+    int64_t splits;
+    int64_t overflow_groups;
+    int64_t missing_ids;           /* identities with no emitted view                        */
+    int64_t duplicate_ids;         /* emitted views beyond the first of their identity       */
+    int64_t bad_views;             /* views emitted more than once (0 unless the library errs) */
+    int64_t second_gather_rounds;  /* emit rounds in which some ready rank had G_r != T     */
+    int64_t max_outstanding;       /* largest |B_r| after a fetch (<= depth)                 */
+    double  pad_fraction;
+    int64_t required_slot_capacity;/* W * S; set on ODB_E_CAPACITY and on success            */
+} odb_stream_info_t;
+
+/* Bytes of device workspace odb_stream_plan needs (0 for invalid arguments).  The
+ * workspace starts with the window workspace, so odb_collate can reuse it. */
+size_t odb_stream_workspace_size(const odb_window_t* w, int32_t depth, int64_t slot_capacity,
+                                 int64_t max_rounds);
+
+/*
+ * One logical iteration of the unified loop (Sec. 2.3 "Unified loop and termination",
+ * App. C state and transition rules, App. F state machine) over the window's samples
+ * taken as dataset identities 0..N-1 (rank_offsets of the window are not used; W is
+ * num_ranks).
+ *
+ * Sampler: d_perm [N] is the iteration's shuffled identity list (a permutation, drawn by
+ * the caller); it is padded by repeating it from its head to M = W * ceil(N / W) views,
+ * view m has identity perm[m mod N] and belongs to rank m mod W (stride sharding), and a
+ * rank visits its views in increasing m.
+ * Round: every rank moves up to rate[r] views into its buffer (never above depth); a rank
+ * is finished when it has nothing pending or buffered, ready when its buffer holds
+ * buffer_size views or nothing is pending.  Join stops when every rank is finished,
+ * non-join when any is (or at the quota).  Otherwise, if an unfinished rank is not ready
+ * the round is a skip round; else every ready rank groups its whole buffer (Sec. 2.2,
+ * ties by view index), T follows Eq. 3 over the ready ranks (S_r = buffered views), and
+ * Algorithm 1 splits or overflows; each ready rank emits T steps, finished ranks IDLE
+ * slots, and overflow stays buffered.  Non-join stops after the first step at which the
+ * cumulative emitted count reaches `quota`.
+ *
+ * Outputs use the plan layout of odb_align_groups (slot k = r * S + j; rows of a group
+ * from its shortest member), so odb_collate and odb_loss_weights take them unchanged:
+ *   d_emit_order     [M] out: identities of the emitted views, slot order, row order
+ *   d_emit_views     [M] out: the emitted views themselves
+ *   slot arrays      as odb_align_groups, capacity slot_capacity (W * S needed)
+ *   d_left_views     [M] out: un-emitted views, per rank in increasing view index
+ *   d_left_off       [W+1] out
+ *   h_trace          [max_rounds] host out, or NULL: one record per round
+ * Synchronises `stream` once per 32 rounds and at the end.  Returns ODB_E_CAPACITY if
+ * slot_capacity < W * S (required_slot_capacity tells the size) or the iteration needs
+ * more than max_rounds rounds, ODB_E_INVALID_DATA for a perm entry outside [0, N) or a
+ * sample length < 1.
+ */
+int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int64_t budget,
+                    const odb_stream_params_t* params, int64_t slot_capacity,
+                    int32_t* d_emit_order, int32_t* d_emit_views, int32_t* d_slot_rows,
+                    int32_t* d_slot_maxlen, int64_t* d_slot_row_off, int64_t* d_slot_tile_off,
+                    int64_t* d_slot_tokens, double* d_slot_tokens_approx, int32_t* d_left_views,
+                    int64_t* d_left_off, odb_stream_round_t* h_trace, odb_stream_info_t* h_info,
+                    void* d_ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

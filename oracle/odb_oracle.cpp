@@ -397,8 +397,9 @@ bool run(Result& R, int32_t W, int64_t n, const int64_t* rank_off, const int64_t
 // (the worker queue is folded into it: a fetched view lands in the buffer in the same
 // round), and emitted views E_r.
 //   reading (sampler): the shuffled identity list perm[0..N) is padded to
-//     M = W * ceil(N / W) views with its own head (perm[0..M-N)), and view m belongs to
-//     rank m mod W (stride sharding); a rank visits its views in increasing m.
+//     M = W * ceil(N / W) views by repeating it from its head (view m has identity
+//     perm[m mod N]), and view m belongs to rank m mod W (stride sharding); a rank visits
+//     its views in increasing m.
 //   reading (arrivals): in every round rank r moves up to rate[r] views from R_r to B_r,
 //     in sampler order, without exceeding the outstanding-depth envelope |B_r| <= D.
 //   reading (status): a rank is finished when R_r and B_r are empty (n_groups = -1); it
@@ -483,7 +484,7 @@ bool run_stream(StreamResult& SR, int32_t W, int64_t N, const int64_t* tok_off, 
     std::vector<int32_t> ident((size_t)M);
     std::vector<int64_t> vlen((size_t)M);
     for (int64_t m = 0; m < M; ++m) {
-        ident[(size_t)m] = perm[m < N ? m : m - N];
+        ident[(size_t)m] = perm[m % N];
         vlen[(size_t)m] = R.len[(size_t)ident[(size_t)m]];
     }
     std::vector<int64_t> cursor((size_t)W, 0);          // next sampler position of each rank

@@ -38,7 +38,7 @@ ODB_WEIGHT_SAMPLE, ODB_WEIGHT_TOKEN_APPROX, ODB_WEIGHT_TOKEN_EXACT = 0, 1, 2
 EXPORTED = [
     "odb_status_string", "odb_last_error_message", "odb_workspace_size", "odb_form_groups",
     "odb_align_groups", "odb_collate", "odb_collate_status", "odb_check_coverage", "odb_loss_weights",
-    "odb_length_sketch",
+    "odb_length_sketch", "odb_stream_workspace_size", "odb_stream_plan",
 ]
 
 
@@ -111,6 +111,54 @@ class LengthSketch(ctypes.Structure):
     ]
 
 
+class StreamParams(ctypes.Structure):
+    _fields_ = [
+        ("mode", ctypes.c_int32),
+        ("buffer_size", ctypes.c_int32),
+        ("depth", ctypes.c_int32),
+        ("reserved0", ctypes.c_int32),
+        ("quota", ctypes.c_int64),
+        ("rate", ctypes.c_void_p),
+        ("slot_capacity", ctypes.c_void_p),
+        ("max_rounds", ctypes.c_int64),
+    ]
+
+
+class StreamRound(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("reserved0", ctypes.c_int32), ("target", ctypes.c_int64),
+                ("emitted", ctypes.c_int64), ("phi", ctypes.c_int64)]
+
+
+class StreamInfo(ctypes.Structure):
+    _fields_ = [
+        ("steps", ctypes.c_int64),
+        ("rounds", ctypes.c_int64),
+        ("emit_rounds", ctypes.c_int64),
+        ("skip_rounds", ctypes.c_int64),
+        ("stop_reason", ctypes.c_int32),
+        ("reserved0", ctypes.c_int32),
+        ("views", ctypes.c_int64),
+        ("emitted_views", ctypes.c_int64),
+        ("undelivered_views", ctypes.c_int64),
+        ("pending_views", ctypes.c_int64),
+        ("real_tokens", ctypes.c_int64),
+        ("padded_elems", ctypes.c_int64),
+        ("max_step_samples", ctypes.c_int64),
+        ("splits", ctypes.c_int64),
+        ("overflow_groups", ctypes.c_int64),
+        ("missing_ids", ctypes.c_int64),
+        ("duplicate_ids", ctypes.c_int64),
+        ("bad_views", ctypes.c_int64),
+        ("second_gather_rounds", ctypes.c_int64),
+        ("max_outstanding", ctypes.c_int64),
+        ("pad_fraction", ctypes.c_double),
+        ("required_slot_capacity", ctypes.c_int64),
+    ]
+
+    def as_dict(self) -> dict:
+        return {f: getattr(self, f) for f, _ in self._fields_ if f != "reserved0"}
+
+
 _lib = None
 
 
@@ -145,6 +193,11 @@ def load():
         lib.odb_loss_weights.argtypes = [I32, I64, I32, P, P, P, P, P, P, P]
         lib.odb_length_sketch.restype = ctypes.c_int
         lib.odb_length_sketch.argtypes = [W, P, I64, I64, ctypes.POINTER(LengthSketch), P, SZ, P]
+        lib.odb_stream_workspace_size.restype = SZ
+        lib.odb_stream_workspace_size.argtypes = [W, I32, I64, I64]
+        lib.odb_stream_plan.restype = ctypes.c_int
+        lib.odb_stream_plan.argtypes = [W, P, I64, ctypes.POINTER(StreamParams), I64, P, P, P, P, P, P, P, P, P, P,
+                                        P, ctypes.POINTER(StreamInfo), P, SZ, P]
         _lib = lib
     return _lib
 
@@ -372,3 +425,117 @@ class Pipeline:
         self.form(stream)
         self.align(stream)
         return self.collate(stream)
+
+
+def stream_round_bound(num_samples: int, num_ranks: int, buffer_size: int, rate) -> int:
+    """Rounds one logical iteration can take: at most ceil(N/W) emitting rounds, between
+    them at most ceil(buffer_size / min rate) fill rounds, and the stop round."""
+    q = -(-int(num_samples) // int(num_ranks)) if num_samples else 0
+    fill = -(-int(buffer_size) // int(np.min(rate)))
+    return q + (q + 1) * fill + 2
+
+
+class StreamPipeline:
+    """Device buffers of one streaming iteration (odb_stream_plan) and its collate and
+    loss weights (odb_collate / odb_loss_weights on the streaming plan)."""
+
+    def __init__(self, win: DeviceWindow, perm, budget: int, buffer_size: int = 1024, depth: Optional[int] = None,
+                 rate=None, mode: str = "join", quota: int = 0, capacity=None, pad_id: int = 0,
+                 max_rounds: Optional[int] = None, slot_capacity: Optional[int] = None):
+        import torch
+
+        self.torch = torch
+        self.win = win
+        self.perm = perm
+        self.budget = int(budget)
+        W, N = win.num_ranks, win.num_samples
+        self.W, self.N = W, N
+        self.q = -(-N // W) if N else 0
+        self.M = self.q * W
+        depth = int(buffer_size if depth is None else depth)
+        rate = np.full(W, buffer_size, np.int32) if rate is None else np.ascontiguousarray(rate, dtype=np.int32)
+        self.rate = rate
+        self.cap = None if capacity is None else np.ascontiguousarray(capacity, dtype=np.int64)
+        if max_rounds is None:
+            max_rounds = stream_round_bound(N, W, buffer_size, rate)
+        self.params = StreamParams(ODB_MODE_NONJOIN_QUOTA if mode == "nonjoin" else ODB_MODE_JOIN, int(buffer_size),
+                                   depth, 0, int(quota), rate.ctypes.data_as(ctypes.c_void_p).value,
+                                   None if self.cap is None else self.cap.ctypes.data_as(ctypes.c_void_p).value,
+                                   int(max_rounds))
+        self.pad_id = int(pad_id)
+        dev = win.token_offsets.device
+        self.device = dev
+        m1 = max(self.M, 1)
+        self.emit_order = torch.empty(m1, dtype=torch.int32, device=dev)
+        self.emit_views = torch.empty(m1, dtype=torch.int32, device=dev)
+        self.left_views = torch.empty(m1, dtype=torch.int32, device=dev)
+        self.left_off = torch.empty(W + 1, dtype=torch.int64, device=dev)
+        self._alloc_slots(max(int(slot_capacity if slot_capacity is not None else W * max(self.q, 1)), W))
+        self.trace = (StreamRound * max(int(max_rounds), 1))()
+        self.info = None
+        self.outputs = None
+
+    def _alloc_slots(self, cap: int):
+        torch = self.torch
+        cap = (cap + self.W - 1) // self.W * self.W
+        self.slot_capacity = cap
+        d = self.device
+        self.slot_rows = torch.empty(cap, dtype=torch.int32, device=d)
+        self.slot_maxlen = torch.empty(cap, dtype=torch.int32, device=d)
+        self.slot_tokens = torch.empty(cap, dtype=torch.int64, device=d)
+        self.slot_tokens_approx = torch.empty(cap, dtype=torch.float64, device=d)
+        self.slot_row_off = torch.empty(cap + 1, dtype=torch.int64, device=d)
+        self.slot_tile_off = torch.empty(cap + 1, dtype=torch.int64, device=d)
+        size = load().odb_stream_workspace_size(self.win.ref, self.params.depth, cap, self.params.max_rounds)
+        if size == 0:
+            _check(ODB_E_INVALID_ARG)
+        self.ws = torch.empty(size, dtype=torch.uint8, device=d)
+
+    def _call(self, stream):
+        info = StreamInfo()
+        st = load().odb_stream_plan(self.win.ref, _dptr(self.perm), self.budget, ctypes.byref(self.params),
+                                    self.slot_capacity, _dptr(self.emit_order), _dptr(self.emit_views),
+                                    _dptr(self.slot_rows), _dptr(self.slot_maxlen), _dptr(self.slot_row_off),
+                                    _dptr(self.slot_tile_off), _dptr(self.slot_tokens),
+                                    _dptr(self.slot_tokens_approx), _dptr(self.left_views), _dptr(self.left_off),
+                                    ctypes.cast(self.trace, ctypes.c_void_p), ctypes.byref(info), _dptr(self.ws),
+                                    self.ws.numel(), _stream(stream))
+        return st, info.as_dict()
+
+    def plan(self, stream=None) -> dict:
+        st, info = self._call(stream)
+        if st == ODB_E_CAPACITY and info["required_slot_capacity"] > self.slot_capacity:
+            self._alloc_slots(int(info["required_slot_capacity"]))
+            st, info = self._call(stream)
+        _check(st)
+        self.info = info
+        return info
+
+    def trace_array(self) -> np.ndarray:
+        """Rounds as rows (kind, target, emitted, phi)."""
+        n = int(self.info["rounds"])
+        return np.array([(self.trace[i].kind, self.trace[i].target, self.trace[i].emitted, self.trace[i].phi)
+                         for i in range(n)], dtype=np.int64).reshape(-1, 4)
+
+    @property
+    def num_slots(self) -> int:
+        return self.W * int(self.info["steps"])
+
+    def collate(self, stream=None):
+        torch = self.torch
+        P = int(self.info["padded_elems"])
+        if self.outputs is None or self.outputs[0].numel() < max(P, 1):
+            self.outputs = tuple(torch.empty(max(P, 1), dtype=torch.int32, device=self.device) for _ in range(4))
+        odb_collate(self.win, self.num_slots, self.emit_order, self.slot_rows, self.slot_maxlen, self.slot_row_off,
+                    self.slot_tile_off, self.pad_id, P, *self.outputs, self.ws, stream)
+        return tuple(o[:P] for o in self.outputs)
+
+    def loss_weights(self, mode: int = ODB_WEIGHT_TOKEN_EXACT, stream=None):
+        torch = self.torch
+        S, K = int(self.info["steps"]), self.num_slots
+        wt = torch.empty(max(K, 1), dtype=torch.float64, device=self.device)
+        st = torch.empty(max(S, 1), dtype=torch.int64, device=self.device)
+        ss = torch.empty(max(S, 1), dtype=torch.int64, device=self.device)
+        odb_loss_weights(self.W, S, mode, self.slot_rows, self.slot_tokens, self.slot_tokens_approx, wt, st, ss,
+                         stream)
+        return wt[:K], st[:S], ss[:S]

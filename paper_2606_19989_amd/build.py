@@ -12,7 +12,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libodb.so")
-SOURCES = ["odb_common.hip", "odb_form.hip", "odb_align.hip", "odb_collate.hip", "odb_weights.hip", "odb_sketch.hip"]
+SOURCES = ["odb_common.hip", "odb_form.hip", "odb_align.hip", "odb_collate.hip", "odb_weights.hip", "odb_sketch.hip",
+           "odb_stream.hip"]
 ARCH = os.environ.get("ODB_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -44,14 +44,14 @@ constexpr int64_t kRunSteps = 128;                                   // consecut
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 __global__ void __launch_bounds__(kBlock) row_info_kernel(const int64_t* __restrict__ tok_off, int64_t n,
-                                                          const int32_t* __restrict__ emit,
+                                                          int64_t max_rows, const int32_t* __restrict__ emit,
                                                           const int64_t* __restrict__ row_off, int64_t num_slots,
                                                           int64_t* __restrict__ row_ts, int32_t* __restrict__ row_len,
                                                           int32_t* err) {
     int64_t rows = row_off[num_slots];
-    if (rows > n || rows < 0) {
+    if (rows > max_rows || rows < 0) {
         if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, 1);
-        rows = rows < 0 ? 0 : n;
+        rows = rows < 0 ? 0 : max_rows;
     }
     bool bad = false;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -83,7 +83,8 @@ struct Plan {
     const int32_t* __restrict__ tokens;
     const int64_t* __restrict__ tok_off;
     int64_t num_slots;
-    int64_t n;           // emitted rows never exceed the window's sample count
+    int64_t n;           // samples of the window
+    int64_t max_rows;    // capacity of the row records: n + W - 1 (sampler padding views)
     int64_t tok_end;     // tokens [0, tok_end) are addressable (tok_off[n], set in the kernel)
     int32_t* err;
 };
@@ -168,7 +169,7 @@ __device__ __forceinline__ void advance(Cursor& c, int64_t e, int64_t delta, con
 
 // Row record of the cursor's row (a bad plan yields an empty row and sets the error word).
 __device__ __forceinline__ RowRec load_row(const Cursor& c, const Plan& p) {
-    const bool ok = c.ri >= 0 && c.ri < c.ri_end && c.ri < p.n;
+    const bool ok = c.ri >= 0 && c.ri < c.ri_end && c.ri < p.max_rows;
     const int32_t i = ok ? c.ri : 0;
     RowRec r;
     r.ts = p.row_ts[i];
@@ -375,14 +376,18 @@ extern "C" int odb_collate(const odb_window_t* w, int64_t num_slots, const int32
     if (n == 0) return ODB_OK;  // no rows: every tile is empty
     if (!d_emit_order) return set_error(ODB_E_INVALID_ARG, "d_emit_order is NULL");
     hipStream_t s = static_cast<hipStream_t>(stream);
+    // a plan may list a sample more than once only through sampler padding: at most
+    // W - 1 extra rows (streaming plans)
+    const int64_t max_rows = n + w->num_ranks - 1;
     int32_t* err = &ws_at<DevStatus>(d_ws, L.status)->collate_err;
     int64_t* row_ts = ws_at<int64_t>(d_ws, L.row_ts);
     int32_t* row_len = ws_at<int32_t>(d_ws, L.row_len);
     hipLaunchKernelGGL(row_info_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock), 0, s,
-                       w->d_token_offsets, n, d_emit_order, d_slot_row_off, num_slots, row_ts, row_len, err);
+                       w->d_token_offsets, n, max_rows, d_emit_order, d_slot_row_off, num_slots, row_ts, row_len,
+                       err);
     ODB_LAUNCHED();
     Plan p{d_slot_tile_off, d_slot_maxlen, d_slot_rows, d_slot_row_off, row_ts, row_len, w->d_tokens,
-           w->d_token_offsets, num_slots, n, 0, err};
+           w->d_token_offsets, num_slots, n, max_rows, 0, err};
     // one resident wave of blocks; runs are dealt round robin over them
     static thread_local int resident = 0;
     if (resident <= 0) {

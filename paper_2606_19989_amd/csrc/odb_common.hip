@@ -108,8 +108,8 @@ bool make_layout(const odb_window_t* w, Layout* L) {
     L->gidx = take(4 * n1);
     L->stage = take(4 * n1);
     L->cover = take(4 * ((nid > n ? nid : n) + 1));
-    L->row_ts = take(8 * n1);
-    L->row_len = take(4 * n1);
+    L->row_ts = take(8 * (n1 + W));
+    L->row_len = take(4 * (n1 + W));
     L->total = o;
     L->num_sort_blocks = nb;
     L->partials_len = partials;

@@ -1,0 +1,976 @@
+// The unified streaming loop (Sec. 2.3 "Unified loop and termination"; App. C, App. F):
+// one logical sampler iteration of W ranks, round by round, on the device.
+//
+// Per-rank state (App. C): sampler-pending views R_r (a cursor into the rank's view
+// sequence), the collate buffer B_r (the worker queue is folded into it: a fetched view
+// lands in the buffer in the same round) and the emitted views E_r (the rank's emit
+// stream).  The shuffled identity list perm[0..N) is padded by repeating it from its
+// head to M = W * ceil(N / W) views (view m has identity perm[m mod N]); view m belongs
+// to rank m mod W, visited in increasing m.
+//
+// One protocol round k is three launches:
+//   stream_form_kernel   one block per rank: fetch up to rate[r] views under the depth
+//                        envelope |B_r| <= D; status (finished / not ready / ready); a ready
+//                        rank sorts its whole buffer by (length desc, view asc) in LDS and
+//                        chases the group starts of Sec. 2.2 (threshold carry, Eq. 1)
+//   stream_emit_kernel   one block per rank: every block reads all ranks' statuses (the
+//                        all_gather) and derives the same round kind and target T (Eq. 3
+//                        over the ready ranks); in an emit round each ready rank applies
+//                        Algorithm 1 (split in closed form, overflow by size rank) and
+//                        writes its T slot records, its emitted views and its new buffer
+//                        (the overflow); finished ranks (join) write IDLE slots
+//   stream_round_kernel  one block: round bookkeeping, the non-join quota cut (Theorem 2),
+//                        termination
+// Rounds are enqueued in chunks; the host reads the done flag once per chunk, and rounds
+// enqueued after the stop return at once.  A final pass turns the per-rank staging into
+// the window plan layout (rank-major slots, row and tile offsets), so odb_collate and
+// odb_loss_weights apply unchanged, and counts coverage.
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "odb_internal.h"
+
+namespace odb {
+
+namespace {
+
+constexpr int kSB = 1024;             // threads of the per-rank blocks
+constexpr int kMaxDepth = 4096;       // largest outstanding-depth envelope (LDS sort)
+constexpr int kRoundsPerCheck = 32;   // rounds enqueued between two looks at the done flag
+
+struct StreamGlobal {
+    int64_t steps;       // aligned steps so far (after quota cuts)
+    int64_t emitted;     // emitted views so far (after quota cuts)
+    int64_t rounds;
+    int64_t emit_rounds;
+    int64_t skip_rounds;
+    int64_t splits;
+    int64_t overflow;
+    int64_t second_gather;
+    int64_t max_step;
+    unsigned long long max_outstanding;
+    int32_t done;
+    int32_t stop;
+    int32_t err;
+    int32_t cap_overflow;
+};
+
+struct RankStream {
+    int64_t cursor;    // sampler position of the next fetch
+    int64_t buf_n;     // |B_r| (rewritten by the emit kernel of the rank's own block)
+    int64_t pub_n;     // |B_r| as published for this round's all_gather (form kernel only)
+    int64_t emitted;   // views written to the rank's emit stream (before a final quota cut)
+    int64_t tok;       // tokens in the buffer when it was grouped
+    int32_t status;    // -1 finished, 0 not ready, G_r > 0 ready with G_r groups
+    int32_t pad;
+};
+
+struct StreamRec {
+    int32_t kind;      // 0 emit, 1 skip, 2 stop
+    int32_t changed;   // an emit round in which some ready rank had G_r != T
+    int64_t target;    // T (emit rounds)
+    int64_t emitted;   // views emitted in the round (after a quota cut)
+    int64_t cut;       // steps kept (emit rounds); stop reason (stop rounds)
+};
+
+enum : int32_t { kSErrIdentity = 1, kSErrLength = 2, kSErrInternal = 4, kSErrRounds = 8 };
+
+struct StreamArgs {
+    int W;
+    int mode;
+    int64_t N;
+    int64_t q;          // views per rank
+    int64_t D;          // depth envelope
+    int64_t bufsize;
+    int64_t budget;
+    int64_t quota;
+    int64_t scap;       // staging slots per rank
+    int64_t max_rounds;
+    const int64_t* tok_off;
+    const int32_t* perm;
+    const int32_t* rate;   // [W]
+    const int64_t* cap;    // [W] or null
+    StreamGlobal* g;
+    RankStream* ranks;
+    StreamRec* rec;
+    int64_t* stepsum;      // [D]
+    int32_t* bufv;         // [W * D]
+    int32_t* sv;           // [W * D] sorted views
+    int32_t* slen;         // [W * D] their lengths
+    int32_t* gs;           // [W * (D + 1)] group starts
+    int32_t* apos;         // [W * D] adjusted group of every sorted position
+    int32_t* srows;        // [W * scap]
+    int32_t* smax;
+    int64_t* stok;
+    double* sadj;
+    int32_t* evw;          // [W * q] emit streams
+};
+
+__device__ __forceinline__ int32_t view_identity(const StreamArgs& a, int64_t m) {
+    return a.perm[m < a.N ? m : m % a.N];
+}
+
+template <typename T>
+__device__ __forceinline__ T sblock_sum(T v) {
+    __shared__ T wt[kSB / kWave];
+    v = wave_sum(v);
+    if ((threadIdx.x & (kWave - 1)) == 0) wt[threadIdx.x / kWave] = v;
+    __syncthreads();
+    T t = 0;
+    for (int i = 0; i < kSB / kWave; ++i) t += wt[i];
+    __syncthreads();
+    return t;
+}
+
+// Exclusive scan of one value per thread over the 1024-thread block; *total = sum.
+template <typename T>
+__device__ __forceinline__ T sblock_excl(T v, T* total) {
+    __shared__ T wt[kSB / kWave];
+    const T inc = wave_incl_sum(v);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == kWave - 1) wt[w] = inc;
+    __syncthreads();
+    T pre = 0, tot = 0;
+    for (int i = 0; i < kSB / kWave; ++i) {
+        pre += i < w ? wt[i] : T(0);
+        tot += wt[i];
+    }
+    __syncthreads();
+    *total = tot;
+    return pre + inc - v;
+}
+
+__global__ void stream_init_kernel(StreamArgs a, int64_t rounds_cap) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i0 == 0) *a.g = StreamGlobal{};
+    for (int64_t i = i0; i < a.W; i += stride) a.ranks[i] = RankStream{};
+    for (int64_t i = i0; i < rounds_cap; i += stride) a.rec[i] = StreamRec{};
+    for (int64_t i = i0; i < a.D; i += stride) a.stepsum[i] = 0;
+}
+
+// ------------------------------------------------------------------ round: fetch + form
+__global__ void __launch_bounds__(kSB) stream_form_kernel(StreamArgs a, int64_t k) {
+    if (*(volatile int32_t*)&a.g->done) return;
+    const int r = blockIdx.x;
+    RankStream* R = a.ranks + r;
+    extern __shared__ unsigned long long keys[];   // next power of two >= D entries
+    __shared__ int64_t s_cursor, s_n, s_f;
+    __shared__ int32_t s_err;
+    if (threadIdx.x == 0) {
+        const int64_t cursor = R->cursor, n = R->buf_n;
+        int64_t f = a.rate[r];
+        f = f < a.D - n ? f : a.D - n;
+        f = f < a.q - cursor ? f : a.q - cursor;
+        s_cursor = cursor;
+        s_n = n;
+        s_f = f > 0 ? f : 0;
+        s_err = 0;
+    }
+    __syncthreads();
+    const int64_t cursor = s_cursor, n0 = s_n, f = s_f;
+    int32_t* buf = a.bufv + (int64_t)r * a.D;
+    for (int64_t i = threadIdx.x; i < f; i += kSB) buf[n0 + i] = (int32_t)((cursor + i) * a.W + r);
+    const int64_t n = n0 + f;
+    const bool drained = cursor + f == a.q;
+    const bool finished = drained && n == 0;
+    const bool ready = !finished && (n >= a.bufsize || drained);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        R->cursor = cursor + f;
+        R->buf_n = n;
+        R->pub_n = n;
+        atomicMax(&a.g->max_outstanding, (unsigned long long)n);
+        if (!ready) R->status = finished ? -1 : 0;
+    }
+    if (!ready) return;
+    // sort the buffer: key = (INT32_MAX - l) << 32 | m, ascending = (length desc, view asc)
+    int64_t p2 = 1;
+    while (p2 < n) p2 <<= 1;
+    int64_t tok = 0;
+    for (int64_t i = threadIdx.x; i < p2; i += kSB) {
+        unsigned long long key = ~0ull;
+        if (i < n) {
+            const int64_t m = buf[i];
+            const int32_t id = view_identity(a, m);
+            int64_t l = 1;
+            if (id < 0 || id >= a.N) {
+                atomicOr(&s_err, kSErrIdentity);
+            } else {
+                l = a.tok_off[id + 1] - a.tok_off[id];
+                if (l < 1 || l > 0x7FFFFFFF) {
+                    atomicOr(&s_err, kSErrLength);
+                    l = 1;
+                }
+            }
+            tok += l;
+            key = ((unsigned long long)(0x7FFFFFFFll - l) << 32) | (unsigned long long)(uint32_t)m;
+        }
+        keys[i] = key;
+    }
+    tok = sblock_sum(tok);   // also a barrier for keys[]
+    for (int64_t size = 2; size <= p2; size <<= 1) {
+        for (int64_t stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int64_t t = threadIdx.x; t < (p2 >> 1); t += kSB) {
+                const int64_t lo = 2 * t - (t & (stride - 1));
+                const int64_t hi = lo + stride;
+                const bool up = (lo & size) == 0;
+                const unsigned long long x = keys[lo], y = keys[hi];
+                if ((x > y) == up) {
+                    keys[lo] = y;
+                    keys[hi] = x;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    int32_t* sv = a.sv + (int64_t)r * a.D;
+    int32_t* sl = a.slen + (int64_t)r * a.D;
+    for (int64_t i = threadIdx.x; i < n; i += kSB) {
+        const unsigned long long key = keys[i];
+        sv[i] = (int32_t)(key & 0xFFFFFFFFull);
+        sl[i] = (int32_t)(0x7FFFFFFFll - (int64_t)(key >> 32));
+    }
+    if (threadIdx.x == 0) {
+        // Sec. 2.2: the group starting at p holds B(l) samples, l = the length just before
+        // p (the shortest of the previous group); the first group is a singleton
+        int32_t* gs = a.gs + (int64_t)r * (a.D + 1);
+        int64_t p = 0, g = 0;
+        while (p < n) {
+            gs[g++] = (int32_t)p;
+            if (p == 0) {
+                p = 1;
+            } else {
+                const int32_t l = (int32_t)(0x7FFFFFFFll - (int64_t)(keys[p - 1] >> 32));
+                const int64_t nx = p + batch_size(a.budget, l);
+                p = nx < n ? nx : n;
+            }
+        }
+        gs[g] = (int32_t)n;
+        R->status = (int32_t)g;
+        R->tok = tok;
+        if (s_err) atomicOr(&a.g->err, s_err);
+    }
+}
+
+// ------------------------------------------------------------------ round: align + emit
+struct RoundView {
+    int kind;
+    int64_t T;
+    int32_t stop;
+};
+
+// The all_gather: every block reduces the same W statuses the same way.
+__device__ RoundView decide_round(const StreamArgs& a) {
+    __shared__ int64_t s_fin, s_unready, s_maxG, s_minS, s_minC;
+    if (threadIdx.x == 0) {
+        s_fin = 0;
+        s_unready = 0;
+        s_maxG = 0;
+        s_minS = LLONG_MAX;
+        s_minC = LLONG_MAX;
+    }
+    __syncthreads();
+    for (int r = threadIdx.x; r < a.W; r += kSB) {
+        const RankStream R = a.ranks[r];
+        if (R.status < 0) {
+            atomicAdd((unsigned long long*)&s_fin, 1ull);
+        } else if (R.status == 0) {
+            atomicAdd((unsigned long long*)&s_unready, 1ull);
+        } else {
+            atomicMax((long long*)&s_maxG, (long long)R.status);
+            atomicMin((long long*)&s_minS, (long long)R.pub_n);
+            if (a.cap && a.cap[r] > 0) atomicMin((long long*)&s_minC, (long long)a.cap[r]);
+        }
+    }
+    __syncthreads();
+    RoundView v{0, 0, 0};
+    if (s_fin == a.W) {
+        v.kind = 2;
+        v.stop = ODB_STOP_DRAINED;
+    } else if (a.mode == ODB_MODE_NONJOIN_QUOTA && s_fin > 0) {
+        v.kind = 2;
+        v.stop = ODB_STOP_RANK_FINISHED;
+    } else if (s_unready > 0) {
+        v.kind = 1;
+    } else {
+        int64_t T = s_maxG;
+        if (s_minC < T) T = s_minC;
+        if (s_minS < T) T = s_minS;
+        v.T = T < 1 ? 1 : T;
+    }
+    return v;
+}
+
+__global__ void __launch_bounds__(kSB) stream_emit_kernel(StreamArgs a, int64_t k) {
+    if (*(volatile int32_t*)&a.g->done) return;
+    const RoundView v = decide_round(a);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        a.rec[k].kind = v.kind;
+        a.rec[k].target = v.T;
+        a.rec[k].cut = v.kind == 2 ? v.stop : 0;
+    }
+    if (v.kind != 0) return;
+    const int r = blockIdx.x;
+    RankStream* R = a.ranks + r;
+    const int64_t T = v.T;
+    const int64_t base = a.g->steps;   // written by the previous round's bookkeeping only
+    const int32_t st = R->status;
+    if (st < 0) {   // finished rank in join mode: IDLE slots
+        for (int64_t j = threadIdx.x; j < T; j += kSB) {
+            const int64_t x = base + j;
+            if (x < a.scap) {
+                const int64_t o = (int64_t)r * a.scap + x;
+                a.srows[o] = 0;
+                a.smax[o] = 0;
+                a.stok[o] = 0;
+                a.sadj[o] = 0.0;
+            } else {
+                a.g->cap_overflow = 1;
+            }
+        }
+        return;
+    }
+    // st > 0: a ready rank with G groups over n sorted positions
+    const int64_t G = st;
+    const int64_t n = R->pub_n;
+    const int32_t* gsg = a.gs + (int64_t)r * (a.D + 1);
+    const int32_t* sv = a.sv + (int64_t)r * a.D;
+    const int32_t* sl = a.slen + (int64_t)r * a.D;
+    int32_t* apos = a.apos + (int64_t)r * a.D;
+    __shared__ int32_t gsl[kMaxDepth + 1];
+    __shared__ int32_t as[kMaxDepth], ae[kMaxDepth], cum[kMaxDepth + 1];
+    __shared__ unsigned long long gtok[kMaxDepth];
+    __shared__ int64_t s_X, s_jstar;
+    __shared__ int32_t s_ret, s_bad;
+    for (int64_t i = threadIdx.x; i <= G; i += kSB) gsl[i] = gsg[i];
+    for (int64_t i = threadIdx.x; i < T; i += kSB) gtok[i] = 0;
+    if (threadIdx.x == 0) {
+        s_ret = 0;
+        s_bad = 0;
+        s_X = 0;
+        s_jstar = 0;
+    }
+    __syncthreads();
+    // Algorithm 1 on this rank: the adjusted groups [as[a], ae[a]) in formation order
+    if (G < T) {
+        // split, closed form: positions [0, X) become singletons, [X, end of group j*)
+        // stays one group, later groups are unchanged; j* is the first group whose
+        // cumulative surplus sum (c_g - 1) reaches k = T - G
+        if (threadIdx.x == 0) {
+            const int64_t need = T - G;
+            int64_t surplus = 0, jstar = -1, X = 0;
+            for (int64_t g = 0; g < G; ++g) {
+                const int64_t c = gsl[g + 1] - gsl[g];
+                if (surplus + (c - 1) >= need) {
+                    jstar = g;
+                    X = gsl[g] + (need - surplus);
+                    break;
+                }
+                surplus += c - 1;
+            }
+            if (jstar < 0 || X + 1 + (G - 1 - jstar) != T) s_bad = 1;
+            s_X = X;
+            s_jstar = jstar < 0 ? 0 : jstar;
+        }
+        __syncthreads();
+        const int64_t X = s_X, js = s_jstar;
+        for (int64_t t = threadIdx.x; t < T; t += kSB) {
+            if (t < X) {
+                as[t] = (int32_t)t;
+                ae[t] = (int32_t)(t + 1);
+            } else if (t == X) {
+                as[t] = (int32_t)X;
+                ae[t] = gsl[js + 1];
+            } else {
+                const int64_t g = js + (t - X);
+                as[t] = g < G ? gsl[g] : (int32_t)n;
+                ae[t] = g < G ? gsl[g + 1] : (int32_t)n;
+            }
+        }
+        __syncthreads();
+        for (int64_t p = threadIdx.x; p < n; p += kSB) {
+            int64_t ap;
+            if (p < X) {
+                ap = p;
+            } else if (p < gsl[js + 1]) {
+                ap = X;
+            } else {
+                // formation group of p (> j*): binary search over the group starts
+                int64_t lo = js + 1, hi = G;
+                while (hi - lo > 1) {
+                    const int64_t mid = (lo + hi) >> 1;
+                    if (gsl[mid] <= p) lo = mid; else hi = mid;
+                }
+                ap = X + (lo - js);
+            }
+            apos[p] = (int32_t)ap;
+        }
+    } else if (G > T) {
+        // overflow: keep the T groups first by (size desc, formation index desc)
+        for (int64_t g = threadIdx.x; g < G; g += kSB) {
+            const int32_t cg = gsl[g + 1] - gsl[g];
+            int64_t rank = 0;
+            for (int64_t h = 0; h < G; ++h) {
+                const int32_t ch = gsl[h + 1] - gsl[h];
+                rank += (ch > cg || (ch == cg && h > g)) ? 1 : 0;
+            }
+            cum[g] = rank < T ? 1 : 0;   // kept flag, turned into the kept index below
+        }
+        __syncthreads();
+        int64_t carry = 0;
+        for (int64_t b = 0; b < G; b += kSB) {
+            const int64_t g = b + threadIdx.x;
+            const int32_t f = g < G ? cum[g] : 0;
+            int32_t tot;
+            const int32_t ex = sblock_excl(f, &tot);
+            if (g < G && f) {
+                const int64_t ki = carry + ex;
+                as[ki] = gsl[g];
+                ae[ki] = gsl[g + 1];
+            }
+            carry += tot;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0 && carry != T) s_bad = 1;
+        for (int64_t p = threadIdx.x; p < n; p += kSB) apos[p] = -1;
+        __syncthreads();
+        for (int64_t t = threadIdx.x; t < T; t += kSB)
+            for (int64_t p = as[t]; p < ae[t]; ++p) apos[p] = (int32_t)t;
+    } else {
+        for (int64_t t = threadIdx.x; t < T; t += kSB) {
+            as[t] = gsl[t];
+            ae[t] = gsl[t + 1];
+        }
+        __syncthreads();
+        for (int64_t t = threadIdx.x; t < T; t += kSB)
+            for (int64_t p = as[t]; p < ae[t]; ++p) apos[p] = (int32_t)t;
+    }
+    __syncthreads();
+    // rows prefix over the adjusted groups, tokens per adjusted group
+    {
+        int64_t carry = 0;
+        for (int64_t b = 0; b < T; b += kSB) {
+            const int64_t t = b + threadIdx.x;
+            const int32_t rows = t < T ? ae[t] - as[t] : 0;
+            int32_t tot;
+            const int32_t ex = sblock_excl(rows, &tot);
+            if (t < T) cum[t] = (int32_t)(carry + ex);
+            carry += tot;
+        }
+        if (threadIdx.x == 0) cum[T] = (int32_t)carry;
+    }
+    for (int64_t p = threadIdx.x; p < n; p += kSB) {
+        const int32_t t = apos[p];
+        if (t >= 0) atomicAdd(&gtok[t], (unsigned long long)sl[p]);
+    }
+    __syncthreads();
+    const int64_t E = cum[T];
+    const int64_t ebase = R->emitted;
+    const double mean = (double)R->tok / (double)n;
+    // slot records: step j of the round is adjusted group T-1-j (short to long)
+    for (int64_t t = threadIdx.x; t < T; t += kSB) {
+        const int64_t j = T - 1 - t;
+        const int64_t x = base + j;
+        const int32_t rows = ae[t] - as[t];
+        if (x < a.scap) {
+            const int64_t o = (int64_t)r * a.scap + x;
+            a.srows[o] = rows;
+            a.smax[o] = rows > 0 ? sl[as[t]] : 0;
+            a.stok[o] = (int64_t)gtok[t];
+            a.sadj[o] = (double)rows * mean;
+        } else {
+            a.g->cap_overflow = 1;
+        }
+        atomicAdd((unsigned long long*)&a.stepsum[j], (unsigned long long)rows);
+    }
+    // emitted views (rows of a group run from its last position to its first) and the
+    // new buffer (overflow returns)
+    int32_t* ev = a.evw + (int64_t)r * a.q;
+    int32_t* buf = a.bufv + (int64_t)r * a.D;
+    for (int64_t p = threadIdx.x; p < n; p += kSB) {
+        const int32_t t = apos[p];
+        if (t >= 0) {
+            const int64_t e = ebase + E - cum[t + 1] + (ae[t] - 1 - p);
+            if (e < a.q) ev[e] = sv[p]; else s_bad = 1;
+        } else {
+            buf[atomicAdd(&s_ret, 1)] = sv[p];
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        R->emitted = ebase + E;
+        R->buf_n = s_ret;
+        if (E + s_ret != n) s_bad = 1;
+        if (G < T) atomicAdd((unsigned long long*)&a.g->splits, (unsigned long long)(T - G));
+        if (G > T) atomicAdd((unsigned long long*)&a.g->overflow, (unsigned long long)(G - T));
+        if (G != T) atomicOr(&a.rec[k].changed, 1);
+        if (s_bad) atomicOr(&a.g->err, kSErrInternal);
+    }
+}
+
+// ------------------------------------------------------------------ round: bookkeeping
+__global__ void __launch_bounds__(kSB) stream_round_kernel(StreamArgs a, int64_t k) {
+    StreamGlobal* g = a.g;
+    if (*(volatile int32_t*)&g->done) return;
+    StreamRec* rec = a.rec + k;
+    const int kind = rec->kind;
+    if (kind == 2) {
+        if (threadIdx.x == 0) {
+            g->stop = (int32_t)rec->cut;
+            g->done = 1;
+            g->rounds = k + 1;
+        }
+        return;
+    }
+    if (kind == 1) {
+        if (threadIdx.x == 0) {
+            g->skip_rounds += 1;
+            g->rounds = k + 1;
+            if (k + 1 >= a.max_rounds) {
+                g->err |= kSErrRounds;
+                g->done = 1;
+            }
+        }
+        return;
+    }
+    // emit round: cumulative step sizes, the quota cut (non-join), per-round totals
+    const int64_t T = rec->target;
+    const int64_t before = g->emitted;
+    __shared__ int64_t s_cut;
+    if (threadIdx.x == 0) s_cut = T;
+    __syncthreads();
+    int64_t carry = 0, mx = 0, kept = 0;
+    for (int64_t b = 0; b < T; b += kSB) {
+        const int64_t j = b + threadIdx.x;
+        const int64_t v = j < T ? a.stepsum[j] : 0;
+        int64_t tot;
+        const int64_t ex = sblock_excl(v, &tot);
+        if (a.mode == ODB_MODE_NONJOIN_QUOTA && j < T && before + carry + ex < a.quota &&
+            before + carry + ex + v >= a.quota)
+            s_cut = j + 1;
+        __syncthreads();
+        carry += tot;
+    }
+    const int64_t cut = s_cut;
+    for (int64_t j = threadIdx.x; j < T; j += kSB) {
+        const int64_t v = a.stepsum[j];
+        if (j < cut) {
+            mx = v > mx ? v : mx;
+            kept += v;
+        }
+        a.stepsum[j] = 0;
+    }
+    __shared__ int64_t wm[kSB / kWave];
+    for (int d = kWave / 2; d > 0; d >>= 1) {
+        const int64_t o = __shfl_xor(mx, d, kWave);
+        mx = o > mx ? o : mx;
+    }
+    if ((threadIdx.x & (kWave - 1)) == 0) wm[threadIdx.x / kWave] = mx;
+    kept = sblock_sum(kept);
+    if (threadIdx.x == 0) {
+        for (int i = 0; i < kSB / kWave; ++i) mx = wm[i] > mx ? wm[i] : mx;
+        rec->emitted = kept;
+        rec->cut = cut;
+        g->steps += cut;
+        g->emitted = before + kept;
+        g->max_step = mx > g->max_step ? mx : g->max_step;
+        g->emit_rounds += 1;
+        g->second_gather += rec->changed ? 1 : 0;
+        g->rounds = k + 1;
+        if (cut < T || (a.mode == ODB_MODE_NONJOIN_QUOTA && before + kept >= a.quota)) {
+            g->stop = ODB_STOP_QUOTA;
+            g->done = 1;
+        } else if (k + 1 >= a.max_rounds) {
+            g->err |= kSErrRounds;
+            g->done = 1;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ final plan
+__global__ void stream_slots_kernel(StreamArgs a, int64_t S, int32_t* rows, int32_t* maxlen, int64_t* tokens,
+                                    double* approx) {
+    const int64_t K = (int64_t)a.W * S;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < K; x += stride) {
+        const int64_t r = x / S, j = x - r * S;
+        const int64_t o = r * a.scap + j;
+        rows[x] = a.srows[o];
+        maxlen[x] = a.smax[o];
+        tokens[x] = a.stok[o];
+        if (approx) approx[x] = a.sadj[o];
+    }
+}
+
+// Rank r's emitted views (slot order, row order) and their identities.
+__global__ void __launch_bounds__(kSB) stream_emit_out_kernel(StreamArgs a, int64_t S, const int64_t* row_off,
+                                                              int32_t* emit_views, int32_t* emit_order,
+                                                              int32_t* vcount, int32_t* icount) {
+    const int r = blockIdx.x;
+    const int64_t lo = row_off[(int64_t)r * S], hi = row_off[(int64_t)(r + 1) * S];
+    const int32_t* ev = a.evw + (int64_t)r * a.q;
+    for (int64_t i = threadIdx.x; i < hi - lo; i += kSB) {
+        const int32_t m = ev[i];
+        const int32_t id = view_identity(a, m);
+        emit_views[lo + i] = m;
+        emit_order[lo + i] = id;
+        atomicAdd(&vcount[m], 1);
+        atomicAdd(&icount[id], 1);
+    }
+}
+
+struct RowsLoadS {
+    const int32_t* rows;
+    int64_t K;
+    __device__ int64_t operator()(int64_t i) const { return i < K ? (int64_t)rows[i] : 0; }
+};
+struct TileLoadS {
+    const int32_t* rows;
+    const int32_t* mx;
+    int64_t K;
+    __device__ int64_t operator()(int64_t i) const { return i < K ? (int64_t)rows[i] * mx[i] : 0; }
+};
+struct StoreS {
+    int64_t* out;
+    __device__ void operator()(int64_t i, int64_t v) const { out[i] = v; }
+};
+
+struct LeftFlag {
+    StreamArgs a;
+    const int32_t* vcount;
+    // rank-major position x = r * q + i <-> view m = i * W + r
+    __device__ int64_t operator()(int64_t x) const {
+        const int64_t r = x / a.q, i = x - r * a.q;
+        return vcount[i * a.W + r] == 0 ? 1 : 0;
+    }
+};
+struct LeftStore {
+    StreamArgs a;
+    const int32_t* vcount;
+    int32_t* left;
+    int64_t* left_off;
+    __device__ void operator()(int64_t x, int64_t ex) const {
+        const int64_t r = x / a.q, i = x - r * a.q;
+        if (i == 0) left_off[r] = ex;
+        if (vcount[i * a.W + r] == 0) left[ex] = (int32_t)(i * a.W + r);
+    }
+};
+
+struct StreamTotals {
+    unsigned long long real_tokens;
+    unsigned long long bad_views;
+    unsigned long long missing_ids;
+    unsigned long long duplicate_ids;
+};
+
+__global__ void stream_totals_kernel(StreamArgs a, int64_t K, const int64_t* tokens, const int32_t* vcount,
+                                     const int32_t* icount, StreamTotals* t) {
+    const int64_t M = a.q * a.W;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    unsigned long long tok = 0, bad = 0, miss = 0, dup = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < K; i += stride) tok += tokens[i];
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < M; i += stride) bad += vcount[i] > 1;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.N; i += stride) {
+        const int32_t c = icount[i];
+        miss += c == 0;
+        dup += c > 1 ? (unsigned long long)(c - 1) : 0ull;
+    }
+    tok = wave_sum(tok);
+    bad = wave_sum(bad);
+    miss = wave_sum(miss);
+    dup = wave_sum(dup);
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        atomicAdd(&t->real_tokens, tok);
+        atomicAdd(&t->bad_views, bad);
+        atomicAdd(&t->missing_ids, miss);
+        atomicAdd(&t->duplicate_ids, dup);
+    }
+}
+
+__global__ void fill_i64s_kernel(int64_t* p, int64_t n) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0;
+}
+
+__global__ void fill_i32_kernel(int32_t* p, int64_t n) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = 0;
+}
+
+__global__ void clear_totals_kernel(StreamTotals* t) {
+    if (threadIdx.x == 0) *t = StreamTotals{};
+}
+
+struct StreamLayout {
+    size_t g, ranks, rec, stepsum, bufv, sv, slen, gs, apos, srows, smax, stok, sadj, evw, vcount, icount,
+        totals, partials, rate, cap, total;
+};
+
+bool stream_layout(size_t at, int64_t W, int64_t N, int64_t D, int64_t scap, int64_t rounds, StreamLayout* L) {
+    const int64_t q = N > 0 ? (N + W - 1) / W : 0;
+    const int64_t M = q * W;
+    const int64_t K1 = W * scap + 1;
+    const int64_t scan_n = (K1 > M + 1 ? K1 : M + 1);
+    size_t o = at;
+    auto take = [&](size_t bytes) {
+        size_t x = o;
+        o = (o + (bytes ? bytes : 1) + 255) & ~(size_t)255;
+        return x;
+    };
+    L->g = take(sizeof(StreamGlobal));
+    L->ranks = take(sizeof(RankStream) * W);
+    L->rec = take(sizeof(StreamRec) * rounds);
+    L->stepsum = take(8 * D);
+    L->bufv = take(4 * W * D);
+    L->sv = take(4 * W * D);
+    L->slen = take(4 * W * D);
+    L->gs = take(4 * W * (D + 1));
+    L->apos = take(4 * W * D);
+    L->srows = take(4 * W * scap);
+    L->smax = take(4 * W * scap);
+    L->stok = take(8 * W * scap);
+    L->sadj = take(8 * W * scap);
+    L->evw = take(4 * (M > 0 ? M : 1));
+    L->vcount = take(4 * (M > 0 ? M : 1));
+    L->icount = take(4 * (N > 0 ? N : 1));
+    L->totals = take(sizeof(StreamTotals));
+    L->partials = take(8 * (scan_n / kScanTile + 4));
+    L->rate = take(4 * W);
+    L->cap = take(8 * W);
+    L->total = o;
+    return true;
+}
+
+int check_stream_params(const odb_window_t* w, const odb_stream_params_t* p, int64_t slot_capacity) {
+    if (!p) return set_error(ODB_E_INVALID_ARG, "params is NULL");
+    if (p->mode != ODB_MODE_JOIN && p->mode != ODB_MODE_NONJOIN_QUOTA)
+        return set_error(ODB_E_INVALID_ARG, "unknown mode %d", p->mode);
+    if (p->reserved0 != 0) return set_error(ODB_E_INVALID_ARG, "params.reserved0 must be 0");
+    if (p->mode == ODB_MODE_NONJOIN_QUOTA && p->quota < 1)
+        return set_error(ODB_E_INVALID_ARG, "quota must be >= 1 in non-join mode");
+    if (p->buffer_size < 1 || p->depth < p->buffer_size || p->depth > kMaxDepth)
+        return set_error(ODB_E_INVALID_ARG, "need 1 <= buffer_size <= depth <= %d", kMaxDepth);
+    if (p->max_rounds < 1) return set_error(ODB_E_INVALID_ARG, "max_rounds must be >= 1");
+    if (slot_capacity < 0) return set_error(ODB_E_INVALID_ARG, "slot_capacity must be >= 0");
+    if (!p->rate) return set_error(ODB_E_INVALID_ARG, "rate is NULL");
+    for (int r = 0; r < w->num_ranks; ++r) {
+        if (p->rate[r] < 1) return set_error(ODB_E_INVALID_ARG, "rate[%d] must be >= 1", r);
+        if (p->slot_capacity && p->slot_capacity[r] < 0)
+            return set_error(ODB_E_INVALID_ARG, "slot_capacity[%d] must be >= 0", r);
+    }
+    if (w->num_samples + w->num_ranks >= 0x7FFFFFFFll)
+        return set_error(ODB_E_INVALID_ARG, "N + W must stay below 2^31 (view ids are int32)");
+    return ODB_OK;
+}
+
+}  // namespace
+
+}  // namespace odb
+
+using namespace odb;
+
+extern "C" size_t odb_stream_workspace_size(const odb_window_t* w, int32_t depth, int64_t slot_capacity,
+                                            int64_t max_rounds) {
+    Layout L;
+    if (!make_layout(w, &L)) return 0;
+    if (depth < 1 || depth > kMaxDepth || slot_capacity < 0 || max_rounds < 1) return 0;
+    StreamLayout S;
+    stream_layout(L.total, w->num_ranks, w->num_samples, depth, slot_capacity / w->num_ranks, max_rounds, &S);
+    return S.total;
+}
+
+extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int64_t budget,
+                               const odb_stream_params_t* params, int64_t slot_capacity, int32_t* d_emit_order,
+                               int32_t* d_emit_views, int32_t* d_slot_rows, int32_t* d_slot_maxlen,
+                               int64_t* d_slot_row_off, int64_t* d_slot_tile_off, int64_t* d_slot_tokens,
+                               double* d_slot_tokens_approx, int32_t* d_left_views, int64_t* d_left_off,
+                               odb_stream_round_t* h_trace, odb_stream_info_t* h_info, void* d_ws, size_t ws_bytes,
+                               void* stream) {
+    Layout L;
+    if (!make_layout(w, &L)) return set_error(ODB_E_INVALID_ARG, "bad window");
+    if (budget < 1) return set_error(ODB_E_INVALID_ARG, "budget must be >= 1");
+    ODB_TRY(check_stream_params(w, params, slot_capacity));
+    if (!h_info) return set_error(ODB_E_INVALID_ARG, "h_info is NULL");
+    const int W = w->num_ranks;
+    const int64_t N = w->num_samples;
+    const int64_t q = N > 0 ? (N + W - 1) / W : 0;
+    const int64_t M = q * W;
+    const int64_t scap = slot_capacity / W;
+    if (N > 0 && !d_perm) return set_error(ODB_E_INVALID_ARG, "d_perm is NULL");
+    if (M > 0 && (!d_emit_order || !d_emit_views || !d_left_views))
+        return set_error(ODB_E_INVALID_ARG, "view arrays must not be NULL");
+    if (!d_slot_row_off || !d_slot_tile_off || !d_left_off)
+        return set_error(ODB_E_INVALID_ARG, "offset arrays must not be NULL");
+    if (scap > 0 && (!d_slot_rows || !d_slot_maxlen || !d_slot_tokens))
+        return set_error(ODB_E_INVALID_ARG, "slot arrays must not be NULL");
+    StreamLayout SL;
+    stream_layout(L.total, W, N, params->depth, scap, params->max_rounds, &SL);
+    if (!d_ws) return set_error(ODB_E_INVALID_ARG, "workspace is NULL");
+    if (reinterpret_cast<uintptr_t>(d_ws) & 255) return set_error(ODB_E_INVALID_ARG, "workspace must be 256-byte aligned");
+    if (ws_bytes < SL.total)
+        return set_error(ODB_E_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, SL.total);
+    memset(h_info, 0, sizeof(*h_info));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // the window part of the workspace: rank offsets and a cleared status word, as after
+    // odb_align_groups, so odb_collate / odb_collate_status work on this workspace
+    ODB_TRY(upload_small(w, L, d_ws, nullptr, s));
+
+    StreamArgs a{};
+    a.W = W;
+    a.mode = params->mode;
+    a.N = N;
+    a.q = q;
+    a.D = params->depth;
+    a.bufsize = params->buffer_size;
+    a.budget = budget;
+    a.quota = params->quota;
+    a.scap = scap;
+    a.max_rounds = params->max_rounds;
+    a.tok_off = w->d_token_offsets;
+    a.perm = d_perm;
+    a.rate = ws_at<int32_t>(d_ws, SL.rate);
+    a.cap = params->slot_capacity ? ws_at<int64_t>(d_ws, SL.cap) : nullptr;
+    a.g = ws_at<StreamGlobal>(d_ws, SL.g);
+    a.ranks = ws_at<RankStream>(d_ws, SL.ranks);
+    a.rec = ws_at<StreamRec>(d_ws, SL.rec);
+    a.stepsum = ws_at<int64_t>(d_ws, SL.stepsum);
+    a.bufv = ws_at<int32_t>(d_ws, SL.bufv);
+    a.sv = ws_at<int32_t>(d_ws, SL.sv);
+    a.slen = ws_at<int32_t>(d_ws, SL.slen);
+    a.gs = ws_at<int32_t>(d_ws, SL.gs);
+    a.apos = ws_at<int32_t>(d_ws, SL.apos);
+    a.srows = ws_at<int32_t>(d_ws, SL.srows);
+    a.smax = ws_at<int32_t>(d_ws, SL.smax);
+    a.stok = ws_at<int64_t>(d_ws, SL.stok);
+    a.sadj = ws_at<double>(d_ws, SL.sadj);
+    a.evw = ws_at<int32_t>(d_ws, SL.evw);
+    ODB_TRY_HIP(hipMemcpyAsync(const_cast<int32_t*>(a.rate), params->rate, 4 * W, hipMemcpyHostToDevice, s));
+    if (a.cap)
+        ODB_TRY_HIP(hipMemcpyAsync(const_cast<int64_t*>(a.cap), params->slot_capacity, 8 * W, hipMemcpyHostToDevice, s));
+    hipLaunchKernelGGL(stream_init_kernel, dim3(grid_for(std::max<int64_t>(params->max_rounds, W), 256, 1024)),
+                       dim3(256), 0, s, a, params->max_rounds);
+    ODB_LAUNCHED();
+
+    // rounds, in chunks, until the done flag is up
+    int64_t p2 = 1;
+    while (p2 < a.D) p2 <<= 1;
+    const size_t sort_lds = sizeof(unsigned long long) * p2;
+    StreamGlobal hg{};
+    for (int64_t k0 = 0; k0 < a.max_rounds; k0 += kRoundsPerCheck) {
+        const int64_t k1 = std::min<int64_t>(a.max_rounds, k0 + kRoundsPerCheck);
+        for (int64_t k = k0; k < k1; ++k) {
+            hipLaunchKernelGGL(stream_form_kernel, dim3(W), dim3(kSB), sort_lds, s, a, k);
+            ODB_LAUNCHED();
+            hipLaunchKernelGGL(stream_emit_kernel, dim3(W), dim3(kSB), 0, s, a, k);
+            ODB_LAUNCHED();
+            hipLaunchKernelGGL(stream_round_kernel, dim3(1), dim3(kSB), 0, s, a, k);
+            ODB_LAUNCHED();
+        }
+        ODB_TRY_HIP(hipMemcpyAsync(&hg, a.g, sizeof(hg), hipMemcpyDeviceToHost, s));
+        ODB_TRY_HIP(hipStreamSynchronize(s));
+        if (hg.done) break;
+    }
+    if (hg.err & kSErrIdentity) return set_error(ODB_E_INVALID_DATA, "perm holds a value outside [0, N)");
+    if (hg.err & kSErrLength) return set_error(ODB_E_INVALID_DATA, "a sample has length < 1 or >= 2^31");
+    if (hg.err & kSErrInternal) return set_error(ODB_E_INTERNAL, "streaming round state inconsistent");
+    h_info->rounds = hg.rounds;
+    if (!hg.done || (hg.err & kSErrRounds)) {
+        h_info->rounds = a.max_rounds;
+        return set_error(ODB_E_CAPACITY, "the iteration did not finish within %lld rounds",
+                         (long long)a.max_rounds);
+    }
+    const int64_t S = hg.steps;
+    const int64_t K = (int64_t)W * S;
+    h_info->steps = S;
+    h_info->emit_rounds = hg.emit_rounds;
+    h_info->skip_rounds = hg.skip_rounds;
+    h_info->stop_reason = hg.stop;
+    h_info->views = M;
+    h_info->emitted_views = hg.emitted;
+    h_info->max_step_samples = hg.max_step;
+    h_info->splits = hg.splits;
+    h_info->overflow_groups = hg.overflow;
+    h_info->second_gather_rounds = hg.second_gather;
+    h_info->max_outstanding = (int64_t)hg.max_outstanding;
+    h_info->required_slot_capacity = K;
+    if (hg.cap_overflow || S > scap)
+        return set_error(ODB_E_CAPACITY, "plan needs %lld slots, capacity is %lld", (long long)K,
+                         (long long)slot_capacity);
+
+    // plan arrays in the window layout
+    const int64_t gcap = (int64_t)num_cus() * 16;
+    int64_t* partials = ws_at<int64_t>(d_ws, SL.partials);
+    if (K > 0) {
+        hipLaunchKernelGGL(stream_slots_kernel, dim3(grid_for(K, 256, gcap)), dim3(256), 0, s, a, S, d_slot_rows,
+                           d_slot_maxlen, d_slot_tokens, d_slot_tokens_approx);
+        ODB_LAUNCHED();
+    }
+    ODB_TRY((device_excl_scan<int64_t>(RowsLoadS{d_slot_rows, K}, StoreS{d_slot_row_off}, K + 1, partials, s)));
+    ODB_TRY((device_excl_scan<int64_t>(TileLoadS{d_slot_rows, d_slot_maxlen, K}, StoreS{d_slot_tile_off}, K + 1,
+                                       partials, s)));
+    int32_t* vcount = ws_at<int32_t>(d_ws, SL.vcount);
+    int32_t* icount = ws_at<int32_t>(d_ws, SL.icount);
+    StreamTotals* tot = ws_at<StreamTotals>(d_ws, SL.totals);
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(std::max<int64_t>(M, 1), 256, gcap)), dim3(256), 0, s, vcount, M);
+    ODB_LAUNCHED();
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(std::max<int64_t>(N, 1), 256, gcap)), dim3(256), 0, s, icount, N);
+    ODB_LAUNCHED();
+    hipLaunchKernelGGL(clear_totals_kernel, dim3(1), dim3(64), 0, s, tot);
+    ODB_LAUNCHED();
+    if (K > 0) {
+        hipLaunchKernelGGL(stream_emit_out_kernel, dim3(W), dim3(kSB), 0, s, a, S, (const int64_t*)d_slot_row_off,
+                           d_emit_views, d_emit_order, vcount, icount);
+        ODB_LAUNCHED();
+    }
+    hipLaunchKernelGGL(fill_i64s_kernel, dim3(1), dim3(256), 0, s, d_left_off, (int64_t)W + 1);
+    ODB_LAUNCHED();
+    ODB_TRY((device_excl_scan<int64_t>(LeftFlag{a, vcount}, LeftStore{a, vcount, d_left_views, d_left_off}, M,
+                                       partials, s)));
+    hipLaunchKernelGGL(stream_totals_kernel, dim3(grid_for(std::max<int64_t>(std::max(K, M), 1), 256, gcap)),
+                       dim3(256), 0, s, a, K, (const int64_t*)d_slot_tokens, (const int32_t*)vcount,
+                       (const int32_t*)icount, tot);
+    ODB_LAUNCHED();
+    StreamTotals ht{};
+    int64_t padded = 0, nleft = 0;
+    std::vector<RankStream> hr(W);
+    ODB_TRY_HIP(hipMemcpyAsync(&ht, tot, sizeof(ht), hipMemcpyDeviceToHost, s));
+    ODB_TRY_HIP(hipMemcpyAsync(&padded, d_slot_tile_off + K, 8, hipMemcpyDeviceToHost, s));
+    ODB_TRY_HIP(hipMemcpyAsync(hr.data(), a.ranks, sizeof(RankStream) * W, hipMemcpyDeviceToHost, s));
+    if (M > 0) ODB_TRY_HIP(hipMemcpyAsync(&nleft, partials + (M + kScanTile - 1) / kScanTile, 8,
+                                          hipMemcpyDeviceToHost, s));
+    std::vector<StreamRec> hrec(h_trace ? hg.rounds : 0);
+    if (h_trace && hg.rounds > 0)
+        ODB_TRY_HIP(hipMemcpyAsync(hrec.data(), a.rec, sizeof(StreamRec) * hg.rounds, hipMemcpyDeviceToHost, s));
+    ODB_TRY_HIP(hipStreamSynchronize(s));
+    // the left-over offsets end with the total; the scan left off[W] unset
+    ODB_TRY_HIP(hipMemcpyAsync(d_left_off + W, &nleft, 8, hipMemcpyHostToDevice, s));
+    ODB_TRY_HIP(hipStreamSynchronize(s));
+    int64_t fetched = 0;
+    for (int r = 0; r < W; ++r) fetched += hr[r].cursor;
+    h_info->real_tokens = (int64_t)ht.real_tokens;
+    h_info->padded_elems = padded;
+    h_info->pad_fraction = padded > 0 ? 1.0 - (double)ht.real_tokens / (double)padded : 0.0;
+    h_info->undelivered_views = fetched - hg.emitted;
+    h_info->pending_views = M - fetched;
+    h_info->bad_views = (int64_t)ht.bad_views;
+    h_info->missing_ids = (int64_t)ht.missing_ids;
+    h_info->duplicate_ids = (int64_t)ht.duplicate_ids;
+    if (h_trace) {
+        int64_t phi = M;
+        for (int64_t i = 0; i < hg.rounds; ++i) {
+            phi -= hrec[i].kind == 0 ? hrec[i].emitted : 0;
+            h_trace[i].kind = hrec[i].kind;
+            h_trace[i].reserved0 = 0;
+            h_trace[i].target = hrec[i].kind == 0 ? hrec[i].target : 0;
+            h_trace[i].emitted = hrec[i].kind == 0 ? hrec[i].emitted : 0;
+            h_trace[i].phi = phi;
+        }
+    }
+    if (nleft != M - hg.emitted || ht.bad_views != 0)
+        return set_error(ODB_E_INTERNAL, "streaming plan does not account for every view exactly once");
+    return ODB_OK;
+}

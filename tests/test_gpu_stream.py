@@ -1,0 +1,129 @@
+"""GPU parity of the unified streaming loop (odb_stream_plan) with the oracle: every plan
+array, the per-round trace, the summary, the loss weights bit for bit and, on small
+cases, every collate element."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from _parity import log
+
+pytestmark = pytest.mark.gpu
+
+STREAM_INFO_EXACT = ["steps", "rounds", "emit_rounds", "skip_rounds", "stop_reason", "views", "emitted_views",
+                     "undelivered_views", "pending_views", "real_tokens", "padded_elems", "max_step_samples",
+                     "splits", "overflow_groups", "missing_ids", "duplicate_ids", "bad_views",
+                     "second_gather_rounds", "max_outstanding"]
+
+
+def offsets(lens):
+    return np.concatenate([[0], np.cumsum(np.asarray(lens, dtype=np.int64))])
+
+
+def run_case(name, lens, perm, W, budget, buffer_size, depth, rate, mode="join", quota=0, cap=None, pad_id=0,
+             full_collate=True, tokens=None):
+    import torch
+    import paper_2606_19989_amd as odb
+
+    N = len(lens)
+    log(f"stream case {name}: N={N} W={W} budget={budget} buffer={buffer_size} depth={depth} mode={mode} "
+        f"quota={quota} rate={list(rate)[:8]}")
+    tok_off = offsets(lens)
+    m_mode = oracle.MODE_NONJOIN if mode == "nonjoin" else oracle.MODE_JOIN
+    ref = oracle.stream(tok_off, perm, W, budget, mode=m_mode, quota=quota, buffer_size=buffer_size, depth=depth,
+                        rate=rate, capacity=cap)
+    rank_off = np.linspace(0, N, W + 1).astype(np.int64)   # not used by the streaming loop
+    d_tok_off = torch.from_numpy(tok_off).cuda()
+    toks = tokens if tokens is not None else synth.fill_tokens_torch(int(tok_off[-1]), "cuda")
+    win = odb.DeviceWindow(rank_off, d_tok_off, toks, None, 0)
+    sp = odb.StreamPipeline(win, torch.from_numpy(np.asarray(perm, dtype=np.int32)).cuda(), budget,
+                            buffer_size=buffer_size, depth=depth, rate=rate, mode=mode, quota=quota, capacity=cap,
+                            pad_id=pad_id)
+    info = sp.plan()
+    torch.cuda.synchronize()
+    for f in STREAM_INFO_EXACT:
+        assert info[f] == ref.sinfo[f], (f, info[f], ref.sinfo[f])
+    assert abs(info["pad_fraction"] - ref.sinfo["pad_fraction"]) <= 1e-12 * max(ref.sinfo["pad_fraction"], 1e-300)
+    assert np.array_equal(sp.trace_array(), ref.trace), "trace"
+    S, K, M = ref.steps, W * ref.steps, ref.sinfo["views"]
+    E = ref.sinfo["emitted_views"]
+    h = lambda t, k: t[:k].cpu().numpy()
+    assert np.array_equal(h(sp.slot_rows, K), ref.slot_rows), "slot_rows"
+    assert np.array_equal(h(sp.slot_maxlen, K), ref.slot_maxlen), "slot_maxlen"
+    assert np.array_equal(h(sp.slot_tokens, K), ref.slot_tokens), "slot_tokens"
+    assert np.array_equal(h(sp.slot_tokens_approx, K).view(np.int64), ref.slot_tokens_approx.view(np.int64))
+    assert np.array_equal(h(sp.slot_row_off, K + 1), ref.slot_row_off), "slot_row_off"
+    assert np.array_equal(h(sp.slot_tile_off, K + 1), ref.slot_tile_off), "slot_tile_off"
+    assert np.array_equal(h(sp.emit_views, E), ref.emit_views), "emit_views"
+    assert np.array_equal(h(sp.emit_order, E), ref.emit_order), "emit_order"
+    assert np.array_equal(h(sp.left_views, M - E), ref.left_views), "left_views"
+    assert np.array_equal(h(sp.left_off, W + 1), ref.left_off), "left_off"
+    for m in (oracle.WEIGHT_SAMPLE, oracle.WEIGHT_TOKEN_APPROX, oracle.WEIGHT_TOKEN_EXACT):
+        wt, st, ss = sp.loss_weights(m)
+        ewt, est, ess = ref.loss_weights(m)
+        assert np.array_equal(wt.cpu().numpy().view(np.int64), ewt.view(np.int64)), ("weights", m)
+        assert np.array_equal(st.cpu().numpy(), est) and np.array_equal(ss.cpu().numpy(), ess)
+    if full_collate:
+        outs = sp.collate()
+        torch.cuda.synchronize()
+        odb.odb_collate_status(sp.ws)
+        want = ref.collate(tok_off, toks.cpu().numpy(), pad_id)
+        for name_, g, e in zip(["input_ids", "labels", "attention_mask", "position_ids"], outs, want):
+            assert np.array_equal(g.cpu().numpy(), e), name_
+    return sp, ref
+
+
+def edge_cases():
+    rng = np.random.default_rng(71)
+    out = []
+    add = lambda name, lens, W, budget, buf, depth, rate, **kw: out.append(
+        (name, np.asarray(lens, dtype=np.int64), W, budget, buf, depth, np.asarray(rate, dtype=np.int32), kw))
+    add("empty", [], 3, 100, 4, 4, [4, 4, 4])
+    add("one_sample_four_ranks", [7], 4, 100, 2, 3, [1, 2, 3, 1])           # padding wraps N = 1 times 3
+    add("fewer_samples_than_ranks", [5, 9, 2], 5, 12, 1, 1, [1] * 5)
+    add("buffer_one", rng.integers(1, 50, 40), 3, 30, 1, 1, [1, 1, 1])
+    add("slow_rank", rng.integers(1, 900, 700), 4, 4096, 64, 64, [1, 64, 64, 64])
+    add("deep_envelope", rng.integers(1, 900, 3000), 3, 8192, 128, 1024, [300, 17, 128])
+    add("tiny_budget", rng.integers(1, 9, 500), 2, 1, 50, 80, [20, 80])
+    add("overflow_capacity", rng.integers(1, 600, 1500), 3, 3000, 200, 256, [256, 100, 50], cap=np.array([3, 0, 5]))
+    add("max_depth", rng.integers(1, 3000, 20000), 2, 16384, 4096, 4096, [4096, 4096])
+    n = 2003
+    for q in (1, 500, n + 1):
+        add(f"nonjoin_q{q}", rng.integers(1, 2000, n), 4, 6000, 100, 150, [150, 90, 40, 150], mode="nonjoin",
+            quota=q)
+    add("nonjoin_capacity", rng.integers(1, 900, 900), 2, 2500, 64, 64, [64, 7], mode="nonjoin", quota=700,
+        cap=np.array([2, 4]))
+    return out
+
+
+@pytest.mark.parametrize("idx", range(len(edge_cases())))
+def test_stream_edge_cases(idx):
+    name, lens, W, budget, buf, depth, rate, kw = edge_cases()[idx]
+    perm = np.random.default_rng(idx).permutation(len(lens)).astype(np.int32)
+    run_case(name, lens, perm, W, budget, buf, depth, rate, pad_id=idx, **kw)
+
+
+def test_stream_random_small():
+    rng = np.random.default_rng(72)
+    for t in range(30):
+        N = int(rng.integers(1, 3000))
+        W = int(rng.integers(1, 9))
+        lens = rng.integers(1, int(rng.integers(2, 4000)), size=N)
+        buf = int(rng.integers(1, 300))
+        depth = buf + int(rng.integers(0, 200))
+        rate = rng.integers(1, depth + 1, size=W).astype(np.int32)
+        mode = "nonjoin" if t % 3 == 2 else "join"
+        cap = rng.integers(0, 6, size=W) if t % 4 == 1 else None
+        run_case(f"random_{t}", lens, rng.permutation(N).astype(np.int32), W, int(rng.integers(1, 30000)), buf, depth,
+                 rate, mode=mode, quota=int(rng.integers(1, N + 2)), cap=cap, pad_id=t % 5)
+
+
+def test_stream_window_workload():
+    # the multimodal window's samples as a dataset streamed through 8 ranks with the
+    # paper's default buffer of 1024 and unequal worker throughput
+    w = synth.WORKLOADS["mm_w8x262144"].window()
+    lens = np.diff(w.tok_off)
+    rng = np.random.default_rng(73)
+    perm = rng.permutation(len(lens)).astype(np.int32)
+    rate = np.array([1024, 512, 1024, 256, 1024, 1024, 768, 1024], dtype=np.int32)
+    run_case("mm_stream", lens, perm, 8, w.budget, 1024, 1024, rate, full_collate=False)

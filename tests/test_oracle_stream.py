@@ -22,7 +22,7 @@ def offsets(lens):
 def view_identity(perm, N, W):
     q = -(-N // W)
     m = np.arange(q * W)
-    return np.where(m < N, perm[np.minimum(m, N - 1)], perm[np.maximum(m - N, 0)]), q
+    return perm[m % N], q
 
 
 def random_case(rng):

@@ -110,6 +110,48 @@ def length_sketch_timing(odb, win, ws, w, dev, reps=5):
             "window_gbs_incl_sync": 8 * (w.n + 1) / (msw * 1e-3) / 1e9}
 
 
+STREAM_CONFIG = dict(ranks=64, budget=16384, buffer_size=1024, depth=1024, rate=1024, seed=74)
+
+
+def stream_timing(odb, w, tok_off, tokens, dev, iters=3):
+    """One logical iteration of the unified streaming loop over the window's samples as
+    a dataset (odb_stream_plan: every round's fetch, grouping, alignment and emission),
+    then the collate of its plan; host clock around each synchronising call."""
+    import numpy as np
+    import torch
+
+    c = STREAM_CONFIG
+    perm = torch.from_numpy(np.random.default_rng(c["seed"]).permutation(w.n).astype(np.int32)).to(dev)
+    win = odb.DeviceWindow(np.linspace(0, w.n, c["ranks"] + 1).astype(np.int64), tok_off, tokens, None, 0)
+    sp = odb.StreamPipeline(win, perm, c["budget"], buffer_size=c["buffer_size"], depth=c["depth"],
+                            rate=np.full(c["ranks"], c["rate"], np.int32))
+    sp.plan()
+    sp.collate()
+    torch.cuda.synchronize()
+    plan_t, coll_t = [], []
+    for _ in range(iters):
+        t0 = time.perf_counter()
+        info = sp.plan()
+        t1 = time.perf_counter()
+        sp.collate()
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        plan_t.append(t1 - t0)
+        coll_t.append(t2 - t1)
+    plan_ms = float(np.median(plan_t)) * 1e3
+    coll_ms = float(np.median(coll_t)) * 1e3
+    out = {"config": dict(c, samples=w.n, lengths=w.name),
+           "plan_ms": plan_ms, "collate_ms": coll_ms,
+           "rounds": info["rounds"], "emit_rounds": info["emit_rounds"], "skip_rounds": info["skip_rounds"],
+           "us_per_round": plan_ms * 1e3 / max(info["rounds"], 1), "steps": info["steps"],
+           "pad_fraction": info["pad_fraction"], "padded_elems": info["padded_elems"],
+           "emitted_views": info["emitted_views"],
+           "samples_per_s": info["emitted_views"] / ((plan_ms + coll_ms) * 1e-3)}
+    del sp
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(workload, tokens_dev, group=4, min_seconds=10.0, pad_id=0):
     """The oracle (plan + full collate), single-threaded, on consecutive groups of
     `group` ranks of the same window until at least `min_seconds` of CPU work."""
@@ -159,6 +201,8 @@ def main():
     ap.add_argument("--workload", default="ln480_w64x262144")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum CPU time of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-stream", dest="stream", action="store_false",
+                    help="skip the unified-streaming-loop measurement")
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="GIB",
                     help="before the steps, run one plain device copy of GIB GiB (int32 -> int32) as a "
                          "known-size reference for hardware byte counters")
@@ -228,6 +272,14 @@ def main():
     sketch = length_sketch_timing(odb, win, pipe.ws, w, dev)
     log(f"[bench] length sketch: cv={sketch['cv']:.3f} f_s={sketch['short_fraction']:.3f} "
         f"window {sketch['window_ms']:.3f} ms")
+    if args.stream:
+        # the window pipeline's 129 GB of outputs and the streaming plan's would not both
+        # fit in 288 GB
+        pipe.outputs = None
+        torch.cuda.empty_cache()
+        stream = stream_timing(odb, w, tok_off, tokens, dev)
+        log(f"[bench] streaming iteration: plan {stream['plan_ms']:.1f} ms over {stream['rounds']} rounds, "
+            f"collate {stream['collate_ms']:.1f} ms")
     copy_gbs = copy_ceiling(dev)
     log(f"[bench] plain 4 GiB device copy: {copy_gbs:.0f} GB/s")
 
@@ -257,6 +309,7 @@ def main():
         "loss_weights_ms": weights_ms,
         "second_gather_rounds": int(info["second_gather_rounds"]),
         "length_sketch": sketch,
+        "stream": stream if args.stream else None,
         "config": {
             "workload": wl.name,
             "description": wl.description,

@@ -135,18 +135,24 @@ def compare_collate_by_rank(w, outs, ref, tokens_dev, pad_id=0, check_tokens=100
         del toks, want
 
 
-def collate_properties(outs, ref, pad_id=0):
-    """Whole-output properties that hold at any size."""
+def collate_properties(outs, ref, pad_id=0, chunk=1 << 30):
+    """Whole-output properties that hold at any size (evaluated chunk by chunk, so the
+    temporaries stay small next to outputs of 100+ GB)."""
     import torch
 
     ids, lab, msk, pos = outs
     P = ref.padded_elems
     assert ids.numel() == P
-    real = int(msk.sum(dtype=torch.int64))
+    real = 0
+    for a in range(0, P, chunk):
+        b = min(P, a + chunk)
+        m = msk[a:b]
+        real += int(m.sum(dtype=torch.int64))
+        pad = m == 0
+        assert int(pad.logical_and(lab[a:b] != -100).sum()) == 0
+        assert int(pad.logical_and(ids[a:b] != pad_id).sum()) == 0
+        assert int(pad.logical_and(pos[a:b] != 0).sum()) == 0
+        assert int((m == 1).logical_and(ids[a:b] != lab[a:b]).sum()) == 0
+        del m, pad
     assert real == ref.info["real_tokens"]
-    assert int((msk == 0).logical_and(lab != -100).sum()) == 0
-    assert int((msk == 1).logical_and(ids != lab).sum()) == 0
-    assert int((msk == 0).logical_and(ids != pad_id).sum()) == 0
-    assert int((msk == 0).logical_and(pos != 0).sum()) == 0
-    # position ids of real tokens sum to sum over samples of l(l-1)/2
     return real

@@ -118,6 +118,35 @@ def test_length_sketch_arguments_checked_on_host():
     assert lib.odb_length_sketch(ctypes.byref(w), None, 3, 10, ref, fake_ws, size - 1, None) == odb.ODB_E_WORKSPACE
 
 
+def test_stream_arguments_checked_on_host():
+    lib = odb.load()
+    w, keep = _window([0, 4, 9])
+    assert lib.odb_stream_workspace_size(ctypes.byref(w), 64, 100, 50) > lib.odb_workspace_size(ctypes.byref(w))
+    assert lib.odb_stream_workspace_size(ctypes.byref(w), 4097, 100, 50) == 0     # deeper than the LDS sort
+    assert lib.odb_stream_workspace_size(ctypes.byref(w), 64, -1, 50) == 0
+    assert lib.odb_stream_workspace_size(ctypes.byref(w), 64, 100, 0) == 0
+    fake_ws = 0x100000  # never dereferenced: every call below fails its host checks first
+    rate = np.array([4, 4], dtype=np.int32)
+    bad_rate = np.array([4, 0], dtype=np.int32)
+    info = odb.StreamInfo()
+
+    def call(params, budget=10, cap=16):
+        return lib.odb_stream_plan(ctypes.byref(w), 1, budget, params, cap, 1, 1, 1, 1, 1, 1, 1, None, 1, 1, None,
+                                   ctypes.byref(info), fake_ws, 1 << 40, None)
+
+    ptr = lambda a: a.ctypes.data_as(ctypes.c_void_p).value
+    good = dict(mode=0, buffer_size=4, depth=8, reserved0=0, quota=0, rate=ptr(rate), slot_capacity=None, max_rounds=9)
+    for bad in (dict(mode=5), dict(buffer_size=0), dict(buffer_size=9), dict(depth=5000, buffer_size=8),
+                dict(reserved0=1), dict(mode=1, quota=0), dict(rate=None), dict(rate=ptr(bad_rate)),
+                dict(max_rounds=0)):
+        p = odb.StreamParams(**{**good, **bad})
+        assert call(ctypes.byref(p)) == odb.ODB_E_INVALID_ARG, bad
+    assert call(None) == odb.ODB_E_INVALID_ARG
+    p = odb.StreamParams(**good)
+    assert call(ctypes.byref(p), budget=0) == odb.ODB_E_INVALID_ARG
+    assert call(ctypes.byref(p), cap=-1) == odb.ODB_E_INVALID_ARG
+
+
 def test_binding_raises_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(odb, "_lib", None)
     monkeypatch.setattr(odb, "LIB_PATH", str(tmp_path / "missing.so"))

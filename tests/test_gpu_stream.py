@@ -127,3 +127,29 @@ def test_stream_window_workload():
     perm = rng.permutation(len(lens)).astype(np.int32)
     rate = np.array([1024, 512, 1024, 256, 1024, 1024, 768, 1024], dtype=np.int32)
     run_case("mm_stream", lens, perm, 8, w.budget, 1024, 1024, rate, full_collate=False)
+
+
+def test_stream_full_size():
+    # the largest window's 16.7M samples streamed by 64 ranks with the paper's buffer
+    # of 1024 and a budget in its L_max range; the benchmark times this configuration.
+    # Plan, trace and weights are compared exactly; collate on sampled elements plus
+    # whole-output properties
+    import torch
+
+    from _parity import collate_properties, compare_collate_sampled
+
+    w = synth.WORKLOADS["ln480_w64x262144"].window()
+    lens = np.diff(w.tok_off)
+    perm = np.random.default_rng(74).permutation(len(lens)).astype(np.int32)
+    toks = synth.fill_tokens_torch(int(w.tok_off[-1]), "cuda")
+    sp, ref = run_case("ln480_stream", lens, perm, 64, 16384, 1024, 1024, np.full(64, 1024, np.int32),
+                       full_collate=False, tokens=toks)
+    outs = sp.collate()
+    torch.cuda.synchronize()
+    import paper_2606_19989_amd as odb
+    odb.odb_collate_status(sp.ws)
+    compare_collate_sampled(w, outs, ref)
+    collate_properties(outs, ref)
+    log("  stream collate sampled and properties equal")
+    del sp, outs, toks
+    torch.cuda.empty_cache()

@@ -606,14 +606,16 @@ __global__ void stream_slots_kernel(StreamArgs a, int64_t S, int32_t* rows, int3
     }
 }
 
-// Rank r's emitted views (slot order, row order) and their identities.
-__global__ void __launch_bounds__(kSB) stream_emit_out_kernel(StreamArgs a, int64_t S, const int64_t* row_off,
+// Rank r's emitted views (slot order, row order) and their identities; blockIdx.x is
+// the rank, blockIdx.y a slice of its stream.
+__global__ void __launch_bounds__(256) stream_emit_out_kernel(StreamArgs a, int64_t S, const int64_t* row_off,
                                                               int32_t* emit_views, int32_t* emit_order,
                                                               int32_t* vcount, int32_t* icount) {
     const int r = blockIdx.x;
     const int64_t lo = row_off[(int64_t)r * S], hi = row_off[(int64_t)(r + 1) * S];
     const int32_t* ev = a.evw + (int64_t)r * a.q;
-    for (int64_t i = threadIdx.x; i < hi - lo; i += kSB) {
+    const int64_t stride = (int64_t)gridDim.y * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.y * blockDim.x + threadIdx.x; i < hi - lo; i += stride) {
         const int32_t m = ev[i];
         const int32_t id = view_identity(a, m);
         emit_views[lo + i] = m;
@@ -667,8 +669,9 @@ struct StreamTotals {
     unsigned long long duplicate_ids;
 };
 
-__global__ void stream_totals_kernel(StreamArgs a, int64_t K, const int64_t* tokens, const int32_t* vcount,
-                                     const int32_t* icount, StreamTotals* t) {
+__global__ void __launch_bounds__(256) stream_totals_kernel(StreamArgs a, int64_t K, const int64_t* tokens,
+                                                            const int32_t* vcount, const int32_t* icount,
+                                                            StreamTotals* t) {
     const int64_t M = a.q * a.W;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     unsigned long long tok = 0, bad = 0, miss = 0, dup = 0;
@@ -679,15 +682,27 @@ __global__ void stream_totals_kernel(StreamArgs a, int64_t K, const int64_t* tok
         miss += c == 0;
         dup += c > 1 ? (unsigned long long)(c - 1) : 0ull;
     }
+    __shared__ unsigned long long part[4][256 / kWave];
+    const int w = threadIdx.x / kWave;
     tok = wave_sum(tok);
     bad = wave_sum(bad);
     miss = wave_sum(miss);
     dup = wave_sum(dup);
     if ((threadIdx.x & (kWave - 1)) == 0) {
-        atomicAdd(&t->real_tokens, tok);
-        atomicAdd(&t->bad_views, bad);
-        atomicAdd(&t->missing_ids, miss);
-        atomicAdd(&t->duplicate_ids, dup);
+        part[0][w] = tok;
+        part[1][w] = bad;
+        part[2][w] = miss;
+        part[3][w] = dup;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long v[4] = {0, 0, 0, 0};
+        for (int f = 0; f < 4; ++f)
+            for (int i = 0; i < 256 / kWave; ++i) v[f] += part[f][i];
+        if (v[0]) atomicAdd(&t->real_tokens, v[0]);
+        if (v[1]) atomicAdd(&t->bad_views, v[1]);
+        if (v[2]) atomicAdd(&t->missing_ids, v[2]);
+        if (v[3]) atomicAdd(&t->duplicate_ids, v[3]);
     }
 }
 
@@ -922,7 +937,7 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     hipLaunchKernelGGL(clear_totals_kernel, dim3(1), dim3(64), 0, s, tot);
     ODB_LAUNCHED();
     if (K > 0) {
-        hipLaunchKernelGGL(stream_emit_out_kernel, dim3(W), dim3(kSB), 0, s, a, S, (const int64_t*)d_slot_row_off,
+        hipLaunchKernelGGL(stream_emit_out_kernel, dim3(W, 64), dim3(256), 0, s, a, S, (const int64_t*)d_slot_row_off,
                            d_emit_views, d_emit_order, vcount, icount);
         ODB_LAUNCHED();
     }

@@ -14,8 +14,17 @@
 // (shortest) sample.  So group 0 is position 0 alone and a group starting at position
 // p > 0 has B(l[p-1]) members (clipped by the end of the rank): next(0) = 1 and
 // next(p) = p + B(l[p-1]).  The group starts are exactly the positions reachable from 0
-// along next(), which pointer jumping finds in O(log G) rounds instead of a serial walk.
+// along next().
+//
+// Two equivalent ways to find them.  Lengths are sorted, so the step b(p) = B(l[p-1]) is
+// constant on runs of positions, and there are at most ~2 sqrt(budget) distinct values
+// of floor(budget / l): inside a run of step b the chain advances by exactly b, so one
+// thread per rank can walk the runs (in LDS) and record each run's first chain position,
+// and every position then knows whether it is a group start by one modulo.  When the
+// number of runs may exceed the LDS table, pointer jumping over the next() links marks
+// the chain in O(log G) doubling rounds instead.
 #include <climits>
+#include <cmath>
 #include <vector>
 
 #include "odb_internal.h"
@@ -291,6 +300,134 @@ __global__ void __launch_bounds__(kBlock) jump_kernel(const int32_t* __restrict_
     if (__ballot(changed) && (threadIdx.x & (kWave - 1)) == 0) st->jump_changed[round] = 1;
 }
 
+// ---- run-based chain walk
+constexpr int kRunCap = 4096;   // runs per rank held in LDS by run_chase_kernel
+
+// Run-start flags: position q >= 1 of a rank starts a run when q = 1 or its step differs
+// from the previous position's.
+__global__ void __launch_bounds__(kBlock) run_flags_kernel(const int32_t* __restrict__ slen,
+                                                           const int64_t* __restrict__ off,
+                                                           const RankState* __restrict__ ranks, int W, int64_t n,
+                                                           int64_t budget, uint8_t* __restrict__ flags) {
+    __shared__ int64_t s_off[kLdsRanks + 1];
+    off = stage_ranks(off, W, s_off);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
+        const int r = rank_of(off, W, p);
+        const int64_t q = p - off[r];
+        uint8_t f = 0;
+        if (q >= 1 && q < ranks[r].cnt)
+            f = q == 1 || batch_size(budget, slen[p - 1]) != batch_size(budget, slen[p - 2]);
+        flags[p] = f;
+    }
+}
+
+// Scan store of the run-start flags: the inclusive count of every position (its run id
+// + 1) and, at each run start, the run table entry: run k (global numbering, rank by
+// rank) starts at rank-local position run_start[k] with step run_b[k].
+struct RunStore {
+    const uint8_t* flags;
+    const int32_t* slen;
+    const int64_t* off;
+    int W;
+    int64_t budget;
+    int32_t* incl;
+    int32_t* run_start;
+    int32_t* run_b;
+    __device__ void operator()(int64_t p, uint32_t ex) const {
+        const uint32_t f = flags[p];
+        incl[p] = (int32_t)(ex + f);
+        if (!f) return;
+        const int r = rank_of(off, W, p);
+        run_start[ex] = (int32_t)(p - off[r]);
+        const int64_t b = batch_size(budget, slen[p - 1]);
+        run_b[ex] = (int32_t)(b < INT32_MAX ? b : INT32_MAX);   // any step >= 2^31 leaves the rank
+    }
+};
+
+// One block per rank: thread 0 walks the chain run by run and records the first chain
+// position of every run (INT32_MAX if the chain skips the run).  Positions and steps stay
+// below 2^31 (larger steps are stored as INT32_MAX), so the walk runs in 32-bit integers;
+// the table and its results sit in LDS when they fit.
+__global__ void __launch_bounds__(kBlock) run_chase_kernel(const int32_t* __restrict__ incl,
+                                                           const int64_t* __restrict__ off,
+                                                           const RankState* __restrict__ ranks,
+                                                           const int32_t* __restrict__ run_start,
+                                                           const int32_t* __restrict__ run_b,
+                                                           int32_t* __restrict__ run_c) {
+    __shared__ uint32_t ls[kRunCap + 1], lb[kRunCap], lc[kRunCap];
+    const int r = blockIdx.x;
+    const int64_t base = off[r];
+    const int64_t c = ranks[r].cnt;
+    if (c < 2) return;   // no position >= 1, no run
+    const int64_t rb = base > 0 ? incl[base - 1] : 0;
+    const int64_t R = incl[base + c - 1] - rb;
+    if (R <= kRunCap) {
+        for (int64_t i = threadIdx.x; i < R; i += blockDim.x) {
+            ls[i] = (uint32_t)run_start[rb + i];
+            lb[i] = (uint32_t)run_b[rb + i];
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            ls[R] = (uint32_t)c;
+            uint32_t cur = 1;   // next(0) = 1: the second group starts at position 1
+#pragma unroll 4
+            for (int i = 0; i < (int)R; ++i) {
+                const uint32_t e = ls[i + 1], b = lb[i];
+                const bool hit = cur < e;
+                lc[i] = hit ? cur : (uint32_t)INT32_MAX;
+                // chain positions cur, cur + b, ... below e; the next one is >= e
+                const uint32_t k = hit ? (e - cur + b - 1) / b : 0u;
+                cur += k * b;
+            }
+        }
+        __syncthreads();
+        for (int64_t i = threadIdx.x; i < R; i += blockDim.x) run_c[rb + i] = (int32_t)lc[i];
+        return;
+    }
+    if (threadIdx.x != 0) return;
+    uint32_t cur = 1;
+    for (int64_t i = 0; i < R; ++i) {
+        const uint32_t e = (uint32_t)(i + 1 < R ? run_start[rb + i + 1] : c);
+        const uint32_t b = (uint32_t)run_b[rb + i];
+        const bool hit = cur < e;
+        run_c[rb + i] = hit ? (int32_t)cur : INT32_MAX;
+        const uint32_t k = hit ? (e - cur + b - 1) / b : 0u;
+        cur += k * b;
+    }
+}
+
+// Group-start marks from the run table: q = 0, and q >= 1 at its run's first chain
+// position plus a multiple of the run's step.
+__global__ void __launch_bounds__(kBlock) run_marks_kernel(const int32_t* __restrict__ incl,
+                                                           const int64_t* __restrict__ off,
+                                                           const RankState* __restrict__ ranks, int W, int64_t n,
+                                                           const int32_t* __restrict__ run_b,
+                                                           const int32_t* __restrict__ run_c,
+                                                           uint8_t* __restrict__ marks) {
+    __shared__ int64_t s_off[kLdsRanks + 1];
+    off = stage_ranks(off, W, s_off);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p <= n; p += stride) {
+        if (p == n) {
+            marks[n] = 0;
+            continue;
+        }
+        const int r = rank_of(off, W, p);
+        const int64_t q = p - off[r];
+        uint8_t m = 0;
+        if (q == 0) {
+            m = ranks[r].cnt > 0;
+        } else if (q < ranks[r].cnt) {
+            const int64_t k = incl[p] - 1;
+            const int64_t c0 = run_c[k];
+            const uint32_t b = (uint32_t)run_b[k];
+            m = q >= c0 && (uint32_t)(q - c0) % b == 0;
+        }
+        marks[p] = m;
+    }
+}
+
 __global__ void init_jump_flags(DevStatus* st) {
     if (threadIdx.x < kMaxJumpRounds) st->jump_changed[threadIdx.x] = 0;
 }
@@ -349,8 +486,26 @@ __global__ void groups_kernel(const int32_t* __restrict__ incl, const int64_t* _
 
 }  // namespace
 
+// Mark scan, group index of every position, global group starts, G_r.
+static int finish_groups(const Layout& L, void* ws, int W, int64_t n, const int64_t* d_off, int32_t* d_gidx,
+                         int32_t* d_groups_out, RankState* d_ranks, hipStream_t s) {
+    uint8_t* marks = ws_at<uint8_t>(ws, L.marks);
+    int32_t* incl = ws_at<int32_t>(ws, L.incl);
+    int32_t* gstart = ws_at<int32_t>(ws, L.gstart);
+    ODB_TRY((device_excl_scan<uint32_t>(MarkLoad{marks}, InclStore{marks, incl}, n,
+                                        ws_at<uint32_t>(ws, L.partials), s)));
+    hipLaunchKernelGGL(gidx_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock), 0, s,
+                       (const uint8_t*)marks, (const int32_t*)incl, d_off, (const RankState*)d_ranks, W, n,
+                       d_gidx, gstart);
+    ODB_LAUNCHED();
+    hipLaunchKernelGGL(groups_kernel, dim3(grid_for(W, kBlock)), dim3(kBlock), 0, s, (const int32_t*)incl, d_off,
+                       W, d_ranks, ws_at<int64_t>(ws, L.gbase), d_groups_out);
+    ODB_LAUNCHED();
+    return ODB_OK;
+}
+
 int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget, const int64_t* d_off,
-                    int64_t max_cnt, const int32_t* d_slen, int32_t* d_gidx,
+                    int64_t max_cnt, int64_t len_range, const int32_t* d_slen, int32_t* d_gidx,
                     int32_t* d_groups_out, RankState* d_ranks, hipStream_t s) {
     int32_t* j0 = ws_at<int32_t>(ws, L.jmp0);
     int32_t* j1 = ws_at<int32_t>(ws, L.jmp1);
@@ -359,6 +514,29 @@ int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget,
     int32_t* gstart = ws_at<int32_t>(ws, L.gstart);
     DevStatus* st = ws_at<DevStatus>(ws, L.status);
     const unsigned grid = grid_for(n + 1, kBlock, (int64_t)num_cus() * 16);
+    // distinct steps per rank: at most the distinct values of floor(budget / l), i.e. at
+    // most 2 sqrt(budget) + 1, and at most the number of distinct lengths
+    int64_t runs_bound = 2 * ((int64_t)std::sqrt((double)budget) + 1) + 1;
+    if (len_range > 0 && len_range < runs_bound) runs_bound = len_range;
+    if (max_cnt < runs_bound) runs_bound = max_cnt;
+    if (runs_bound <= kRunCap && n < INT32_MAX) {
+        int32_t* run_start = j0;
+        int32_t* run_b = j1;
+        int32_t* run_c = ws_at<int32_t>(ws, L.gsize);
+        hipLaunchKernelGGL(run_flags_kernel, dim3(grid), dim3(kBlock), 0, s, d_slen, d_off, (const RankState*)d_ranks,
+                           W, n, budget, marks);
+        ODB_LAUNCHED();
+        ODB_TRY((device_excl_scan<uint32_t>(MarkLoad{marks},
+                                            RunStore{marks, d_slen, d_off, W, budget, incl, run_start, run_b}, n,
+                                            ws_at<uint32_t>(ws, L.partials), s)));
+        hipLaunchKernelGGL(run_chase_kernel, dim3(W), dim3(kBlock), 0, s, (const int32_t*)incl, d_off,
+                           (const RankState*)d_ranks, (const int32_t*)run_start, (const int32_t*)run_b, run_c);
+        ODB_LAUNCHED();
+        hipLaunchKernelGGL(run_marks_kernel, dim3(grid), dim3(kBlock), 0, s, (const int32_t*)incl, d_off,
+                           (const RankState*)d_ranks, W, n, (const int32_t*)run_b, (const int32_t*)run_c, marks);
+        ODB_LAUNCHED();
+        return finish_groups(L, ws, W, n, d_off, d_gidx, d_groups_out, d_ranks, s);
+    }
     hipLaunchKernelGGL(links_kernel, dim3(grid), dim3(kBlock), 0, s, d_slen, d_off,
                        (const RankState*)d_ranks, W, n, budget, j0, marks);
     ODB_LAUNCHED();
@@ -374,16 +552,7 @@ int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget,
         hipLaunchKernelGGL(jump_kernel, dim3(grid), dim3(kBlock), 0, s, jin, jout, marks, n, st, k);
         ODB_LAUNCHED();
     }
-    ODB_TRY((device_excl_scan<uint32_t>(MarkLoad{marks}, InclStore{marks, incl}, n,
-                                        ws_at<uint32_t>(ws, L.partials), s)));
-    hipLaunchKernelGGL(gidx_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock), 0, s,
-                       (const uint8_t*)marks, (const int32_t*)incl, d_off, (const RankState*)d_ranks, W, n,
-                       d_gidx, gstart);
-    ODB_LAUNCHED();
-    hipLaunchKernelGGL(groups_kernel, dim3(grid_for(W, kBlock)), dim3(kBlock), 0, s, (const int32_t*)incl, d_off,
-                       W, d_ranks, ws_at<int64_t>(ws, L.gbase), d_groups_out);
-    ODB_LAUNCHED();
-    return ODB_OK;
+    return finish_groups(L, ws, W, n, d_off, d_gidx, d_groups_out, d_ranks, s);
 }
 
 }  // namespace odb
@@ -483,6 +652,6 @@ extern "C" int odb_form_groups(const odb_window_t* w, int64_t budget, int32_t* d
         const int64_t c = w->rank_offsets[r + 1] - w->rank_offsets[r];
         if (c > max_cnt) max_cnt = c;
     }
-    return group_sequences(L, d_ws, W, n, budget, d_off, max_cnt, d_sorted_len, d_group_index,
-                           d_groups_per_rank, d_ranks, s);
+    return group_sequences(L, d_ws, W, n, budget, d_off, max_cnt, n > 0 ? (int64_t)hs.max_len - hs.min_len + 1 : 0,
+                           d_sorted_len, d_group_index, d_groups_per_rank, d_ranks, s);
 }

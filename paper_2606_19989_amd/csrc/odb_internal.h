@@ -309,8 +309,10 @@ int device_excl_scan(Load load, Store store, int64_t n, Out* partials, hipStream
 // position (d_gidx), the global position of every group start (workspace gstart, group
 // ids numbered rank by rank), G_r and the first group id of every rank (d_ranks[r].G,
 // .gbase and workspace gbase[W+1]), and optionally G_r to d_groups_out.
+// len_range = max_len - min_len + 1 of the sequences if known (0 otherwise); it only
+// selects between two equivalent ways of finding the chain (see odb_form.hip).
 int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget,
-                    const int64_t* d_rank_off, int64_t max_cnt,
+                    const int64_t* d_rank_off, int64_t max_cnt, int64_t len_range,
                     const int32_t* d_slen, int32_t* d_gidx, int32_t* d_groups_out,
                     RankState* d_ranks, hipStream_t s);
 

@@ -13,6 +13,14 @@
 //                    apart) and stores each group as one aligned 16-byte non-temporal
 //                    store per output.
 //
+// Row edges.  A group whose 4 elements cross from one row into the next (the next row in
+// the same tile, rows of at least 4 elements) takes the first row's part from its own
+// vector load and the next row's record and first tokens from uniform-address scalar
+// loads, one boundary lane of the wave at a time.  Scalar loads complete on their own
+// counter, so waiting for them does not wait for the stores the wave has in flight,
+// which a late vector load would (see below).  Other edge cases (tile edges, rows
+// shorter than 4) are finished element by element.
+//
 // Software pipeline.  On CDNA the vector-memory counter covers loads and stores alike
 // and retires in order, so waiting for a load also waits for every store issued before
 // it.  Under a saturated write stream that wait is long.  The kernel therefore keeps
@@ -219,6 +227,11 @@ struct Stage {
     v4i t;
 };
 
+// Loads through these (with wave-uniform addresses) become scalar loads.
+typedef __attribute__((address_space(4))) const int64_t* cptr64;
+typedef __attribute__((address_space(4))) const int32_t* cptr32;
+typedef __attribute__((address_space(4))) const v4i* cptrv4;
+
 // Values of the 4 elements at e (the stage's position); elements at or past `total` are
 // left unspecified (the caller does not store them).
 __device__ __forceinline__ void stage_values(const Stage& a, int64_t e, int64_t total, const Plan& p, int vec_ok,
@@ -226,7 +239,49 @@ __device__ __forceinline__ void stage_values(const Stage& a, int64_t e, int64_t 
     const Cursor& c = a.c;
     const RowRec& r = a.r;
     const int32_t nreal = r.l - c.col;
-    if (vec_ok && c.col + (kVec - 1) < c.ml && (nreal <= 0 || r.ts + c.col + kVec <= p.tok_end)) {
+    // one row edge inside the tile: row B's record and first tokens come through the
+    // scalar cache, one boundary lane at a time (scalar loads wait on their own counter,
+    // so they never wait for this wave's outstanding stores)
+    bool edge = vec_ok && c.ml >= kVec && c.col + kVec > c.ml && c.ri >= 0 && c.ri + 1 < c.ri_end &&
+                c.ri + 1 < p.max_rows && r.ts + c.col + kVec <= p.tok_end;
+    int32_t bl = 0;
+    v4i bt = {0, 0, 0, 0};
+    {
+        uint64_t need = __ballot(edge);
+        const int lane = threadIdx.x & (kWave - 1);
+        while (need) {
+            const int l = __builtin_ctzll(need);
+            need &= need - 1;
+            const int32_t ri1 = __builtin_amdgcn_readlane(c.ri, l) + 1;
+            const int64_t ts = *(cptr64)(p.row_ts + ri1);
+            const int32_t len = *(cptr32)(p.row_len + ri1);
+            const bool fits = ts + kVec <= p.tok_end;
+            const v4i h = *(cptrv4)(p.tokens + (fits ? ts : 0));
+            if (lane == l) {
+                bl = len;
+                bt = h;
+                edge = edge && fits;
+            }
+        }
+    }
+    if (edge) {
+        const int32_t inA = c.ml - c.col;   // elements left in row A (1..3)
+#pragma unroll
+        for (int i = 0; i < kVec; ++i) {
+            const bool b = i >= inA;
+            const int32_t col = b ? i - inA : c.col + i;
+            const int32_t len = b ? bl : r.l;
+            const bool real = col < len;
+            int32_t tb = bt[0];
+            tb = col == 1 ? bt[1] : tb;
+            tb = col == 2 ? bt[2] : tb;
+            const int32_t tok = b ? tb : a.t[i];
+            vid[i] = real ? tok : pad_id;
+            vlab[i] = real ? tok : -100;
+            vmsk[i] = real ? 1 : 0;
+            vpos[i] = real ? col : 0;
+        }
+    } else if (vec_ok && c.col + (kVec - 1) < c.ml && (nreal <= 0 || r.ts + c.col + kVec <= p.tok_end)) {
         // the 4 elements sit in one row and the vector load covered them
 #pragma unroll
         for (int i = 0; i < kVec; ++i) {

@@ -58,6 +58,11 @@ def adversarial_windows():
         quota=1000, capacity=np.array([2, 4]))
     add("nonjoin_empty_rank", [rng.integers(1, 900, 70), [], rng.integers(1, 900, 5)], 2500, mode="nonjoin", quota=10)
     add("empty_window", [[], []], 100)
+    # group discovery: a huge budget with a wide length range takes the pointer-jumping
+    # path; a 4M budget with lengths up to 5000 gives ~4000 distinct steps, close to the
+    # run walk's LDS table
+    add("huge_budget_jumping", [rng.integers(1, 20000, 9000), rng.integers(1, 20000, 5000)], 1 << 40)
+    add("many_step_runs", [rng.integers(1, 5000, 12000), rng.integers(1, 5000, 7000)], 4_000_000)
     per = [rng.integers(100, 3000, 47 - r) for r in range(15)] + [np.zeros(0, np.int64)]
     add("empty_rank_audit_w16", per, 8192)
     return out

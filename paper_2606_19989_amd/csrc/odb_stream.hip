@@ -8,7 +8,7 @@
 // head to M = W * ceil(N / W) views (view m has identity perm[m mod N]); view m belongs
 // to rank m mod W, visited in increasing m.
 //
-// One protocol round k is three launches:
+// One protocol round k is two launches:
 //   stream_form_kernel   one block per rank: fetch up to rate[r] views under the depth
 //                        envelope |B_r| <= D; status (finished / not ready / ready); a ready
 //                        rank sorts its whole buffer by (length desc, view asc) in LDS and
@@ -18,9 +18,9 @@
 //                        over the ready ranks); in an emit round each ready rank applies
 //                        Algorithm 1 (split in closed form, overflow by size rank) and
 //                        writes its T slot records, its emitted views and its new buffer
-//                        (the overflow); finished ranks (join) write IDLE slots
-//   stream_round_kernel  one block: round bookkeeping, the non-join quota cut (Theorem 2),
-//                        termination
+//                        (the overflow); finished ranks (join) write IDLE slots.  The last
+//                        block to finish (a ticket counter, no waiting) does the round's
+//                        bookkeeping: the non-join quota cut (Theorem 2) and termination
 // Rounds are enqueued in chunks; the host reads the done flag once per chunk, and rounds
 // enqueued after the stop return at once.  A final pass turns the per-rank staging into
 // the window plan layout (rank-major slots, row and tile offsets), so odb_collate and
@@ -71,6 +71,8 @@ struct RankStream {
 struct StreamRec {
     int32_t kind;      // 0 emit, 1 skip, 2 stop
     int32_t changed;   // an emit round in which some ready rank had G_r != T
+    int32_t ticket;    // blocks of the round's emit kernel that have finished
+    int32_t pad;
     int64_t target;    // T (emit rounds)
     int64_t emitted;   // views emitted in the round (after a quota cut)
     int64_t cut;       // steps kept (emit rounds); stop reason (stop rounds)
@@ -305,8 +307,9 @@ __device__ RoundView decide_round(const StreamArgs& a) {
     return v;
 }
 
-__global__ void __launch_bounds__(kSB) stream_emit_kernel(StreamArgs a, int64_t k) {
-    if (*(volatile int32_t*)&a.g->done) return;
+__device__ void round_bookkeeping(const StreamArgs& a, int64_t k);
+
+__device__ void emit_round(const StreamArgs& a, int64_t k) {
     const RoundView v = decide_round(a);
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         a.rec[k].kind = v.kind;
@@ -513,9 +516,9 @@ __global__ void __launch_bounds__(kSB) stream_emit_kernel(StreamArgs a, int64_t 
 }
 
 // ------------------------------------------------------------------ round: bookkeeping
-__global__ void __launch_bounds__(kSB) stream_round_kernel(StreamArgs a, int64_t k) {
+// Round bookkeeping, run by the last block of the round's emit kernel.
+__device__ void round_bookkeeping(const StreamArgs& a, int64_t k) {
     StreamGlobal* g = a.g;
-    if (*(volatile int32_t*)&g->done) return;
     StreamRec* rec = a.rec + k;
     const int kind = rec->kind;
     if (kind == 2) {
@@ -588,6 +591,23 @@ __global__ void __launch_bounds__(kSB) stream_round_kernel(StreamArgs a, int64_t
             g->err |= kSErrRounds;
             g->done = 1;
         }
+    }
+}
+
+__global__ void __launch_bounds__(kSB) stream_emit_kernel(StreamArgs a, int64_t k) {
+    if (*(volatile int32_t*)&a.g->done) return;
+    emit_round(a, k);
+    // the last block of the round does the bookkeeping once every block's writes are visible
+    __shared__ int32_t s_last;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __threadfence();
+        s_last = atomicAdd(&a.rec[k].ticket, 1) == (int32_t)gridDim.x - 1;
+    }
+    __syncthreads();
+    if (s_last) {
+        __threadfence();
+        round_bookkeeping(a, k);
     }
 }
 
@@ -881,8 +901,6 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
             hipLaunchKernelGGL(stream_form_kernel, dim3(W), dim3(kSB), sort_lds, s, a, k);
             ODB_LAUNCHED();
             hipLaunchKernelGGL(stream_emit_kernel, dim3(W), dim3(kSB), 0, s, a, k);
-            ODB_LAUNCHED();
-            hipLaunchKernelGGL(stream_round_kernel, dim3(1), dim3(kSB), 0, s, a, k);
             ODB_LAUNCHED();
         }
         ODB_TRY_HIP(hipMemcpyAsync(&hg, a.g, sizeof(hg), hipMemcpyDeviceToHost, s));

@@ -214,19 +214,45 @@ __global__ void __launch_bounds__(kSB) stream_form_kernel(StreamArgs a, int64_t 
         keys[i] = key;
     }
     tok = sblock_sum(tok);   // also a barrier for keys[]
-    for (int64_t size = 2; size <= p2; size <<= 1) {
-        for (int64_t stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int64_t t = threadIdx.x; t < (p2 >> 1); t += kSB) {
-                const int64_t lo = 2 * t - (t & (stride - 1));
-                const int64_t hi = lo + stride;
-                const bool up = (lo & size) == 0;
-                const unsigned long long x = keys[lo], y = keys[hi];
-                if ((x > y) == up) {
-                    keys[lo] = y;
-                    keys[hi] = x;
+    if (p2 <= kSB) {
+        // one key per thread: exchanges with a partner less than a wave away are lane
+        // shuffles, only the longer strides go through LDS (10 of 55 stages at 1024)
+        const int i = threadIdx.x;
+        const bool in = i < p2;
+        unsigned long long x = in ? keys[i] : ~0ull;
+        for (int size = 2; size <= (int)p2; size <<= 1) {
+            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                unsigned long long y;
+                if (stride >= kWave) {
+                    __syncthreads();
+                    if (in) keys[i] = x;
+                    __syncthreads();
+                    y = in ? keys[i ^ stride] : x;
+                } else {
+                    y = __shfl_xor(x, stride, kWave);
                 }
+                const bool keep_min = ((i & stride) == 0) == ((i & size) == 0);
+                x = keep_min ? (x < y ? x : y) : (x < y ? y : x);
             }
-            __syncthreads();
+        }
+        __syncthreads();
+        if (in) keys[i] = x;
+        __syncthreads();
+    } else {
+        for (int64_t size = 2; size <= p2; size <<= 1) {
+            for (int64_t stride = size >> 1; stride > 0; stride >>= 1) {
+                for (int64_t t = threadIdx.x; t < (p2 >> 1); t += kSB) {
+                    const int64_t lo = 2 * t - (t & (stride - 1));
+                    const int64_t hi = lo + stride;
+                    const bool up = (lo & size) == 0;
+                    const unsigned long long x = keys[lo], y = keys[hi];
+                    if ((x > y) == up) {
+                        keys[lo] = y;
+                        keys[hi] = x;
+                    }
+                }
+                __syncthreads();
+            }
         }
     }
     int32_t* sv = a.sv + (int64_t)r * a.D;

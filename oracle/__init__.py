@@ -96,38 +96,49 @@ ROUND_EMIT, ROUND_SKIP, ROUND_STOP = 0, 1, 2
 _lib = None
 
 
+def _bind(path: str):
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    lib.oracle_plan.restype = P
+    lib.oracle_plan.argtypes = [ctypes.c_int32, ctypes.c_int64, P, P, P, ctypes.c_int64,
+                                ctypes.c_int64, ctypes.c_int32, ctypes.c_int64, P]
+    lib.oracle_last_error.restype = ctypes.c_char_p
+    lib.oracle_free.argtypes = [P]
+    lib.oracle_info.argtypes = [P, ctypes.POINTER(_Info)]
+    lib.oracle_form.argtypes = [P, P, P, P, P]
+    lib.oracle_slots.argtypes = [P, P, P, P, P, P]
+    lib.oracle_emit.argtypes = [P, P, P, P]
+    lib.oracle_collate.argtypes = [P, P, P, ctypes.c_int32, P, P, P, P]
+    lib.oracle_collate_rank.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int32, P, P, P, P]
+    lib.oracle_collate_rank.restype = ctypes.c_int
+    lib.oracle_round_targets.argtypes = [P, P]
+    lib.oracle_slots_approx.argtypes = [P, P]
+    lib.oracle_loss_weights.argtypes = [P, ctypes.c_int32, P, P, P]
+    lib.oracle_loss_weights.restype = ctypes.c_int
+    lib.oracle_stream.restype = P
+    lib.oracle_stream.argtypes = [ctypes.c_int32, ctypes.c_int64, P, P, ctypes.c_int64, ctypes.c_int32,
+                                  ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, P, P, ctypes.c_int64]
+    lib.oracle_stream_free.argtypes = [P]
+    lib.oracle_stream_info.argtypes = [P, ctypes.POINTER(_StreamInfo)]
+    lib.oracle_stream_trace.argtypes = [P, P]
+    lib.oracle_stream_views.argtypes = [P, P, P, P]
+    return lib
+
+
 def _load():
     global _lib
     if _lib is None:
         if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
             build(force=True)
-        lib = ctypes.CDLL(_LIB)
-        P = ctypes.c_void_p
-        lib.oracle_plan.restype = P
-        lib.oracle_plan.argtypes = [ctypes.c_int32, ctypes.c_int64, P, P, P, ctypes.c_int64,
-                                    ctypes.c_int64, ctypes.c_int32, ctypes.c_int64, P]
-        lib.oracle_last_error.restype = ctypes.c_char_p
-        lib.oracle_free.argtypes = [P]
-        lib.oracle_info.argtypes = [P, ctypes.POINTER(_Info)]
-        lib.oracle_form.argtypes = [P, P, P, P, P]
-        lib.oracle_slots.argtypes = [P, P, P, P, P, P]
-        lib.oracle_emit.argtypes = [P, P, P, P]
-        lib.oracle_collate.argtypes = [P, P, P, ctypes.c_int32, P, P, P, P]
-        lib.oracle_collate_rank.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int32, P, P, P, P]
-        lib.oracle_collate_rank.restype = ctypes.c_int
-        lib.oracle_round_targets.argtypes = [P, P]
-        lib.oracle_slots_approx.argtypes = [P, P]
-        lib.oracle_loss_weights.argtypes = [P, ctypes.c_int32, P, P, P]
-        lib.oracle_loss_weights.restype = ctypes.c_int
-        lib.oracle_stream.restype = P
-        lib.oracle_stream.argtypes = [ctypes.c_int32, ctypes.c_int64, P, P, ctypes.c_int64, ctypes.c_int32,
-                                      ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, P, P, ctypes.c_int64]
-        lib.oracle_stream_free.argtypes = [P]
-        lib.oracle_stream_info.argtypes = [P, ctypes.POINTER(_StreamInfo)]
-        lib.oracle_stream_trace.argtypes = [P, P]
-        lib.oracle_stream_views.argtypes = [P, P, P, P]
-        _lib = lib
+        _lib = _bind(_LIB)
     return _lib
+
+
+def _use_library(path: str) -> None:
+    """Test hook: make every oracle call go to the library at `path` (used to check that
+    the pins reject deliberately mutated builds of the oracle)."""
+    global _lib
+    _lib = _bind(path)
 
 
 def _ptr(a: Optional[np.ndarray]):
@@ -388,7 +399,7 @@ class StreamPlan(Plan):
 
 
 def stream(tok_off, perm, W: int, budget: int, mode: int = MODE_JOIN, quota: int = 0, buffer_size: int = 1024,
-           depth: Optional[int] = None, rate=None, capacity=None, max_rounds: int = 1 << 40) -> StreamPlan:
+           depth: Optional[int] = None, rate=None, capacity=None, max_rounds: Optional[int] = None) -> StreamPlan:
     """One logical iteration of the unified loop (Sec. 2.3, App. C) over identities
     0..N-1 with lengths from ``tok_off``, the shuffled identity list ``perm``, ``W``
     ranks, the collate buffer size, the outstanding-depth envelope ``depth`` (default
@@ -402,6 +413,11 @@ def stream(tok_off, perm, W: int, budget: int, mode: int = MODE_JOIN, quota: int
     depth = buffer_size if depth is None else int(depth)
     rate = np.full(W, buffer_size, np.int32) if rate is None else np.ascontiguousarray(rate, dtype=np.int32)
     cap = None if capacity is None else np.ascontiguousarray(capacity, dtype=np.int64)
+    if max_rounds is None:
+        # at most ceil(N/W) emitting rounds, at most ceil(buffer / min rate) fill rounds
+        # before each, and the round that observes the stop
+        q = -(-N // W) if N else 0
+        max_rounds = q + (q + 1) * -(-int(buffer_size) // int(rate.min())) + 2
     h = lib.oracle_stream(int(W), N, _ptr(tok_off), _ptr(perm), int(budget), int(mode), int(quota),
                           int(buffer_size), int(depth), _ptr(rate), _ptr(cap), int(max_rounds))
     if not h:

@@ -417,7 +417,7 @@ def stream(tok_off, perm, W: int, budget: int, mode: int = MODE_JOIN, quota: int
         # at most ceil(N/W) emitting rounds, at most ceil(buffer / min rate) fill rounds
         # before each, and the round that observes the stop
         q = -(-N // W) if N else 0
-        max_rounds = q + (q + 1) * -(-int(buffer_size) // int(rate.min())) + 2
+        max_rounds = q + (q + 1) * -(-int(buffer_size) // max(1, int(rate.min()))) + 2
     h = lib.oracle_stream(int(W), N, _ptr(tok_off), _ptr(perm), int(budget), int(mode), int(quota),
                           int(buffer_size), int(depth), _ptr(rate), _ptr(cap), int(max_rounds))
     if not h:

@@ -3,7 +3,10 @@
 One step = grouping (odb_form_groups) + alignment with coverage check
 (odb_align_groups) + padded collation (odb_collate) + exact token-level loss-scaling
 weights (odb_loss_weights) of a whole window whose CSR token stream is already resident
-in HBM.  Prints one JSON line:
+in HBM.  Steps run double-buffered on two HIP streams: the grouping and alignment of
+step i+1 (plan stream) run while the collate of step i (collate stream) streams its
+outputs; each step has its own plan buffers, the outputs are shared.  The serial
+schedule (one stream, plan then collate) is timed too.  Prints one JSON line:
 
   value        emitted samples per second (whole job)
   roofline     the collate stage (dominant): algorithmic bytes per odb_collate call /
@@ -34,6 +37,58 @@ def collate_alg_bytes(n, real_tokens, padded, slots):
     # 16 B written per padded element (4 int32 outputs), 4 B read per real token,
     # 8 B per token offset, 4 B per emitted id, 24 B of slot tables per slot
     return 16 * padded + 4 * real_tokens + 8 * (n + 1) + 4 * n + 24 * slots
+
+
+def pipelined_steps(pipes, plan_stream, collate_stream, steps):
+    """`steps` window steps, double-buffered over the two Pipelines in `pipes` (shared
+    outputs): step i plans into pipes[i % 2] on `plan_stream` once that pipeline's
+    previous collate has finished, and collates on `collate_stream` once its plan is
+    done.  odb_align_groups synchronises only the plan stream, so while the host waits
+    for step i's plan the collate stream is still writing step i-1.  Returns the host
+    seconds of the whole loop (the collate stream drained) and per step the HIP-event
+    milliseconds of odb_collate and of odb_loss_weights."""
+    import torch
+
+    free = [torch.cuda.Event(), torch.cuda.Event()]
+    for e in free:
+        e.record(collate_stream)
+    marks = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        p = pipes[i % 2]
+        plan_stream.wait_event(free[i % 2])
+        p.form(plan_stream)
+        p.align(plan_stream)
+        planned = torch.cuda.Event()
+        planned.record(plan_stream)
+        collate_stream.wait_event(planned)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record(collate_stream)
+        p.collate(collate_stream)
+        ev[1].record(collate_stream)
+        p.loss_weights(stream=collate_stream)
+        ev[2].record(collate_stream)
+        free[i % 2].record(collate_stream)
+        marks.append(ev)
+    torch.cuda.synchronize()
+    sec = time.perf_counter() - t0
+    return sec, [a.elapsed_time(b) for a, b, _ in marks], [b.elapsed_time(c) for _, b, c in marks]
+
+
+def serial_steps(pipe, stream, steps):
+    """`steps` window steps on one stream, each planned and then collated."""
+    import torch
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        pipe.form(stream)
+        pipe.align(stream)
+        pipe.collate(stream)
+        pipe.loss_weights(stream=stream)
+    torch.cuda.synchronize()
+    return time.perf_counter() - t0
 
 
 def measured_traffic(workload):
@@ -196,8 +251,8 @@ def cpu_baseline(workload, tokens_dev, group=4, min_seconds=10.0, pad_id=0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--workload", default="ln480_w64x262144")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum CPU time of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -223,10 +278,16 @@ def main():
     w = wl.window()
     log(f"[bench] {wl.name}: W={w.W} n={w.n} tokens={w.total_tokens} (drawn in {time.time() - t:.1f} s)")
     dev = torch.device("cuda:0")
+    torch.cuda.init()
+    # the two streams are created before any other stream is used, so the runtime puts
+    # them on different hardware queues (streams sharing a queue run one after another)
+    plan_stream = torch.cuda.Stream(device=dev)
+    collate_stream = torch.cuda.Stream(device=dev)
     tok_off, tokens, ident = synth.device_tensors(w, dev)
     torch.cuda.synchronize()
     win = odb.DeviceWindow(w.rank_off, tok_off, tokens, ident, w.num_identities)
-    pipe = odb.Pipeline(win, w.budget, mode=w.mode, quota=w.quota, pad_id=0)
+    pipes = [odb.Pipeline(win, w.budget, mode=w.mode, quota=w.quota, pad_id=0) for _ in range(2)]
+    pipe = pipes[0]
     log(f"[bench] inputs resident: {(tok_off.numel() * 8 + tokens.numel() * 4) / 1e9:.1f} GB")
 
     if args.calibrate_copy > 0:
@@ -239,35 +300,29 @@ def main():
         log(f"[bench] calibration copy: {m * 4} bytes read, {m * 4} bytes written")
         del src, dst
         torch.cuda.empty_cache()
-    for i in range(args.warmup):
-        pipe.run()
-        pipe.loss_weights(odb.ODB_WEIGHT_TOKEN_EXACT)
-        torch.cuda.synchronize()
-        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+    for p in pipes:
+        p.run()
+        p.loss_weights(odb.ODB_WEIGHT_TOKEN_EXACT)
+        pipes[1].outputs = pipes[0].outputs  # one set of outputs, written step by step
+    torch.cuda.synchronize()
     info = dict(pipe.info)
-    odb.odb_collate_status(pipe.ws)
+    for p in pipes:
+        odb.odb_collate_status(p.ws)
+    # warm-up in the timed schedule (the first overlapped step runs slow)
+    pipelined_steps(pipes, plan_stream, collate_stream, args.warmup)
+    log(f"[bench] {args.warmup} warm-up steps done")
 
-    stream = torch.cuda.current_stream()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    lw = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    for i in range(args.steps):
-        pipe.form()
-        pipe.align()
-        ev[i][0].record(stream)
-        pipe.collate()
-        ev[i][1].record(stream)
-        pipe.loss_weights(odb.ODB_WEIGHT_TOKEN_EXACT)
-        lw[i].record(stream)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    log(f"[bench] timed {args.steps} steps")
-    sec_per_step = (t1 - t0) / args.steps
-    collate_all = [a.elapsed_time(b) for a, b in ev]
-    weights_ms = float(np.mean([b.elapsed_time(c) for (a, b), c in zip(ev, lw)]))
+    sec, collate_all, weights_all = pipelined_steps(pipes, plan_stream, collate_stream, args.steps)
+    log(f"[bench] timed {args.steps} steps (two streams)")
+    for p in pipes:
+        assert p.info["steps"] == info["steps"] and p.info["padded_elems"] == info["padded_elems"]
+        odb.odb_collate_status(p.ws)
+    sec_per_step = sec / args.steps
     collate_ms = float(np.mean(collate_all))
-    assert pipe.info["steps"] == info["steps"] and pipe.info["padded_elems"] == info["padded_elems"]
+    weights_ms = float(np.mean(weights_all))
+    serial_n = min(max(3, args.steps // 2), 20)
+    serial_sec_per_step = serial_steps(pipe, plan_stream, serial_n) / serial_n
+    log(f"[bench] serial schedule: {serial_sec_per_step * 1e3:.2f} ms/step")
 
     sketch = length_sketch_timing(odb, win, pipe.ws, w, dev)
     log(f"[bench] length sketch: cv={sketch['cv']:.3f} f_s={sketch['short_fraction']:.3f} "
@@ -275,7 +330,8 @@ def main():
     if args.stream:
         # the window pipeline's 129 GB of outputs and the streaming plan's would not both
         # fit in 288 GB
-        pipe.outputs = None
+        for p in pipes:
+            p.outputs = None
         torch.cuda.empty_cache()
         stream = stream_timing(odb, w, tok_off, tokens, dev)
         log(f"[bench] streaming iteration: plan {stream['plan_ms']:.1f} ms over {stream['rounds']} rounds, "
@@ -298,6 +354,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": sec_per_step * 1e3,
+        "serial_ms_per_step": serial_sec_per_step * 1e3,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -321,6 +378,8 @@ def main():
             "budget": w.budget,
             "mode": w.mode,
             "pad_fraction": info["pad_fraction"],
+            "schedule": "two HIP streams, double-buffered plans: grouping + alignment of step i+1 run "
+                        "beside the collate of step i",
         },
         "roofline": {
             "bound": "hbm",

@@ -825,19 +825,57 @@ int run_coverage_exact(const odb_window_t* w, const Layout& L, void* ws, const i
 // more than once = |twice|, extra listings = dup.  An id of another rank in these lists
 // is an internal error.
 constexpr int kCovBlock = 1024;
-constexpr int kCovUnroll = 8;
 
-template <typename T>
-__device__ __forceinline__ T cov_block_sum(T v) {
-    __shared__ T part[kCovBlock / kWave];
-    v = wave_sum(v);
-    if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = v;
-    __syncthreads();
-    T t = 0;
+// The chunk's view of one listed id.  Ids, ranks and chunks stay below 2^31, so the
+// range tests are single unsigned compares: (uint32)(x - base) < nr holds exactly for
+// base <= x < base + nr, negative x included.
+struct CovChunk {
+    uint32_t* once;
+    uint32_t* twice;
+    uint32_t base, nr;  // the rank's views [base, base + nr)
+    uint32_t lo, span;  // this chunk's views [lo, lo + span)
+    int32_t dup, foreign;
+    int first;          // chunk 0 of its rank counts the foreign ids
+
+    __device__ __forceinline__ void add(int32_t x) {
+        if ((uint32_t)x - base >= nr) {
+            foreign += first;
+            return;
+        }
+        const uint32_t d = (uint32_t)x - lo;
+        if (d >= span) return;
+        const uint32_t bit = 1u << (d & 31);
+        if (atomicOr(&once[d >> 5], bit) & bit) {
+            atomicOr(&twice[d >> 5], bit);
+            dup += 1;
+        }
+    }
+};
+
+typedef int v4i_cov __attribute__((ext_vector_type(4)));
+
+// Feeds ids[a, b) to the chunk: a scalar head up to the first 16-byte aligned address,
+// two 16-byte loads per thread and iteration, a scalar tail.
+__device__ __forceinline__ void cov_scan(CovChunk& c, const int32_t* __restrict__ ids, int64_t a, int64_t b) {
+    if (b <= a) return;
+    int64_t a4 = a + ((4 - ((reinterpret_cast<uintptr_t>(ids + a) >> 2) & 3)) & 3);
+    if (a4 > b) a4 = b;
+    const int64_t b4 = a4 + ((b - a4) & ~(int64_t)3);
+    if (a + threadIdx.x < a4) c.add(ids[a + threadIdx.x]);
+    if (b4 + threadIdx.x < b) c.add(ids[b4 + threadIdx.x]);
+    const v4i_cov* v = reinterpret_cast<const v4i_cov*>(ids + a4);
+    const int32_t nv = (int32_t)((b4 - a4) >> 2);
+    for (int32_t q = threadIdx.x; q < nv; q += 2 * kCovBlock) {
+        const v4i_cov x = __builtin_nontemporal_load(v + q);
+        const bool two = q + kCovBlock < nv;
+        const v4i_cov y = __builtin_nontemporal_load(v + (two ? q + kCovBlock : q));
 #pragma unroll
-    for (int i = 0; i < kCovBlock / kWave; ++i) t += part[i];
-    __syncthreads();
-    return t;
+        for (int k = 0; k < 4; ++k) c.add(x[k]);
+        if (two) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) c.add(y[k]);
+        }
+    }
 }
 
 __global__ void __launch_bounds__(kCovBlock) coverage_lds_kernel(
@@ -847,66 +885,47 @@ __global__ void __launch_bounds__(kCovBlock) coverage_lds_kernel(
     DevStatus* st) {
     extern __shared__ uint32_t lds[];
     const int64_t words = C / 32;
-    uint32_t* once = lds;
-    uint32_t* twice = lds + words;
     const int64_t b = blockIdx.x;
     const int r = rank_of(chunk_first, W, b);
     const int64_t j = b - chunk_first[r];
     const int64_t base = off[r], end = off[r + 1];
     const int64_t lo = base + j * C;
     const int64_t hi = lo + C < end ? lo + C : end;
-    for (int64_t i = threadIdx.x; i < words; i += kCovBlock) {
-        once[i] = 0;
-        twice[i] = 0;
+    CovChunk c{lds, lds + words, (uint32_t)base, (uint32_t)(end - base), (uint32_t)lo, (uint32_t)(hi - lo), 0, 0,
+               j == 0 ? 1 : 0};
+    for (int64_t i = threadIdx.x; i < 2 * words; i += kCovBlock) lds[i] = 0;
+    __syncthreads();
+    cov_scan(c, emit, row_off[(int64_t)r * S], row_off[(int64_t)(r + 1) * S]);
+    cov_scan(c, left, loff[r], loff[r + 1]);
+    __syncthreads();
+    int32_t distinct = 0, multi = 0;
+    const int32_t nw = (int32_t)((hi - lo + 31) / 32);
+    for (int32_t i = threadIdx.x; i < nw; i += kCovBlock) {
+        distinct += __popc(c.once[i]);
+        multi += __popc(c.twice[i]);
+    }
+    // block sums of the four counters: per-wave partials in LDS, summed by wave 0
+    __shared__ int64_t part[kCovBlock / kWave][4];
+    const int64_t v0 = wave_sum((int64_t)distinct), v1 = wave_sum((int64_t)multi);
+    const int64_t v2 = wave_sum((int64_t)c.dup), v3 = wave_sum((int64_t)c.foreign);
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        int64_t* q = part[threadIdx.x / kWave];
+        q[0] = v0;
+        q[1] = v1;
+        q[2] = v2;
+        q[3] = v3;
     }
     __syncthreads();
-    int64_t dup = 0, foreign = 0;
-    const int32_t* lists[2] = {emit, left};
-    const int64_t from[2] = {row_off[(int64_t)r * S], loff[r]};
-    const int64_t to[2] = {row_off[(int64_t)(r + 1) * S], loff[r + 1]};
-#pragma unroll
-    for (int li = 0; li < 2; ++li) {
-        const int32_t* ids = lists[li];
-        for (int64_t i0 = from[li] + threadIdx.x; i0 < to[li]; i0 += (int64_t)kCovBlock * kCovUnroll) {
-            int32_t v[kCovUnroll];
-#pragma unroll
-            for (int u = 0; u < kCovUnroll; ++u) {
-                const int64_t i = i0 + (int64_t)u * kCovBlock;
-                v[u] = i < to[li] ? ids[i] : -1;
-            }
-#pragma unroll
-            for (int u = 0; u < kCovUnroll; ++u) {
-                const int64_t i = i0 + (int64_t)u * kCovBlock;
-                if (i >= to[li]) continue;
-                const int64_t x = v[u];
-                if (x < base || x >= end) {
-                    foreign += j == 0 ? 1 : 0;
-                    continue;
-                }
-                if (x < lo || x >= hi) continue;
-                const uint32_t bit = 1u << ((x - lo) & 31);
-                const int64_t wd = (x - lo) >> 5;
-                if (atomicOr(&once[wd], bit) & bit) {
-                    atomicOr(&twice[wd], bit);
-                    dup += 1;
-                }
-            }
-        }
-    }
-    __syncthreads();
-    int64_t distinct = 0, multi = 0;
-    const int64_t nw = (hi - lo + 31) / 32;
-    for (int64_t i = threadIdx.x; i < nw; i += kCovBlock) {
-        distinct += __popc(once[i]);
-        multi += __popc(twice[i]);
-    }
-    distinct = cov_block_sum(distinct);
-    multi = cov_block_sum(multi);
-    dup = cov_block_sum(dup);
-    foreign = cov_block_sum(foreign);
-    if (threadIdx.x == 0) {
-        const int64_t missing = (hi - lo) - distinct;
-        const int64_t bad = missing + multi;
+    if (threadIdx.x < kWave) {
+        const int i = threadIdx.x;
+        const bool has = i < kCovBlock / kWave;
+        const int64_t d_sum = wave_sum(has ? part[i][0] : (int64_t)0);
+        const int64_t m_sum = wave_sum(has ? part[i][1] : (int64_t)0);
+        const int64_t dup = wave_sum(has ? part[i][2] : (int64_t)0);
+        const int64_t foreign = wave_sum(has ? part[i][3] : (int64_t)0);
+        if (i != 0) return;
+        const int64_t missing = (hi - lo) - d_sum;
+        const int64_t bad = missing + m_sum;
         if (bad) atomicAdd((unsigned long long*)&info->bad_views, (unsigned long long)bad);
         if (want_ids && missing) atomicAdd((unsigned long long*)&info->missing_ids, (unsigned long long)missing);
         if (want_ids && dup) atomicAdd((unsigned long long*)&info->duplicate_ids, (unsigned long long)dup);

@@ -165,6 +165,10 @@ typedef struct odb_plan_info {
  *   slot_capacity     capacity of the slot arrays in slots; >= W * S is required
  *   d_emit_order      [n] out: emitted ids; slot k's rows are
  *                     d_emit_order[d_slot_row_off[k] .. d_slot_row_off[k+1])
+ *   d_row_token_start [n] out, or NULL (then d_row_len must be NULL too): row records,
+ *   d_row_len         [n] out   parallel to d_emit_order: d_token_offsets[s] and l_s of
+ *                     the row's sample s.  odb_collate reads them instead of gathering
+ *                     the CSR offsets of the emitted ids itself.
  *   d_slot_rows       [slot_capacity] out: rows of slot k (0 = IDLE)
  *   d_slot_maxlen     [slot_capacity] out: longest l in slot k (0 = IDLE)
  *   d_slot_row_off    [slot_capacity+1] out: exclusive prefix sum of rows
@@ -181,14 +185,19 @@ typedef struct odb_plan_info {
  *
  * Synchronises `stream` once per alignment round and once at the end.  Returns
  * ODB_E_CAPACITY (with h_info->required_slot_capacity) if slot_capacity < W * S,
- * ODB_E_INVALID_DATA if the stage-1 arrays are inconsistent, and ODB_E_COVERAGE if the
- * coverage self-check finds a view that is not emitted (or left over) exactly once.
+ * ODB_E_INVALID_DATA if the stage-1 arrays are inconsistent (an order that is not each
+ * rank's ids by (length desc, id asc), a group index that does not step by 0 or 1, a
+ * sorted length < 1 or different from the sample's CSR length; the last is checked
+ * once the plan is built, against every emitted and left-over sample), and
+ * ODB_E_COVERAGE if the coverage self-check finds a view that is not emitted (or left
+ * over) exactly once.
  */
 int odb_align_groups(const odb_window_t* w, int64_t budget, const odb_align_params_t* params,
                      const int32_t* d_order, const int32_t* d_sorted_len,
                      const int32_t* d_group_index, const int32_t* d_groups_per_rank,
                      int64_t slot_capacity,
-                     int32_t* d_emit_order, int32_t* d_slot_rows, int32_t* d_slot_maxlen,
+                     int32_t* d_emit_order, int64_t* d_row_token_start, int32_t* d_row_len,
+                     int32_t* d_slot_rows, int32_t* d_slot_maxlen,
                      int64_t* d_slot_row_off, int64_t* d_slot_tile_off, int64_t* d_slot_tokens,
                      double* d_slot_tokens_approx, int32_t* d_leftover, int64_t* d_leftover_off,
                      odb_plan_info_t* h_info, void* d_ws, size_t ws_bytes, void* stream);
@@ -206,15 +215,23 @@ int odb_align_groups(const odb_window_t* w, int64_t budget, const odb_align_para
  *   num_slots           W * S from odb_align_groups or odb_stream_plan (>= 0)
  *   plan arrays         as written by odb_align_groups or odb_stream_plan (device); the
  *                       emitted rows number at most n + W - 1 (sampler padding views)
+ *   d_row_token_start,  the plan's row records (token start and length of each emitted
+ *   d_row_len           row), or both NULL: then the rows' samples are read from
+ *                       d_emit_order and their CSR offsets gathered here (one more
+ *                       kernel, one random 16-byte read per row); with row records
+ *                       d_emit_order is not read and may be NULL
  *   out_capacity_elems  length of each output array; elements beyond it are not written
- *   d_ws / ws_bytes     the workspace (only a small status word is used)
+ *   d_ws / ws_bytes     the workspace: a status word, and the gathered row records when
+ *                       none are passed
  *
- * Asynchronous (launches two kernels).  Accesses are bounds-checked against the
- * window and the plan; an inconsistent plan sets a device status word that
- * odb_collate_status() reads.
+ * Asynchronous (one kernel with row records, two without).  Accesses are bounds-checked
+ * against the window and the plan: a row record outside the token stream or longer
+ * than its tile, or an emitted id outside [0, n), sets a device status word that
+ * odb_collate_status() reads (such a row is written as padding).
  */
 int odb_collate(const odb_window_t* w, int64_t num_slots,
-                const int32_t* d_emit_order, const int32_t* d_slot_rows,
+                const int32_t* d_emit_order, const int64_t* d_row_token_start,
+                const int32_t* d_row_len, const int32_t* d_slot_rows,
                 const int32_t* d_slot_maxlen, const int64_t* d_slot_row_off,
                 const int64_t* d_slot_tile_off, int32_t pad_id, int64_t out_capacity_elems,
                 int32_t* d_input_ids, int32_t* d_labels, int32_t* d_attention_mask,
@@ -380,6 +397,8 @@ size_t odb_stream_workspace_size(const odb_window_t* w, int32_t depth, int64_t s
  * from its shortest member), so odb_collate and odb_loss_weights take them unchanged:
  *   d_emit_order     [M] out: identities of the emitted views, slot order, row order
  *   d_emit_views     [M] out: the emitted views themselves
+ *   d_row_token_start, d_row_len  [M] out, or both NULL: row records of the emitted
+ *                    views (token start and length of their identities), as odb_align_groups
  *   slot arrays      as odb_align_groups, capacity slot_capacity (W * S needed)
  *   d_left_views     [M] out: un-emitted views, per rank in increasing view index
  *   d_left_off       [W+1] out
@@ -391,7 +410,8 @@ size_t odb_stream_workspace_size(const odb_window_t* w, int32_t depth, int64_t s
  */
 int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int64_t budget,
                     const odb_stream_params_t* params, int64_t slot_capacity,
-                    int32_t* d_emit_order, int32_t* d_emit_views, int32_t* d_slot_rows,
+                    int32_t* d_emit_order, int32_t* d_emit_views, int64_t* d_row_token_start,
+                    int32_t* d_row_len, int32_t* d_slot_rows,
                     int32_t* d_slot_maxlen, int64_t* d_slot_row_off, int64_t* d_slot_tile_off,
                     int64_t* d_slot_tokens, double* d_slot_tokens_approx, int32_t* d_left_views,
                     int64_t* d_left_off, odb_stream_round_t* h_trace, odb_stream_info_t* h_info,

@@ -182,9 +182,9 @@ def load():
         lib.odb_form_groups.argtypes = [W, I64, P, P, P, P, P, SZ, P]
         lib.odb_align_groups.restype = ctypes.c_int
         lib.odb_align_groups.argtypes = [W, I64, ctypes.POINTER(AlignParams), P, P, P, P, I64,
-                                         P, P, P, P, P, P, P, P, P, ctypes.POINTER(PlanInfo), P, SZ, P]
+                                         P, P, P, P, P, P, P, P, P, P, P, ctypes.POINTER(PlanInfo), P, SZ, P]
         lib.odb_collate.restype = ctypes.c_int
-        lib.odb_collate.argtypes = [W, I64, P, P, P, P, P, I32, I64, P, P, P, P, P, SZ, P]
+        lib.odb_collate.argtypes = [W, I64, P, P, P, P, P, P, P, I32, I64, P, P, P, P, P, SZ, P]
         lib.odb_collate_status.restype = ctypes.c_int
         lib.odb_collate_status.argtypes = [P, SZ, P]
         lib.odb_check_coverage.restype = ctypes.c_int
@@ -196,7 +196,7 @@ def load():
         lib.odb_stream_workspace_size.restype = SZ
         lib.odb_stream_workspace_size.argtypes = [W, I32, I64, I64]
         lib.odb_stream_plan.restype = ctypes.c_int
-        lib.odb_stream_plan.argtypes = [W, P, I64, ctypes.POINTER(StreamParams), I64, P, P, P, P, P, P, P, P, P, P,
+        lib.odb_stream_plan.argtypes = [W, P, I64, ctypes.POINTER(StreamParams), I64, P, P, P, P, P, P, P, P, P, P, P, P,
                                         P, ctypes.POINTER(StreamInfo), P, SZ, P]
         _lib = lib
     return _lib
@@ -266,7 +266,7 @@ def odb_form_groups(win, budget, order, sorted_len, group_index, groups_per_rank
 def odb_align_groups(win, budget, mode, quota, slot_capacity_per_rank, order, sorted_len, group_index,
                      groups_per_rank, slot_capacity, emit_order, slot_rows, slot_maxlen, slot_row_off,
                      slot_tile_off, slot_tokens, leftover, leftover_off, ws, stream=None, raise_on_capacity=True,
-                     slot_tokens_approx=None):
+                     slot_tokens_approx=None, row_token_start=None, row_len=None):
     cap = None
     if slot_capacity_per_rank is not None:
         cap = np.ascontiguousarray(slot_capacity_per_rank, dtype=np.int64)
@@ -274,7 +274,7 @@ def odb_align_groups(win, budget, mode, quota, slot_capacity_per_rank, order, so
     info = PlanInfo()
     st = load().odb_align_groups(win.ref, int(budget), ctypes.byref(params), _dptr(order), _dptr(sorted_len),
                                  _dptr(group_index), _dptr(groups_per_rank), int(slot_capacity), _dptr(emit_order),
-                                 _dptr(slot_rows), _dptr(slot_maxlen), _dptr(slot_row_off), _dptr(slot_tile_off),
+                                 _dptr(row_token_start), _dptr(row_len), _dptr(slot_rows), _dptr(slot_maxlen), _dptr(slot_row_off), _dptr(slot_tile_off),
                                  _dptr(slot_tokens), _dptr(slot_tokens_approx), _dptr(leftover), _dptr(leftover_off),
                                  ctypes.byref(info),
                                  _dptr(ws), ws.numel() * ws.element_size(), _stream(stream))
@@ -285,8 +285,10 @@ def odb_align_groups(win, budget, mode, quota, slot_capacity_per_rank, order, so
 
 
 def odb_collate(win, num_slots, emit_order, slot_rows, slot_maxlen, slot_row_off, slot_tile_off, pad_id,
-                out_capacity, input_ids, labels, attention_mask, position_ids, ws, stream=None):
-    _check(load().odb_collate(win.ref, int(num_slots), _dptr(emit_order), _dptr(slot_rows), _dptr(slot_maxlen),
+                out_capacity, input_ids, labels, attention_mask, position_ids, ws, stream=None, row_token_start=None,
+                row_len=None):
+    _check(load().odb_collate(win.ref, int(num_slots), _dptr(emit_order), _dptr(row_token_start), _dptr(row_len),
+                              _dptr(slot_rows), _dptr(slot_maxlen),
                               _dptr(slot_row_off), _dptr(slot_tile_off), int(pad_id), int(out_capacity),
                               _dptr(input_ids), _dptr(labels), _dptr(attention_mask), _dptr(position_ids),
                               _dptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
@@ -352,6 +354,8 @@ class Pipeline:
         self.group_index = torch.empty(n1, **i32)
         self.groups_per_rank = torch.empty(W, **i32)
         self.emit_order = torch.empty(n1, **i32)
+        self.row_token_start = torch.empty(n1, **i64)
+        self.row_len = torch.empty(n1, **i32)
         self.leftover = torch.empty(n1, **i32)
         self.leftover_off = torch.empty(W + 1, **i64)
         if slot_capacity is None:
@@ -380,10 +384,12 @@ class Pipeline:
                         self.group_index, self.groups_per_rank, self.slot_capacity, self.emit_order,
                         self.slot_rows, self.slot_maxlen, self.slot_row_off, self.slot_tile_off, self.slot_tokens,
                         self.leftover, self.leftover_off, self.ws, stream)
-        st, info = odb_align_groups(*args(), raise_on_capacity=False, slot_tokens_approx=self.slot_tokens_approx)
+        rec = dict(slot_tokens_approx=self.slot_tokens_approx, row_token_start=self.row_token_start,
+                   row_len=self.row_len)
+        st, info = odb_align_groups(*args(), raise_on_capacity=False, **rec)
         if st == ODB_E_CAPACITY:
             self._alloc_slots(int(info["required_slot_capacity"]))
-            st, info = odb_align_groups(*args(), slot_tokens_approx=self.slot_tokens_approx)
+            st, info = odb_align_groups(*args(), **rec)
         self.info = info
         return info
 
@@ -402,7 +408,8 @@ class Pipeline:
         P = int(self.info["padded_elems"])
         outs = self.alloc_outputs(P)
         odb_collate(self.win, self.num_slots, self.emit_order, self.slot_rows, self.slot_maxlen, self.slot_row_off,
-                    self.slot_tile_off, self.pad_id, P, *outs, self.ws, stream)
+                    self.slot_tile_off, self.pad_id, P, *outs, self.ws, stream, row_token_start=self.row_token_start,
+                    row_len=self.row_len)
         return tuple(o[:P] for o in outs)
 
     def loss_weights(self, mode: int = ODB_WEIGHT_TOKEN_EXACT, stream=None):
@@ -468,6 +475,8 @@ class StreamPipeline:
         m1 = max(self.M, 1)
         self.emit_order = torch.empty(m1, dtype=torch.int32, device=dev)
         self.emit_views = torch.empty(m1, dtype=torch.int32, device=dev)
+        self.row_token_start = torch.empty(m1, dtype=torch.int64, device=dev)
+        self.row_len = torch.empty(m1, dtype=torch.int32, device=dev)
         self.left_views = torch.empty(m1, dtype=torch.int32, device=dev)
         self.left_off = torch.empty(W + 1, dtype=torch.int64, device=dev)
         self._alloc_slots(max(int(slot_capacity if slot_capacity is not None else W * max(self.q, 1)), W))
@@ -495,7 +504,7 @@ class StreamPipeline:
         info = StreamInfo()
         st = load().odb_stream_plan(self.win.ref, _dptr(self.perm), self.budget, ctypes.byref(self.params),
                                     self.slot_capacity, _dptr(self.emit_order), _dptr(self.emit_views),
-                                    _dptr(self.slot_rows), _dptr(self.slot_maxlen), _dptr(self.slot_row_off),
+                                    _dptr(self.row_token_start), _dptr(self.row_len), _dptr(self.slot_rows), _dptr(self.slot_maxlen), _dptr(self.slot_row_off),
                                     _dptr(self.slot_tile_off), _dptr(self.slot_tokens),
                                     _dptr(self.slot_tokens_approx), _dptr(self.left_views), _dptr(self.left_off),
                                     ctypes.cast(self.trace, ctypes.c_void_p), ctypes.byref(info), _dptr(self.ws),
@@ -527,7 +536,8 @@ class StreamPipeline:
         if self.outputs is None or self.outputs[0].numel() < max(P, 1):
             self.outputs = tuple(torch.empty(max(P, 1), dtype=torch.int32, device=self.device) for _ in range(4))
         odb_collate(self.win, self.num_slots, self.emit_order, self.slot_rows, self.slot_maxlen, self.slot_row_off,
-                    self.slot_tile_off, self.pad_id, P, *self.outputs, self.ws, stream)
+                    self.slot_tile_off, self.pad_id, P, *self.outputs, self.ws, stream,
+                    row_token_start=self.row_token_start, row_len=self.row_len)
         return tuple(o[:P] for o in self.outputs)
 
     def loss_weights(self, mode: int = ODB_WEIGHT_TOKEN_EXACT, stream=None):

@@ -126,10 +126,13 @@ __global__ void __launch_bounds__(kBlock) round0_ranks_kernel(const int64_t* __r
 }
 
 // Checks that stage-1 arrays describe this window: order[p] is a sample of p's rank,
-// sorted_len[p] its length, the order strictly (length desc, id asc) and the group
-// indices run 0, 0|+1, ..., G_r - 1.  Records every group start.
+// sorted_len[p] >= 1, the order strictly (length desc, id asc) -- so each rank's segment
+// is a permutation of its ids -- and the group indices run 0, 0|+1, ..., G_r - 1.
+// Records every group start.  That sorted_len[p] is the CSR length of order[p] is
+// checked once the plan is built (row_check_kernel, leftover_kernel), where the CSR
+// offsets of every emitted sample are gathered anyway for the row records.
 __global__ void __launch_bounds__(kBlock) round0_check_kernel(
-    const int64_t* __restrict__ tok_off, const int64_t* __restrict__ off, const RankState* __restrict__ ranks,
+    const int64_t* __restrict__ off, const RankState* __restrict__ ranks,
     int W, int64_t n, const int32_t* __restrict__ order, const int32_t* __restrict__ slen,
     const int32_t* __restrict__ gidx, int32_t* __restrict__ gstart, DevStatus* st) {
     __shared__ int64_t s_off[kLdsRanks + 1];
@@ -142,8 +145,7 @@ __global__ void __launch_bounds__(kBlock) round0_check_kernel(
         const int64_t G = ranks[r].G;
         const int32_t id = order[p];
         const int32_t l = slen[p];
-        bool ok = id >= base && id < base + nr;
-        if (ok) ok = tok_off[id + 1] - tok_off[id] == (int64_t)l;
+        bool ok = id >= base && id < base + nr && l >= 1;
         const int32_t g = gidx[p];
         bool gok = g >= 0 && g < G;
         if (q == 0) {
@@ -520,7 +522,7 @@ __global__ void __launch_bounds__(kBlock) emit_kernel(
     int64_t n, const int32_t* __restrict__ cur_ids, const int32_t* __restrict__ cur_len,
     const int32_t* __restrict__ gidx, const int32_t* __restrict__ gstart, const int32_t* __restrict__ gsize,
     const int32_t* __restrict__ ov_slot, const int32_t* __restrict__ ov_lo, int32_t* __restrict__ dst,
-    int32_t* __restrict__ next_ids, int32_t* __restrict__ next_len) {
+    int32_t* __restrict__ dst_len, int32_t* __restrict__ next_ids, int32_t* __restrict__ next_len) {
     __shared__ int64_t s_off[kLdsRanks + 1];
     off = stage_ranks(off, W, s_off);
     const int64_t cut = rs->cut;
@@ -535,7 +537,9 @@ __global__ void __launch_bounds__(kBlock) emit_kernel(
         const int32_t id = cur_ids[p];
         if (R.action != kActOverflow) {
             if (q >= R.qcut) {
-                dst[base + R.ebase + (cnt - 1 - q)] = id;
+                const int64_t o = base + R.ebase + (cnt - 1 - q);
+                dst[o] = id;
+                dst_len[o] = cur_len[p];
             } else {
                 next_ids[base + q] = id;
                 next_len[base + q] = cur_len[p];
@@ -545,7 +549,9 @@ __global__ void __launch_bounds__(kBlock) emit_kernel(
             const int32_t sl = ov_slot[g];
             const int64_t st = (int64_t)gstart[g] - base;
             if (sl >= 0 && sl < cut) {
-                dst[base + R.ebase + ov_lo[g] + (st + gsize[g] - 1 - q)] = id;
+                const int64_t o = base + R.ebase + ov_lo[g] + (st + gsize[g] - 1 - q);
+                dst[o] = id;
+                dst_len[o] = cur_len[p];
             } else {
                 const int64_t o = ov_lo[g] + (q - st);
                 next_ids[base + o] = id;
@@ -606,17 +612,42 @@ struct Store64 {
 };
 
 __global__ void __launch_bounds__(kBlock) compact_emit_kernel(const int32_t* __restrict__ stage,
+                                                              const int32_t* __restrict__ stage_len,
                                                               const int64_t* __restrict__ off,
                                                               const RankState* __restrict__ ranks, int W, int64_t n,
                                                               const int64_t* __restrict__ row_off, int64_t S,
-                                                              int32_t* __restrict__ emit) {
+                                                              int32_t* __restrict__ emit, int32_t* __restrict__ len) {
     __shared__ int64_t s_off[kLdsRanks + 1];
     off = stage_ranks(off, W, s_off);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
         const int r = rank_of(off, W, p);
         const int64_t e = p - off[r];
-        if (e < ranks[r].emitted) emit[row_off[(int64_t)r * S] + e] = stage[p];
+        if (e < ranks[r].emitted) {
+            const int64_t o = row_off[(int64_t)r * S] + e;
+            emit[o] = stage[p];
+            len[o] = stage_len[p];
+        }
+    }
+}
+
+// Row records of the emitted rows: the CSR token start of each row's sample (written
+// when `ts` is not NULL) and the check that the length the plan carried for it (from
+// the stage-1 sorted lengths) is the sample's CSR length.  Ids are in range here:
+// round0_check_kernel verified that every rank's order is a permutation of its ids.
+__global__ void __launch_bounds__(kBlock) row_check_kernel(const int64_t* __restrict__ tok_off,
+                                                           const int32_t* __restrict__ emit,
+                                                           const int32_t* __restrict__ len, int64_t rows,
+                                                           int64_t* __restrict__ ts, DevStatus* st) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < rows; k += stride) {
+        const int32_t s = emit[k];
+        const int64_t a = tok_off[s];
+        if (tok_off[s + 1] - a != (int64_t)len[k]) {
+            atomicOr(&st->err, kErrSortedLen);
+            atomicMin((unsigned long long*)&st->first_bad, (unsigned long long)s);
+        }
+        if (ts) ts[k] = a;
     }
 }
 
@@ -639,18 +670,28 @@ __global__ void __launch_bounds__(kBlock) leftover_off_kernel(const RankState* _
     if (threadIdx.x == 0) loff[W] = carry;
 }
 
+// Left-over ids, and the length check of row_check_kernel for them.
 __global__ void __launch_bounds__(kBlock) leftover_kernel(const int32_t* __restrict__ cur_ids,
+                                                          const int32_t* __restrict__ cur_len,
+                                                          const int64_t* __restrict__ tok_off,
                                                           const int64_t* __restrict__ off,
                                                           const RankState* __restrict__ ranks, int W, int64_t n,
                                                           const int64_t* __restrict__ loff,
-                                                          int32_t* __restrict__ left) {
+                                                          int32_t* __restrict__ left, DevStatus* st) {
     __shared__ int64_t s_off[kLdsRanks + 1];
     off = stage_ranks(off, W, s_off);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
         const int r = rank_of(off, W, p);
         const int64_t q = p - off[r];
-        if (q < ranks[r].cnt) left[loff[r] + q] = cur_ids[p];
+        if (q < ranks[r].cnt) {
+            const int32_t s = cur_ids[p];
+            left[loff[r] + q] = s;
+            if (tok_off[s + 1] - tok_off[s] != (int64_t)cur_len[p]) {
+                atomicOr(&st->err, kErrSortedLen);
+                atomicMin((unsigned long long*)&st->first_bad, (unsigned long long)s);
+            }
+        }
     }
 }
 
@@ -1039,7 +1080,7 @@ using namespace odb;
 extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb_align_params_t* params,
                                 const int32_t* d_order, const int32_t* d_sorted_len, const int32_t* d_group_index,
                                 const int32_t* d_groups_per_rank, int64_t slot_capacity, int32_t* d_emit_order,
-                                int32_t* d_slot_rows, int32_t* d_slot_maxlen, int64_t* d_slot_row_off,
+                                int64_t* d_row_token_start, int32_t* d_row_len, int32_t* d_slot_rows, int32_t* d_slot_maxlen, int64_t* d_slot_row_off,
                                 int64_t* d_slot_tile_off, int64_t* d_slot_tokens, double* d_slot_tokens_approx,
                                 int32_t* d_leftover, int64_t* d_leftover_off, odb_plan_info_t* h_info, void* d_ws,
                                 size_t ws_bytes, void* stream) {
@@ -1054,6 +1095,8 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     if (nonjoin && params->quota < 1) return set_error(ODB_E_INVALID_ARG, "quota must be >= 1 in non-join mode");
     if (!h_info) return set_error(ODB_E_INVALID_ARG, "h_info is NULL");
     if (slot_capacity < 0) return set_error(ODB_E_INVALID_ARG, "slot_capacity must be >= 0");
+    if ((d_row_token_start == nullptr) != (d_row_len == nullptr))
+        return set_error(ODB_E_INVALID_ARG, "d_row_token_start and d_row_len are given together or not at all");
     const int W = w->num_ranks;
     const int64_t n = w->num_samples;
     if (n > 0 && (!d_order || !d_sorted_len || !d_group_index || !d_emit_order || !d_leftover))
@@ -1092,6 +1135,10 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     int32_t* blen[2] = {ws_at<int32_t>(d_ws, L.buf_len0), ws_at<int32_t>(d_ws, L.buf_len1)};
     int32_t* wgidx = ws_at<int32_t>(d_ws, L.gidx);
     int32_t* dst = nonjoin ? ws_at<int32_t>(d_ws, L.stage) : d_emit_order;
+    // the length each emitted row carries (from the stage-1 sorted lengths): the row
+    // records' lengths, checked against the CSR offsets once the plan is built
+    int32_t* row_len = d_row_len ? d_row_len : ws_at<int32_t>(d_ws, L.row_len);
+    int32_t* dst_len = nonjoin ? ws_at<int32_t>(d_ws, L.stage_len) : row_len;
     const int64_t gcap = (int64_t)num_cus() * 16;
     const unsigned gridn = grid_for(n, kBlock, gcap);
 
@@ -1101,8 +1148,8 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
                        d_gbase, st);
     ODB_LAUNCHED();
     if (n > 0) {
-        hipLaunchKernelGGL(round0_check_kernel, dim3(gridn), dim3(kBlock), 0, s, w->d_token_offsets, d_off,
-                           (const RankState*)d_ranks, W, n, d_order, d_sorted_len, d_group_index, gstart, st);
+        hipLaunchKernelGGL(round0_check_kernel, dim3(gridn), dim3(kBlock), 0, s, d_off, (const RankState*)d_ranks, W,
+                           n, d_order, d_sorted_len, d_group_index, gstart, st);
         ODB_LAUNCHED();
     }
     {
@@ -1173,8 +1220,8 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
         ODB_LAUNCHED();
         hipLaunchKernelGGL(emit_kernel, dim3(gridn), dim3(kBlock), 0, s, (const RankState*)d_ranks,
                            (const RoundState*)d_rs, d_off, W, n, cur.ids, cur.len, cur.gidx, (const int32_t*)gstart,
-                           (const int32_t*)gsize, (const int32_t*)ov_slot, (const int32_t*)ov_lo, dst, bids[flip],
-                           blen[flip]);
+                           (const int32_t*)gsize, (const int32_t*)ov_slot, (const int32_t*)ov_lo, dst, dst_len,
+                           bids[flip], blen[flip]);
         ODB_LAUNCHED();
         hipLaunchKernelGGL(advance_kernel, dim3(grid_for(W, kBlock)), dim3(kBlock), 0, s, d_ranks, W);
         ODB_LAUNCHED();
@@ -1220,8 +1267,16 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     ODB_TRY((device_excl_scan<int64_t>(TileLoad{d_slot_rows, d_slot_maxlen, K}, Store64{d_slot_tile_off}, K + 1,
                                        ws_at<int64_t>(d_ws, L.partials), s)));
     if (nonjoin && n > 0) {
-        hipLaunchKernelGGL(compact_emit_kernel, dim3(gridn), dim3(kBlock), 0, s, (const int32_t*)dst, d_off,
-                           (const RankState*)d_ranks, W, n, (const int64_t*)d_slot_row_off, S, d_emit_order);
+        hipLaunchKernelGGL(compact_emit_kernel, dim3(gridn), dim3(kBlock), 0, s, (const int32_t*)dst,
+                           (const int32_t*)dst_len, d_off, (const RankState*)d_ranks, W, n,
+                           (const int64_t*)d_slot_row_off, S, d_emit_order, row_len);
+        ODB_LAUNCHED();
+    }
+    const int64_t nemit = hrs.emitted_total;
+    if (nemit > 0) {
+        hipLaunchKernelGGL(row_check_kernel, dim3(grid_for(nemit, kBlock, gcap)), dim3(kBlock), 0, s,
+                           w->d_token_offsets, (const int32_t*)d_emit_order, (const int32_t*)row_len, nemit,
+                           d_row_token_start, st);
         ODB_LAUNCHED();
     }
     hipLaunchKernelGGL(leftover_off_kernel, dim3(1), dim3(kBlock), 0, s, (const RankState*)d_ranks, W,
@@ -1230,8 +1285,8 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     int64_t nleft = 0;
     for (int r = 0; r < W; ++r) nleft += cnt[r];
     if (nleft > 0) {
-        hipLaunchKernelGGL(leftover_kernel, dim3(gridn), dim3(kBlock), 0, s, cur.ids, d_off,
-                           (const RankState*)d_ranks, W, n, (const int64_t*)d_leftover_off, d_leftover);
+        hipLaunchKernelGGL(leftover_kernel, dim3(gridn), dim3(kBlock), 0, s, cur.ids, cur.len, w->d_token_offsets,
+                           d_off, (const RankState*)d_ranks, W, n, (const int64_t*)d_leftover_off, d_leftover, st);
         ODB_LAUNCHED();
     }
     // stats (Sec. 2.1 / App. I padding fraction) and coverage (App. C)
@@ -1243,7 +1298,6 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     hipLaunchKernelGGL(finish_info_kernel, dim3(1), dim3(64), 0, s, (const int64_t*)d_slot_row_off,
                        (const int64_t*)d_slot_tile_off, K, d_info);
     ODB_LAUNCHED();
-    const int64_t nemit = hrs.emitted_total;
     ODB_TRY(run_plan_coverage(w, L, d_ws, d_emit_order, d_slot_row_off, S, d_leftover, d_leftover_off, nemit, nleft,
                               s));
 
@@ -1260,6 +1314,10 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     h_info->duplicate_ids = hi.duplicate_ids;
     h_info->bad_views = hi.bad_views;
     h_info->pad_fraction = hi.pad_fraction;
+    if (hs.err & kErrSortedLen)
+        return set_error(ODB_E_INVALID_DATA,
+                         "stage-1 arrays do not describe this window (sorted length of sample %lld is not its CSR "
+                         "length)", (long long)hs.first_bad);
     if (hs.err & kErrIdentity)
         return set_error(ODB_E_INVALID_DATA, "identity map holds a value outside [0, num_identities)");
     if ((hs.err & kErrInternal) || hi.emitted != nemit)

@@ -1,9 +1,10 @@
 // Stage 4 of the ODB window pipeline: padded collation (Sec. 2.1, Fig. 1 -- every
 // aligned group is padded to its own longest sample).
 //
-// Two launches:
+// One or two launches:
 //   row_info_kernel  token start and length of every emitted row (one gather of the CSR
-//                    offsets per row), so the hot loop never chases emit -> offsets.
+//                    offsets per row), so the hot loop never chases emit -> offsets; not
+//                    launched when the plan brings these row records itself.
 //   collate_kernel   stationary on the flat output: the four outputs share one element
 //                    index space [0, padded_elems).  The output is cut into steps of
 //                    kBlockStep elements; runs of kRunSteps consecutive steps are dealt
@@ -97,7 +98,8 @@ struct Plan {
     const int64_t* __restrict__ tok_off;
     int64_t num_slots;
     int64_t n;           // samples of the window
-    int64_t max_rows;    // capacity of the row records: n + W - 1 (sampler padding views)
+    int64_t max_rows;    // rows addressable: the plan's row count, at most n + W - 1 (sampler
+                         // padding views); set in the kernel
     int64_t tok_end;     // tokens [0, tok_end) are addressable (tok_off[n], set in the kernel)
     int32_t* err;
 };
@@ -180,14 +182,16 @@ __device__ __forceinline__ void advance(Cursor& c, int64_t e, int64_t delta, con
     }
 }
 
-// Row record of the cursor's row (a bad plan yields an empty row and sets the error word).
+// Row record of the cursor's row.  A row index outside the tile, or a record that is not
+// a token range inside the stream no longer than the tile, is a bad plan: the row is
+// treated as empty and the error word is set.
 __device__ __forceinline__ RowRec load_row(const Cursor& c, const Plan& p) {
     const bool ok = c.ri >= 0 && c.ri < c.ri_end && c.ri < p.max_rows;
     const int32_t i = ok ? c.ri : 0;
     RowRec r;
     r.ts = p.row_ts[i];
     r.l = p.row_len[i];
-    if (!ok) {
+    if (!ok || r.ts < 0 || r.l < 0 || r.l > c.ml || r.ts > p.tok_end - r.l) {
         atomicOr(p.err, 1);
         r.ts = 0;
         r.l = 0;
@@ -252,7 +256,7 @@ __device__ __forceinline__ void stage_values(const Stage& a, int64_t e, int64_t 
             const int32_t ri1 = __builtin_amdgcn_readlane(c.ri, l) + 1;
             const int64_t ts = *(cptr64)(p.row_ts + ri1);
             const int32_t len = *(cptr32)(p.row_len + ri1);
-            const bool fits = ts + kVec <= p.tok_end;
+            const bool fits = ts >= 0 && ts + kVec <= p.tok_end;
             const v4i h = *(cptrv4)(p.tokens + (fits ? ts : 0));
             if (lane == l) {
                 bl = len;
@@ -321,6 +325,10 @@ __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t 
                                                                 int32_t* __restrict__ o_msk,
                                                                 int32_t* __restrict__ o_pos) {
     p.tok_end = p.tok_off[p.n];
+    {
+        const int64_t rows = p.row_off[p.num_slots];
+        p.max_rows = rows < 0 ? 0 : (rows < p.max_rows ? rows : p.max_rows);
+    }
     const int vec_ok = p.tok_end >= kVec;
     const int64_t total_plan = p.tile_off[p.num_slots];
     const int64_t total = total_plan < capacity ? total_plan : capacity;
@@ -406,7 +414,8 @@ __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t 
 using namespace odb;
 
 extern "C" int odb_collate(const odb_window_t* w, int64_t num_slots, const int32_t* d_emit_order,
-                           const int32_t* d_slot_rows, const int32_t* d_slot_maxlen, const int64_t* d_slot_row_off,
+                           const int64_t* d_row_token_start, const int32_t* d_row_len, const int32_t* d_slot_rows,
+                           const int32_t* d_slot_maxlen, const int64_t* d_slot_row_off,
                            const int64_t* d_slot_tile_off, int32_t pad_id, int64_t out_capacity_elems,
                            int32_t* d_input_ids, int32_t* d_labels, int32_t* d_attention_mask,
                            int32_t* d_position_ids, void* d_ws, size_t ws_bytes, void* stream) {
@@ -415,6 +424,8 @@ extern "C" int odb_collate(const odb_window_t* w, int64_t num_slots, const int32
     if (num_slots < 0 || num_slots >= 0x7FFFFFFFll)
         return set_error(ODB_E_INVALID_ARG, "num_slots must be in [0, 2^31 - 1)");
     if (out_capacity_elems < 0) return set_error(ODB_E_INVALID_ARG, "out_capacity_elems must be >= 0");
+    if ((d_row_token_start == nullptr) != (d_row_len == nullptr))
+        return set_error(ODB_E_INVALID_ARG, "d_row_token_start and d_row_len are given together or not at all");
     if (num_slots == 0 || out_capacity_elems == 0) return ODB_OK;
     if (!d_slot_rows || !d_slot_maxlen || !d_slot_row_off || !d_slot_tile_off)
         return set_error(ODB_E_INVALID_ARG, "plan arrays must not be NULL");
@@ -426,18 +437,24 @@ extern "C" int odb_collate(const odb_window_t* w, int64_t num_slots, const int32
         return set_error(ODB_E_INVALID_ARG, "output arrays must be 16-byte aligned");
     const int64_t n = w->num_samples;
     if (n == 0) return ODB_OK;  // no rows: every tile is empty
-    if (!d_emit_order) return set_error(ODB_E_INVALID_ARG, "d_emit_order is NULL");
+    const bool have_rows = d_row_token_start != nullptr;
+    if (!have_rows && !d_emit_order) return set_error(ODB_E_INVALID_ARG, "d_emit_order is NULL");
     hipStream_t s = static_cast<hipStream_t>(stream);
     // a plan may list a sample more than once only through sampler padding: at most
     // W - 1 extra rows (streaming plans)
     const int64_t max_rows = n + w->num_ranks - 1;
     int32_t* err = &ws_at<DevStatus>(d_ws, L.status)->collate_err;
-    int64_t* row_ts = ws_at<int64_t>(d_ws, L.row_ts);
-    int32_t* row_len = ws_at<int32_t>(d_ws, L.row_len);
-    hipLaunchKernelGGL(row_info_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock), 0, s,
-                       w->d_token_offsets, n, max_rows, d_emit_order, d_slot_row_off, num_slots, row_ts, row_len,
-                       err);
-    ODB_LAUNCHED();
+    const int64_t* row_ts = d_row_token_start;
+    const int32_t* row_len = d_row_len;
+    if (!have_rows) {
+        int64_t* ts = ws_at<int64_t>(d_ws, L.row_ts);
+        int32_t* len = ws_at<int32_t>(d_ws, L.row_len);
+        hipLaunchKernelGGL(row_info_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock), 0, s,
+                           w->d_token_offsets, n, max_rows, d_emit_order, d_slot_row_off, num_slots, ts, len, err);
+        ODB_LAUNCHED();
+        row_ts = ts;
+        row_len = len;
+    }
     Plan p{d_slot_tile_off, d_slot_maxlen, d_slot_rows, d_slot_row_off, row_ts, row_len, w->d_tokens,
            w->d_token_offsets, num_slots, n, max_rows, 0, err};
     // kCollateBlocksPerCU blocks per compute unit, all resident at once; runs are dealt

@@ -107,6 +107,7 @@ bool make_layout(const odb_window_t* w, Layout* L) {
     L->buf_len1 = take(4 * n1);
     L->gidx = take(4 * n1);
     L->stage = take(4 * n1);
+    L->stage_len = take(4 * n1);
     L->cover = take(4 * ((nid > n ? nid : n) + 1));
     L->row_ts = take(8 * (n1 + W));
     L->row_len = take(4 * (n1 + W));

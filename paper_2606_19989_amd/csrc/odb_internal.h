@@ -47,7 +47,8 @@ enum : int32_t {
     kErrGroupIndex = 8,  // stage-1 group indices inconsistent
     kErrIdentity = 16,   // identity outside [0, num_identities)
     kErrCollate = 32,    // collate met an inconsistent plan
-    kErrInternal = 64
+    kErrInternal = 64,
+    kErrSortedLen = 128  // a stage-1 sorted length differs from the sample's CSR length
 };
 
 struct DevStatus {
@@ -111,7 +112,7 @@ struct Layout {
     size_t jmp0, jmp1, marks, incl;
     size_t gstart, gsize, gmax, sadj, cs, ov_slot, ov_lo, kept;
     size_t srows, smax, stok, steps;
-    size_t buf_ids0, buf_ids1, buf_len0, buf_len1, gidx, stage, cover, row_ts, row_len;
+    size_t buf_ids0, buf_ids1, buf_len0, buf_len1, gidx, stage, stage_len, cover, row_ts, row_len;
     size_t info, sketch;
     size_t total;
     int64_t num_sort_blocks;

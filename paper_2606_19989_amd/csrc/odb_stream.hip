@@ -652,10 +652,12 @@ __global__ void stream_slots_kernel(StreamArgs a, int64_t S, int32_t* rows, int3
     }
 }
 
-// Rank r's emitted views (slot order, row order) and their identities; blockIdx.x is
-// the rank, blockIdx.y a slice of its stream.
+// Rank r's emitted views (slot order, row order), their identities and, when asked for,
+// the row records (token start and length of each identity); blockIdx.x is the rank,
+// blockIdx.y a slice of its stream.
 __global__ void __launch_bounds__(256) stream_emit_out_kernel(StreamArgs a, int64_t S, const int64_t* row_off,
                                                               int32_t* emit_views, int32_t* emit_order,
+                                                              int64_t* row_ts, int32_t* row_len,
                                                               int32_t* vcount, int32_t* icount) {
     const int r = blockIdx.x;
     const int64_t lo = row_off[(int64_t)r * S], hi = row_off[(int64_t)(r + 1) * S];
@@ -666,6 +668,11 @@ __global__ void __launch_bounds__(256) stream_emit_out_kernel(StreamArgs a, int6
         const int32_t id = view_identity(a, m);
         emit_views[lo + i] = m;
         emit_order[lo + i] = id;
+        if (row_ts) {
+            const int64_t t0 = a.tok_off[id];
+            row_ts[lo + i] = t0;
+            row_len[lo + i] = (int32_t)(a.tok_off[id + 1] - t0);
+        }
         atomicAdd(&vcount[m], 1);
         atomicAdd(&icount[id], 1);
     }
@@ -846,7 +853,8 @@ extern "C" size_t odb_stream_workspace_size(const odb_window_t* w, int32_t depth
 
 extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int64_t budget,
                                const odb_stream_params_t* params, int64_t slot_capacity, int32_t* d_emit_order,
-                               int32_t* d_emit_views, int32_t* d_slot_rows, int32_t* d_slot_maxlen,
+                               int32_t* d_emit_views, int64_t* d_row_token_start, int32_t* d_row_len,
+                               int32_t* d_slot_rows, int32_t* d_slot_maxlen,
                                int64_t* d_slot_row_off, int64_t* d_slot_tile_off, int64_t* d_slot_tokens,
                                double* d_slot_tokens_approx, int32_t* d_left_views, int64_t* d_left_off,
                                odb_stream_round_t* h_trace, odb_stream_info_t* h_info, void* d_ws, size_t ws_bytes,
@@ -856,6 +864,8 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     if (budget < 1) return set_error(ODB_E_INVALID_ARG, "budget must be >= 1");
     ODB_TRY(check_stream_params(w, params, slot_capacity));
     if (!h_info) return set_error(ODB_E_INVALID_ARG, "h_info is NULL");
+    if ((d_row_token_start == nullptr) != (d_row_len == nullptr))
+        return set_error(ODB_E_INVALID_ARG, "d_row_token_start and d_row_len are given together or not at all");
     const int W = w->num_ranks;
     const int64_t N = w->num_samples;
     const int64_t q = N > 0 ? (N + W - 1) / W : 0;
@@ -982,7 +992,7 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     ODB_LAUNCHED();
     if (K > 0) {
         hipLaunchKernelGGL(stream_emit_out_kernel, dim3(W, 64), dim3(256), 0, s, a, S, (const int64_t*)d_slot_row_off,
-                           d_emit_views, d_emit_order, vcount, icount);
+                           d_emit_views, d_emit_order, d_row_token_start, d_row_len, vcount, icount);
         ODB_LAUNCHED();
     }
     hipLaunchKernelGGL(fill_i64s_kernel, dim3(1), dim3(256), 0, s, d_left_off, (int64_t)W + 1);

@@ -62,8 +62,18 @@ def compare_plan(w, pipe, ref):
     assert np.array_equal(h(pipe.slot_tile_off, K + 1), ref.slot_tile_off), "slot_tile_off"
     E, Lf = ref.info["emitted_samples"], ref.info["leftover_samples"]
     assert np.array_equal(h(pipe.emit_order, E), ref.emit_order), "emit_order"
+    compare_row_records(w.tok_off, pipe, ref.emit_order)
     assert np.array_equal(h(pipe.leftover, Lf), ref.leftover), "leftover"
     assert np.array_equal(h(pipe.leftover_off), ref.leftover_off), "leftover_off"
+
+
+def compare_row_records(tok_off, pipe, emit_order):
+    """Row records of the plan: token start and length of each emitted row's sample,
+    read off the CSR offsets at the oracle's emitted ids."""
+    E = len(emit_order)
+    ids = np.asarray(emit_order, dtype=np.int64)
+    assert np.array_equal(h(pipe.row_token_start, E), tok_off[ids]), "row_token_start"
+    assert np.array_equal(h(pipe.row_len, E), (tok_off[ids + 1] - tok_off[ids]).astype(np.int32)), "row_len"
 
 
 def compare_loss_weights(pipe, ref):

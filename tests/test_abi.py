@@ -78,13 +78,25 @@ def test_bad_arguments_rejected_on_host():
     info = odb.PlanInfo()
     for mode, quota, cap in [(1, 0, None), (7, 1, None), (0, 0, np.array([-1], dtype=np.int64))]:
         p = odb.AlignParams(mode, 0, quota, None if cap is None else cap.ctypes.data_as(ctypes.c_void_p).value)
-        st = lib.odb_align_groups(ctypes.byref(w), 10, ctypes.byref(p), 1, 1, 1, 1, 16, 1, 1, 1, 1, 1, 1, None,
-                                  1, 1, ctypes.byref(info), fake_ws, size, None)
+        st = lib.odb_align_groups(ctypes.byref(w), 10, ctypes.byref(p), 1, 1, 1, 1, 16, 1, None, None, 1, 1, 1, 1,
+                                  1, None, 1, 1, ctypes.byref(info), fake_ws, size, None)
         assert st == odb.ODB_E_INVALID_ARG, (mode, quota, cap)
+    # row records come as a pair or not at all
+    p = odb.AlignParams(0, 0, 0, None)
+    for ts, ln in [(1, None), (None, 1)]:
+        st = lib.odb_align_groups(ctypes.byref(w), 10, ctypes.byref(p), 1, 1, 1, 1, 16, 1, ts, ln, 1, 1, 1, 1,
+                                  1, None, 1, 1, ctypes.byref(info), fake_ws, size, None)
+        assert st == odb.ODB_E_INVALID_ARG
+        st = lib.odb_collate(ctypes.byref(w), 3, 1, ts, ln, 1, 1, 1, 1, 0, 10, 1, 1, 1, 1, fake_ws, size, None)
+        assert st == odb.ODB_E_INVALID_ARG
     # collate with negative sizes
-    st = lib.odb_collate(ctypes.byref(w), -1, 1, 1, 1, 1, 1, 0, 10, 1, 1, 1, 1, fake_ws, size, None)
+    st = lib.odb_collate(ctypes.byref(w), -1, 1, None, None, 1, 1, 1, 1, 0, 10, 1, 1, 1, 1, fake_ws, size, None)
     assert st == odb.ODB_E_INVALID_ARG
-    st = lib.odb_collate(ctypes.byref(w), 3, 1, 1, 1, 1, 1, 0, -5, 1, 1, 1, 1, fake_ws, size, None)
+    st = lib.odb_collate(ctypes.byref(w), 3, 1, None, None, 1, 1, 1, 1, 0, -5, 1, 1, 1, 1, fake_ws, size, None)
+    assert st == odb.ODB_E_INVALID_ARG
+    # collate without row records needs the emitted ids
+    st = lib.odb_collate(ctypes.byref(w), 3, None, None, None, 1, 1, 1, 1, 0, 10, 16, 16, 16, 16, fake_ws, size,
+                         None)
     assert st == odb.ODB_E_INVALID_ARG
 
 
@@ -130,9 +142,9 @@ def test_stream_arguments_checked_on_host():
     bad_rate = np.array([4, 0], dtype=np.int32)
     info = odb.StreamInfo()
 
-    def call(params, budget=10, cap=16):
-        return lib.odb_stream_plan(ctypes.byref(w), 1, budget, params, cap, 1, 1, 1, 1, 1, 1, 1, None, 1, 1, None,
-                                   ctypes.byref(info), fake_ws, 1 << 40, None)
+    def call(params, budget=10, cap=16, ts=None, ln=None):
+        return lib.odb_stream_plan(ctypes.byref(w), 1, budget, params, cap, 1, 1, ts, ln, 1, 1, 1, 1, 1, None, 1, 1,
+                                   None, ctypes.byref(info), fake_ws, 1 << 40, None)
 
     ptr = lambda a: a.ctypes.data_as(ctypes.c_void_p).value
     good = dict(mode=0, buffer_size=4, depth=8, reserved0=0, quota=0, rate=ptr(rate), slot_capacity=None, max_rounds=9)
@@ -145,6 +157,8 @@ def test_stream_arguments_checked_on_host():
     p = odb.StreamParams(**good)
     assert call(ctypes.byref(p), budget=0) == odb.ODB_E_INVALID_ARG
     assert call(ctypes.byref(p), cap=-1) == odb.ODB_E_INVALID_ARG
+    assert call(ctypes.byref(p), ts=1) == odb.ODB_E_INVALID_ARG
+    assert call(ctypes.byref(p), ln=1) == odb.ODB_E_INVALID_ARG
 
 
 def test_binding_raises_without_library(monkeypatch, tmp_path):

@@ -226,3 +226,88 @@ def test_length_sketch_whole_window_and_edge_cases():
     with pytest.raises(odb.OdbError) as e:
         odb.odb_length_sketch(win, bad, 2, w.budget, ws)
     assert e.value.status == odb.ODB_E_INVALID_DATA
+
+
+def test_collate_from_emit_order():
+    # odb_collate without row records gathers them from the emitted ids itself; both
+    # routes give the oracle's outputs
+    import torch
+    import paper_2606_19989_amd as odb
+
+    for w in (synth.WORKLOADS["ln512_w2x2048"].window(), adversarial_windows()[4], adversarial_windows()[16]):
+        log(f"collate from emit order: {w.name}")
+        ref = oracle.plan_window(w)
+        pipe, outs = run_gpu(w, pad_id=3)
+        P = int(pipe.info["padded_elems"])
+        alt = tuple(torch.empty(max(P, 1), dtype=torch.int32, device="cuda") for _ in range(4))
+        odb.odb_collate(pipe.win, pipe.num_slots, pipe.emit_order, pipe.slot_rows, pipe.slot_maxlen,
+                        pipe.slot_row_off, pipe.slot_tile_off, 3, P, *alt, pipe.ws)
+        torch.cuda.synchronize()
+        odb.odb_collate_status(pipe.ws)
+        compare_collate_full(w, tuple(a[:P] for a in alt), ref, 3)
+        for a, b in zip(alt, outs):
+            assert torch.equal(a[:P], b)
+
+
+def _formed(w):
+    import torch
+    import paper_2606_19989_amd as odb
+
+    tok_off, toks, ident = synth.device_tensors(w, "cuda")
+    win_ = odb.DeviceWindow(w.rank_off, tok_off, toks, ident, w.num_identities)
+    pipe = odb.Pipeline(win_, w.budget, mode=w.mode, quota=w.quota, capacity=w.capacity)
+    pipe.form()
+    torch.cuda.synchronize()
+    return pipe
+
+
+@pytest.mark.parametrize("mode", ["join", "nonjoin"])
+def test_align_rejects_a_wrong_sorted_length(mode):
+    # a stage-1 sorted length that keeps the order valid but is not the sample's CSR
+    # length is found once the plan is built (emitted rows, or leftovers in non-join)
+    import paper_2606_19989_amd as odb
+
+    rng = np.random.default_rng(31)
+    w = win([rng.integers(10, 3000, 5000), rng.integers(10, 3000, 3000)], 8192, mode=mode,
+            quota=2000 if mode == "nonjoin" else 0)
+    pipe = _formed(w)
+    ref = oracle.plan_window(w)
+    slen = pipe.sorted_len.cpu().numpy()
+    # a position strictly inside a run of descending lengths: lowering its length by one
+    # keeps (length desc, id asc).  Non-join emits the shortest samples first, so a long
+    # one (an early position) is left over and checked on that path
+    cand = [p for p in range(1, 4999) if slen[p - 1] > slen[p] > slen[p + 1] + 1]
+    p = cand[len(cand) // 2] if mode == "join" else cand[0]
+    order = pipe.order.cpu().numpy()
+    if mode == "nonjoin":
+        assert order[p] in set(ref.leftover.tolist())
+    bad = pipe.sorted_len.clone()
+    bad[p] -= 1
+    pipe.sorted_len.copy_(bad)
+    log(f"wrong sorted length at position {p} ({mode}); the oracle leaves {ref.info['leftover_samples']} over")
+    with pytest.raises(odb.OdbError) as e:
+        pipe.align()
+    assert e.value.status == odb.ODB_E_INVALID_DATA
+    assert "sorted length" in str(e.value)
+
+
+def test_collate_flags_a_bad_row_record():
+    # a row record outside the token stream is written as padding and reported
+    import torch
+    import paper_2606_19989_amd as odb
+
+    w = synth.WORKLOADS["ln512_w2x2048"].window()
+    pipe, outs = run_gpu(w)
+    P = int(pipe.info["padded_elems"])
+    pipe.row_token_start[5] = int(w.tok_off[-1])   # starts at the end of the stream
+    pipe.collate()
+    torch.cuda.synchronize()
+    with pytest.raises(odb.OdbError) as e:
+        odb.odb_collate_status(pipe.ws)
+    assert e.value.status == odb.ODB_E_INVALID_DATA
+    pipe.row_token_start[5] = int(w.tok_off[int(pipe.emit_order[5])])
+    pipe.collate()
+    torch.cuda.synchronize()
+    odb.odb_collate_status(pipe.ws)
+    ref = oracle.plan_window(w)
+    compare_collate_full(w, tuple(o[:P] for o in pipe.outputs), ref)

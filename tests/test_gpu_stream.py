@@ -6,7 +6,7 @@ import pytest
 
 import oracle
 import synth
-from _parity import log
+from _parity import compare_row_records, log
 
 pytestmark = pytest.mark.gpu
 
@@ -56,6 +56,7 @@ def run_case(name, lens, perm, W, budget, buffer_size, depth, rate, mode="join",
     assert np.array_equal(h(sp.slot_tile_off, K + 1), ref.slot_tile_off), "slot_tile_off"
     assert np.array_equal(h(sp.emit_views, E), ref.emit_views), "emit_views"
     assert np.array_equal(h(sp.emit_order, E), ref.emit_order), "emit_order"
+    compare_row_records(tok_off, sp, ref.emit_order)
     assert np.array_equal(h(sp.left_views, M - E), ref.left_views), "left_views"
     assert np.array_equal(h(sp.left_off, W + 1), ref.left_off), "left_off"
     for m in (oracle.WEIGHT_SAMPLE, oracle.WEIGHT_TOKEN_APPROX, oracle.WEIGHT_TOKEN_EXACT):

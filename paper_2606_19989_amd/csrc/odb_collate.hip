@@ -119,6 +119,11 @@ struct RowRec {
     int32_t l;   // its length
 };
 
+// Loads through these (with wave-uniform addresses) become scalar loads.
+typedef __attribute__((address_space(4))) const int64_t* cptr64;
+typedef __attribute__((address_space(4))) const int32_t* cptr32;
+typedef __attribute__((address_space(4))) const v4i* cptrv4;
+
 // Last slot k in [lo, num_slots) with tile_off[k] <= e, given tile_off[lo] <= e < total.
 __device__ __forceinline__ int64_t advance_slot(const int64_t* __restrict__ tile_off, int64_t num_slots,
                                                 int64_t lo, int64_t e) {
@@ -166,12 +171,86 @@ __device__ __forceinline__ void enter_slot(Cursor& c, int64_t k, int64_t e, cons
     c.ri_end = (int32_t)(r0 + p.rows[k]);
 }
 
-// Move a cursor forward to element e (e - delta is its current element).
-__device__ __forceinline__ void advance(Cursor& c, int64_t e, int64_t delta, const Plan& p) {
-    if (e >= c.t1) {
-        enter_slot(c, advance_slot(p.tile_off, p.num_slots, c.k, e), e, p);
-        return;
+// The same search with wave-uniform lo and e, through scalar loads.
+__device__ __forceinline__ int64_t advance_slot_uniform(const int64_t* __restrict__ tile_off, int64_t num_slots,
+                                                        int64_t lo, int64_t e) {
+    const cptr64 t = (cptr64)tile_off;
+    if (t[lo + 1] > e) return lo;
+    int64_t step = 1, hi;
+    for (;;) {
+        hi = lo + step;
+        if (hi >= num_slots) {
+            hi = num_slots;
+            break;
+        }
+        if (t[hi] > e) break;
+        lo = hi;
+        step <<= 1;
     }
+    while (hi - lo > 1) {
+        const int64_t mid = lo + ((hi - lo) >> 1);
+        if (t[mid] <= e) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ int64_t readlane64(int64_t v, int l) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), l);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Slot entry for the lanes of a wave whose element e has passed the end of their tile
+// (`cross`).  One crossing lane at a time searches for its slot and reads the slot's
+// fields with wave-uniform scalar loads; every crossing lane whose element falls in that
+// slot takes it, so a wave entering one tile does one search.  Scalar loads complete on
+// their own counter: unlike vector loads, waiting for them does not wait for the stores
+// the wave has in flight.  Called in wave-uniform control flow.
+__device__ __forceinline__ void enter_slots_uniform(Cursor& c, int64_t e, bool cross, const Plan& p) {
+    const int lane = threadIdx.x & (kWave - 1);
+    uint64_t need = __ballot(cross);
+    while (need) {
+        const int l = __builtin_ctzll(need);
+        const int64_t el = readlane64(e, l);
+        const int64_t k = advance_slot_uniform(p.tile_off, p.num_slots, __builtin_amdgcn_readlane(c.k, l), el);
+        const int64_t t0 = ((cptr64)p.tile_off)[k];
+        const int64_t t1 = ((cptr64)p.tile_off)[k + 1];
+        const int32_t ml_raw = ((cptr32)p.maxlen)[k];
+        const int64_t r0 = ((cptr64)p.row_off)[k];
+        const int32_t rows = ((cptr32)p.rows)[k];
+        const bool take = ((need >> lane) & 1) && e >= t0 && e < t1;
+        need &= ~(uint64_t)__ballot(take);
+        if (take) {
+            int32_t ml = ml_raw;
+            if (ml <= 0) {
+                atomicOr(p.err, 1);
+                ml = 1;
+            }
+            c.k = (int32_t)k;
+            c.t1 = t1;
+            c.ml = ml;
+            const int64_t local = e - t0;
+            int64_t row;
+            if (local <= 0xFFFFFFFFll) {
+                const uint32_t q = (uint32_t)local / (uint32_t)ml;
+                row = q;
+                c.col = (int32_t)((uint32_t)local - q * (uint32_t)ml);
+            } else {
+                row = local / ml;
+                c.col = (int32_t)(local - row * ml);
+            }
+            c.ri = (int32_t)(r0 + row);
+            c.ri_end = (int32_t)(r0 + rows);
+        }
+    }
+}
+
+// Move a cursor forward to element e (e - delta is its current element).  Called in
+// wave-uniform control flow.
+__device__ __forceinline__ void advance(Cursor& c, int64_t e, int64_t delta, const Plan& p) {
+    const bool cross = e >= c.t1;
+    if (__ballot(cross)) enter_slots_uniform(c, e, cross, p);
+    if (cross) return;
     const int64_t col = (int64_t)c.col + delta;
     if (col >= c.ml) {
         const int64_t adv = col <= 0xFFFFFFFFll ? (int64_t)((uint32_t)col / (uint32_t)c.ml) : col / c.ml;
@@ -228,11 +307,6 @@ struct Stage {
     v4i t;
 };
 
-// Loads through these (with wave-uniform addresses) become scalar loads.
-typedef __attribute__((address_space(4))) const int64_t* cptr64;
-typedef __attribute__((address_space(4))) const int32_t* cptr32;
-typedef __attribute__((address_space(4))) const v4i* cptrv4;
-
 // Values of the 4 elements at e (the stage's position); elements at or past `total` are
 // left unspecified (the caller does not store them).
 __device__ __forceinline__ void stage_values(const Stage& a, int64_t e, int64_t total, const Plan& p, int vec_ok,
@@ -240,10 +314,14 @@ __device__ __forceinline__ void stage_values(const Stage& a, int64_t e, int64_t 
     const Cursor& c = a.c;
     const RowRec& r = a.r;
     const int32_t nreal = r.l - c.col;
-    // one row edge inside the tile: row B's record and first tokens come through the
-    // scalar cache, one boundary lane at a time (scalar loads wait on their own counter,
-    // so they never wait for this wave's outstanding stores)
-    bool edge = vec_ok && c.ml >= kVec && c.col + kVec > c.ml && c.ri >= 0 && c.ri + 1 < c.ri_end &&
+    // one row edge: row B's record and first tokens come through the scalar cache, one
+    // boundary lane at a time (scalar loads wait on their own counter, so they never wait
+    // for this wave's outstanding stores).  Row B is row ri + 1 also when row A is the last
+    // row of its tile: rows and tiles are both packed in slot order, so the next row is the
+    // first row of the next non-empty tile, which starts right after row A.  Its width is
+    // not at hand then, so that case needs row B to hold the group's remaining elements.
+    const bool same_tile = c.ri + 1 < c.ri_end;
+    bool edge = vec_ok && c.ml >= kVec && c.col + kVec > c.ml && c.ri >= 0 && c.ri < c.ri_end &&
                 c.ri + 1 < p.max_rows && r.ts + c.col + kVec <= p.tok_end;
     int32_t bl = 0;
     v4i bt = {0, 0, 0, 0};
@@ -261,7 +339,7 @@ __device__ __forceinline__ void stage_values(const Stage& a, int64_t e, int64_t 
             if (lane == l) {
                 bl = len;
                 bt = h;
-                edge = edge && fits;
+                edge = edge && fits && (same_tile || bl >= kVec - (c.ml - c.col));
             }
         }
     }

@@ -311,3 +311,35 @@ def test_collate_flags_a_bad_row_record():
     odb.odb_collate_status(pipe.ws)
     ref = oracle.plan_window(w)
     compare_collate_full(w, tuple(o[:P] for o in pipe.outputs), ref)
+
+
+def test_two_stream_schedule():
+    # the benchmark's schedule: step i+1's plan on one stream beside step i's collate on
+    # another, two plan buffers, one set of outputs; after several steps the outputs and
+    # both plans are the oracle's
+    import torch
+    import paper_2606_19989_amd as odb
+    import bench
+
+    w = synth.WORKLOADS["text_w8x65536"].window()
+    log(f"two-stream schedule on {w.name}")
+    plan_stream, collate_stream = torch.cuda.Stream(), torch.cuda.Stream()
+    tok_off, toks, ident = synth.device_tensors(w, "cuda")
+    dwin = odb.DeviceWindow(w.rank_off, tok_off, toks, ident, w.num_identities)
+    pipes = [odb.Pipeline(dwin, w.budget, mode=w.mode, quota=w.quota) for _ in range(2)]
+    for p in pipes:
+        p.run()
+        pipes[1].outputs = pipes[0].outputs
+    torch.cuda.synchronize()
+    pipes[0].outputs[0].fill_(-7)
+    sec, coll, _ = bench.pipelined_steps(pipes, plan_stream, collate_stream, 5)
+    assert len(coll) == 5 and sec > 0
+    ref = oracle.plan_window(w)
+    for p in pipes:
+        odb.odb_collate_status(p.ws)
+        compare_plan(w, p, ref)
+    P = ref.padded_elems
+    outs = tuple(o[:P] for o in pipes[0].outputs)
+    compare_collate_sampled(w, outs, ref)
+    collate_properties(outs, ref)
+    compare_collate_by_rank(w, outs, ref, toks)

@@ -34,8 +34,9 @@ def log(msg):
 
 
 def collate_alg_bytes(n, real_tokens, padded, slots):
-    # 16 B written per padded element (4 int32 outputs), 4 B read per real token,
-    # 8 B per token offset, 4 B per emitted id, 24 B of slot tables per slot
+    # 16 B written per padded element (4 int32 outputs), 4 B read per real token, 12 B
+    # per row (its sample's token start and length: the plan's row records, or an
+    # emitted id and two CSR offsets), 24 B of slot tables per slot
     return 16 * padded + 4 * real_tokens + 8 * (n + 1) + 4 * n + 24 * slots
 
 
@@ -383,7 +384,7 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "odb_collate (row_info_kernel + collate_kernel)",
+            "kernel": "odb_collate (collate_kernel, row records from the plan)",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",

@@ -25,6 +25,7 @@
 // so equal sizes favour the later-formed group).  With sigma = the largest size such
 // that at least T groups have size >= sigma, every group larger than sigma is kept and
 // the remaining places go to the size-sigma groups with the highest formation index.
+#include <algorithm>
 #include <climits>
 #include <cstring>
 #include <vector>
@@ -635,19 +636,39 @@ __global__ void __launch_bounds__(kBlock) compact_emit_kernel(const int32_t* __r
 // when `ts` is not NULL) and the check that the length the plan carried for it (from
 // the stage-1 sorted lengths) is the sample's CSR length.  Ids are in range here:
 // round0_check_kernel verified that every rank's order is a permutation of its ids.
+//
+// The offsets are gathered in random order, one 128-byte line per 8-byte read unless the
+// line is still cached.  A rank's rows hold only that rank's ids, whose offsets span
+// 8 B per sample (2 MB at 262,144 samples), so with `xcd_ranks` set, rank r is gathered
+// only by the blocks of group r mod kXcds (workgroups are dealt to the XCDs round
+// robin, so block b runs on XCD b mod kXcds): each rank's offsets then stay in one XCD's
+// L2 and are read from HBM about once.
+constexpr int kXcds = 8;
+
 __global__ void __launch_bounds__(kBlock) row_check_kernel(const int64_t* __restrict__ tok_off,
                                                            const int32_t* __restrict__ emit,
-                                                           const int32_t* __restrict__ len, int64_t rows,
-                                                           int64_t* __restrict__ ts, DevStatus* st) {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < rows; k += stride) {
-        const int32_t s = emit[k];
-        const int64_t a = tok_off[s];
-        if (tok_off[s + 1] - a != (int64_t)len[k]) {
-            atomicOr(&st->err, kErrSortedLen);
-            atomicMin((unsigned long long*)&st->first_bad, (unsigned long long)s);
+                                                           const int32_t* __restrict__ len,
+                                                           const int64_t* __restrict__ row_off, int64_t S, int W,
+                                                           int xcd_ranks, int64_t* __restrict__ ts, DevStatus* st) {
+    const int group = xcd_ranks ? (int)(blockIdx.x % kXcds) : 0;
+    const int groups = xcd_ranks ? kXcds : 1;
+    const int64_t gb = xcd_ranks ? blockIdx.x / kXcds : blockIdx.x;   // block within its group
+    const int64_t nb = xcd_ranks ? gridDim.x / kXcds : gridDim.x;
+    const int64_t stride = nb * blockDim.x;
+    for (int r = group; r < W; r += groups) {
+        // all ranks at once in the plain mode: the rows of ranks group .. W-1 are contiguous
+        const int64_t lo = row_off[(int64_t)r * S];
+        const int64_t hi = row_off[(int64_t)(xcd_ranks ? r + 1 : W) * S];
+        for (int64_t k = lo + gb * blockDim.x + threadIdx.x; k < hi; k += stride) {
+            const int32_t s = emit[k];
+            const int64_t a = tok_off[s];
+            if (tok_off[s + 1] - a != (int64_t)len[k]) {
+                atomicOr(&st->err, kErrSortedLen);
+                atomicMin((unsigned long long*)&st->first_bad, (unsigned long long)s);
+            }
+            if (ts) ts[k] = a;
         }
-        if (ts) ts[k] = a;
+        if (!xcd_ranks) break;
     }
 }
 
@@ -1273,10 +1294,18 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
         ODB_LAUNCHED();
     }
     const int64_t nemit = hrs.emitted_total;
-    if (nemit > 0) {
-        hipLaunchKernelGGL(row_check_kernel, dim3(grid_for(nemit, kBlock, gcap)), dim3(kBlock), 0, s,
-                           w->d_token_offsets, (const int32_t*)d_emit_order, (const int32_t*)row_len, nemit,
-                           d_row_token_start, st);
+    if (nemit > 0 && K > 0) {
+        // rank-per-XCD gathers pay off when every XCD has a rank and a rank's offsets fit
+        // in its L2 with room to spare
+        int64_t max_nr = 0;
+        for (int r = 0; r < W; ++r) max_nr = std::max(max_nr, w->rank_offsets[r + 1] - w->rank_offsets[r]);
+        const int xcd = W >= kXcds && max_nr * 8 <= (int64_t)2 << 20;
+        const unsigned grid = xcd ? (unsigned)(kXcds * std::max<int64_t>(1, std::min<int64_t>(
+                                        (int64_t)num_cus() * 2 / kXcds, (max_nr + kBlock - 1) / kBlock)))
+                                  : grid_for(nemit, kBlock, gcap);
+        hipLaunchKernelGGL(row_check_kernel, dim3(grid), dim3(kBlock), 0, s, w->d_token_offsets,
+                           (const int32_t*)d_emit_order, (const int32_t*)row_len, (const int64_t*)d_slot_row_off, S,
+                           W, xcd, d_row_token_start, st);
         ODB_LAUNCHED();
     }
     hipLaunchKernelGGL(leftover_off_kernel, dim3(1), dim3(kBlock), 0, s, (const RankState*)d_ranks, W,

@@ -810,7 +810,7 @@ int run_coverage(const odb_window_t* w, const Layout& L, void* ws, const int32_t
     int32_t* cover = ws_at<int32_t>(ws, L.cover);
     DevStatus* st = ws_at<DevStatus>(ws, L.status);
     DevInfo* info = ws_at<DevInfo>(ws, L.info);
-    const int64_t cap = (int64_t)num_cus() * 16;
+    const int64_t cap = (int64_t)num_cus() * kPlanBlocksPerCU;
     if (n > 0) {
         uint32_t* bits = reinterpret_cast<uint32_t*>(cover);
         const int64_t words = (n + 31) / 32;
@@ -860,7 +860,7 @@ int run_coverage_exact(const odb_window_t* w, const Layout& L, void* ws, const i
     int32_t* cover = ws_at<int32_t>(ws, L.cover);
     DevStatus* st = ws_at<DevStatus>(ws, L.status);
     DevInfo* info = ws_at<DevInfo>(ws, L.info);
-    const int64_t cap = (int64_t)num_cus() * 16;
+    const int64_t cap = (int64_t)num_cus() * kPlanBlocksPerCU;
     hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(n, kBlock, cap)), dim3(kBlock), 0, s, cover, n, 0);
     ODB_LAUNCHED();
     if (ne > 0) {
@@ -1044,7 +1044,7 @@ int run_plan_coverage(const odb_window_t* w, const Layout& L, void* ws, const in
         int32_t* cover = ws_at<int32_t>(ws, L.cover);
         DevStatus* st = ws_at<DevStatus>(ws, L.status);
         const int64_t nid = w->num_identities;
-        const int64_t cap = (int64_t)num_cus() * 16;
+        const int64_t cap = (int64_t)num_cus() * kPlanBlocksPerCU;
         hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(nid, kBlock, cap)), dim3(kBlock), 0, s, cover, nid, 0);
         ODB_LAUNCHED();
         if (ne > 0) {
@@ -1160,7 +1160,7 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     // records' lengths, checked against the CSR offsets once the plan is built
     int32_t* row_len = d_row_len ? d_row_len : ws_at<int32_t>(d_ws, L.row_len);
     int32_t* dst_len = nonjoin ? ws_at<int32_t>(d_ws, L.stage_len) : row_len;
-    const int64_t gcap = (int64_t)num_cus() * 16;
+    const int64_t gcap = (int64_t)num_cus() * kPlanBlocksPerCU;
     const unsigned gridn = grid_for(n, kBlock, gcap);
 
     hipLaunchKernelGGL(init_align_kernel, dim3(1), dim3(64), 0, s, d_rs, d_info);

@@ -527,7 +527,7 @@ extern "C" int odb_collate(const odb_window_t* w, int64_t num_slots, const int32
     if (!have_rows) {
         int64_t* ts = ws_at<int64_t>(d_ws, L.row_ts);
         int32_t* len = ws_at<int32_t>(d_ws, L.row_len);
-        hipLaunchKernelGGL(row_info_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock), 0, s,
+        hipLaunchKernelGGL(row_info_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * kPlanBlocksPerCU)), dim3(kBlock), 0, s,
                            w->d_token_offsets, n, max_rows, d_emit_order, d_slot_row_off, num_slots, ts, len, err);
         ODB_LAUNCHED();
         row_ts = ts;

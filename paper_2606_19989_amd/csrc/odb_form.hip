@@ -525,7 +525,7 @@ static int finish_groups(const Layout& L, void* ws, int W, int64_t n, const int6
     int32_t* gstart = ws_at<int32_t>(ws, L.gstart);
     ODB_TRY((device_excl_scan<uint32_t>(MarkLoad{marks}, InclStore{marks, incl}, n,
                                         ws_at<uint32_t>(ws, L.partials), s)));
-    hipLaunchKernelGGL(gidx_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock), 0, s,
+    hipLaunchKernelGGL(gidx_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * kPlanBlocksPerCU)), dim3(kBlock), 0, s,
                        (const uint8_t*)marks, (const int32_t*)incl, d_off, (const RankState*)d_ranks, W, n,
                        d_gidx, gstart);
     ODB_LAUNCHED();
@@ -544,7 +544,7 @@ int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget,
     int32_t* incl = ws_at<int32_t>(ws, L.incl);
     int32_t* gstart = ws_at<int32_t>(ws, L.gstart);
     DevStatus* st = ws_at<DevStatus>(ws, L.status);
-    const unsigned grid = grid_for(n + 1, kBlock, (int64_t)num_cus() * 16);
+    const unsigned grid = grid_for(n + 1, kBlock, (int64_t)num_cus() * kPlanBlocksPerCU);
     // distinct steps per rank: at most the distinct values of floor(budget / l), i.e. at
     // most 2 sqrt(budget) + 1, and at most the number of distinct lengths
     int64_t runs_bound = 2 * ((int64_t)std::sqrt((double)budget) + 1) + 1;
@@ -611,7 +611,7 @@ extern "C" int odb_form_groups(const odb_window_t* w, int64_t budget, int32_t* d
     ODB_LAUNCHED();
 
     // (a1) lengths and their validity; the one synchronisation of this call
-    hipLaunchKernelGGL(lengths_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock), 0, s,
+    hipLaunchKernelGGL(lengths_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * kPlanBlocksPerCU)), dim3(kBlock), 0, s,
                        w->d_token_offsets, n, len, st);
     ODB_LAUNCHED();
     DevStatus hs;
@@ -634,7 +634,7 @@ extern "C" int odb_form_groups(const odb_window_t* w, int64_t budget, int32_t* d
     while (bits < 32 && ((maxl - minl) >> bits) != 0) ++bits;
     const int passes = (bits + 7) / 8;
     if (passes == 0) {
-        hipLaunchKernelGGL(identity_order_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * 16)), dim3(kBlock),
+        hipLaunchKernelGGL(identity_order_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * kPlanBlocksPerCU)), dim3(kBlock),
                            0, s, n, (const int32_t*)len, d_order, d_sorted_len);
         ODB_LAUNCHED();
     } else {

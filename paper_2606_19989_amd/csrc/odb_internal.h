@@ -17,6 +17,9 @@ constexpr int kSortTile = kBlock * kSortItems;
 constexpr int kScanItems = 16;
 constexpr int kScanTile = kBlock * kScanItems;
 constexpr int kMaxJumpRounds = 40;
+// grid cap of the grid-stride kernels of the plan stages, in blocks per compute unit
+// (64 or 256 were slower: per-block setup and same-address atomics grow with the grid)
+constexpr int kPlanBlocksPerCU = 16;
 
 // ------------------------------------------------------------------ host error state
 int set_error(int code, const char* fmt, ...);

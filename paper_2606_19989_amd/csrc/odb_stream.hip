@@ -971,7 +971,7 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
                          (long long)slot_capacity);
 
     // plan arrays in the window layout
-    const int64_t gcap = (int64_t)num_cus() * 16;
+    const int64_t gcap = (int64_t)num_cus() * kPlanBlocksPerCU;
     int64_t* partials = ws_at<int64_t>(d_ws, SL.partials);
     if (K > 0) {
         hipLaunchKernelGGL(stream_slots_kernel, dim3(grid_for(K, 256, gcap)), dim3(256), 0, s, a, S, d_slot_rows,

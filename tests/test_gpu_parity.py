@@ -65,6 +65,12 @@ def adversarial_windows():
     add("many_step_runs", [rng.integers(1, 5000, 12000), rng.integers(1, 5000, 7000)], 4_000_000)
     per = [rng.integers(100, 3000, 47 - r) for r in range(15)] + [np.zeros(0, np.int64)]
     add("empty_rank_audit_w16", per, 8192)
+    # narrow tiles (widths 3..9, a few rows each): groups straddle tile edges at every
+    # offset, the next tile's first row is sometimes shorter than the group's remainder,
+    # and an empty rank leaves zero-size IDLE tiles between non-empty ones
+    add("narrow_tile_edges", [rng.integers(3, 10, 3000), [], rng.integers(3, 10, 1500), rng.integers(1, 4, 700)], 24)
+    add("narrow_tile_edges_nonjoin", [rng.integers(3, 10, 3000), rng.integers(3, 10, 1501)], 31, mode="nonjoin",
+        quota=2500)
     return out
 
 

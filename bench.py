@@ -40,14 +40,24 @@ def collate_alg_bytes(n, real_tokens, padded, slots):
     return 16 * padded + 4 * real_tokens + 8 * (n + 1) + 4 * n + 24 * slots
 
 
-def pipelined_steps(pipes, plan_stream, collate_stream, steps):
-    """`steps` window steps, double-buffered over the two Pipelines in `pipes` (shared
-    outputs): step i plans into pipes[i % 2] on `plan_stream` once that pipeline's
-    previous collate has finished, and collates on `collate_stream` once its plan is
-    done.  odb_align_groups synchronises only the plan stream, so while the host waits
-    for step i's plan the collate stream is still writing step i-1.  Returns the host
-    seconds of the whole loop (the collate stream drained) and per step the HIP-event
-    milliseconds of odb_collate and of odb_loss_weights."""
+def window_plan(p, stream):
+    p.form(stream)
+    p.align(stream)
+
+
+def window_weights(p, stream):
+    p.loss_weights(stream=stream)
+
+
+def pipelined_steps(pipes, plan_stream, collate_stream, steps, plan=window_plan, weights=window_weights):
+    """`steps` steps, double-buffered over the two pipelines in `pipes` (shared outputs):
+    step i plans into pipes[i % 2] on `plan_stream` (`plan`: odb_form_groups +
+    odb_align_groups for a window, odb_stream_plan for a streaming iteration) once that
+    pipeline's previous collate has finished, and collates on `collate_stream` once its
+    plan is done.  The plan calls synchronise only the plan stream, so while the host
+    waits for step i's plan the collate stream is still writing step i-1.  Returns the
+    host seconds of the whole loop (the collate stream drained) and per step the
+    HIP-event milliseconds of odb_collate and of the loss weights."""
     import torch
 
     free = [torch.cuda.Event(), torch.cuda.Event()]
@@ -59,8 +69,7 @@ def pipelined_steps(pipes, plan_stream, collate_stream, steps):
     for i in range(steps):
         p = pipes[i % 2]
         plan_stream.wait_event(free[i % 2])
-        p.form(plan_stream)
-        p.align(plan_stream)
+        plan(p, plan_stream)
         planned = torch.cuda.Event()
         planned.record(plan_stream)
         collate_stream.wait_event(planned)
@@ -68,7 +77,7 @@ def pipelined_steps(pipes, plan_stream, collate_stream, steps):
         ev[0].record(collate_stream)
         p.collate(collate_stream)
         ev[1].record(collate_stream)
-        p.loss_weights(stream=collate_stream)
+        weights(p, collate_stream)
         ev[2].record(collate_stream)
         free[i % 2].record(collate_stream)
         marks.append(ev)
@@ -169,21 +178,35 @@ def length_sketch_timing(odb, win, ws, w, dev, reps=5):
 STREAM_CONFIG = dict(ranks=64, budget=16384, buffer_size=1024, depth=1024, rate=1024, seed=74)
 
 
-def stream_timing(odb, w, tok_off, tokens, dev, iters=3):
-    """One logical iteration of the unified streaming loop over the window's samples as
-    a dataset (odb_stream_plan: every round's fetch, grouping, alignment and emission),
-    then the collate of its plan; host clock around each synchronising call."""
+def stream_plan(sp, stream):
+    sp.plan(stream)
+
+
+def stream_weights(sp, stream):
+    sp.loss_weights(stream=stream)
+
+
+def stream_timing(odb, w, tok_off, tokens, dev, plan_stream, collate_stream, iters=3, pipelined_iters=8):
+    """Logical iterations of the unified streaming loop over the window's samples as a
+    dataset (odb_stream_plan: every round's fetch, grouping, alignment and emission), each
+    followed by the collate of its plan.  Serial (host clock around each synchronising
+    call, one pipeline) and two-stream (iteration i+1's plan beside iteration i's collate
+    and loss weights, two pipelines sharing the outputs)."""
     import numpy as np
     import torch
 
     c = STREAM_CONFIG
     perm = torch.from_numpy(np.random.default_rng(c["seed"]).permutation(w.n).astype(np.int32)).to(dev)
     win = odb.DeviceWindow(np.linspace(0, w.n, c["ranks"] + 1).astype(np.int64), tok_off, tokens, None, 0)
-    sp = odb.StreamPipeline(win, perm, c["budget"], buffer_size=c["buffer_size"], depth=c["depth"],
-                            rate=np.full(c["ranks"], c["rate"], np.int32))
-    sp.plan()
-    sp.collate()
+    sps = [odb.StreamPipeline(win, perm, c["budget"], buffer_size=c["buffer_size"], depth=c["depth"],
+                              rate=np.full(c["ranks"], c["rate"], np.int32)) for _ in range(2)]
+    for sp in sps:
+        sp.plan()
+        sp.collate()
+        sp.loss_weights()
+        sps[1].outputs = sps[0].outputs
     torch.cuda.synchronize()
+    sp = sps[0]
     plan_t, coll_t = [], []
     for _ in range(iters):
         t0 = time.perf_counter()
@@ -196,14 +219,27 @@ def stream_timing(odb, w, tok_off, tokens, dev, iters=3):
         coll_t.append(t2 - t1)
     plan_ms = float(np.median(plan_t)) * 1e3
     coll_ms = float(np.median(coll_t)) * 1e3
+    pipelined_steps(sps, plan_stream, collate_stream, 2, plan=stream_plan, weights=stream_weights)
+    sec, coll_ev, _ = pipelined_steps(sps, plan_stream, collate_stream, pipelined_iters, plan=stream_plan,
+                                      weights=stream_weights)
+    for x in sps:
+        odb.odb_collate_status(x.ws)
+        assert x.info["steps"] == info["steps"] and x.info["padded_elems"] == info["padded_elems"]
+    two_ms = sec / pipelined_iters * 1e3
     out = {"config": dict(c, samples=w.n, lengths=w.name),
            "plan_ms": plan_ms, "collate_ms": coll_ms,
            "rounds": info["rounds"], "emit_rounds": info["emit_rounds"], "skip_rounds": info["skip_rounds"],
            "us_per_round": plan_ms * 1e3 / max(info["rounds"], 1), "steps": info["steps"],
            "pad_fraction": info["pad_fraction"], "padded_elems": info["padded_elems"],
            "emitted_views": info["emitted_views"],
-           "samples_per_s": info["emitted_views"] / ((plan_ms + coll_ms) * 1e-3)}
-    del sp
+           "serial_ms_per_iteration": plan_ms + coll_ms,
+           "two_stream_ms_per_iteration": two_ms,
+           "two_stream_collate_ms": float(np.mean(coll_ev)),
+           "samples_per_s": info["emitted_views"] / (two_ms * 1e-3),
+           "serial_samples_per_s": info["emitted_views"] / ((plan_ms + coll_ms) * 1e-3)}
+    for x in sps:
+        x.outputs = None
+    del sps, sp
     torch.cuda.empty_cache()
     return out
 
@@ -334,9 +370,10 @@ def main():
         for p in pipes:
             p.outputs = None
         torch.cuda.empty_cache()
-        stream = stream_timing(odb, w, tok_off, tokens, dev)
+        stream = stream_timing(odb, w, tok_off, tokens, dev, plan_stream, collate_stream)
         log(f"[bench] streaming iteration: plan {stream['plan_ms']:.1f} ms over {stream['rounds']} rounds, "
-            f"collate {stream['collate_ms']:.1f} ms")
+            f"collate {stream['collate_ms']:.1f} ms; two streams {stream['two_stream_ms_per_iteration']:.1f} ms "
+            f"per iteration")
     copy_gbs = copy_ceiling(dev)
     log(f"[bench] plain 4 GiB device copy: {copy_gbs:.0f} GB/s")
 

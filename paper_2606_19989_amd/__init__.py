@@ -541,11 +541,16 @@ class StreamPipeline:
         return tuple(o[:P] for o in self.outputs)
 
     def loss_weights(self, mode: int = ODB_WEIGHT_TOKEN_EXACT, stream=None):
+        """As Pipeline.loss_weights; the output buffers are kept and reused (views of
+        them are returned), so a call on another stream never writes freed memory."""
         torch = self.torch
         S, K = int(self.info["steps"]), self.num_slots
-        wt = torch.empty(max(K, 1), dtype=torch.float64, device=self.device)
-        st = torch.empty(max(S, 1), dtype=torch.int64, device=self.device)
-        ss = torch.empty(max(S, 1), dtype=torch.int64, device=self.device)
+        if getattr(self, "_weights", None) is None or self._weights[0].numel() < max(K, 1) \
+                or self._weights[1].numel() < max(S, 1):
+            self._weights = (torch.empty(max(K, 1), dtype=torch.float64, device=self.device),
+                             torch.empty(max(S, 1), dtype=torch.int64, device=self.device),
+                             torch.empty(max(S, 1), dtype=torch.int64, device=self.device))
+        wt, st, ss = self._weights
         odb_loss_weights(self.W, S, mode, self.slot_rows, self.slot_tokens, self.slot_tokens_approx, wt, st, ss,
                          stream)
         return wt[:K], st[:S], ss[:S]

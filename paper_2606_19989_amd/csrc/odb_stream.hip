@@ -8,7 +8,7 @@
 // head to M = W * ceil(N / W) views (view m has identity perm[m mod N]); view m belongs
 // to rank m mod W, visited in increasing m.
 //
-// One protocol round k is two launches:
+// One protocol round k is three launches:
 //   stream_form_kernel   one block per rank: fetch up to rate[r] views under the depth
 //                        envelope |B_r| <= D; status (finished / not ready / ready); a ready
 //                        rank sorts its whole buffer by (length desc, view asc) in LDS and
@@ -18,9 +18,12 @@
 //                        over the ready ranks); in an emit round each ready rank applies
 //                        Algorithm 1 (split in closed form, overflow by size rank) and
 //                        writes its T slot records, its emitted views and its new buffer
-//                        (the overflow); finished ranks (join) write IDLE slots.  The last
-//                        block to finish (a ticket counter, no waiting) does the round's
-//                        bookkeeping: the non-join quota cut (Theorem 2) and termination
+//                        (the overflow); finished ranks (join) write IDLE slots
+//   stream_round_kernel  one block: the round's bookkeeping, the non-join quota cut
+//                        (Theorem 2) and termination.  A launch of its own rather than the
+//                        last emit block (picked by a ticket counter): the ticket needs a
+//                        device-scope fence in every block, an L2 write-back on this GPU,
+//                        which beside a running collate waits behind its write stream
 // Rounds are enqueued in chunks; the host reads the done flag once per chunk, and rounds
 // enqueued after the stop return at once.  A final pass turns the per-rank staging into
 // the window plan layout (rank-major slots, row and tile offsets), so odb_collate and
@@ -37,7 +40,10 @@ namespace odb {
 
 namespace {
 
-constexpr int kSB = 1024;             // threads of the per-rank blocks
+constexpr int kSB = 1024;             // threads of the per-rank form blocks
+// threads of the per-rank emit blocks: at 512 (2 waves per SIMD) an emit block fits beside
+// a running collate (3 waves per SIMD), so a plan can run beside another plan's collate
+constexpr int kSE = 512;
 constexpr int kMaxDepth = 4096;       // largest outstanding-depth envelope (LDS sort)
 constexpr int kRoundsPerCheck = 32;   // rounds enqueued between two looks at the done flag
 
@@ -71,7 +77,6 @@ struct RankStream {
 struct StreamRec {
     int32_t kind;      // 0 emit, 1 skip, 2 stop
     int32_t changed;   // an emit round in which some ready rank had G_r != T
-    int32_t ticket;    // blocks of the round's emit kernel that have finished
     int32_t pad;
     int64_t target;    // T (emit rounds)
     int64_t emitted;   // views emitted in the round (after a quota cut)
@@ -111,32 +116,36 @@ struct StreamArgs {
     int32_t* evw;          // [W * q] emit streams
 };
 
+// Dynamic LDS of stream_emit_kernel for depth D: gtok (8 B) and gsl, as, ae, cum (4 B).
+inline size_t emit_lds_bytes(int64_t D) { return (size_t)(8 * D + 4 * (4 * D + 2)); }
+
 __device__ __forceinline__ int32_t view_identity(const StreamArgs& a, int64_t m) {
     return a.perm[m < a.N ? m : m % a.N];
 }
 
-template <typename T>
+// Sum of one value per thread over an NT-thread block.
+template <int NT, typename T>
 __device__ __forceinline__ T sblock_sum(T v) {
-    __shared__ T wt[kSB / kWave];
+    __shared__ T wt[NT / kWave];
     v = wave_sum(v);
     if ((threadIdx.x & (kWave - 1)) == 0) wt[threadIdx.x / kWave] = v;
     __syncthreads();
     T t = 0;
-    for (int i = 0; i < kSB / kWave; ++i) t += wt[i];
+    for (int i = 0; i < NT / kWave; ++i) t += wt[i];
     __syncthreads();
     return t;
 }
 
-// Exclusive scan of one value per thread over the 1024-thread block; *total = sum.
-template <typename T>
+// Exclusive scan of one value per thread over an NT-thread block; *total = sum.
+template <int NT, typename T>
 __device__ __forceinline__ T sblock_excl(T v, T* total) {
-    __shared__ T wt[kSB / kWave];
+    __shared__ T wt[NT / kWave];
     const T inc = wave_incl_sum(v);
     const int w = threadIdx.x / kWave;
     if ((threadIdx.x & (kWave - 1)) == kWave - 1) wt[w] = inc;
     __syncthreads();
     T pre = 0, tot = 0;
-    for (int i = 0; i < kSB / kWave; ++i) {
+    for (int i = 0; i < NT / kWave; ++i) {
         pre += i < w ? wt[i] : T(0);
         tot += wt[i];
     }
@@ -213,7 +222,7 @@ __global__ void __launch_bounds__(kSB) stream_form_kernel(StreamArgs a, int64_t 
         }
         keys[i] = key;
     }
-    tok = sblock_sum(tok);   // also a barrier for keys[]
+    tok = sblock_sum<kSB>(tok);   // also a barrier for keys[]
     if (p2 <= kSB) {
         // one key per thread: exchanges with a partner less than a wave away are lane
         // shuffles, only the longer strides go through LDS (10 of 55 stages at 1024)
@@ -302,7 +311,7 @@ __device__ RoundView decide_round(const StreamArgs& a) {
         s_minC = LLONG_MAX;
     }
     __syncthreads();
-    for (int r = threadIdx.x; r < a.W; r += kSB) {
+    for (int r = threadIdx.x; r < a.W; r += kSE) {
         const RankStream R = a.ranks[r];
         if (R.status < 0) {
             atomicAdd((unsigned long long*)&s_fin, 1ull);
@@ -349,7 +358,7 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
     const int64_t base = a.g->steps;   // written by the previous round's bookkeeping only
     const int32_t st = R->status;
     if (st < 0) {   // finished rank in join mode: IDLE slots
-        for (int64_t j = threadIdx.x; j < T; j += kSB) {
+        for (int64_t j = threadIdx.x; j < T; j += kSE) {
             const int64_t x = base + j;
             if (x < a.scap) {
                 const int64_t o = (int64_t)r * a.scap + x;
@@ -370,13 +379,20 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
     const int32_t* sv = a.sv + (int64_t)r * a.D;
     const int32_t* sl = a.slen + (int64_t)r * a.D;
     int32_t* apos = a.apos + (int64_t)r * a.D;
-    __shared__ int32_t gsl[kMaxDepth + 1];
-    __shared__ int32_t as[kMaxDepth], ae[kMaxDepth], cum[kMaxDepth + 1];
-    __shared__ unsigned long long gtok[kMaxDepth];
+    // per-rank tables of up to D groups in dynamic LDS (emit_lds_bytes(D) bytes): sized by
+    // the depth envelope rather than its maximum, the block stays small enough to run
+    // beside another kernel (a static 96 KB also made the compiler reserve 169 registers
+    // per lane, since that much LDS already capped the occupancy)
+    extern __shared__ unsigned long long s_dyn[];
+    unsigned long long* gtok = s_dyn;
+    int32_t* gsl = reinterpret_cast<int32_t*>(s_dyn + a.D);
+    int32_t* as = gsl + (a.D + 1);
+    int32_t* ae = as + a.D;
+    int32_t* cum = ae + a.D;
     __shared__ int64_t s_X, s_jstar;
     __shared__ int32_t s_ret, s_bad;
-    for (int64_t i = threadIdx.x; i <= G; i += kSB) gsl[i] = gsg[i];
-    for (int64_t i = threadIdx.x; i < T; i += kSB) gtok[i] = 0;
+    for (int64_t i = threadIdx.x; i <= G; i += kSE) gsl[i] = gsg[i];
+    for (int64_t i = threadIdx.x; i < T; i += kSE) gtok[i] = 0;
     if (threadIdx.x == 0) {
         s_ret = 0;
         s_bad = 0;
@@ -407,7 +423,7 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
         }
         __syncthreads();
         const int64_t X = s_X, js = s_jstar;
-        for (int64_t t = threadIdx.x; t < T; t += kSB) {
+        for (int64_t t = threadIdx.x; t < T; t += kSE) {
             if (t < X) {
                 as[t] = (int32_t)t;
                 ae[t] = (int32_t)(t + 1);
@@ -421,7 +437,7 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
             }
         }
         __syncthreads();
-        for (int64_t p = threadIdx.x; p < n; p += kSB) {
+        for (int64_t p = threadIdx.x; p < n; p += kSE) {
             int64_t ap;
             if (p < X) {
                 ap = p;
@@ -440,7 +456,7 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
         }
     } else if (G > T) {
         // overflow: keep the T groups first by (size desc, formation index desc)
-        for (int64_t g = threadIdx.x; g < G; g += kSB) {
+        for (int64_t g = threadIdx.x; g < G; g += kSE) {
             const int32_t cg = gsl[g + 1] - gsl[g];
             int64_t rank = 0;
             for (int64_t h = 0; h < G; ++h) {
@@ -451,11 +467,11 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
         }
         __syncthreads();
         int64_t carry = 0;
-        for (int64_t b = 0; b < G; b += kSB) {
+        for (int64_t b = 0; b < G; b += kSE) {
             const int64_t g = b + threadIdx.x;
             const int32_t f = g < G ? cum[g] : 0;
             int32_t tot;
-            const int32_t ex = sblock_excl(f, &tot);
+            const int32_t ex = sblock_excl<kSE>(f, &tot);
             if (g < G && f) {
                 const int64_t ki = carry + ex;
                 as[ki] = gsl[g];
@@ -465,34 +481,34 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
         }
         __syncthreads();
         if (threadIdx.x == 0 && carry != T) s_bad = 1;
-        for (int64_t p = threadIdx.x; p < n; p += kSB) apos[p] = -1;
+        for (int64_t p = threadIdx.x; p < n; p += kSE) apos[p] = -1;
         __syncthreads();
-        for (int64_t t = threadIdx.x; t < T; t += kSB)
+        for (int64_t t = threadIdx.x; t < T; t += kSE)
             for (int64_t p = as[t]; p < ae[t]; ++p) apos[p] = (int32_t)t;
     } else {
-        for (int64_t t = threadIdx.x; t < T; t += kSB) {
+        for (int64_t t = threadIdx.x; t < T; t += kSE) {
             as[t] = gsl[t];
             ae[t] = gsl[t + 1];
         }
         __syncthreads();
-        for (int64_t t = threadIdx.x; t < T; t += kSB)
+        for (int64_t t = threadIdx.x; t < T; t += kSE)
             for (int64_t p = as[t]; p < ae[t]; ++p) apos[p] = (int32_t)t;
     }
     __syncthreads();
     // rows prefix over the adjusted groups, tokens per adjusted group
     {
         int64_t carry = 0;
-        for (int64_t b = 0; b < T; b += kSB) {
+        for (int64_t b = 0; b < T; b += kSE) {
             const int64_t t = b + threadIdx.x;
             const int32_t rows = t < T ? ae[t] - as[t] : 0;
             int32_t tot;
-            const int32_t ex = sblock_excl(rows, &tot);
+            const int32_t ex = sblock_excl<kSE>(rows, &tot);
             if (t < T) cum[t] = (int32_t)(carry + ex);
             carry += tot;
         }
         if (threadIdx.x == 0) cum[T] = (int32_t)carry;
     }
-    for (int64_t p = threadIdx.x; p < n; p += kSB) {
+    for (int64_t p = threadIdx.x; p < n; p += kSE) {
         const int32_t t = apos[p];
         if (t >= 0) atomicAdd(&gtok[t], (unsigned long long)sl[p]);
     }
@@ -501,7 +517,7 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
     const int64_t ebase = R->emitted;
     const double mean = (double)R->tok / (double)n;
     // slot records: step j of the round is adjusted group T-1-j (short to long)
-    for (int64_t t = threadIdx.x; t < T; t += kSB) {
+    for (int64_t t = threadIdx.x; t < T; t += kSE) {
         const int64_t j = T - 1 - t;
         const int64_t x = base + j;
         const int32_t rows = ae[t] - as[t];
@@ -520,7 +536,7 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
     // new buffer (overflow returns)
     int32_t* ev = a.evw + (int64_t)r * a.q;
     int32_t* buf = a.bufv + (int64_t)r * a.D;
-    for (int64_t p = threadIdx.x; p < n; p += kSB) {
+    for (int64_t p = threadIdx.x; p < n; p += kSE) {
         const int32_t t = apos[p];
         if (t >= 0) {
             const int64_t e = ebase + E - cum[t + 1] + (ae[t] - 1 - p);
@@ -573,11 +589,11 @@ __device__ void round_bookkeeping(const StreamArgs& a, int64_t k) {
     if (threadIdx.x == 0) s_cut = T;
     __syncthreads();
     int64_t carry = 0, mx = 0, kept = 0;
-    for (int64_t b = 0; b < T; b += kSB) {
+    for (int64_t b = 0; b < T; b += kSE) {
         const int64_t j = b + threadIdx.x;
         const int64_t v = j < T ? a.stepsum[j] : 0;
         int64_t tot;
-        const int64_t ex = sblock_excl(v, &tot);
+        const int64_t ex = sblock_excl<kSE>(v, &tot);
         if (a.mode == ODB_MODE_NONJOIN_QUOTA && j < T && before + carry + ex < a.quota &&
             before + carry + ex + v >= a.quota)
             s_cut = j + 1;
@@ -585,7 +601,7 @@ __device__ void round_bookkeeping(const StreamArgs& a, int64_t k) {
         carry += tot;
     }
     const int64_t cut = s_cut;
-    for (int64_t j = threadIdx.x; j < T; j += kSB) {
+    for (int64_t j = threadIdx.x; j < T; j += kSE) {
         const int64_t v = a.stepsum[j];
         if (j < cut) {
             mx = v > mx ? v : mx;
@@ -593,15 +609,15 @@ __device__ void round_bookkeeping(const StreamArgs& a, int64_t k) {
         }
         a.stepsum[j] = 0;
     }
-    __shared__ int64_t wm[kSB / kWave];
+    __shared__ int64_t wm[kSE / kWave];
     for (int d = kWave / 2; d > 0; d >>= 1) {
         const int64_t o = __shfl_xor(mx, d, kWave);
         mx = o > mx ? o : mx;
     }
     if ((threadIdx.x & (kWave - 1)) == 0) wm[threadIdx.x / kWave] = mx;
-    kept = sblock_sum(kept);
+    kept = sblock_sum<kSE>(kept);
     if (threadIdx.x == 0) {
-        for (int i = 0; i < kSB / kWave; ++i) mx = wm[i] > mx ? wm[i] : mx;
+        for (int i = 0; i < kSE / kWave; ++i) mx = wm[i] > mx ? wm[i] : mx;
         rec->emitted = kept;
         rec->cut = cut;
         g->steps += cut;
@@ -620,21 +636,14 @@ __device__ void round_bookkeeping(const StreamArgs& a, int64_t k) {
     }
 }
 
-__global__ void __launch_bounds__(kSB) stream_emit_kernel(StreamArgs a, int64_t k) {
+__global__ void __launch_bounds__(kSE) stream_emit_kernel(StreamArgs a, int64_t k) {
     if (*(volatile int32_t*)&a.g->done) return;
     emit_round(a, k);
-    // the last block of the round does the bookkeeping once every block's writes are visible
-    __shared__ int32_t s_last;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        __threadfence();
-        s_last = atomicAdd(&a.rec[k].ticket, 1) == (int32_t)gridDim.x - 1;
-    }
-    __syncthreads();
-    if (s_last) {
-        __threadfence();
-        round_bookkeeping(a, k);
-    }
+}
+
+__global__ void __launch_bounds__(kSE) stream_round_kernel(StreamArgs a, int64_t k) {
+    if (*(volatile int32_t*)&a.g->done) return;
+    round_bookkeeping(a, k);
 }
 
 // ------------------------------------------------------------------ final plan
@@ -930,13 +939,16 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     int64_t p2 = 1;
     while (p2 < a.D) p2 <<= 1;
     const size_t sort_lds = sizeof(unsigned long long) * p2;
+    const size_t emit_lds = emit_lds_bytes(a.D);
     StreamGlobal hg{};
     for (int64_t k0 = 0; k0 < a.max_rounds; k0 += kRoundsPerCheck) {
         const int64_t k1 = std::min<int64_t>(a.max_rounds, k0 + kRoundsPerCheck);
         for (int64_t k = k0; k < k1; ++k) {
             hipLaunchKernelGGL(stream_form_kernel, dim3(W), dim3(kSB), sort_lds, s, a, k);
             ODB_LAUNCHED();
-            hipLaunchKernelGGL(stream_emit_kernel, dim3(W), dim3(kSB), 0, s, a, k);
+            hipLaunchKernelGGL(stream_emit_kernel, dim3(W), dim3(kSE), emit_lds, s, a, k);
+            ODB_LAUNCHED();
+            hipLaunchKernelGGL(stream_round_kernel, dim3(1), dim3(kSE), 0, s, a, k);
             ODB_LAUNCHED();
         }
         ODB_TRY_HIP(hipMemcpyAsync(&hg, a.g, sizeof(hg), hipMemcpyDeviceToHost, s));

@@ -154,3 +154,49 @@ def test_stream_full_size():
     log("  stream collate sampled and properties equal")
     del sp, outs, toks
     torch.cuda.empty_cache()
+
+
+def test_stream_two_stream_schedule():
+    # the benchmark's streaming schedule: iteration i+1's odb_stream_plan on one stream
+    # beside iteration i's collate on another, two plan buffers, one set of outputs
+    import torch
+    import paper_2606_19989_amd as odb
+    import bench
+
+    from _parity import collate_properties, compare_collate_sampled
+
+    w = synth.WORKLOADS["text_w8x65536"].window()
+    lens = np.diff(w.tok_off)
+    N, W = len(lens), 8
+    perm = np.random.default_rng(75).permutation(N).astype(np.int32)
+    log(f"two-stream streaming schedule: N={N} W={W}")
+    ref = oracle.stream(w.tok_off, perm, W, 16384, buffer_size=1024, depth=1024, rate=np.full(W, 1024))
+    plan_stream, collate_stream = torch.cuda.Stream(), torch.cuda.Stream()
+    toks = synth.fill_tokens_torch(int(w.tok_off[-1]), "cuda")
+    win = odb.DeviceWindow(np.linspace(0, N, W + 1).astype(np.int64), torch.from_numpy(w.tok_off).cuda(), toks,
+                           None, 0)
+    d_perm = torch.from_numpy(perm).cuda()
+    sps = [odb.StreamPipeline(win, d_perm, 16384, buffer_size=1024, depth=1024, rate=np.full(W, 1024, np.int32))
+           for _ in range(2)]
+    for sp in sps:
+        sp.plan()
+        sp.collate()
+        sps[1].outputs = sps[0].outputs
+    torch.cuda.synchronize()
+    sps[0].outputs[0].fill_(-7)
+    sec, coll, _ = bench.pipelined_steps(sps, plan_stream, collate_stream, 5, plan=bench.stream_plan,
+                                         weights=bench.stream_weights)
+    assert len(coll) == 5 and sec > 0
+    S, E = ref.steps, ref.sinfo["emitted_views"]
+    for sp in sps:
+        odb.odb_collate_status(sp.ws)
+        assert sp.info["steps"] == S
+        assert np.array_equal(sp.slot_tile_off[:W * S + 1].cpu().numpy(), ref.slot_tile_off)
+        assert np.array_equal(sp.emit_order[:E].cpu().numpy(), ref.emit_order)
+        compare_row_records(w.tok_off, sp, ref.emit_order)
+    outs = tuple(o[:ref.padded_elems] for o in sps[0].outputs)
+    compare_collate_sampled(w, outs, ref)
+    collate_properties(outs, ref)
+    wt, st, ss = sps[0].loss_weights(oracle.WEIGHT_TOKEN_EXACT)
+    ewt, est, ess = ref.loss_weights(oracle.WEIGHT_TOKEN_EXACT)
+    assert np.array_equal(wt.cpu().numpy().view(np.int64), ewt.view(np.int64))

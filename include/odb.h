@@ -403,10 +403,12 @@ size_t odb_stream_workspace_size(const odb_window_t* w, int32_t depth, int64_t s
  *   d_left_views     [M] out: un-emitted views, per rank in increasing view index
  *   d_left_off       [W+1] out
  *   h_trace          [max_rounds] host out, or NULL: one record per round
- * Synchronises `stream` once per 32 rounds and at the end.  Returns ODB_E_CAPACITY if
+ * Rounds are enqueued in chunks, each as long as a lower bound on the rounds left (from
+ * the sampler cursors, the rates and, non-join, the quota; at least 8 after the first);
+ * the call synchronises `stream` once per chunk and at the end.  Returns ODB_E_CAPACITY if
  * slot_capacity < W * S (required_slot_capacity tells the size) or the iteration needs
  * more than max_rounds rounds, ODB_E_INVALID_DATA for a perm entry outside [0, N) or a
- * sample length < 1.
+ * sample length < 1 met among the views the iteration fetches.
  */
 int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int64_t budget,
                     const odb_stream_params_t* params, int64_t slot_capacity,

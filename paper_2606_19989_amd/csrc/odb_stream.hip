@@ -8,26 +8,33 @@
 // head to M = W * ceil(N / W) views (view m has identity perm[m mod N]); view m belongs
 // to rank m mod W, visited in increasing m.
 //
-// One protocol round k is three launches:
-//   stream_form_kernel   one block per rank: fetch up to rate[r] views under the depth
-//                        envelope |B_r| <= D; status (finished / not ready / ready); a ready
-//                        rank sorts its whole buffer by (length desc, view asc) in LDS and
-//                        chases the group starts of Sec. 2.2 (threshold carry, Eq. 1)
-//   stream_emit_kernel   one block per rank: every block reads all ranks' statuses (the
-//                        all_gather) and derives the same round kind and target T (Eq. 3
-//                        over the ready ranks); in an emit round each ready rank applies
-//                        Algorithm 1 (split in closed form, overflow by size rank) and
-//                        writes its T slot records, its emitted views and its new buffer
-//                        (the overflow); finished ranks (join) write IDLE slots
-//   stream_round_kernel  one block: the round's bookkeeping, the non-join quota cut
-//                        (Theorem 2) and termination.  A launch of its own rather than the
-//                        last emit block (picked by a ticket counter): the ticket needs a
-//                        device-scope fence in every block, an L2 write-back on this GPU,
-//                        which beside a running collate waits behind its write stream
-// Rounds are enqueued in chunks; the host reads the done flag once per chunk, and rounds
-// enqueued after the stop return at once.  A final pass turns the per-rank staging into
-// the window plan layout (rank-major slots, row and tile offsets), so odb_collate and
-// odb_loss_weights apply unchanged, and counts coverage.
+// One protocol round k takes the form of one launch and the emit of the next: launch j
+// (one block per rank) does, in order,
+//   booking of round j-2  the round's step sizes, the non-join quota cut (Theorem 2) and
+//                         termination.  Every block computes it the same way from what the
+//                         previous launch wrote (so every block knows whether to go on) and
+//                         block 0 stores it; no block waits for another
+//   emit of round j-1     every block reads all ranks' published fetch records (the
+//                         all_gather) and derives the same round kind and target T (Eq. 3
+//                         over the ready ranks); the rank commits its fetch, and in an emit
+//                         round applies Algorithm 1 (split in closed form, overflow by size
+//                         rank) and writes its T slot records, its emitted views and its new
+//                         buffer (the overflow); finished ranks (join) write IDLE slots
+//   form of round j       fetch up to rate[r] views under the depth envelope |B_r| <= D;
+//                         status (finished / not ready / ready); a ready rank sorts its whole
+//                         buffer by (length desc, view asc) and chases the group starts of
+//                         Sec. 2.2 (threshold carry, Eq. 1).  The form is kept apart (by
+//                         round parity) from the rank's committed state until the next
+//                         launch's emit phase commits it, so a form made after the round
+//                         that ends the iteration changes nothing
+// A grid-wide barrier between the phases would need a device-scope fence in every block,
+// an L2 write-back on this GPU, which beside a running collate waits behind its write
+// stream; the launch boundary is the barrier instead.  Rounds are enqueued in chunks sized
+// by a lower bound on the rounds left, each chunk closed by a one-block launch that books
+// its last round; the host reads the done flag once per chunk, and launches enqueued after
+// the stop return at once.  A final pass turns the per-rank staging into the window plan
+// layout (rank-major slots, row and tile offsets), so odb_collate and odb_loss_weights
+// apply unchanged, and counts coverage.
 #include <algorithm>
 #include <climits>
 #include <cmath>
@@ -40,12 +47,9 @@ namespace odb {
 
 namespace {
 
-constexpr int kSB = 1024;             // threads of the per-rank form blocks
-// threads of the per-rank emit blocks: at 512 (2 waves per SIMD) an emit block fits beside
-// a running collate (3 waves per SIMD), so a plan can run beside another plan's collate
-constexpr int kSE = 512;
-constexpr int kMaxDepth = 4096;       // largest outstanding-depth envelope (LDS sort)
-constexpr int kRoundsPerCheck = 32;   // rounds enqueued between two looks at the done flag
+constexpr int kST = 512;              // threads of a round block (one block per rank)
+constexpr int kMaxDepth = 4096;       // largest outstanding-depth envelope
+constexpr int64_t kMinChunk = 8;      // fewest rounds enqueued after an estimate fell short
 
 struct StreamGlobal {
     int64_t steps;       // aligned steps so far (after quota cuts)
@@ -64,23 +68,33 @@ struct StreamGlobal {
     int32_t cap_overflow;
 };
 
+// A rank's committed state, written by the emit phase of every round that runs.
 struct RankStream {
     int64_t cursor;    // sampler position of the next fetch
-    int64_t buf_n;     // |B_r| (rewritten by the emit kernel of the rank's own block)
-    int64_t pub_n;     // |B_r| as published for this round's all_gather (form kernel only)
+    int64_t buf_n;     // |B_r|
     int64_t emitted;   // views written to the rank's emit stream (before a final quota cut)
-    int64_t tok;       // tokens in the buffer when it was grouped
+    int64_t pad;
+};
+
+// A rank's fetch and grouping for one round (kept by round parity until committed).
+struct RankForm {
+    int64_t cursor;    // sampler position after the fetch
+    int64_t n;         // |B_r| after the fetch, as published for the round's all_gather
+    int64_t tok;       // tokens in the buffer (ready ranks)
     int32_t status;    // -1 finished, 0 not ready, G_r > 0 ready with G_r groups
-    int32_t pad;
+    int32_t err;       // data errors met by the fetch (raised when it is committed)
 };
 
 struct StreamRec {
-    int32_t kind;      // 0 emit, 1 skip, 2 stop
-    int32_t changed;   // an emit round in which some ready rank had G_r != T
+    int32_t kind;          // 0 emit, 1 skip, 2 stop
+    int32_t changed;       // an emit round in which some ready rank had G_r != T
+    int32_t booked;        // booked by the launch that closes a chunk
     int32_t pad;
-    int64_t target;    // T (emit rounds)
-    int64_t emitted;   // views emitted in the round (after a quota cut)
-    int64_t cut;       // steps kept (emit rounds); stop reason (stop rounds)
+    int64_t target;        // T (emit rounds)
+    int64_t emitted;       // views emitted in the round (after a quota cut)
+    int64_t cut;           // steps kept (emit rounds); stop reason (stop rounds)
+    int64_t cum_steps;     // steps after the round
+    int64_t cum_emitted;   // views emitted after the round
 };
 
 enum : int32_t { kSErrIdentity = 1, kSErrLength = 2, kSErrInternal = 4, kSErrRounds = 8 };
@@ -101,9 +115,10 @@ struct StreamArgs {
     const int32_t* rate;   // [W]
     const int64_t* cap;    // [W] or null
     StreamGlobal* g;
-    RankStream* ranks;
+    RankStream* ranks;     // [W]
+    RankForm* form;        // [2 * W], round parity major
     StreamRec* rec;
-    int64_t* stepsum;      // [D]
+    int64_t* stepsum;      // [3 * D], round mod 3 major
     int32_t* bufv;         // [W * D]
     int32_t* sv;           // [W * D] sorted views
     int32_t* slen;         // [W * D] their lengths
@@ -116,8 +131,20 @@ struct StreamArgs {
     int32_t* evw;          // [W * q] emit streams
 };
 
-// Dynamic LDS of stream_emit_kernel for depth D: gtok (8 B) and gsl, as, ae, cum (4 B).
-inline size_t emit_lds_bytes(int64_t D) { return (size_t)(8 * D + 4 * (4 * D + 2)); }
+// Sort keys of the form phase: the buffer is padded to P = KPT * kST keys, P >= D.
+inline int sort_kpt(int64_t D) {
+    int64_t p = kST;
+    while (p < D) p <<= 1;
+    return (int)(p / kST);
+}
+
+// Dynamic LDS of a round launch: the emit tables for depth D (gtok 8 B; gsl, as, ae,
+// cum 4 B) and the form's keys (8 B), sorted lengths and next-start links (4 B) share it.
+inline size_t round_lds_bytes(int64_t D) {
+    const size_t emit = (size_t)(8 * D + 4 * (4 * D + 2));
+    const size_t form = (size_t)16 * kST * sort_kpt(D);
+    return emit > form ? emit : form;
+}
 
 __device__ __forceinline__ int32_t view_identity(const StreamArgs& a, int64_t m) {
     return a.perm[m < a.N ? m : m % a.N];
@@ -132,6 +159,22 @@ __device__ __forceinline__ T sblock_sum(T v) {
     __syncthreads();
     T t = 0;
     for (int i = 0; i < NT / kWave; ++i) t += wt[i];
+    __syncthreads();
+    return t;
+}
+
+// Maximum of one non-negative value per thread over an NT-thread block.
+template <int NT>
+__device__ __forceinline__ int64_t sblock_max(int64_t v) {
+    __shared__ int64_t wt[NT / kWave];
+    for (int d = kWave / 2; d > 0; d >>= 1) {
+        const int64_t o = __shfl_xor(v, d, kWave);
+        v = o > v ? o : v;
+    }
+    if ((threadIdx.x & (kWave - 1)) == 0) wt[threadIdx.x / kWave] = v;
+    __syncthreads();
+    int64_t t = 0;
+    for (int i = 0; i < NT / kWave; ++i) t = wt[i] > t ? wt[i] : t;
     __syncthreads();
     return t;
 }
@@ -159,138 +202,100 @@ __global__ void stream_init_kernel(StreamArgs a, int64_t rounds_cap) {
     const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i0 == 0) *a.g = StreamGlobal{};
     for (int64_t i = i0; i < a.W; i += stride) a.ranks[i] = RankStream{};
+    for (int64_t i = i0; i < 2 * a.W; i += stride) a.form[i] = RankForm{};
     for (int64_t i = i0; i < rounds_cap; i += stride) a.rec[i] = StreamRec{};
-    for (int64_t i = i0; i < a.D; i += stride) a.stepsum[i] = 0;
+    for (int64_t i = i0; i < 3 * a.D; i += stride) a.stepsum[i] = 0;
 }
 
-// ------------------------------------------------------------------ round: fetch + form
-__global__ void __launch_bounds__(kSB) stream_form_kernel(StreamArgs a, int64_t k) {
-    if (*(volatile int32_t*)&a.g->done) return;
-    const int r = blockIdx.x;
-    RankStream* R = a.ranks + r;
-    extern __shared__ unsigned long long keys[];   // next power of two >= D entries
-    __shared__ int64_t s_cursor, s_n, s_f;
-    __shared__ int32_t s_err;
-    if (threadIdx.x == 0) {
-        const int64_t cursor = R->cursor, n = R->buf_n;
-        int64_t f = a.rate[r];
-        f = f < a.D - n ? f : a.D - n;
-        f = f < a.q - cursor ? f : a.q - cursor;
-        s_cursor = cursor;
-        s_n = n;
-        s_f = f > 0 ? f : 0;
-        s_err = 0;
-    }
-    __syncthreads();
-    const int64_t cursor = s_cursor, n0 = s_n, f = s_f;
-    int32_t* buf = a.bufv + (int64_t)r * a.D;
-    for (int64_t i = threadIdx.x; i < f; i += kSB) buf[n0 + i] = (int32_t)((cursor + i) * a.W + r);
-    const int64_t n = n0 + f;
-    const bool drained = cursor + f == a.q;
-    const bool finished = drained && n == 0;
-    const bool ready = !finished && (n >= a.bufsize || drained);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        R->cursor = cursor + f;
-        R->buf_n = n;
-        R->pub_n = n;
-        atomicMax(&a.g->max_outstanding, (unsigned long long)n);
-        if (!ready) R->status = finished ? -1 : 0;
-    }
-    if (!ready) return;
-    // sort the buffer: key = (INT32_MAX - l) << 32 | m, ascending = (length desc, view asc)
-    int64_t p2 = 1;
-    while (p2 < n) p2 <<= 1;
-    int64_t tok = 0;
-    for (int64_t i = threadIdx.x; i < p2; i += kSB) {
-        unsigned long long key = ~0ull;
-        if (i < n) {
-            const int64_t m = buf[i];
-            const int32_t id = view_identity(a, m);
-            int64_t l = 1;
-            if (id < 0 || id >= a.N) {
-                atomicOr(&s_err, kSErrIdentity);
-            } else {
-                l = a.tok_off[id + 1] - a.tok_off[id];
-                if (l < 1 || l > 0x7FFFFFFF) {
-                    atomicOr(&s_err, kSErrLength);
-                    l = 1;
-                }
-            }
-            tok += l;
-            key = ((unsigned long long)(0x7FFFFFFFll - l) << 32) | (unsigned long long)(uint32_t)m;
+// ------------------------------------------------------------------ round: bookkeeping
+struct Booked {
+    bool done;        // the iteration ends with this round
+    int64_t steps;    // aligned steps after the round
+};
+
+// Round k's bookkeeping from what the launches before wrote: every block of a launch
+// reaches the same result; `writer` stores it.
+__device__ Booked book_round(const StreamArgs& a, int64_t k, bool writer) {
+    StreamRec* rec = a.rec + k;
+    if (rec->booked) return Booked{false, rec->cum_steps};   // done was seen at launch start
+    StreamGlobal* g = a.g;
+    const int kind = rec->kind;
+    const int64_t prev_steps = k > 0 ? a.rec[k - 1].cum_steps : 0;
+    const int64_t prev_emitted = k > 0 ? a.rec[k - 1].cum_emitted : 0;
+    const bool last = k + 1 >= a.max_rounds;
+    if (kind == 2) {
+        if (writer && threadIdx.x == 0) {
+            g->stop = (int32_t)rec->cut;
+            g->done = 1;
+            g->rounds = k + 1;
         }
-        keys[i] = key;
+        return Booked{true, prev_steps};
     }
-    tok = sblock_sum<kSB>(tok);   // also a barrier for keys[]
-    if (p2 <= kSB) {
-        // one key per thread: exchanges with a partner less than a wave away are lane
-        // shuffles, only the longer strides go through LDS (10 of 55 stages at 1024)
-        const int i = threadIdx.x;
-        const bool in = i < p2;
-        unsigned long long x = in ? keys[i] : ~0ull;
-        for (int size = 2; size <= (int)p2; size <<= 1) {
-            for (int stride = size >> 1; stride > 0; stride >>= 1) {
-                unsigned long long y;
-                if (stride >= kWave) {
-                    __syncthreads();
-                    if (in) keys[i] = x;
-                    __syncthreads();
-                    y = in ? keys[i ^ stride] : x;
-                } else {
-                    y = __shfl_xor(x, stride, kWave);
-                }
-                const bool keep_min = ((i & stride) == 0) == ((i & size) == 0);
-                x = keep_min ? (x < y ? x : y) : (x < y ? y : x);
+    if (kind == 1) {
+        if (writer && threadIdx.x == 0) {
+            rec->cum_steps = prev_steps;
+            rec->cum_emitted = prev_emitted;
+            g->skip_rounds += 1;
+            g->rounds = k + 1;
+            if (last) {
+                atomicOr(&g->err, kSErrRounds);
+                g->done = 1;
             }
+        }
+        return Booked{last, prev_steps};
+    }
+    // emit round: cumulative step sizes, the quota cut (non-join), per-round totals
+    const int64_t T = rec->target;
+    const bool nonjoin = a.mode == ODB_MODE_NONJOIN_QUOTA;
+    if (!writer && !nonjoin) return Booked{last, prev_steps + T};
+    const int64_t* ss = a.stepsum + (k % 3) * a.D;
+    __shared__ int64_t s_cut;
+    if (threadIdx.x == 0) s_cut = T;
+    __syncthreads();
+    if (nonjoin) {
+        // every step holds at least one row, so the running total crosses Q at most once
+        int64_t carry = 0;
+        for (int64_t b = 0; b < T; b += kST) {
+            const int64_t j = b + threadIdx.x;
+            const int64_t v = j < T ? ss[j] : 0;
+            int64_t tot;
+            const int64_t ex = sblock_excl<kST>(v, &tot);
+            if (j < T && prev_emitted + carry + ex < a.quota && prev_emitted + carry + ex + v >= a.quota)
+                s_cut = j + 1;
+            carry += tot;
         }
         __syncthreads();
-        if (in) keys[i] = x;
-        __syncthreads();
-    } else {
-        for (int64_t size = 2; size <= p2; size <<= 1) {
-            for (int64_t stride = size >> 1; stride > 0; stride >>= 1) {
-                for (int64_t t = threadIdx.x; t < (p2 >> 1); t += kSB) {
-                    const int64_t lo = 2 * t - (t & (stride - 1));
-                    const int64_t hi = lo + stride;
-                    const bool up = (lo & size) == 0;
-                    const unsigned long long x = keys[lo], y = keys[hi];
-                    if ((x > y) == up) {
-                        keys[lo] = y;
-                        keys[hi] = x;
-                    }
-                }
-                __syncthreads();
-            }
+    }
+    const int64_t cut = s_cut;
+    int64_t kept = 0, mx = 0;
+    for (int64_t j = threadIdx.x; j < cut; j += kST) {
+        const int64_t v = ss[j];
+        kept += v;
+        mx = v > mx ? v : mx;
+    }
+    kept = sblock_sum<kST>(kept);
+    mx = sblock_max<kST>(mx);
+    const bool done = cut < T || (nonjoin && prev_emitted + kept >= a.quota) || last;
+    if (writer && threadIdx.x == 0) {
+        rec->emitted = kept;
+        rec->cut = cut;
+        rec->cum_steps = prev_steps + cut;
+        rec->cum_emitted = prev_emitted + kept;
+        g->steps = prev_steps + cut;
+        g->emitted = prev_emitted + kept;
+        g->max_step = mx > g->max_step ? mx : g->max_step;
+        g->emit_rounds += 1;
+        g->second_gather += rec->changed ? 1 : 0;
+        g->rounds = k + 1;
+        if (cut < T || (nonjoin && prev_emitted + kept >= a.quota)) {
+            g->stop = ODB_STOP_QUOTA;
+            g->done = 1;
+        } else if (last) {
+            atomicOr(&g->err, kSErrRounds);
+            g->done = 1;
         }
     }
-    int32_t* sv = a.sv + (int64_t)r * a.D;
-    int32_t* sl = a.slen + (int64_t)r * a.D;
-    for (int64_t i = threadIdx.x; i < n; i += kSB) {
-        const unsigned long long key = keys[i];
-        sv[i] = (int32_t)(key & 0xFFFFFFFFull);
-        sl[i] = (int32_t)(0x7FFFFFFFll - (int64_t)(key >> 32));
-    }
-    if (threadIdx.x == 0) {
-        // Sec. 2.2: the group starting at p holds B(l) samples, l = the length just before
-        // p (the shortest of the previous group); the first group is a singleton
-        int32_t* gs = a.gs + (int64_t)r * (a.D + 1);
-        int64_t p = 0, g = 0;
-        while (p < n) {
-            gs[g++] = (int32_t)p;
-            if (p == 0) {
-                p = 1;
-            } else {
-                const int32_t l = (int32_t)(0x7FFFFFFFll - (int64_t)(keys[p - 1] >> 32));
-                const int64_t nx = p + batch_size(a.budget, l);
-                p = nx < n ? nx : n;
-            }
-        }
-        gs[g] = (int32_t)n;
-        R->status = (int32_t)g;
-        R->tok = tok;
-        if (s_err) atomicOr(&a.g->err, s_err);
-    }
+    return Booked{done, prev_steps + cut};
 }
 
 // ------------------------------------------------------------------ round: align + emit
@@ -300,8 +305,9 @@ struct RoundView {
     int32_t stop;
 };
 
-// The all_gather: every block reduces the same W statuses the same way.
-__device__ RoundView decide_round(const StreamArgs& a) {
+// The all_gather: every block reduces the same W published fetch records the same way.
+__device__ RoundView decide_round(const StreamArgs& a, int64_t k) {
+    const RankForm* F = a.form + (k & 1) * a.W;
     __shared__ int64_t s_fin, s_unready, s_maxG, s_minS, s_minC;
     if (threadIdx.x == 0) {
         s_fin = 0;
@@ -311,15 +317,15 @@ __device__ RoundView decide_round(const StreamArgs& a) {
         s_minC = LLONG_MAX;
     }
     __syncthreads();
-    for (int r = threadIdx.x; r < a.W; r += kSE) {
-        const RankStream R = a.ranks[r];
-        if (R.status < 0) {
+    for (int r = threadIdx.x; r < a.W; r += kST) {
+        const int32_t st = F[r].status;
+        if (st < 0) {
             atomicAdd((unsigned long long*)&s_fin, 1ull);
-        } else if (R.status == 0) {
+        } else if (st == 0) {
             atomicAdd((unsigned long long*)&s_unready, 1ull);
         } else {
-            atomicMax((long long*)&s_maxG, (long long)R.status);
-            atomicMin((long long*)&s_minS, (long long)R.pub_n);
+            atomicMax((long long*)&s_maxG, (long long)st);
+            atomicMin((long long*)&s_minS, (long long)F[r].n);
             if (a.cap && a.cap[r] > 0) atomicMin((long long*)&s_minC, (long long)a.cap[r]);
         }
     }
@@ -342,23 +348,33 @@ __device__ RoundView decide_round(const StreamArgs& a) {
     return v;
 }
 
-__device__ void round_bookkeeping(const StreamArgs& a, int64_t k);
-
-__device__ void emit_round(const StreamArgs& a, int64_t k) {
-    const RoundView v = decide_round(a);
+// Round k's emit phase for rank r = blockIdx.x; `base` is the number of aligned steps
+// before the round.  Commits the rank's fetch and returns the round kind; *s_cursor and
+// *s_bufn receive the rank's committed state (after a __syncthreads of the caller).
+__device__ int emit_phase(const StreamArgs& a, int64_t k, int64_t base, unsigned char* lds, int64_t* s_cursor,
+                          int64_t* s_bufn) {
+    const RoundView v = decide_round(a, k);
+    const int r = blockIdx.x;
+    RankStream* R = a.ranks + r;
+    const RankForm Fr = a.form[(k & 1) * a.W + r];
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         a.rec[k].kind = v.kind;
         a.rec[k].target = v.T;
         a.rec[k].cut = v.kind == 2 ? v.stop : 0;
     }
-    if (v.kind != 0) return;
-    const int r = blockIdx.x;
-    RankStream* R = a.ranks + r;
+    if (threadIdx.x == 0) {
+        R->cursor = Fr.cursor;
+        R->buf_n = Fr.n;
+        atomicMax(&a.g->max_outstanding, (unsigned long long)Fr.n);
+        if (Fr.err) atomicOr(&a.g->err, Fr.err);
+        *s_cursor = Fr.cursor;
+        *s_bufn = Fr.n;
+    }
+    if (v.kind != 0) return v.kind;
     const int64_t T = v.T;
-    const int64_t base = a.g->steps;   // written by the previous round's bookkeeping only
-    const int32_t st = R->status;
+    const int32_t st = Fr.status;
     if (st < 0) {   // finished rank in join mode: IDLE slots
-        for (int64_t j = threadIdx.x; j < T; j += kSE) {
+        for (int64_t j = threadIdx.x; j < T; j += kST) {
             const int64_t x = base + j;
             if (x < a.scap) {
                 const int64_t o = (int64_t)r * a.scap + x;
@@ -370,29 +386,26 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
                 a.g->cap_overflow = 1;
             }
         }
-        return;
+        return 0;
     }
     // st > 0: a ready rank with G groups over n sorted positions
     const int64_t G = st;
-    const int64_t n = R->pub_n;
+    const int64_t n = Fr.n;
     const int32_t* gsg = a.gs + (int64_t)r * (a.D + 1);
     const int32_t* sv = a.sv + (int64_t)r * a.D;
     const int32_t* sl = a.slen + (int64_t)r * a.D;
     int32_t* apos = a.apos + (int64_t)r * a.D;
-    // per-rank tables of up to D groups in dynamic LDS (emit_lds_bytes(D) bytes): sized by
-    // the depth envelope rather than its maximum, the block stays small enough to run
-    // beside another kernel (a static 96 KB also made the compiler reserve 169 registers
-    // per lane, since that much LDS already capped the occupancy)
-    extern __shared__ unsigned long long s_dyn[];
-    unsigned long long* gtok = s_dyn;
-    int32_t* gsl = reinterpret_cast<int32_t*>(s_dyn + a.D);
+    // per-rank tables of up to D groups, sized by the depth envelope rather than its
+    // maximum so that the block stays small enough to run beside another kernel
+    unsigned long long* gtok = reinterpret_cast<unsigned long long*>(lds);
+    int32_t* gsl = reinterpret_cast<int32_t*>(gtok + a.D);
     int32_t* as = gsl + (a.D + 1);
     int32_t* ae = as + a.D;
     int32_t* cum = ae + a.D;
     __shared__ int64_t s_X, s_jstar;
     __shared__ int32_t s_ret, s_bad;
-    for (int64_t i = threadIdx.x; i <= G; i += kSE) gsl[i] = gsg[i];
-    for (int64_t i = threadIdx.x; i < T; i += kSE) gtok[i] = 0;
+    for (int64_t i = threadIdx.x; i <= G; i += kST) gsl[i] = gsg[i];
+    for (int64_t i = threadIdx.x; i < T; i += kST) gtok[i] = 0;
     if (threadIdx.x == 0) {
         s_ret = 0;
         s_bad = 0;
@@ -423,7 +436,7 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
         }
         __syncthreads();
         const int64_t X = s_X, js = s_jstar;
-        for (int64_t t = threadIdx.x; t < T; t += kSE) {
+        for (int64_t t = threadIdx.x; t < T; t += kST) {
             if (t < X) {
                 as[t] = (int32_t)t;
                 ae[t] = (int32_t)(t + 1);
@@ -437,7 +450,7 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
             }
         }
         __syncthreads();
-        for (int64_t p = threadIdx.x; p < n; p += kSE) {
+        for (int64_t p = threadIdx.x; p < n; p += kST) {
             int64_t ap;
             if (p < X) {
                 ap = p;
@@ -456,7 +469,7 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
         }
     } else if (G > T) {
         // overflow: keep the T groups first by (size desc, formation index desc)
-        for (int64_t g = threadIdx.x; g < G; g += kSE) {
+        for (int64_t g = threadIdx.x; g < G; g += kST) {
             const int32_t cg = gsl[g + 1] - gsl[g];
             int64_t rank = 0;
             for (int64_t h = 0; h < G; ++h) {
@@ -467,11 +480,11 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
         }
         __syncthreads();
         int64_t carry = 0;
-        for (int64_t b = 0; b < G; b += kSE) {
+        for (int64_t b = 0; b < G; b += kST) {
             const int64_t g = b + threadIdx.x;
             const int32_t f = g < G ? cum[g] : 0;
             int32_t tot;
-            const int32_t ex = sblock_excl<kSE>(f, &tot);
+            const int32_t ex = sblock_excl<kST>(f, &tot);
             if (g < G && f) {
                 const int64_t ki = carry + ex;
                 as[ki] = gsl[g];
@@ -481,43 +494,44 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
         }
         __syncthreads();
         if (threadIdx.x == 0 && carry != T) s_bad = 1;
-        for (int64_t p = threadIdx.x; p < n; p += kSE) apos[p] = -1;
+        for (int64_t p = threadIdx.x; p < n; p += kST) apos[p] = -1;
         __syncthreads();
-        for (int64_t t = threadIdx.x; t < T; t += kSE)
+        for (int64_t t = threadIdx.x; t < T; t += kST)
             for (int64_t p = as[t]; p < ae[t]; ++p) apos[p] = (int32_t)t;
     } else {
-        for (int64_t t = threadIdx.x; t < T; t += kSE) {
+        for (int64_t t = threadIdx.x; t < T; t += kST) {
             as[t] = gsl[t];
             ae[t] = gsl[t + 1];
         }
         __syncthreads();
-        for (int64_t t = threadIdx.x; t < T; t += kSE)
+        for (int64_t t = threadIdx.x; t < T; t += kST)
             for (int64_t p = as[t]; p < ae[t]; ++p) apos[p] = (int32_t)t;
     }
     __syncthreads();
     // rows prefix over the adjusted groups, tokens per adjusted group
     {
         int64_t carry = 0;
-        for (int64_t b = 0; b < T; b += kSE) {
+        for (int64_t b = 0; b < T; b += kST) {
             const int64_t t = b + threadIdx.x;
             const int32_t rows = t < T ? ae[t] - as[t] : 0;
             int32_t tot;
-            const int32_t ex = sblock_excl<kSE>(rows, &tot);
+            const int32_t ex = sblock_excl<kST>(rows, &tot);
             if (t < T) cum[t] = (int32_t)(carry + ex);
             carry += tot;
         }
         if (threadIdx.x == 0) cum[T] = (int32_t)carry;
     }
-    for (int64_t p = threadIdx.x; p < n; p += kSE) {
+    for (int64_t p = threadIdx.x; p < n; p += kST) {
         const int32_t t = apos[p];
         if (t >= 0) atomicAdd(&gtok[t], (unsigned long long)sl[p]);
     }
     __syncthreads();
     const int64_t E = cum[T];
     const int64_t ebase = R->emitted;
-    const double mean = (double)R->tok / (double)n;
+    const double mean = (double)Fr.tok / (double)n;
+    int64_t* stepsum = a.stepsum + (k % 3) * a.D;
     // slot records: step j of the round is adjusted group T-1-j (short to long)
-    for (int64_t t = threadIdx.x; t < T; t += kSE) {
+    for (int64_t t = threadIdx.x; t < T; t += kST) {
         const int64_t j = T - 1 - t;
         const int64_t x = base + j;
         const int32_t rows = ae[t] - as[t];
@@ -530,13 +544,13 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
         } else {
             a.g->cap_overflow = 1;
         }
-        atomicAdd((unsigned long long*)&a.stepsum[j], (unsigned long long)rows);
+        atomicAdd((unsigned long long*)&stepsum[j], (unsigned long long)rows);
     }
     // emitted views (rows of a group run from its last position to its first) and the
     // new buffer (overflow returns)
     int32_t* ev = a.evw + (int64_t)r * a.q;
     int32_t* buf = a.bufv + (int64_t)r * a.D;
-    for (int64_t p = threadIdx.x; p < n; p += kSE) {
+    for (int64_t p = threadIdx.x; p < n; p += kST) {
         const int32_t t = apos[p];
         if (t >= 0) {
             const int64_t e = ebase + E - cum[t + 1] + (ae[t] - 1 - p);
@@ -549,101 +563,193 @@ __device__ void emit_round(const StreamArgs& a, int64_t k) {
     if (threadIdx.x == 0) {
         R->emitted = ebase + E;
         R->buf_n = s_ret;
+        *s_bufn = s_ret;
         if (E + s_ret != n) s_bad = 1;
         if (G < T) atomicAdd((unsigned long long*)&a.g->splits, (unsigned long long)(T - G));
         if (G > T) atomicAdd((unsigned long long*)&a.g->overflow, (unsigned long long)(G - T));
         if (G != T) atomicOr(&a.rec[k].changed, 1);
         if (s_bad) atomicOr(&a.g->err, kSErrInternal);
     }
+    return 0;
 }
 
-// ------------------------------------------------------------------ round: bookkeeping
-// Round bookkeeping, run by the last block of the round's emit kernel.
-__device__ void round_bookkeeping(const StreamArgs& a, int64_t k) {
-    StreamGlobal* g = a.g;
-    StreamRec* rec = a.rec + k;
-    const int kind = rec->kind;
-    if (kind == 2) {
-        if (threadIdx.x == 0) {
-            g->stop = (int32_t)rec->cut;
-            g->done = 1;
-            g->rounds = k + 1;
-        }
-        return;
-    }
-    if (kind == 1) {
-        if (threadIdx.x == 0) {
-            g->skip_rounds += 1;
-            g->rounds = k + 1;
-            if (k + 1 >= a.max_rounds) {
-                g->err |= kSErrRounds;
-                g->done = 1;
+// ------------------------------------------------------------------ round: fetch + form
+// One bitonic compare-exchange stage between a thread's own keys, CS slots apart.
+template <int KPT, int CS>
+__device__ __forceinline__ void sort_stage_regs(unsigned long long (&x)[KPT], int size) {
+    if constexpr (CS < KPT) {
+#pragma unroll
+        for (int c = 0; c < KPT; ++c) {
+            if ((c & CS) == 0) {
+                const bool up = ((threadIdx.x + c * kST) & size) == 0;
+                const unsigned long long lo = x[c], hi = x[c + CS];
+                const bool swap = (lo > hi) == up;
+                x[c] = swap ? hi : lo;
+                x[c + CS] = swap ? lo : hi;
             }
         }
+    }
+}
+
+// Round j's fetch and grouping for rank r = blockIdx.x from its committed cursor and
+// buffer size n0.  The buffer is sorted as P = KPT * kST keys, slot c of thread t
+// holding position t + c * kST: partners a wave or more apart but in another thread
+// exchange through LDS, partners less than a wave apart by lane shuffles, partners in
+// the same thread in registers.
+template <int KPT>
+__device__ void form_phase(const StreamArgs& a, int64_t j, int64_t cursor, int64_t n0, unsigned char* lds) {
+    constexpr int P = KPT * kST;
+    const int r = blockIdx.x;
+    RankForm* F = a.form + (j & 1) * a.W + r;
+    int64_t f = a.rate[r];
+    f = f < a.D - n0 ? f : a.D - n0;
+    f = f < a.q - cursor ? f : a.q - cursor;
+    f = f > 0 ? f : 0;
+    // the fetched views join the buffer (a ready rank keeps them there when another rank
+    // is not ready and the round is a skip round)
+    int32_t* buf = a.bufv + (int64_t)r * a.D;
+    for (int64_t i = threadIdx.x; i < f; i += kST) buf[n0 + i] = (int32_t)((cursor + i) * a.W + r);
+    const int64_t n = n0 + f;
+    const bool drained = cursor + f == a.q;
+    const bool finished = drained && n == 0;
+    const bool ready = !finished && (n >= a.bufsize || drained);
+    if (!ready) {
+        if (threadIdx.x == 0) *F = RankForm{cursor + f, n, 0, finished ? -1 : 0, 0};
         return;
     }
-    // emit round: cumulative step sizes, the quota cut (non-join), per-round totals
-    const int64_t T = rec->target;
-    const int64_t before = g->emitted;
-    __shared__ int64_t s_cut;
-    if (threadIdx.x == 0) s_cut = T;
+    unsigned long long* keys = reinterpret_cast<unsigned long long*>(lds);   // [P]
+    int32_t* len = reinterpret_cast<int32_t*>(keys + P);                      // [P]
+    int32_t* nxt = len + P;                                                   // [P]
+    __shared__ int32_t s_err;
+    if (threadIdx.x == 0) s_err = 0;
     __syncthreads();
-    int64_t carry = 0, mx = 0, kept = 0;
-    for (int64_t b = 0; b < T; b += kSE) {
-        const int64_t j = b + threadIdx.x;
-        const int64_t v = j < T ? a.stepsum[j] : 0;
-        int64_t tot;
-        const int64_t ex = sblock_excl<kSE>(v, &tot);
-        if (a.mode == ODB_MODE_NONJOIN_QUOTA && j < T && before + carry + ex < a.quota &&
-            before + carry + ex + v >= a.quota)
-            s_cut = j + 1;
-        __syncthreads();
-        carry += tot;
-    }
-    const int64_t cut = s_cut;
-    for (int64_t j = threadIdx.x; j < T; j += kSE) {
-        const int64_t v = a.stepsum[j];
-        if (j < cut) {
-            mx = v > mx ? v : mx;
-            kept += v;
+    // key = (INT32_MAX - l) << 32 | m, ascending = (length desc, view asc); views the
+    // rank held before the fetch are read back, fetched ones follow from the cursor
+    unsigned long long x[KPT];
+    int64_t tok = 0;
+#pragma unroll
+    for (int c = 0; c < KPT; ++c) {
+        const int64_t i = threadIdx.x + c * kST;
+        unsigned long long key = ~0ull;
+        if (i < n) {
+            const int64_t m = i < n0 ? (int64_t)buf[i] : (cursor + (i - n0)) * a.W + r;
+            const int32_t id = view_identity(a, m);
+            int64_t l = 1;
+            if (id < 0 || id >= a.N) {
+                atomicOr(&s_err, kSErrIdentity);
+            } else {
+                l = a.tok_off[id + 1] - a.tok_off[id];
+                if (l < 1 || l > 0x7FFFFFFF) {
+                    atomicOr(&s_err, kSErrLength);
+                    l = 1;
+                }
+            }
+            tok += l;
+            key = ((unsigned long long)(0x7FFFFFFFll - l) << 32) | (unsigned long long)(uint32_t)m;
         }
-        a.stepsum[j] = 0;
+        x[c] = key;
     }
-    __shared__ int64_t wm[kSE / kWave];
-    for (int d = kWave / 2; d > 0; d >>= 1) {
-        const int64_t o = __shfl_xor(mx, d, kWave);
-        mx = o > mx ? o : mx;
+    tok = sblock_sum<kST>(tok);
+    for (int size = 2; size <= P; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            if (stride >= kST) {
+                if (stride == kST) sort_stage_regs<KPT, 1>(x, size);
+                else if (stride == 2 * kST) sort_stage_regs<KPT, 2>(x, size);
+                else sort_stage_regs<KPT, 4>(x, size);
+                continue;
+            }
+            unsigned long long y[KPT];
+            if (stride >= kWave) {
+                __syncthreads();
+#pragma unroll
+                for (int c = 0; c < KPT; ++c) keys[threadIdx.x + c * kST] = x[c];
+                __syncthreads();
+#pragma unroll
+                for (int c = 0; c < KPT; ++c) y[c] = keys[(threadIdx.x ^ stride) + c * kST];
+            } else {
+#pragma unroll
+                for (int c = 0; c < KPT; ++c) y[c] = __shfl_xor(x[c], stride, kWave);
+            }
+#pragma unroll
+            for (int c = 0; c < KPT; ++c) {
+                const int i = threadIdx.x + c * kST;
+                const bool keep_min = ((i & stride) == 0) == ((i & size) == 0);
+                x[c] = keep_min ? (x[c] < y[c] ? x[c] : y[c]) : (x[c] < y[c] ? y[c] : x[c]);
+            }
+        }
     }
-    if ((threadIdx.x & (kWave - 1)) == 0) wm[threadIdx.x / kWave] = mx;
-    kept = sblock_sum<kSE>(kept);
+    int32_t* sv = a.sv + (int64_t)r * a.D;
+    int32_t* sl = a.slen + (int64_t)r * a.D;
+#pragma unroll
+    for (int c = 0; c < KPT; ++c) {
+        const int64_t i = threadIdx.x + c * kST;
+        if (i < n) {
+            const int32_t l = (int32_t)(0x7FFFFFFFll - (int64_t)(x[c] >> 32));
+            sv[i] = (int32_t)(x[c] & 0xFFFFFFFFull);
+            sl[i] = l;
+            len[i] = l;
+        }
+    }
+    __syncthreads();
+    // Sec. 2.2: the group starting at p holds B(l) samples, l = the length just before p
+    // (the shortest of the previous group); the first group is a singleton
+#pragma unroll
+    for (int c = 0; c < KPT; ++c) {
+        const int64_t i = threadIdx.x + c * kST;
+        if (i < n) {
+            const int64_t nx = i == 0 ? 1 : i + batch_size(a.budget, len[i - 1]);
+            nxt[i] = (int32_t)(nx < n ? nx : n);
+        }
+    }
+    __syncthreads();
     if (threadIdx.x == 0) {
-        for (int i = 0; i < kSE / kWave; ++i) mx = wm[i] > mx ? wm[i] : mx;
-        rec->emitted = kept;
-        rec->cut = cut;
-        g->steps += cut;
-        g->emitted = before + kept;
-        g->max_step = mx > g->max_step ? mx : g->max_step;
-        g->emit_rounds += 1;
-        g->second_gather += rec->changed ? 1 : 0;
-        g->rounds = k + 1;
-        if (cut < T || (a.mode == ODB_MODE_NONJOIN_QUOTA && before + kept >= a.quota)) {
-            g->stop = ODB_STOP_QUOTA;
-            g->done = 1;
-        } else if (k + 1 >= a.max_rounds) {
-            g->err |= kSErrRounds;
-            g->done = 1;
+        int32_t* gs = a.gs + (int64_t)r * (a.D + 1);
+        int64_t p = 0, g = 0;
+        while (p < n) {
+            gs[g++] = (int32_t)p;
+            p = nxt[p];
         }
+        gs[g] = (int32_t)n;
+        *F = RankForm{cursor + f, n, tok, (int32_t)g, s_err};
     }
 }
 
-__global__ void __launch_bounds__(kSE) stream_emit_kernel(StreamArgs a, int64_t k) {
+// Launch j: books round j-2, emits round j-1, forms round j (see the top of this file).
+template <int KPT>
+__global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t j) {
     if (*(volatile int32_t*)&a.g->done) return;
-    emit_round(a, k);
+    extern __shared__ unsigned long long s_dyn[];
+    unsigned char* lds = reinterpret_cast<unsigned char*>(s_dyn);
+    int64_t base = 0;
+    if (j >= 2) {
+        const Booked b = book_round(a, j - 2, blockIdx.x == 0);
+        if (b.done) return;
+        base = b.steps;
+    }
+    // the step sums of round j, added up by the next launch: last read when round j-3
+    // was booked
+    if (blockIdx.x == 0) {
+        int64_t* ss = a.stepsum + (j % 3) * a.D;
+        for (int64_t i = threadIdx.x; i < a.D; i += kST) ss[i] = 0;
+    }
+    __shared__ int64_t s_cursor, s_bufn;
+    int kind = 0;
+    if (j >= 1) {
+        kind = emit_phase(a, j - 1, base, lds, &s_cursor, &s_bufn);
+    } else if (threadIdx.x == 0) {
+        s_cursor = 0;
+        s_bufn = 0;
+    }
+    __syncthreads();
+    if (kind == 2) return;   // a stop round: the next launch's booking ends the iteration
+    form_phase<KPT>(a, j, s_cursor, s_bufn, lds);
 }
 
-__global__ void __launch_bounds__(kSE) stream_round_kernel(StreamArgs a, int64_t k) {
+// Books round k at the end of a chunk of launches, so that the host sees its outcome.
+__global__ void __launch_bounds__(kST) stream_book_kernel(StreamArgs a, int64_t k) {
     if (*(volatile int32_t*)&a.g->done) return;
-    round_bookkeeping(a, k);
+    book_round(a, k, true);
+    if (threadIdx.x == 0) a.rec[k].booked = 1;
 }
 
 // ------------------------------------------------------------------ final plan
@@ -783,7 +889,7 @@ __global__ void clear_totals_kernel(StreamTotals* t) {
 }
 
 struct StreamLayout {
-    size_t g, ranks, rec, stepsum, bufv, sv, slen, gs, apos, srows, smax, stok, sadj, evw, vcount, icount,
+    size_t g, ranks, form, rec, stepsum, bufv, sv, slen, gs, apos, srows, smax, stok, sadj, evw, vcount, icount,
         totals, partials, rate, cap, total;
 };
 
@@ -800,8 +906,9 @@ bool stream_layout(size_t at, int64_t W, int64_t N, int64_t D, int64_t scap, int
     };
     L->g = take(sizeof(StreamGlobal));
     L->ranks = take(sizeof(RankStream) * W);
+    L->form = take(sizeof(RankForm) * 2 * W);
     L->rec = take(sizeof(StreamRec) * rounds);
-    L->stepsum = take(8 * D);
+    L->stepsum = take(8 * 3 * D);
     L->bufv = take(4 * W * D);
     L->sv = take(4 * W * D);
     L->slen = take(4 * W * D);
@@ -820,6 +927,27 @@ bool stream_layout(size_t at, int64_t W, int64_t N, int64_t D, int64_t scap, int
     L->cap = take(8 * W);
     L->total = o;
     return true;
+}
+
+// A lower bound on the rounds still to run after the committed state `hr`: a rank fetches
+// at most rate[r] views a round, and its last fetch is followed by the round that finds
+// it finished (join: every rank; non-join: the first); a non-join quota needs at least
+// (Q - emitted) / (W * D) more rounds, since a round emits at most a full buffer per rank.
+int64_t stream_rounds_left(const StreamArgs& a, const int32_t* rate, const std::vector<RankStream>& hr,
+                           const StreamGlobal& hg, int64_t at_least) {
+    int64_t hi = 0, lo = LLONG_MAX;
+    for (int r = 0; r < a.W; ++r) {
+        const int64_t need = (a.q - hr[r].cursor + rate[r] - 1) / rate[r];
+        hi = std::max(hi, need);
+        lo = std::min(lo, need);
+    }
+    const bool nonjoin = a.mode == ODB_MODE_NONJOIN_QUOTA;
+    int64_t b = (nonjoin ? lo : hi) + 1;
+    if (nonjoin) {
+        const int64_t per = (int64_t)a.W * a.D;
+        b = std::min(b, std::max<int64_t>(1, (a.quota - hg.emitted + per - 1) / per));
+    }
+    return std::max(b, at_least);
 }
 
 int check_stream_params(const odb_window_t* w, const odb_stream_params_t* p, int64_t slot_capacity) {
@@ -916,6 +1044,7 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     a.cap = params->slot_capacity ? ws_at<int64_t>(d_ws, SL.cap) : nullptr;
     a.g = ws_at<StreamGlobal>(d_ws, SL.g);
     a.ranks = ws_at<RankStream>(d_ws, SL.ranks);
+    a.form = ws_at<RankForm>(d_ws, SL.form);
     a.rec = ws_at<StreamRec>(d_ws, SL.rec);
     a.stepsum = ws_at<int64_t>(d_ws, SL.stepsum);
     a.bufv = ws_at<int32_t>(d_ws, SL.bufv);
@@ -936,24 +1065,37 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     ODB_LAUNCHED();
 
     // rounds, in chunks, until the done flag is up
-    int64_t p2 = 1;
-    while (p2 < a.D) p2 <<= 1;
-    const size_t sort_lds = sizeof(unsigned long long) * p2;
-    const size_t emit_lds = emit_lds_bytes(a.D);
+    const int kpt = sort_kpt(a.D);
+    const size_t lds = round_lds_bytes(a.D);
+    auto launch_round = [&](int64_t j) {
+        switch (kpt) {
+            case 1: hipLaunchKernelGGL(stream_round_kernel<1>, dim3(W), dim3(kST), lds, s, a, j); break;
+            case 2: hipLaunchKernelGGL(stream_round_kernel<2>, dim3(W), dim3(kST), lds, s, a, j); break;
+            case 4: hipLaunchKernelGGL(stream_round_kernel<4>, dim3(W), dim3(kST), lds, s, a, j); break;
+            default: hipLaunchKernelGGL(stream_round_kernel<8>, dim3(W), dim3(kST), lds, s, a, j); break;
+        }
+    };
+    static_assert(kMaxDepth <= 8 * kST, "sort slots per thread");
     StreamGlobal hg{};
-    for (int64_t k0 = 0; k0 < a.max_rounds; k0 += kRoundsPerCheck) {
-        const int64_t k1 = std::min<int64_t>(a.max_rounds, k0 + kRoundsPerCheck);
-        for (int64_t k = k0; k < k1; ++k) {
-            hipLaunchKernelGGL(stream_form_kernel, dim3(W), dim3(kSB), sort_lds, s, a, k);
-            ODB_LAUNCHED();
-            hipLaunchKernelGGL(stream_emit_kernel, dim3(W), dim3(kSE), emit_lds, s, a, k);
-            ODB_LAUNCHED();
-            hipLaunchKernelGGL(stream_round_kernel, dim3(1), dim3(kSE), 0, s, a, k);
+    std::vector<RankStream> hr(W);   // committed state after the last booked round
+    launch_round(0);                  // round 0's form
+    ODB_LAUNCHED();
+    for (int64_t k0 = 0; k0 < a.max_rounds;) {
+        // rounds k0 .. k0+cnt-1: launch k+1 emits round k; the chunk's last round is then
+        // booked on its own
+        const int64_t cnt = std::min<int64_t>(a.max_rounds - k0, stream_rounds_left(a, params->rate, hr, hg,
+                                                                                    k0 == 0 ? 1 : kMinChunk));
+        for (int64_t k = k0; k < k0 + cnt; ++k) {
+            launch_round(k + 1);
             ODB_LAUNCHED();
         }
+        hipLaunchKernelGGL(stream_book_kernel, dim3(1), dim3(kST), 0, s, a, k0 + cnt - 1);
+        ODB_LAUNCHED();
         ODB_TRY_HIP(hipMemcpyAsync(&hg, a.g, sizeof(hg), hipMemcpyDeviceToHost, s));
+        ODB_TRY_HIP(hipMemcpyAsync(hr.data(), a.ranks, sizeof(RankStream) * W, hipMemcpyDeviceToHost, s));
         ODB_TRY_HIP(hipStreamSynchronize(s));
         if (hg.done) break;
+        k0 += cnt;
     }
     if (hg.err & kSErrIdentity) return set_error(ODB_E_INVALID_DATA, "perm holds a value outside [0, N)");
     if (hg.err & kSErrLength) return set_error(ODB_E_INVALID_DATA, "a sample has length < 1 or >= 2^31");
@@ -1017,7 +1159,6 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     ODB_LAUNCHED();
     StreamTotals ht{};
     int64_t padded = 0, nleft = 0;
-    std::vector<RankStream> hr(W);
     ODB_TRY_HIP(hipMemcpyAsync(&ht, tot, sizeof(ht), hipMemcpyDeviceToHost, s));
     ODB_TRY_HIP(hipMemcpyAsync(&padded, d_slot_tile_off + K, 8, hipMemcpyDeviceToHost, s));
     ODB_TRY_HIP(hipMemcpyAsync(hr.data(), a.ranks, sizeof(RankStream) * W, hipMemcpyDeviceToHost, s));

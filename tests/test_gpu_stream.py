@@ -21,7 +21,7 @@ def offsets(lens):
 
 
 def run_case(name, lens, perm, W, budget, buffer_size, depth, rate, mode="join", quota=0, cap=None, pad_id=0,
-             full_collate=True, tokens=None):
+             full_collate=True, tokens=None, max_rounds=None, device_perm=None):
     import torch
     import paper_2606_19989_amd as odb
 
@@ -36,9 +36,10 @@ def run_case(name, lens, perm, W, budget, buffer_size, depth, rate, mode="join",
     d_tok_off = torch.from_numpy(tok_off).cuda()
     toks = tokens if tokens is not None else synth.fill_tokens_torch(int(tok_off[-1]), "cuda")
     win = odb.DeviceWindow(rank_off, d_tok_off, toks, None, 0)
-    sp = odb.StreamPipeline(win, torch.from_numpy(np.asarray(perm, dtype=np.int32)).cuda(), budget,
+    dperm = perm if device_perm is None else device_perm
+    sp = odb.StreamPipeline(win, torch.from_numpy(np.asarray(dperm, dtype=np.int32)).cuda(), budget,
                             buffer_size=buffer_size, depth=depth, rate=rate, mode=mode, quota=quota, capacity=cap,
-                            pad_id=pad_id)
+                            pad_id=pad_id, max_rounds=max_rounds)
     info = sp.plan()
     torch.cuda.synchronize()
     for f in STREAM_INFO_EXACT:
@@ -117,6 +118,78 @@ def test_stream_random_small():
         cap = rng.integers(0, 6, size=W) if t % 4 == 1 else None
         run_case(f"random_{t}", lens, rng.permutation(N).astype(np.int32), W, int(rng.integers(1, 30000)), buf, depth,
                  rate, mode=mode, quota=int(rng.integers(1, N + 2)), cap=cap, pad_id=t % 5)
+
+
+def _stream_pipeline(lens, perm, W, budget, buffer_size, depth, rate, **kw):
+    import torch
+    import paper_2606_19989_amd as odb
+
+    tok_off = offsets(lens)
+    win = odb.DeviceWindow(np.linspace(0, len(lens), W + 1).astype(np.int64), torch.from_numpy(tok_off).cuda(),
+                           synth.fill_tokens_torch(int(tok_off[-1]), "cuda"), None, 0)
+    return odb.StreamPipeline(win, torch.from_numpy(np.asarray(perm, dtype=np.int32)).cuda(), budget,
+                              buffer_size=buffer_size, depth=depth, rate=np.asarray(rate, dtype=np.int32), **kw)
+
+
+@pytest.mark.parametrize("mode", ["join", "nonjoin"])
+def test_stream_round_limit(mode):
+    # rounds are enqueued in chunks sized by a lower bound on the rounds left (a slow rank
+    # makes the first bound short, so later chunks follow): a limit equal to the rounds
+    # the iteration takes passes and matches the oracle, one round fewer is a capacity
+    # error, and so is a limit of one round
+    import paper_2606_19989_amd as odb
+
+    rng = np.random.default_rng(76)
+    N, W = 700, 4
+    lens = rng.integers(1, 900, N)
+    perm = rng.permutation(N).astype(np.int32)
+    rate = np.array([3, 64, 64, 64], np.int32)
+    kw = dict(mode=mode, quota=N // 2 if mode == "nonjoin" else 0)
+    m_mode = oracle.MODE_NONJOIN if mode == "nonjoin" else oracle.MODE_JOIN
+    ref = oracle.stream(offsets(lens), perm, W, 4096, mode=m_mode, quota=kw["quota"], buffer_size=64, depth=64,
+                        rate=rate)
+    R = int(ref.sinfo["rounds"])
+    log(f"round limit {mode}: the iteration takes {R} rounds")
+    assert R > 20
+    run_case(f"round_limit_{mode}", lens, perm, W, 4096, 64, 64, rate, max_rounds=R, **kw)
+    for limit in (R - 1, 1):
+        sp = _stream_pipeline(lens, perm, W, 4096, 64, 64, rate, max_rounds=limit, **kw)
+        with pytest.raises(odb.OdbError) as e:
+            sp.plan()
+        assert e.value.status == odb.ODB_E_CAPACITY, limit
+
+
+@pytest.mark.parametrize("bad", ["perm", "length"])
+def test_stream_rejects_bad_data(bad):
+    import paper_2606_19989_amd as odb
+
+    rng = np.random.default_rng(77)
+    N, W = 60, 3
+    lens = rng.integers(1, 50, N)
+    perm = rng.permutation(N).astype(np.int32)
+    if bad == "perm":
+        perm[17] = N       # outside [0, N)
+    else:
+        lens[perm[17]] = 0
+    sp = _stream_pipeline(lens, perm, W, 200, 4, 4, [4, 4, 4])
+    with pytest.raises(odb.OdbError) as e:
+        sp.plan()
+    assert e.value.status == odb.ODB_E_INVALID_DATA
+
+
+def test_stream_ignores_views_after_the_stop():
+    # the grouping of the round after the one that meets a non-join quota runs before the
+    # quota is known, and must leave no trace: a perm entry outside [0, N) for a view only
+    # that round fetches does not fail the call, and the plan is the one of the valid perm
+    rng = np.random.default_rng(78)
+    N, W = 40, 2
+    lens = rng.integers(1, 30, N)
+    perm = rng.permutation(N).astype(np.int32)
+    bad = perm.copy()
+    bad[8] = N          # view 8: rank 0's first view of the second round
+    sp, ref = run_case("stop_then_bad_view", lens, perm, W, 100, 4, 4, [4, 4], mode="nonjoin", quota=1,
+                       device_perm=bad)
+    assert ref.sinfo["rounds"] == 1 and ref.sinfo["stop_reason"] == oracle.STOP_QUOTA
 
 
 def test_stream_window_workload():

@@ -186,7 +186,7 @@ def stream_weights(sp, stream):
     sp.loss_weights(stream=stream)
 
 
-def stream_timing(odb, w, tok_off, tokens, dev, plan_stream, collate_stream, iters=3, pipelined_iters=8):
+def stream_timing(odb, w, tok_off, tokens, dev, plan_stream, collate_stream, iters=3, pipelined_iters=16):
     """Logical iterations of the unified streaming loop over the window's samples as a
     dataset (odb_stream_plan: every round's fetch, grouping, alignment and emission), each
     followed by the collate of its plan.  Serial (host clock around each synchronising

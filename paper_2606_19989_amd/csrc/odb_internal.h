@@ -197,6 +197,66 @@ __device__ __forceinline__ T wave_sum(T v) {
     return v;
 }
 
+// DPP lane moves (data-parallel primitives of this ISA): row_shr:n (control 0x110 + n)
+// moves a value n lanes up within each row of 16 lanes, row_bcast:15 (0x142) hands the
+// last lane of each row to the next row and row_bcast:31 (0x143) lane 31 to rows 2 and 3;
+// rows and banks (groups of 4 lanes in a row) left out by the masks, and lanes a shift
+// cannot reach, read 0.  A 64-bit value moves as two halves.
+template <int CTRL, int ROWS, int BANKS, typename T>
+__device__ __forceinline__ T dpp_move(T v) {
+    if constexpr (sizeof(T) == 8) {
+        const uint64_t u = (uint64_t)v;
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, ROWS, BANKS, true);
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, ROWS, BANKS, true);
+        return (T)(((uint64_t)hi << 32) | lo);
+    } else {
+        return (T)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROWS, BANKS, true);
+    }
+}
+
+struct OpAdd {
+    template <typename T>
+    __device__ static T apply(T a, T b) { return a + b; }
+};
+struct OpMax {   // for values >= 0 (a lane that reads nothing reads 0)
+    template <typename T>
+    __device__ static T apply(T a, T b) { return a > b ? a : b; }
+};
+
+// Inclusive scan over the 64 lanes of a wave without LDS: shifts 1-3 give windows of 4
+// lanes, shift 4 on banks 1-3 and shift 8 on banks 2-3 complete each row of 16, the two
+// broadcasts carry row totals into the rows above.  Every lane of the wave must be active.
+template <typename Op, typename T>
+__device__ __forceinline__ T wave_scan_dpp(T x) {
+    T s = x;
+    s = Op::apply(s, dpp_move<0x111, 0xf, 0xf>(x));
+    s = Op::apply(s, dpp_move<0x112, 0xf, 0xf>(x));
+    s = Op::apply(s, dpp_move<0x113, 0xf, 0xf>(x));
+    s = Op::apply(s, dpp_move<0x114, 0xf, 0xe>(s));
+    s = Op::apply(s, dpp_move<0x118, 0xf, 0xc>(s));
+    s = Op::apply(s, dpp_move<0x142, 0xa, 0xf>(s));
+    s = Op::apply(s, dpp_move<0x143, 0xc, 0xf>(s));
+    return s;
+}
+
+// Value of lane 63 (a wave's inclusive-scan total), uniform over the wave.
+template <typename T>
+__device__ __forceinline__ T wave_last(T v) {
+    if constexpr (sizeof(T) == 8) {
+        const uint64_t u = (uint64_t)v;
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, kWave - 1);
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), kWave - 1);
+        return (T)(((uint64_t)hi << 32) | lo);
+    } else {
+        return (T)__builtin_amdgcn_readlane((int)v, kWave - 1);
+    }
+}
+
+// Lanes below this one whose bit is set in a 64-lane mask.
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
 // Exclusive block scan for blockDim.x == kBlock; *total receives the block sum.
 template <typename T>
 __device__ __forceinline__ T block_excl_sum(T v, T* total) {

@@ -120,10 +120,8 @@ struct StreamArgs {
     StreamRec* rec;
     int64_t* stepsum;      // [3 * D], round mod 3 major
     int32_t* bufv;         // [W * D]
-    int32_t* sv;           // [W * D] sorted views
-    int32_t* slen;         // [W * D] their lengths
+    unsigned long long* skey;   // [W * D] sorted keys (length desc, view asc) of ready ranks
     int32_t* gs;           // [W * (D + 1)] group starts
-    int32_t* apos;         // [W * D] adjusted group of every sorted position
     int32_t* srows;        // [W * scap]
     int32_t* smax;
     int64_t* stok;
@@ -138,11 +136,13 @@ inline int sort_kpt(int64_t D) {
     return (int)(p / kST);
 }
 
-// Dynamic LDS of a round launch: the emit tables for depth D (gtok 8 B; gsl, as, ae,
-// cum 4 B) and the form's keys (8 B), sorted lengths and next-start links (4 B) share it.
+// Dynamic LDS of a round launch: the emit tables for depth D (gtok 8 B, gsl, as, ae, cum
+// 4 B per group; sorted keys 8 B and adjusted groups 4 B per position) and the form's
+// radix counters (4 B per digit, slot and wave), keys (8 B), sorted lengths and
+// next-start links (4 B per position) share it.
 inline size_t round_lds_bytes(int64_t D) {
-    const size_t emit = (size_t)(8 * D + 4 * (4 * D + 2));
-    const size_t form = (size_t)16 * kST * sort_kpt(D);
+    const size_t emit = (size_t)(8 * D + 4 * (4 * D + 2) + 12 * D);
+    const size_t form = (size_t)(4 * 16 * (kST / kWave) + 16 * kST) * sort_kpt(D);
     return emit > form ? emit : form;
 }
 
@@ -150,40 +150,36 @@ __device__ __forceinline__ int32_t view_identity(const StreamArgs& a, int64_t m)
     return a.perm[m < a.N ? m : m % a.N];
 }
 
-// Sum of one value per thread over an NT-thread block.
-template <int NT, typename T>
-__device__ __forceinline__ T sblock_sum(T v) {
+// Block reductions and scans over an NT-thread block: DPP scans inside each wave, one
+// LDS slot per wave across waves.  Every thread of the block must take part.
+template <int NT, typename Op, typename T>
+__device__ __forceinline__ T sblock_reduce(T v) {
     __shared__ T wt[NT / kWave];
-    v = wave_sum(v);
-    if ((threadIdx.x & (kWave - 1)) == 0) wt[threadIdx.x / kWave] = v;
+    const T w = wave_last(wave_scan_dpp<Op>(v));
+    if ((threadIdx.x & (kWave - 1)) == 0) wt[threadIdx.x / kWave] = w;
     __syncthreads();
-    T t = 0;
-    for (int i = 0; i < NT / kWave; ++i) t += wt[i];
+    T t = wt[0];
+    for (int i = 1; i < NT / kWave; ++i) t = Op::apply(t, wt[i]);
     __syncthreads();
     return t;
 }
 
-// Maximum of one non-negative value per thread over an NT-thread block.
+template <int NT, typename T>
+__device__ __forceinline__ T sblock_sum(T v) {
+    return sblock_reduce<NT, OpAdd>(v);
+}
+
+// Maximum of one non-negative value per thread.
 template <int NT>
 __device__ __forceinline__ int64_t sblock_max(int64_t v) {
-    __shared__ int64_t wt[NT / kWave];
-    for (int d = kWave / 2; d > 0; d >>= 1) {
-        const int64_t o = __shfl_xor(v, d, kWave);
-        v = o > v ? o : v;
-    }
-    if ((threadIdx.x & (kWave - 1)) == 0) wt[threadIdx.x / kWave] = v;
-    __syncthreads();
-    int64_t t = 0;
-    for (int i = 0; i < NT / kWave; ++i) t = wt[i] > t ? wt[i] : t;
-    __syncthreads();
-    return t;
+    return sblock_reduce<NT, OpMax>(v);
 }
 
 // Exclusive scan of one value per thread over an NT-thread block; *total = sum.
 template <int NT, typename T>
 __device__ __forceinline__ T sblock_excl(T v, T* total) {
     __shared__ T wt[NT / kWave];
-    const T inc = wave_incl_sum(v);
+    const T inc = wave_scan_dpp<OpAdd>(v);
     const int w = threadIdx.x / kWave;
     if ((threadIdx.x & (kWave - 1)) == kWave - 1) wt[w] = inc;
     __syncthreads();
@@ -213,25 +209,24 @@ struct Booked {
     int64_t steps;    // aligned steps after the round
 };
 
-// Round k's bookkeeping from what the launches before wrote: every block of a launch
-// reaches the same result; `writer` stores it.
-__device__ Booked book_round(const StreamArgs& a, int64_t k, bool writer) {
-    StreamRec* rec = a.rec + k;
-    if (rec->booked) return Booked{false, rec->cum_steps};   // done was seen at launch start
+// Round k's bookkeeping from its record rk and the previous round's rp, both written by
+// earlier launches: every block of a launch reaches the same result; `writer` stores it.
+__device__ Booked book_round(const StreamArgs& a, int64_t k, const StreamRec& rk, const StreamRec& rp, bool writer) {
+    if (rk.booked) return Booked{false, rk.cum_steps};   // done was seen at launch start
     StreamGlobal* g = a.g;
-    const int kind = rec->kind;
-    const int64_t prev_steps = k > 0 ? a.rec[k - 1].cum_steps : 0;
-    const int64_t prev_emitted = k > 0 ? a.rec[k - 1].cum_emitted : 0;
+    StreamRec* rec = a.rec + k;
+    const int64_t prev_steps = k > 0 ? rp.cum_steps : 0;
+    const int64_t prev_emitted = k > 0 ? rp.cum_emitted : 0;
     const bool last = k + 1 >= a.max_rounds;
-    if (kind == 2) {
+    if (rk.kind == 2) {
         if (writer && threadIdx.x == 0) {
-            g->stop = (int32_t)rec->cut;
+            g->stop = (int32_t)rk.cut;
             g->done = 1;
             g->rounds = k + 1;
         }
         return Booked{true, prev_steps};
     }
-    if (kind == 1) {
+    if (rk.kind == 1) {
         if (writer && threadIdx.x == 0) {
             rec->cum_steps = prev_steps;
             rec->cum_emitted = prev_emitted;
@@ -245,7 +240,7 @@ __device__ Booked book_round(const StreamArgs& a, int64_t k, bool writer) {
         return Booked{last, prev_steps};
     }
     // emit round: cumulative step sizes, the quota cut (non-join), per-round totals
-    const int64_t T = rec->target;
+    const int64_t T = rk.target;
     const bool nonjoin = a.mode == ODB_MODE_NONJOIN_QUOTA;
     if (!writer && !nonjoin) return Booked{last, prev_steps + T};
     const int64_t* ss = a.stepsum + (k % 3) * a.D;
@@ -285,7 +280,7 @@ __device__ Booked book_round(const StreamArgs& a, int64_t k, bool writer) {
         g->emitted = prev_emitted + kept;
         g->max_step = mx > g->max_step ? mx : g->max_step;
         g->emit_rounds += 1;
-        g->second_gather += rec->changed ? 1 : 0;
+        g->second_gather += rk.changed ? 1 : 0;
         g->rounds = k + 1;
         if (cut < T || (nonjoin && prev_emitted + kept >= a.quota)) {
             g->stop = ODB_STOP_QUOTA;
@@ -305,8 +300,9 @@ struct RoundView {
     int32_t stop;
 };
 
-// The all_gather: every block reduces the same W published fetch records the same way.
-__device__ RoundView decide_round(const StreamArgs& a, int64_t k) {
+// The all_gather: every block reduces the same W published fetch records of round k the
+// same way; ft / cap_t are the record and capacity of rank threadIdx.x, loaded early.
+__device__ RoundView decide_round(const StreamArgs& a, int64_t k, const RankForm& ft, int64_t cap_t) {
     const RankForm* F = a.form + (k & 1) * a.W;
     __shared__ int64_t s_fin, s_unready, s_maxG, s_minS, s_minC;
     if (threadIdx.x == 0) {
@@ -317,18 +313,19 @@ __device__ RoundView decide_round(const StreamArgs& a, int64_t k) {
         s_minC = LLONG_MAX;
     }
     __syncthreads();
-    for (int r = threadIdx.x; r < a.W; r += kST) {
-        const int32_t st = F[r].status;
-        if (st < 0) {
+    auto tally = [&](const RankForm& x, int64_t c) {
+        if (x.status < 0) {
             atomicAdd((unsigned long long*)&s_fin, 1ull);
-        } else if (st == 0) {
+        } else if (x.status == 0) {
             atomicAdd((unsigned long long*)&s_unready, 1ull);
         } else {
-            atomicMax((long long*)&s_maxG, (long long)st);
-            atomicMin((long long*)&s_minS, (long long)F[r].n);
-            if (a.cap && a.cap[r] > 0) atomicMin((long long*)&s_minC, (long long)a.cap[r]);
+            atomicMax((long long*)&s_maxG, (long long)x.status);
+            atomicMin((long long*)&s_minS, (long long)x.n);
+            if (c > 0) atomicMin((long long*)&s_minC, (long long)c);
         }
-    }
+    };
+    if ((int)threadIdx.x < a.W) tally(ft, cap_t);
+    for (int r = threadIdx.x + kST; r < a.W; r += kST) tally(F[r], a.cap ? a.cap[r] : 0);
     __syncthreads();
     RoundView v{0, 0, 0};
     if (s_fin == a.W) {
@@ -348,94 +345,77 @@ __device__ RoundView decide_round(const StreamArgs& a, int64_t k) {
     return v;
 }
 
-// Round k's emit phase for rank r = blockIdx.x; `base` is the number of aligned steps
-// before the round.  Commits the rank's fetch and returns the round kind; *s_cursor and
-// *s_bufn receive the rank's committed state (after a __syncthreads of the caller).
-__device__ int emit_phase(const StreamArgs& a, int64_t k, int64_t base, unsigned char* lds, int64_t* s_cursor,
-                          int64_t* s_bufn) {
-    const RoundView v = decide_round(a, k);
+// LDS of the emit phase for depth D: gtok (8 B per group), gsl, as, ae, cum (4 B per
+// group), then the rank's sorted keys kl (8 B per position) and adjusted groups apos
+// (4 B per position).
+struct EmitLds {
+    unsigned long long* gtok;
+    int32_t *gsl, *as, *ae, *cum;
+    unsigned long long* kl;
+    int32_t* apos;
+};
+
+__device__ __forceinline__ EmitLds emit_lds(unsigned char* lds, int64_t D) {
+    EmitLds e;
+    e.gtok = reinterpret_cast<unsigned long long*>(lds);
+    e.gsl = reinterpret_cast<int32_t*>(e.gtok + D);
+    e.as = e.gsl + (D + 1);
+    e.ae = e.as + D;
+    e.cum = e.ae + D;
+    e.kl = reinterpret_cast<unsigned long long*>(e.cum + (D + 1));   // 24 D + 8 bytes in
+    e.apos = reinterpret_cast<int32_t*>(e.kl + D);
+    return e;
+}
+
+__device__ __forceinline__ int32_t key_view(unsigned long long key) { return (int32_t)(key & 0xFFFFFFFFull); }
+__device__ __forceinline__ int32_t key_len(unsigned long long key) {
+    return (int32_t)(0x7FFFFFFFll - (int64_t)(key >> 32));
+}
+__device__ __forceinline__ unsigned long long make_key(int64_t l, int64_t m) {
+    return ((unsigned long long)(0x7FFFFFFFll - l) << 32) | (unsigned long long)(uint32_t)m;
+}
+
+// Algorithm 1 and the emission of round k for ready rank r = blockIdx.x, whose G group
+// starts and n sorted keys are in LDS: T slot records at steps base.., the emitted views
+// and the returns (overflow), compacted in sorted order into kl[0..) and the rank's
+// buffer.  Returns the number of returns.
+__device__ int64_t emit_rank(const StreamArgs& a, int64_t k, int64_t base, const EmitLds& L, int64_t T, int64_t G,
+                             int64_t n, int64_t tok, int64_t ebase) {
     const int r = blockIdx.x;
-    RankStream* R = a.ranks + r;
-    const RankForm Fr = a.form[(k & 1) * a.W + r];
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        a.rec[k].kind = v.kind;
-        a.rec[k].target = v.T;
-        a.rec[k].cut = v.kind == 2 ? v.stop : 0;
-    }
-    if (threadIdx.x == 0) {
-        R->cursor = Fr.cursor;
-        R->buf_n = Fr.n;
-        atomicMax(&a.g->max_outstanding, (unsigned long long)Fr.n);
-        if (Fr.err) atomicOr(&a.g->err, Fr.err);
-        *s_cursor = Fr.cursor;
-        *s_bufn = Fr.n;
-    }
-    if (v.kind != 0) return v.kind;
-    const int64_t T = v.T;
-    const int32_t st = Fr.status;
-    if (st < 0) {   // finished rank in join mode: IDLE slots
-        for (int64_t j = threadIdx.x; j < T; j += kST) {
-            const int64_t x = base + j;
-            if (x < a.scap) {
-                const int64_t o = (int64_t)r * a.scap + x;
-                a.srows[o] = 0;
-                a.smax[o] = 0;
-                a.stok[o] = 0;
-                a.sadj[o] = 0.0;
-            } else {
-                a.g->cap_overflow = 1;
-            }
-        }
-        return 0;
-    }
-    // st > 0: a ready rank with G groups over n sorted positions
-    const int64_t G = st;
-    const int64_t n = Fr.n;
-    const int32_t* gsg = a.gs + (int64_t)r * (a.D + 1);
-    const int32_t* sv = a.sv + (int64_t)r * a.D;
-    const int32_t* sl = a.slen + (int64_t)r * a.D;
-    int32_t* apos = a.apos + (int64_t)r * a.D;
-    // per-rank tables of up to D groups, sized by the depth envelope rather than its
-    // maximum so that the block stays small enough to run beside another kernel
-    unsigned long long* gtok = reinterpret_cast<unsigned long long*>(lds);
-    int32_t* gsl = reinterpret_cast<int32_t*>(gtok + a.D);
-    int32_t* as = gsl + (a.D + 1);
-    int32_t* ae = as + a.D;
-    int32_t* cum = ae + a.D;
+    int32_t *gsl = L.gsl, *as = L.as, *ae = L.ae, *cum = L.cum, *apos = L.apos;
+    unsigned long long *gtok = L.gtok, *kl = L.kl;
     __shared__ int64_t s_X, s_jstar;
-    __shared__ int32_t s_ret, s_bad;
-    for (int64_t i = threadIdx.x; i <= G; i += kST) gsl[i] = gsg[i];
+    __shared__ int32_t s_bad;
     for (int64_t i = threadIdx.x; i < T; i += kST) gtok[i] = 0;
     if (threadIdx.x == 0) {
-        s_ret = 0;
         s_bad = 0;
         s_X = 0;
         s_jstar = 0;
     }
     __syncthreads();
-    // Algorithm 1 on this rank: the adjusted groups [as[a], ae[a]) in formation order
+    // the adjusted groups [as[t], ae[t]) in formation order
     if (G < T) {
         // split, closed form: positions [0, X) become singletons, [X, end of group j*)
         // stays one group, later groups are unchanged; j* is the first group whose
         // cumulative surplus sum (c_g - 1) reaches k = T - G
-        if (threadIdx.x == 0) {
-            const int64_t need = T - G;
-            int64_t surplus = 0, jstar = -1, X = 0;
-            for (int64_t g = 0; g < G; ++g) {
-                const int64_t c = gsl[g + 1] - gsl[g];
-                if (surplus + (c - 1) >= need) {
-                    jstar = g;
-                    X = gsl[g] + (need - surplus);
-                    break;
-                }
-                surplus += c - 1;
+        if (threadIdx.x == 0) s_jstar = -1;
+        __syncthreads();
+        const int64_t need = T - G;
+        int64_t carry = 0;
+        for (int64_t b = 0; b < G; b += kST) {
+            const int64_t g = b + threadIdx.x;
+            const int64_t v = g < G ? (int64_t)(gsl[g + 1] - gsl[g]) - 1 : 0;
+            int64_t tot;
+            const int64_t ex = carry + sblock_excl<kST>(v, &tot);
+            if (g < G && ex < need && ex + v >= need) {   // surpluses are >= 0: one crossing
+                s_jstar = g;
+                s_X = gsl[g] + (need - ex);
             }
-            if (jstar < 0 || X + 1 + (G - 1 - jstar) != T) s_bad = 1;
-            s_X = X;
-            s_jstar = jstar < 0 ? 0 : jstar;
+            carry += tot;
         }
         __syncthreads();
-        const int64_t X = s_X, js = s_jstar;
+        const int64_t X = s_X, js = s_jstar < 0 ? 0 : s_jstar;
+        if (threadIdx.x == 0 && (s_jstar < 0 || X + 1 + (G - 1 - s_jstar) != T)) s_bad = 1;
         for (int64_t t = threadIdx.x; t < T; t += kST) {
             if (t < X) {
                 as[t] = (int32_t)t;
@@ -523,12 +503,11 @@ __device__ int emit_phase(const StreamArgs& a, int64_t k, int64_t base, unsigned
     }
     for (int64_t p = threadIdx.x; p < n; p += kST) {
         const int32_t t = apos[p];
-        if (t >= 0) atomicAdd(&gtok[t], (unsigned long long)sl[p]);
+        if (t >= 0) atomicAdd(&gtok[t], (unsigned long long)key_len(kl[p]));
     }
     __syncthreads();
     const int64_t E = cum[T];
-    const int64_t ebase = R->emitted;
-    const double mean = (double)Fr.tok / (double)n;
+    const double mean = (double)tok / (double)n;
     int64_t* stepsum = a.stepsum + (k % 3) * a.D;
     // slot records: step j of the round is adjusted group T-1-j (short to long)
     for (int64_t t = threadIdx.x; t < T; t += kST) {
@@ -538,7 +517,7 @@ __device__ int emit_phase(const StreamArgs& a, int64_t k, int64_t base, unsigned
         if (x < a.scap) {
             const int64_t o = (int64_t)r * a.scap + x;
             a.srows[o] = rows;
-            a.smax[o] = rows > 0 ? sl[as[t]] : 0;
+            a.smax[o] = rows > 0 ? key_len(kl[as[t]]) : 0;
             a.stok[o] = (int64_t)gtok[t];
             a.sadj[o] = (double)rows * mean;
         } else {
@@ -546,148 +525,298 @@ __device__ int emit_phase(const StreamArgs& a, int64_t k, int64_t base, unsigned
         }
         atomicAdd((unsigned long long*)&stepsum[j], (unsigned long long)rows);
     }
-    // emitted views (rows of a group run from its last position to its first) and the
-    // new buffer (overflow returns)
+    // emitted views (rows of a group run from its last position to its first); returns
+    // are compacted in place, in sorted order, into kl[0..) and the buffer: a position
+    // never moves up and every read of a chunk precedes the scan's barriers, so no key
+    // is overwritten before it is read
     int32_t* ev = a.evw + (int64_t)r * a.q;
     int32_t* buf = a.bufv + (int64_t)r * a.D;
-    for (int64_t p = threadIdx.x; p < n; p += kST) {
-        const int32_t t = apos[p];
-        if (t >= 0) {
+    int64_t nret = 0;
+    for (int64_t b = 0; b < n; b += kST) {
+        const int64_t p = b + threadIdx.x;
+        const unsigned long long key = p < n ? kl[p] : 0ull;
+        const int32_t t = p < n ? apos[p] : 0;
+        if (p < n && t >= 0) {
             const int64_t e = ebase + E - cum[t + 1] + (ae[t] - 1 - p);
-            if (e < a.q) ev[e] = sv[p]; else s_bad = 1;
-        } else {
-            buf[atomicAdd(&s_ret, 1)] = sv[p];
+            if (e < a.q) ev[e] = key_view(key); else s_bad = 1;
         }
+        const int32_t ret = (p < n && t < 0) ? 1 : 0;
+        int32_t tot;
+        const int32_t ex = sblock_excl<kST>(ret, &tot);
+        if (ret) {
+            kl[nret + ex] = key;
+            buf[nret + ex] = key_view(key);
+        }
+        nret += tot;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        R->emitted = ebase + E;
-        R->buf_n = s_ret;
-        *s_bufn = s_ret;
-        if (E + s_ret != n) s_bad = 1;
+        a.ranks[r].emitted = ebase + E;
+        a.ranks[r].buf_n = nret;
+        if (E + nret != n) s_bad = 1;
         if (G < T) atomicAdd((unsigned long long*)&a.g->splits, (unsigned long long)(T - G));
         if (G > T) atomicAdd((unsigned long long*)&a.g->overflow, (unsigned long long)(G - T));
         if (G != T) atomicOr(&a.rec[k].changed, 1);
         if (s_bad) atomicOr(&a.g->err, kSErrInternal);
     }
-    return 0;
+    return nret;
 }
 
 // ------------------------------------------------------------------ round: fetch + form
-// One bitonic compare-exchange stage between a thread's own keys, CS slots apart.
-template <int KPT, int CS>
-__device__ __forceinline__ void sort_stage_regs(unsigned long long (&x)[KPT], int size) {
-    if constexpr (CS < KPT) {
-#pragma unroll
-        for (int c = 0; c < KPT; ++c) {
-            if ((c & CS) == 0) {
-                const bool up = ((threadIdx.x + c * kST) & size) == 0;
-                const unsigned long long lo = x[c], hi = x[c + CS];
-                const bool swap = (lo > hi) == up;
-                x[c] = swap ? hi : lo;
-                x[c + CS] = swap ? lo : hi;
-            }
+// Key of sample identity id for view m (length from the CSR offsets); flags bad data.
+__device__ __forceinline__ unsigned long long view_key(const StreamArgs& a, int64_t m, int32_t id, int32_t* err) {
+    int64_t l = 1;
+    if (id < 0 || id >= a.N) {
+        *err |= kSErrIdentity;
+    } else {
+        l = a.tok_off[id + 1] - a.tok_off[id];
+        if (l < 1 || l > 0x7FFFFFFF) {
+            *err |= kSErrLength;
+            l = 1;
         }
     }
+    return make_key(l, m);
 }
 
-// Round j's fetch and grouping for rank r = blockIdx.x from its committed cursor and
-// buffer size n0.  The buffer is sorted as P = KPT * kST keys, slot c of thread t
-// holding position t + c * kST: partners a wave or more apart but in another thread
-// exchange through LDS, partners less than a wave apart by lane shuffles, partners in
-// the same thread in registers.
+// Launch j: books round j-2, emits round j-1, forms round j (see the top of this file).
+// Global loads are issued in two batches ahead of the work that needs them (the
+// control state, then the rank's group starts, sorted keys and the next fetch's
+// identities), so that a round costs few memory round trips beside a running collate.
 template <int KPT>
-__device__ void form_phase(const StreamArgs& a, int64_t j, int64_t cursor, int64_t n0, unsigned char* lds) {
+__global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t j) {
     constexpr int P = KPT * kST;
+    extern __shared__ unsigned long long s_dyn[];
+    unsigned char* lds = reinterpret_cast<unsigned char*>(s_dyn);
     const int r = blockIdx.x;
-    RankForm* F = a.form + (j & 1) * a.W + r;
-    int64_t f = a.rate[r];
-    f = f < a.D - n0 ? f : a.D - n0;
-    f = f < a.q - cursor ? f : a.q - cursor;
-    f = f > 0 ? f : 0;
-    // the fetched views join the buffer (a ready rank keeps them there when another rank
-    // is not ready and the round is a skip round)
-    int32_t* buf = a.bufv + (int64_t)r * a.D;
-    for (int64_t i = threadIdx.x; i < f; i += kST) buf[n0 + i] = (int32_t)((cursor + i) * a.W + r);
-    const int64_t n = n0 + f;
-    const bool drained = cursor + f == a.q;
-    const bool finished = drained && n == 0;
-    const bool ready = !finished && (n >= a.bufsize || drained);
-    if (!ready) {
-        if (threadIdx.x == 0) *F = RankForm{cursor + f, n, 0, finished ? -1 : 0, 0};
-        return;
+    const int tid = threadIdx.x;
+    // ---- first batch: control state and the fetch records published for round j-1
+    const int32_t done = *(volatile int32_t*)&a.g->done;
+    const int64_t kb = j >= 2 ? j - 2 : 0;
+    const StreamRec rk = a.rec[kb];
+    const StreamRec rp = a.rec[kb > 0 ? kb - 1 : 0];
+    const RankForm* Fe = a.form + ((j + 1) & 1) * a.W;   // round j-1
+    RankForm ft{}, fr{};
+    int64_t cap_t = 0;
+    if (j >= 1) {
+        if (tid < a.W) {
+            ft = Fe[tid];
+            cap_t = a.cap ? a.cap[tid] : 0;
+        }
+        fr = Fe[r];
     }
-    unsigned long long* keys = reinterpret_cast<unsigned long long*>(lds);   // [P]
-    int32_t* len = reinterpret_cast<int32_t*>(keys + P);                      // [P]
-    int32_t* nxt = len + P;                                                   // [P]
-    __shared__ int32_t s_err;
-    if (threadIdx.x == 0) s_err = 0;
-    __syncthreads();
-    // key = (INT32_MAX - l) << 32 | m, ascending = (length desc, view asc); views the
-    // rank held before the fetch are read back, fetched ones follow from the cursor
-    unsigned long long x[KPT];
-    int64_t tok = 0;
+    const int64_t ebase = a.ranks[r].emitted;
+    const int64_t rate = a.rate[r];
+    if (done) return;
+    // ---- second batch, before the booking and the round decision are known: this rank's
+    // group starts and sorted keys (used if round j-1 emits) and the identities of the
+    // views round j can fetch
+    const bool may_emit = j >= 1 && fr.status > 0;
+    const int64_t G = may_emit ? fr.status : 0;
+    const int64_t n = may_emit ? fr.n : 0;
+    const int32_t* gsg = a.gs + (int64_t)r * (a.D + 1);
+    const unsigned long long* skey = a.skey + (int64_t)r * a.D;
+    int32_t gv[KPT + 1];
+    unsigned long long kv[KPT];
+#pragma unroll
+    for (int c = 0; c <= KPT; ++c) {
+        const int64_t i = tid + c * kST;
+        gv[c] = i <= G ? gsg[i] : 0;
+    }
 #pragma unroll
     for (int c = 0; c < KPT; ++c) {
-        const int64_t i = threadIdx.x + c * kST;
-        unsigned long long key = ~0ull;
-        if (i < n) {
-            const int64_t m = i < n0 ? (int64_t)buf[i] : (cursor + (i - n0)) * a.W + r;
-            const int32_t id = view_identity(a, m);
-            int64_t l = 1;
-            if (id < 0 || id >= a.N) {
-                atomicOr(&s_err, kSErrIdentity);
-            } else {
-                l = a.tok_off[id + 1] - a.tok_off[id];
-                if (l < 1 || l > 0x7FFFFFFF) {
-                    atomicOr(&s_err, kSErrLength);
-                    l = 1;
+        const int64_t i = tid + c * kST;
+        kv[c] = i < n ? skey[i] : 0ull;
+    }
+    const int64_t cursor = j >= 1 ? fr.cursor : 0;   // committed by the emit phase below
+    int64_t fmax = a.q - cursor;
+    fmax = fmax < rate ? fmax : rate;
+    fmax = fmax < a.D ? fmax : a.D;
+    int32_t pid[KPT];
+#pragma unroll
+    for (int c = 0; c < KPT; ++c) {
+        const int64_t i = tid + c * kST;
+        pid[c] = i < fmax ? view_identity(a, (cursor + i) * a.W + r) : 0;
+    }
+    int64_t base = 0;
+    if (j >= 2) {
+        const Booked b = book_round(a, j - 2, rk, rp, r == 0);
+        if (b.done) return;
+        base = b.steps;
+    }
+    // the step sums of round j, added up by the next launch: last read when round j-3
+    // was booked
+    if (r == 0) {
+        int64_t* ss = a.stepsum + (j % 3) * a.D;
+        for (int64_t i = tid; i < a.D; i += kST) ss[i] = 0;
+    }
+    const EmitLds L = emit_lds(lds, a.D);
+    __shared__ int32_t s_err;
+    if (tid == 0) s_err = 0;
+    __syncthreads();
+    // ---- emit phase of round j-1: the all_gather, the commit of the rank's fetch, and
+    // in an emit round the rank's groups
+    int64_t n0 = 0;          // the rank's buffer after round j-1
+    bool in_lds = false;     // its keys are in L.kl[0..n0)
+    if (j >= 1) {
+        const RoundView v = decide_round(a, j - 1, ft, cap_t);
+        if (r == 0 && tid == 0) {
+            a.rec[j - 1].kind = v.kind;
+            a.rec[j - 1].target = v.T;
+            a.rec[j - 1].cut = v.kind == 2 ? v.stop : 0;
+        }
+        if (tid == 0) {
+            a.ranks[r].cursor = fr.cursor;
+            a.ranks[r].buf_n = fr.n;
+            atomicMax(&a.g->max_outstanding, (unsigned long long)fr.n);
+            if (fr.err) atomicOr(&a.g->err, fr.err);
+        }
+        if (v.kind == 2) return;   // a stop round: the next launch's booking ends the iteration
+        n0 = fr.n;
+        if (v.kind == 0 && fr.status < 0) {   // finished rank in join mode: IDLE slots
+            for (int64_t t = tid; t < v.T; t += kST) {
+                const int64_t x = base + t;
+                if (x < a.scap) {
+                    const int64_t o = (int64_t)r * a.scap + x;
+                    a.srows[o] = 0;
+                    a.smax[o] = 0;
+                    a.stok[o] = 0;
+                    a.sadj[o] = 0.0;
+                } else {
+                    a.g->cap_overflow = 1;
                 }
             }
-            tok += l;
-            key = ((unsigned long long)(0x7FFFFFFFll - l) << 32) | (unsigned long long)(uint32_t)m;
-        }
-        x[c] = key;
-    }
-    tok = sblock_sum<kST>(tok);
-    for (int size = 2; size <= P; size <<= 1) {
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            if (stride >= kST) {
-                if (stride == kST) sort_stage_regs<KPT, 1>(x, size);
-                else if (stride == 2 * kST) sort_stage_regs<KPT, 2>(x, size);
-                else sort_stage_regs<KPT, 4>(x, size);
-                continue;
-            }
-            unsigned long long y[KPT];
-            if (stride >= kWave) {
-                __syncthreads();
+        } else if (v.kind == 0) {
 #pragma unroll
-                for (int c = 0; c < KPT; ++c) keys[threadIdx.x + c * kST] = x[c];
-                __syncthreads();
-#pragma unroll
-                for (int c = 0; c < KPT; ++c) y[c] = keys[(threadIdx.x ^ stride) + c * kST];
-            } else {
-#pragma unroll
-                for (int c = 0; c < KPT; ++c) y[c] = __shfl_xor(x[c], stride, kWave);
+            for (int c = 0; c <= KPT; ++c) {
+                const int64_t i = tid + c * kST;
+                if (i <= G) L.gsl[i] = gv[c];
             }
 #pragma unroll
             for (int c = 0; c < KPT; ++c) {
-                const int i = threadIdx.x + c * kST;
-                const bool keep_min = ((i & stride) == 0) == ((i & size) == 0);
-                x[c] = keep_min ? (x[c] < y[c] ? x[c] : y[c]) : (x[c] < y[c] ? y[c] : x[c]);
+                const int64_t i = tid + c * kST;
+                if (i < n) L.kl[i] = kv[c];
             }
+            n0 = emit_rank(a, j - 1, base, L, v.T, G, n, fr.tok, ebase);
+            in_lds = true;
         }
     }
-    int32_t* sv = a.sv + (int64_t)r * a.D;
-    int32_t* sl = a.slen + (int64_t)r * a.D;
+    // ---- form phase of round j: fetch, status, and for a ready rank sort and group starts
+    int32_t* buf = a.bufv + (int64_t)r * a.D;
+    int64_t f = a.D - n0;
+    f = f < fmax ? f : fmax;
+    f = f > 0 ? f : 0;
+    const int64_t nn = n0 + f;
+    const bool drained = cursor + f == a.q;
+    const bool finished = drained && nn == 0;
+    const bool ready = !finished && (nn >= a.bufsize || drained);
+    RankForm* F = a.form + (j & 1) * a.W + r;
+    // the fetched views join the buffer (a ready rank keeps them there when another rank
+    // is not ready and the round is a skip round)
+    int32_t err = 0;
+    unsigned long long fk[KPT];
 #pragma unroll
     for (int c = 0; c < KPT; ++c) {
-        const int64_t i = threadIdx.x + c * kST;
-        if (i < n) {
-            const int32_t l = (int32_t)(0x7FFFFFFFll - (int64_t)(x[c] >> 32));
-            sv[i] = (int32_t)(x[c] & 0xFFFFFFFFull);
-            sl[i] = l;
-            len[i] = l;
+        const int64_t i = tid + c * kST;
+        fk[c] = 0;
+        if (i < f) {
+            const int64_t m = (cursor + i) * a.W + r;
+            buf[n0 + i] = (int32_t)m;
+            if (ready) fk[c] = view_key(a, m, pid[c], &err);
+        }
+    }
+    if (!ready) {
+        if (tid == 0) *F = RankForm{cursor + f, nn, 0, finished ? -1 : 0, 0};
+        return;
+    }
+    // keys of the whole buffer into kl[0..nn): the returns are there already when the
+    // rank emitted in this launch, otherwise they are read back
+    if (!in_lds) {
+        for (int64_t i = tid; i < n0; i += kST) {
+            const int64_t m = buf[i];
+            L.kl[i] = view_key(a, m, view_identity(a, m), &err);
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < KPT; ++c) {
+        const int64_t i = tid + c * kST;
+        if (i < f) L.kl[n0 + i] = fk[c];
+    }
+    if (err) atomicOr(&s_err, err);
+    __syncthreads();
+    unsigned long long x[KPT];
+    int64_t tok = 0, mylen = 0;
+#pragma unroll
+    for (int c = 0; c < KPT; ++c) {
+        const int64_t i = tid + c * kST;
+        x[c] = i < nn ? L.kl[i] : ~0ull;
+        const int64_t l = i < nn ? key_len(x[c]) : 0;
+        tok += l;
+        mylen = l > mylen ? l : mylen;
+    }
+    tok = sblock_sum<kST>(tok);
+    const int64_t maxlen = sblock_max<kST>(mylen);
+    // sort to (length desc, view asc).  The buffer is already in view order within each
+    // length: the returns come first, sorted, and every fetched view follows all views
+    // fetched before it.  So a stable LSD radix sort on the length alone, 4-bit digits
+    // taken descending, gives that order.  A digit's rank among equal digits comes from
+    // lane ballots; the counts per (digit, slot, wave) are scanned in that order, which is
+    // the order of positions t + c * kST.
+    constexpr int kWaves = kST / kWave;
+    constexpr int kCnt = 16 * KPT * kWaves;
+    int32_t* cnt = reinterpret_cast<int32_t*>(lds);                                         // [kCnt]
+    unsigned long long* sk_l = reinterpret_cast<unsigned long long*>(lds + 4 * kCnt);        // [P]
+    int32_t* len = reinterpret_cast<int32_t*>(sk_l + P);                                     // [P]
+    int32_t* nxt = len + P;                                                                  // [P]
+    const int wv = tid / kWave;
+    const int bits = 32 - __clz((int)maxlen);
+    for (int sh = 0; sh < bits; sh += 4) {
+        for (int i = tid; i < kCnt; i += kST) cnt[i] = 0;
+        __syncthreads();
+        int dg[KPT], rk[KPT];
+#pragma unroll
+        for (int c = 0; c < KPT; ++c) {
+            const bool valid = tid + c * kST < nn;
+            const int d = 15 - ((key_len(x[c]) >> sh) & 15);
+            uint64_t m = __ballot(valid);
+#pragma unroll
+            for (int bt = 0; bt < 4; ++bt) {
+                const bool on = (d >> bt) & 1;
+                const uint64_t bb = __ballot(valid && on);
+                m &= on ? bb : ~bb;
+            }
+            dg[c] = d;
+            rk[c] = lanes_below(m);
+            if (valid && rk[c] == 0) cnt[(d * KPT + c) * kWaves + wv] = __popcll(m);
+        }
+        __syncthreads();
+        int carry = 0;
+        for (int b0 = 0; b0 < kCnt; b0 += kST) {
+            const int i = b0 + tid;
+            const int v = i < kCnt ? cnt[i] : 0;
+            int tot;
+            const int ex = sblock_excl<kST>(v, &tot);
+            if (i < kCnt) cnt[i] = carry + ex;
+            carry += tot;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < KPT; ++c)
+            if (tid + c * kST < nn) sk_l[cnt[(dg[c] * KPT + c) * kWaves + wv] + rk[c]] = x[c];
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < KPT; ++c) {
+            const int64_t i = tid + c * kST;
+            x[c] = i < nn ? sk_l[i] : ~0ull;
+        }
+    }
+    __syncthreads();
+    unsigned long long* sk = a.skey + (int64_t)r * a.D;
+#pragma unroll
+    for (int c = 0; c < KPT; ++c) {
+        const int64_t i = tid + c * kST;
+        if (i < nn) {
+            sk[i] = x[c];
+            len[i] = key_len(x[c]);
         }
     }
     __syncthreads();
@@ -695,60 +824,32 @@ __device__ void form_phase(const StreamArgs& a, int64_t j, int64_t cursor, int64
     // (the shortest of the previous group); the first group is a singleton
 #pragma unroll
     for (int c = 0; c < KPT; ++c) {
-        const int64_t i = threadIdx.x + c * kST;
-        if (i < n) {
+        const int64_t i = tid + c * kST;
+        if (i < nn) {
             const int64_t nx = i == 0 ? 1 : i + batch_size(a.budget, len[i - 1]);
-            nxt[i] = (int32_t)(nx < n ? nx : n);
+            nxt[i] = (int32_t)(nx < nn ? nx : nn);
         }
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
         int32_t* gs = a.gs + (int64_t)r * (a.D + 1);
         int64_t p = 0, g = 0;
-        while (p < n) {
+        while (p < nn) {
             gs[g++] = (int32_t)p;
             p = nxt[p];
         }
-        gs[g] = (int32_t)n;
-        *F = RankForm{cursor + f, n, tok, (int32_t)g, s_err};
+        gs[g] = (int32_t)nn;
+        *F = RankForm{cursor + f, nn, tok, (int32_t)g, s_err};
     }
-}
-
-// Launch j: books round j-2, emits round j-1, forms round j (see the top of this file).
-template <int KPT>
-__global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t j) {
-    if (*(volatile int32_t*)&a.g->done) return;
-    extern __shared__ unsigned long long s_dyn[];
-    unsigned char* lds = reinterpret_cast<unsigned char*>(s_dyn);
-    int64_t base = 0;
-    if (j >= 2) {
-        const Booked b = book_round(a, j - 2, blockIdx.x == 0);
-        if (b.done) return;
-        base = b.steps;
-    }
-    // the step sums of round j, added up by the next launch: last read when round j-3
-    // was booked
-    if (blockIdx.x == 0) {
-        int64_t* ss = a.stepsum + (j % 3) * a.D;
-        for (int64_t i = threadIdx.x; i < a.D; i += kST) ss[i] = 0;
-    }
-    __shared__ int64_t s_cursor, s_bufn;
-    int kind = 0;
-    if (j >= 1) {
-        kind = emit_phase(a, j - 1, base, lds, &s_cursor, &s_bufn);
-    } else if (threadIdx.x == 0) {
-        s_cursor = 0;
-        s_bufn = 0;
-    }
-    __syncthreads();
-    if (kind == 2) return;   // a stop round: the next launch's booking ends the iteration
-    form_phase<KPT>(a, j, s_cursor, s_bufn, lds);
 }
 
 // Books round k at the end of a chunk of launches, so that the host sees its outcome.
 __global__ void __launch_bounds__(kST) stream_book_kernel(StreamArgs a, int64_t k) {
-    if (*(volatile int32_t*)&a.g->done) return;
-    book_round(a, k, true);
+    const int32_t done = *(volatile int32_t*)&a.g->done;
+    const StreamRec rk = a.rec[k];
+    const StreamRec rp = a.rec[k > 0 ? k - 1 : 0];
+    if (done) return;
+    book_round(a, k, rk, rp, true);
     if (threadIdx.x == 0) a.rec[k].booked = 1;
 }
 
@@ -889,7 +990,7 @@ __global__ void clear_totals_kernel(StreamTotals* t) {
 }
 
 struct StreamLayout {
-    size_t g, ranks, form, rec, stepsum, bufv, sv, slen, gs, apos, srows, smax, stok, sadj, evw, vcount, icount,
+    size_t g, ranks, form, rec, stepsum, bufv, skey, gs, srows, smax, stok, sadj, evw, vcount, icount,
         totals, partials, rate, cap, total;
 };
 
@@ -910,10 +1011,8 @@ bool stream_layout(size_t at, int64_t W, int64_t N, int64_t D, int64_t scap, int
     L->rec = take(sizeof(StreamRec) * rounds);
     L->stepsum = take(8 * 3 * D);
     L->bufv = take(4 * W * D);
-    L->sv = take(4 * W * D);
-    L->slen = take(4 * W * D);
+    L->skey = take(8 * W * D);
     L->gs = take(4 * W * (D + 1));
-    L->apos = take(4 * W * D);
     L->srows = take(4 * W * scap);
     L->smax = take(4 * W * scap);
     L->stok = take(8 * W * scap);
@@ -1048,10 +1147,8 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     a.rec = ws_at<StreamRec>(d_ws, SL.rec);
     a.stepsum = ws_at<int64_t>(d_ws, SL.stepsum);
     a.bufv = ws_at<int32_t>(d_ws, SL.bufv);
-    a.sv = ws_at<int32_t>(d_ws, SL.sv);
-    a.slen = ws_at<int32_t>(d_ws, SL.slen);
+    a.skey = ws_at<unsigned long long>(d_ws, SL.skey);
     a.gs = ws_at<int32_t>(d_ws, SL.gs);
-    a.apos = ws_at<int32_t>(d_ws, SL.apos);
     a.srows = ws_at<int32_t>(d_ws, SL.srows);
     a.smax = ws_at<int32_t>(d_ws, SL.smax);
     a.stok = ws_at<int64_t>(d_ws, SL.stok);

@@ -379,8 +379,11 @@ size_t odb_stream_workspace_size(const odb_window_t* w, int32_t depth, int64_t s
  * taken as dataset identities 0..N-1 (rank_offsets of the window are not used; W is
  * num_ranks).
  *
- * Sampler: d_perm [N] is the iteration's shuffled identity list (a permutation, drawn by
- * the caller); it is padded by repeating it from its head to M = W * ceil(N / W) views,
+ * Sampler: d_perm [N] is the iteration's shuffled identity list, a permutation of [0, N)
+ * drawn by the caller (entries outside [0, N) among the fetched views are rejected,
+ * repeated entries are not detected: missing_ids and duplicate_ids are counted from the
+ * emitted views under the permutation contract); it is padded by repeating it from its
+ * head to M = W * ceil(N / W) views,
  * view m has identity perm[m mod N] and belongs to rank m mod W (stride sharding), and a
  * rank visits its views in increasing m.
  * Round: every rank moves up to rate[r] views into its buffer (never above depth); a rank

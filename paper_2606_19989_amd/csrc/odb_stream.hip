@@ -50,6 +50,7 @@ namespace {
 constexpr int kST = 512;              // threads of a round block (one block per rank)
 constexpr int kMaxDepth = 4096;       // largest outstanding-depth envelope
 constexpr int64_t kMinChunk = 8;      // fewest rounds enqueued after an estimate fell short
+constexpr int64_t kViewBitsLds = 64 * 1024;   // a rank's emitted-view bits in LDS up to this size
 
 struct StreamGlobal {
     int64_t steps;       // aligned steps so far (after quota cuts)
@@ -873,8 +874,7 @@ __global__ void stream_slots_kernel(StreamArgs a, int64_t S, int32_t* rows, int3
 // blockIdx.y a slice of its stream.
 __global__ void __launch_bounds__(256) stream_emit_out_kernel(StreamArgs a, int64_t S, const int64_t* row_off,
                                                               int32_t* emit_views, int32_t* emit_order,
-                                                              int64_t* row_ts, int32_t* row_len,
-                                                              int32_t* vcount, int32_t* icount) {
+                                                              int64_t* row_ts, int32_t* row_len) {
     const int r = blockIdx.x;
     const int64_t lo = row_off[(int64_t)r * S], hi = row_off[(int64_t)(r + 1) * S];
     const int32_t* ev = a.evw + (int64_t)r * a.q;
@@ -889,9 +889,50 @@ __global__ void __launch_bounds__(256) stream_emit_out_kernel(StreamArgs a, int6
             row_ts[lo + i] = t0;
             row_len[lo + i] = (int32_t)(a.tok_off[id + 1] - t0);
         }
-        atomicAdd(&vcount[m], 1);
-        atomicAdd(&icount[id], 1);
     }
+}
+
+// Emitted-view bits, word-interleaved over ranks: bit i & 31 of word (i / 32) * W + r is
+// view i * W + r (the i-th view of rank r), so the words of the W ranks for the same 32
+// views are adjacent.
+__device__ __forceinline__ bool view_emitted(const uint32_t* vbits, int64_t W, int64_t r, int64_t i) {
+    return (vbits[(i >> 5) * W + r] >> (i & 31)) & 1;
+}
+
+// Rank r = blockIdx.x: the bits of its emitted views, set in LDS (a bit already set is a
+// view emitted twice, a view of another rank or outside [0, M) is a library error; both
+// count as bad views), then written out.  kLds: the rank's q bits fit in LDS; otherwise
+// the bits are set in global memory, cleared beforehand.
+template <bool kLds>
+__global__ void __launch_bounds__(1024) stream_view_bits_kernel(StreamArgs a, int64_t S, const int64_t* row_off,
+                                                                uint32_t* vbits, unsigned long long* bad_views) {
+    extern __shared__ uint32_t s_bits[];
+    const int r = blockIdx.x;
+    const int64_t W = a.W, M = a.q * a.W, qw = (a.q + 31) / 32;
+    const int64_t lo = row_off[(int64_t)r * S], hi = row_off[(int64_t)(r + 1) * S];
+    const int32_t* ev = a.evw + (int64_t)r * a.q;
+    if (kLds) {
+        for (int64_t k = threadIdx.x; k < qw; k += blockDim.x) s_bits[k] = 0;
+        __syncthreads();
+    }
+    unsigned long long bad = 0;
+    for (int64_t e = threadIdx.x; e < hi - lo; e += blockDim.x) {
+        const int64_t m = ev[e];
+        if (m < 0 || m >= M || m % W != r) {
+            bad += 1;
+            continue;
+        }
+        const int64_t i = m / W;
+        const uint32_t b = 1u << (i & 31);
+        const uint32_t old = kLds ? atomicOr(&s_bits[i >> 5], b) : atomicOr(&vbits[(i >> 5) * W + r], b);
+        bad += (old & b) ? 1 : 0;
+    }
+    if (kLds) {
+        __syncthreads();
+        for (int64_t k = threadIdx.x; k < qw; k += blockDim.x) vbits[k * W + r] = s_bits[k];
+    }
+    bad = wave_sum(bad);
+    if ((threadIdx.x & (kWave - 1)) == 0 && bad) atomicAdd(bad_views, bad);
 }
 
 struct RowsLoadS {
@@ -912,22 +953,22 @@ struct StoreS {
 
 struct LeftFlag {
     StreamArgs a;
-    const int32_t* vcount;
+    const uint32_t* vbits;
     // rank-major position x = r * q + i <-> view m = i * W + r
     __device__ int64_t operator()(int64_t x) const {
         const int64_t r = x / a.q, i = x - r * a.q;
-        return vcount[i * a.W + r] == 0 ? 1 : 0;
+        return view_emitted(vbits, a.W, r, i) ? 0 : 1;
     }
 };
 struct LeftStore {
     StreamArgs a;
-    const int32_t* vcount;
+    const uint32_t* vbits;
     int32_t* left;
     int64_t* left_off;
     __device__ void operator()(int64_t x, int64_t ex) const {
         const int64_t r = x / a.q, i = x - r * a.q;
         if (i == 0) left_off[r] = ex;
-        if (vcount[i * a.W + r] == 0) left[ex] = (int32_t)(i * a.W + r);
+        if (!view_emitted(vbits, a.W, r, i)) left[ex] = (int32_t)(i * a.W + r);
     }
 };
 
@@ -938,18 +979,21 @@ struct StreamTotals {
     unsigned long long duplicate_ids;
 };
 
+// Real tokens over the slots, and the identity counts.  perm is a permutation of [0, N),
+// so identity perm[m] (m < N) is carried by the views m, m + N, m + 2N, ... below M (the
+// padding repeats the list from its head) and by nothing else: its emission count is the
+// sum of those views' bits.
 __global__ void __launch_bounds__(256) stream_totals_kernel(StreamArgs a, int64_t K, const int64_t* tokens,
-                                                            const int32_t* vcount, const int32_t* icount,
-                                                            StreamTotals* t) {
+                                                            const uint32_t* vbits, StreamTotals* t) {
     const int64_t M = a.q * a.W;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     unsigned long long tok = 0, bad = 0, miss = 0, dup = 0;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < K; i += stride) tok += tokens[i];
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < M; i += stride) bad += vcount[i] > 1;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.N; i += stride) {
-        const int32_t c = icount[i];
+    for (int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; m < a.N; m += stride) {
+        int64_t c = 0;
+        for (int64_t v = m; v < M; v += a.N) c += view_emitted(vbits, a.W, v % a.W, v / a.W) ? 1 : 0;
         miss += c == 0;
-        dup += c > 1 ? (unsigned long long)(c - 1) : 0ull;
+        dup += c > 0 ? (unsigned long long)(c - 1) : 0ull;
     }
     __shared__ unsigned long long part[4][256 / kWave];
     const int w = threadIdx.x / kWave;
@@ -990,7 +1034,7 @@ __global__ void clear_totals_kernel(StreamTotals* t) {
 }
 
 struct StreamLayout {
-    size_t g, ranks, form, rec, stepsum, bufv, skey, gs, srows, smax, stok, sadj, evw, vcount, icount,
+    size_t g, ranks, form, rec, stepsum, bufv, skey, gs, srows, smax, stok, sadj, evw, vbits,
         totals, partials, rate, cap, total;
 };
 
@@ -1018,8 +1062,7 @@ bool stream_layout(size_t at, int64_t W, int64_t N, int64_t D, int64_t scap, int
     L->stok = take(8 * W * scap);
     L->sadj = take(8 * W * scap);
     L->evw = take(4 * (M > 0 ? M : 1));
-    L->vcount = take(4 * (M > 0 ? M : 1));
-    L->icount = take(4 * (N > 0 ? N : 1));
+    L->vbits = take(4 * W * ((q + 31) / 32));
     L->totals = take(sizeof(StreamTotals));
     L->partials = take(8 * (scan_n / kScanTile + 4));
     L->rate = take(4 * W);
@@ -1232,27 +1275,37 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     ODB_TRY((device_excl_scan<int64_t>(RowsLoadS{d_slot_rows, K}, StoreS{d_slot_row_off}, K + 1, partials, s)));
     ODB_TRY((device_excl_scan<int64_t>(TileLoadS{d_slot_rows, d_slot_maxlen, K}, StoreS{d_slot_tile_off}, K + 1,
                                        partials, s)));
-    int32_t* vcount = ws_at<int32_t>(d_ws, SL.vcount);
-    int32_t* icount = ws_at<int32_t>(d_ws, SL.icount);
+    uint32_t* vbits = ws_at<uint32_t>(d_ws, SL.vbits);
+    const int64_t qw = (q + 31) / 32;
+    const bool bits_in_lds = 4 * qw <= kViewBitsLds;
     StreamTotals* tot = ws_at<StreamTotals>(d_ws, SL.totals);
-    hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(std::max<int64_t>(M, 1), 256, gcap)), dim3(256), 0, s, vcount, M);
-    ODB_LAUNCHED();
-    hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(std::max<int64_t>(N, 1), 256, gcap)), dim3(256), 0, s, icount, N);
-    ODB_LAUNCHED();
+    if (!bits_in_lds && qw > 0) {
+        hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(W * qw, 256, gcap)), dim3(256), 0, s,
+                           reinterpret_cast<int32_t*>(vbits), W * qw);
+        ODB_LAUNCHED();
+    }
     hipLaunchKernelGGL(clear_totals_kernel, dim3(1), dim3(64), 0, s, tot);
     ODB_LAUNCHED();
     if (K > 0) {
         hipLaunchKernelGGL(stream_emit_out_kernel, dim3(W, 64), dim3(256), 0, s, a, S, (const int64_t*)d_slot_row_off,
-                           d_emit_views, d_emit_order, d_row_token_start, d_row_len, vcount, icount);
+                           d_emit_views, d_emit_order, d_row_token_start, d_row_len);
+        ODB_LAUNCHED();
+    }
+    if (M > 0) {
+        if (bits_in_lds)
+            hipLaunchKernelGGL(stream_view_bits_kernel<true>, dim3(W), dim3(1024), 4 * qw, s, a, S,
+                               (const int64_t*)d_slot_row_off, vbits, &tot->bad_views);
+        else
+            hipLaunchKernelGGL(stream_view_bits_kernel<false>, dim3(W), dim3(1024), 0, s, a, S,
+                               (const int64_t*)d_slot_row_off, vbits, &tot->bad_views);
         ODB_LAUNCHED();
     }
     hipLaunchKernelGGL(fill_i64s_kernel, dim3(1), dim3(256), 0, s, d_left_off, (int64_t)W + 1);
     ODB_LAUNCHED();
-    ODB_TRY((device_excl_scan<int64_t>(LeftFlag{a, vcount}, LeftStore{a, vcount, d_left_views, d_left_off}, M,
+    ODB_TRY((device_excl_scan<int64_t>(LeftFlag{a, vbits}, LeftStore{a, vbits, d_left_views, d_left_off}, M,
                                        partials, s)));
-    hipLaunchKernelGGL(stream_totals_kernel, dim3(grid_for(std::max<int64_t>(std::max(K, M), 1), 256, gcap)),
-                       dim3(256), 0, s, a, K, (const int64_t*)d_slot_tokens, (const int32_t*)vcount,
-                       (const int32_t*)icount, tot);
+    hipLaunchKernelGGL(stream_totals_kernel, dim3(grid_for(std::max<int64_t>(std::max(K, N), 1), 256, gcap)),
+                       dim3(256), 0, s, a, K, (const int64_t*)d_slot_tokens, (const uint32_t*)vbits, tot);
     ODB_LAUNCHED();
     StreamTotals ht{};
     int64_t padded = 0, nleft = 0;

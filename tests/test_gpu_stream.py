@@ -89,6 +89,11 @@ def edge_cases():
     add("tiny_budget", rng.integers(1, 9, 500), 2, 1, 50, 80, [20, 80])
     add("overflow_capacity", rng.integers(1, 600, 1500), 3, 3000, 200, 256, [256, 100, 50], cap=np.array([3, 0, 5]))
     add("max_depth", rng.integers(1, 3000, 20000), 2, 16384, 4096, 4096, [4096, 4096])
+    # depth 1500: four sort keys per thread; skip rounds while the slow rank fills
+    add("depth_1500", rng.integers(1, 5000, 12000), 3, 12000, 1200, 1500, [1500, 700, 1500])
+    # one rank with 600,000 views: its emitted-view bits exceed the LDS budget and are set
+    # in global memory
+    add("long_rank", rng.integers(1, 12, 600000), 1, 64, 1024, 1024, [1024])
     n = 2003
     for q in (1, 500, n + 1):
         add(f"nonjoin_q{q}", rng.integers(1, 2000, n), 4, 6000, 100, 150, [150, 90, 40, 150], mode="nonjoin",

@@ -115,6 +115,12 @@ struct StreamArgs {
     const int32_t* perm;
     const int32_t* rate;   // [W]
     const int64_t* cap;    // [W] or null
+    // every view's identity, token start and length code, rank-major (x = r * q + i is
+    // view i * W + r); the code is the length, 0 for an identity outside [0, N), -1 for a
+    // length outside [1, 2^31)
+    const int32_t* vid;
+    const int64_t* vts;
+    const int32_t* vlen;
     StreamGlobal* g;
     RankStream* ranks;     // [W]
     RankForm* form;        // [2 * W], round parity major
@@ -192,6 +198,28 @@ __device__ __forceinline__ T sblock_excl(T v, T* total) {
     __syncthreads();
     *total = tot;
     return pre + inc - v;
+}
+
+// The staged view table: every view's identity (perm), token start and length code (CSR
+// offsets), gathered once per iteration so that a round's fetch reads its views' codes
+// in order and the final pass reads identities and row records near each other.
+__global__ void __launch_bounds__(256) stream_views_kernel(StreamArgs a, int32_t* vid, int64_t* vts, int32_t* vlen) {
+    const int64_t M = a.q * a.W;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < M; x += stride) {
+        const int64_t r = x / a.q, i = x - r * a.q;
+        const int32_t id = view_identity(a, i * a.W + r);
+        int32_t code = 0;
+        int64_t t0 = 0;
+        if (id >= 0 && id < a.N) {
+            t0 = a.tok_off[id];
+            const int64_t l = a.tok_off[id + 1] - t0;
+            code = (l < 1 || l > 0x7FFFFFFF) ? -1 : (int32_t)l;
+        }
+        vid[x] = id;
+        vts[x] = t0;
+        vlen[x] = code;
+    }
 }
 
 __global__ void stream_init_kernel(StreamArgs a, int64_t rounds_cap) {
@@ -564,25 +592,20 @@ __device__ int64_t emit_rank(const StreamArgs& a, int64_t k, int64_t base, const
 }
 
 // ------------------------------------------------------------------ round: fetch + form
-// Key of sample identity id for view m (length from the CSR offsets); flags bad data.
-__device__ __forceinline__ unsigned long long view_key(const StreamArgs& a, int64_t m, int32_t id, int32_t* err) {
-    int64_t l = 1;
-    if (id < 0 || id >= a.N) {
-        *err |= kSErrIdentity;
-    } else {
-        l = a.tok_off[id + 1] - a.tok_off[id];
-        if (l < 1 || l > 0x7FFFFFFF) {
-            *err |= kSErrLength;
-            l = 1;
-        }
+// Key of view m from its staged length code; flags bad data.
+__device__ __forceinline__ unsigned long long staged_key(int32_t code, int64_t m, int32_t* err) {
+    int64_t l = code;
+    if (code <= 0) {
+        *err |= code == 0 ? kSErrIdentity : kSErrLength;
+        l = 1;
     }
     return make_key(l, m);
 }
 
 // Launch j: books round j-2, emits round j-1, forms round j (see the top of this file).
 // Global loads are issued in two batches ahead of the work that needs them (the
-// control state, then the rank's group starts, sorted keys and the next fetch's
-// identities), so that a round costs few memory round trips beside a running collate.
+// control state, then the rank's group starts, sorted keys and the next fetch's length
+// codes), so that a round costs few memory round trips beside a running collate.
 template <int KPT>
 __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t j) {
     constexpr int P = KPT * kST;
@@ -632,11 +655,12 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
     int64_t fmax = a.q - cursor;
     fmax = fmax < rate ? fmax : rate;
     fmax = fmax < a.D ? fmax : a.D;
-    int32_t pid[KPT];
+    const int32_t* vlen_r = a.vlen + (int64_t)r * a.q;
+    int32_t code[KPT];
 #pragma unroll
     for (int c = 0; c < KPT; ++c) {
         const int64_t i = tid + c * kST;
-        pid[c] = i < fmax ? view_identity(a, (cursor + i) * a.W + r) : 0;
+        code[c] = i < fmax ? vlen_r[cursor + i] : 1;
     }
     int64_t base = 0;
     if (j >= 2) {
@@ -722,7 +746,7 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
         if (i < f) {
             const int64_t m = (cursor + i) * a.W + r;
             buf[n0 + i] = (int32_t)m;
-            if (ready) fk[c] = view_key(a, m, pid[c], &err);
+            if (ready) fk[c] = staged_key(code[c], m, &err);
         }
     }
     if (!ready) {
@@ -734,7 +758,7 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
     if (!in_lds) {
         for (int64_t i = tid; i < n0; i += kST) {
             const int64_t m = buf[i];
-            L.kl[i] = view_key(a, m, view_identity(a, m), &err);
+            L.kl[i] = staged_key(vlen_r[m / a.W], m, &err);
         }
     }
 #pragma unroll
@@ -870,24 +894,25 @@ __global__ void stream_slots_kernel(StreamArgs a, int64_t S, int32_t* rows, int3
 }
 
 // Rank r's emitted views (slot order, row order), their identities and, when asked for,
-// the row records (token start and length of each identity); blockIdx.x is the rank,
-// blockIdx.y a slice of its stream.
+// the row records (token start and length of each identity), read from the staged view
+// table; blockIdx.x is the rank, blockIdx.y a slice of its stream.
 __global__ void __launch_bounds__(256) stream_emit_out_kernel(StreamArgs a, int64_t S, const int64_t* row_off,
                                                               int32_t* emit_views, int32_t* emit_order,
                                                               int64_t* row_ts, int32_t* row_len) {
     const int r = blockIdx.x;
     const int64_t lo = row_off[(int64_t)r * S], hi = row_off[(int64_t)(r + 1) * S];
     const int32_t* ev = a.evw + (int64_t)r * a.q;
+    const int64_t M = a.q * a.W;
     const int64_t stride = (int64_t)gridDim.y * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.y * blockDim.x + threadIdx.x; i < hi - lo; i += stride) {
         const int32_t m = ev[i];
-        const int32_t id = view_identity(a, m);
+        if (m < 0 || m >= M) continue;   // a library error, counted by the view bits
+        const int64_t x = (int64_t)r * a.q + m / a.W;
         emit_views[lo + i] = m;
-        emit_order[lo + i] = id;
+        emit_order[lo + i] = a.vid[x];
         if (row_ts) {
-            const int64_t t0 = a.tok_off[id];
-            row_ts[lo + i] = t0;
-            row_len[lo + i] = (int32_t)(a.tok_off[id + 1] - t0);
+            row_ts[lo + i] = a.vts[x];
+            row_len[lo + i] = a.vlen[x];
         }
     }
 }
@@ -1034,7 +1059,7 @@ __global__ void clear_totals_kernel(StreamTotals* t) {
 }
 
 struct StreamLayout {
-    size_t g, ranks, form, rec, stepsum, bufv, skey, gs, srows, smax, stok, sadj, evw, vbits,
+    size_t g, ranks, form, rec, stepsum, bufv, skey, gs, srows, smax, stok, sadj, evw, vbits, vid, vts, vlen,
         totals, partials, rate, cap, total;
 };
 
@@ -1063,6 +1088,9 @@ bool stream_layout(size_t at, int64_t W, int64_t N, int64_t D, int64_t scap, int
     L->sadj = take(8 * W * scap);
     L->evw = take(4 * (M > 0 ? M : 1));
     L->vbits = take(4 * W * ((q + 31) / 32));
+    L->vid = take(4 * (M > 0 ? M : 1));
+    L->vts = take(8 * (M > 0 ? M : 1));
+    L->vlen = take(4 * (M > 0 ? M : 1));
     L->totals = take(sizeof(StreamTotals));
     L->partials = take(8 * (scan_n / kScanTile + 4));
     L->rate = take(4 * W);
@@ -1197,9 +1225,18 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     a.stok = ws_at<int64_t>(d_ws, SL.stok);
     a.sadj = ws_at<double>(d_ws, SL.sadj);
     a.evw = ws_at<int32_t>(d_ws, SL.evw);
+    a.vid = ws_at<int32_t>(d_ws, SL.vid);
+    a.vts = ws_at<int64_t>(d_ws, SL.vts);
+    a.vlen = ws_at<int32_t>(d_ws, SL.vlen);
     ODB_TRY_HIP(hipMemcpyAsync(const_cast<int32_t*>(a.rate), params->rate, 4 * W, hipMemcpyHostToDevice, s));
     if (a.cap)
         ODB_TRY_HIP(hipMemcpyAsync(const_cast<int64_t*>(a.cap), params->slot_capacity, 8 * W, hipMemcpyHostToDevice, s));
+    if (M > 0) {
+        hipLaunchKernelGGL(stream_views_kernel, dim3(grid_for(M, 256, (int64_t)num_cus() * kPlanBlocksPerCU)),
+                           dim3(256), 0, s, a, const_cast<int32_t*>(a.vid), const_cast<int64_t*>(a.vts),
+                           const_cast<int32_t*>(a.vlen));
+        ODB_LAUNCHED();
+    }
     hipLaunchKernelGGL(stream_init_kernel, dim3(grid_for(std::max<int64_t>(params->max_rounds, W), 256, 1024)),
                        dim3(256), 0, s, a, params->max_rounds);
     ODB_LAUNCHED();

@@ -331,44 +331,60 @@ struct RoundView {
 
 // The all_gather: every block reduces the same W published fetch records of round k the
 // same way; ft / cap_t are the record and capacity of rank threadIdx.x, loaded early.
+// Each thread tallies its ranks in registers; the waves combine by DPP scans and one LDS
+// slot per wave (minima as maxima of LLONG_MAX - v, so that 0 means none).
 __device__ RoundView decide_round(const StreamArgs& a, int64_t k, const RankForm& ft, int64_t cap_t) {
     const RankForm* F = a.form + (k & 1) * a.W;
-    __shared__ int64_t s_fin, s_unready, s_maxG, s_minS, s_minC;
-    if (threadIdx.x == 0) {
-        s_fin = 0;
-        s_unready = 0;
-        s_maxG = 0;
-        s_minS = LLONG_MAX;
-        s_minC = LLONG_MAX;
-    }
-    __syncthreads();
+    int64_t cnt = 0, mg = 0, xs = 0, xc = 0;   // cnt: finished << 32 | not ready
     auto tally = [&](const RankForm& x, int64_t c) {
         if (x.status < 0) {
-            atomicAdd((unsigned long long*)&s_fin, 1ull);
+            cnt += 1ll << 32;
         } else if (x.status == 0) {
-            atomicAdd((unsigned long long*)&s_unready, 1ull);
+            cnt += 1;
         } else {
-            atomicMax((long long*)&s_maxG, (long long)x.status);
-            atomicMin((long long*)&s_minS, (long long)x.n);
-            if (c > 0) atomicMin((long long*)&s_minC, (long long)c);
+            mg = x.status > mg ? x.status : mg;
+            xs = LLONG_MAX - x.n > xs ? LLONG_MAX - x.n : xs;
+            if (c > 0) xc = LLONG_MAX - c > xc ? LLONG_MAX - c : xc;
         }
     };
     if ((int)threadIdx.x < a.W) tally(ft, cap_t);
     for (int r = threadIdx.x + kST; r < a.W; r += kST) tally(F[r], a.cap ? a.cap[r] : 0);
+    cnt = wave_last(wave_scan_dpp<OpAdd>(cnt));
+    mg = wave_last(wave_scan_dpp<OpMax>(mg));
+    xs = wave_last(wave_scan_dpp<OpMax>(xs));
+    xc = wave_last(wave_scan_dpp<OpMax>(xc));
+    __shared__ int64_t part[4][kST / kWave];
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        part[0][w] = cnt;
+        part[1][w] = mg;
+        part[2][w] = xs;
+        part[3][w] = xc;
+    }
     __syncthreads();
+    cnt = 0;
+    mg = xs = xc = 0;
+    for (int i = 0; i < kST / kWave; ++i) {
+        cnt += part[0][i];
+        mg = part[1][i] > mg ? part[1][i] : mg;
+        xs = part[2][i] > xs ? part[2][i] : xs;
+        xc = part[3][i] > xc ? part[3][i] : xc;
+    }
+    const int64_t fin = cnt >> 32, unready = cnt & 0xFFFFFFFFll;
+    const int64_t minS = LLONG_MAX - xs, minC = LLONG_MAX - xc;
     RoundView v{0, 0, 0};
-    if (s_fin == a.W) {
+    if (fin == a.W) {
         v.kind = 2;
         v.stop = ODB_STOP_DRAINED;
-    } else if (a.mode == ODB_MODE_NONJOIN_QUOTA && s_fin > 0) {
+    } else if (a.mode == ODB_MODE_NONJOIN_QUOTA && fin > 0) {
         v.kind = 2;
         v.stop = ODB_STOP_RANK_FINISHED;
-    } else if (s_unready > 0) {
+    } else if (unready > 0) {
         v.kind = 1;
     } else {
-        int64_t T = s_maxG;
-        if (s_minC < T) T = s_minC;
-        if (s_minS < T) T = s_minS;
+        int64_t T = mg;
+        if (minC < T) T = minC;
+        if (minS < T) T = minS;
         v.T = T < 1 ? 1 : T;
     }
     return v;
@@ -530,9 +546,20 @@ __device__ int64_t emit_rank(const StreamArgs& a, int64_t k, int64_t base, const
         }
         if (threadIdx.x == 0) cum[T] = (int32_t)carry;
     }
-    for (int64_t p = threadIdx.x; p < n; p += kST) {
-        const int32_t t = apos[p];
-        if (t >= 0) atomicAdd(&gtok[t], (unsigned long long)key_len(kl[p]));
+    // tokens per adjusted group: a group's positions are contiguous, so each wave sums its
+    // piece of a group with a DPP scan and adds it with one atomic (a per-position atomic
+    // would queue up to a wave of lanes on one LDS address)
+    for (int64_t b = 0; b < n; b += kST) {
+        const int64_t p = b + threadIdx.x;
+        const int lane = threadIdx.x & (kWave - 1);
+        const int32_t t = p < n ? apos[p] : -1;
+        const int64_t l = t >= 0 ? key_len(kl[p]) : 0;
+        const int64_t inc = wave_scan_dpp<OpAdd>(l);
+        const int32_t t_prev = __shfl_up(t, 1, kWave), t_next = __shfl_down(t, 1, kWave);
+        const int head = wave_scan_dpp<OpMax>((lane == 0 || t_prev != t) ? lane : 0);
+        const int64_t before = __shfl(inc, head > 0 ? head - 1 : 0, kWave);
+        if (t >= 0 && (lane == kWave - 1 || t_next != t))
+            atomicAdd(&gtok[t], (unsigned long long)(inc - (head > 0 ? before : 0)));
     }
     __syncthreads();
     const int64_t E = cum[T];
@@ -614,7 +641,7 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
     const int r = blockIdx.x;
     const int tid = threadIdx.x;
     // ---- first batch: control state and the fetch records published for round j-1
-    const int32_t done = *(volatile int32_t*)&a.g->done;
+    const int32_t done = a.g->done;   // written by an earlier launch
     const int64_t kb = j >= 2 ? j - 2 : 0;
     const StreamRec rk = a.rec[kb];
     const StreamRec rp = a.rec[kb > 0 ? kb - 1 : 0];
@@ -631,6 +658,9 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
     const int64_t ebase = a.ranks[r].emitted;
     const int64_t rate = a.rate[r];
     if (done) return;
+    // the first batch is complete here (one wait), so the second one below is not drained
+    // by a later first use of this batch
+    asm volatile("" ::"v"(ft.status), "v"(ft.n), "v"(cap_t));
     // ---- second batch, before the booking and the round decision are known: this rank's
     // group starts and sorted keys (used if round j-1 emits) and the identities of the
     // views round j can fetch
@@ -870,7 +900,7 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
 
 // Books round k at the end of a chunk of launches, so that the host sees its outcome.
 __global__ void __launch_bounds__(kST) stream_book_kernel(StreamArgs a, int64_t k) {
-    const int32_t done = *(volatile int32_t*)&a.g->done;
+    const int32_t done = a.g->done;   // written by an earlier launch
     const StreamRec rk = a.rec[k];
     const StreamRec rp = a.rec[k > 0 ? k - 1 : 0];
     if (done) return;

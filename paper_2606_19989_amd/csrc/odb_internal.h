@@ -18,8 +18,9 @@ constexpr int kScanItems = 16;
 constexpr int kScanTile = kBlock * kScanItems;
 constexpr int kMaxJumpRounds = 40;
 // grid cap of the grid-stride kernels of the plan stages, in blocks per compute unit
-// (64 or 256 were slower: per-block setup and same-address atomics grow with the grid)
-constexpr int kPlanBlocksPerCU = 16;
+// (8 measured best: 4 too few loads in flight, 16 to 256 slower as per-block setup and
+// same-address atomics grow with the grid)
+constexpr int kPlanBlocksPerCU = 8;
 
 // ------------------------------------------------------------------ host error state
 int set_error(int code, const char* fmt, ...);

@@ -662,7 +662,7 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
     // by a later first use of this batch
     asm volatile("" ::"v"(ft.status), "v"(ft.n), "v"(cap_t));
     // ---- second batch, before the booking and the round decision are known: this rank's
-    // group starts and sorted keys (used if round j-1 emits) and the identities of the
+    // group starts and sorted keys (used if round j-1 emits) and the length codes of the
     // views round j can fetch
     const bool may_emit = j >= 1 && fr.status > 0;
     const int64_t G = may_emit ? fr.status : 0;
@@ -827,7 +827,7 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
     for (int sh = 0; sh < bits; sh += 4) {
         for (int i = tid; i < kCnt; i += kST) cnt[i] = 0;
         __syncthreads();
-        int dg[KPT], rk[KPT];
+        int dg[KPT], drank[KPT];   // digit, rank among equal digits of the wave
 #pragma unroll
         for (int c = 0; c < KPT; ++c) {
             const bool valid = tid + c * kST < nn;
@@ -840,8 +840,8 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
                 m &= on ? bb : ~bb;
             }
             dg[c] = d;
-            rk[c] = lanes_below(m);
-            if (valid && rk[c] == 0) cnt[(d * KPT + c) * kWaves + wv] = __popcll(m);
+            drank[c] = lanes_below(m);
+            if (valid && drank[c] == 0) cnt[(d * KPT + c) * kWaves + wv] = __popcll(m);
         }
         __syncthreads();
         int carry = 0;
@@ -856,7 +856,7 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
         __syncthreads();
 #pragma unroll
         for (int c = 0; c < KPT; ++c)
-            if (tid + c * kST < nn) sk_l[cnt[(dg[c] * KPT + c) * kWaves + wv] + rk[c]] = x[c];
+            if (tid + c * kST < nn) sk_l[cnt[(dg[c] * KPT + c) * kWaves + wv] + drank[c]] = x[c];
         __syncthreads();
 #pragma unroll
         for (int c = 0; c < KPT; ++c) {
@@ -887,6 +887,8 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
     }
     __syncthreads();
     if (tid == 0) {
+        // one thread walks the links (about one per group); pointer doubling over all
+        // positions took longer, each of its rounds needing two block barriers
         int32_t* gs = a.gs + (int64_t)r * (a.D + 1);
         int64_t p = 0, g = 0;
         while (p < nn) {

@@ -533,8 +533,12 @@ __device__ int64_t emit_rank(const StreamArgs& a, int64_t k, int64_t base, const
             for (int64_t p = as[t]; p < ae[t]; ++p) apos[p] = (int32_t)t;
     }
     __syncthreads();
-    // rows prefix over the adjusted groups, tokens per adjusted group
-    {
+    // rows prefix over the adjusted groups, tokens per adjusted group.  Without overflow
+    // the adjusted groups tile positions 0..n in order, so the prefix is the group start
+    if (G <= T) {
+        for (int64_t t = threadIdx.x; t < T; t += kST) cum[t] = as[t];
+        if (threadIdx.x == 0) cum[T] = (int32_t)n;
+    } else {
         int64_t carry = 0;
         for (int64_t b = 0; b < T; b += kST) {
             const int64_t t = b + threadIdx.x;
@@ -588,7 +592,13 @@ __device__ int64_t emit_rank(const StreamArgs& a, int64_t k, int64_t base, const
     int32_t* ev = a.evw + (int64_t)r * a.q;
     int32_t* buf = a.bufv + (int64_t)r * a.D;
     int64_t nret = 0;
-    for (int64_t b = 0; b < n; b += kST) {
+    if (G <= T) {   // every position is emitted
+        for (int64_t p = threadIdx.x; p < n; p += kST) {
+            const int32_t t = apos[p];
+            const int64_t e = ebase + E - cum[t + 1] + (ae[t] - 1 - p);
+            if (e < a.q) ev[e] = key_view(kl[p]); else s_bad = 1;
+        }
+    } else for (int64_t b = 0; b < n; b += kST) {
         const int64_t p = b + threadIdx.x;
         const unsigned long long key = p < n ? kl[p] : 0ull;
         const int32_t t = p < n ? apos[p] : 0;

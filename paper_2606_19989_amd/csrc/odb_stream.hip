@@ -149,7 +149,8 @@ inline int sort_kpt(int64_t D) {
 // next-start links (4 B per position) share it.
 inline size_t round_lds_bytes(int64_t D) {
     const size_t emit = (size_t)(8 * D + 4 * (4 * D + 2) + 12 * D);
-    const size_t form = (size_t)(4 * 16 * (kST / kWave) + 16 * kST) * sort_kpt(D);
+    const int kpt = sort_kpt(D);
+    const size_t form = (size_t)(4 * (kpt <= 2 ? 32 : 16) * (kST / kWave) + 16 * kST) * kpt;
     return emit > form ? emit : form;
 }
 
@@ -822,29 +823,32 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
     const int64_t maxlen = sblock_max<kST>(mylen);
     // sort to (length desc, view asc).  The buffer is already in view order within each
     // length: the returns come first, sorted, and every fetched view follows all views
-    // fetched before it.  So a stable LSD radix sort on the length alone, 4-bit digits
-    // taken descending, gives that order.  A digit's rank among equal digits comes from
+    // fetched before it.  So a stable LSD radix sort on the length alone, digits taken
+    // descending, gives that order (5-bit digits up to two keys per thread, 4-bit
+    // beyond, so that the counters fit one scan).  A digit's rank among equal digits comes from
     // lane ballots; the counts per (digit, slot, wave) are scanned in that order, which is
     // the order of positions t + c * kST.
     constexpr int kWaves = kST / kWave;
-    constexpr int kCnt = 16 * KPT * kWaves;
+    constexpr int kDig = KPT <= 2 ? 5 : 4;   // digit bits
+    constexpr int kBins = 1 << kDig;
+    constexpr int kCnt = kBins * KPT * kWaves;
     int32_t* cnt = reinterpret_cast<int32_t*>(lds);                                         // [kCnt]
     unsigned long long* sk_l = reinterpret_cast<unsigned long long*>(lds + 4 * kCnt);        // [P]
     int32_t* len = reinterpret_cast<int32_t*>(sk_l + P);                                     // [P]
     int32_t* nxt = len + P;                                                                  // [P]
     const int wv = tid / kWave;
     const int bits = 32 - __clz((int)maxlen);
-    for (int sh = 0; sh < bits; sh += 4) {
+    for (int sh = 0; sh < bits; sh += kDig) {
         for (int i = tid; i < kCnt; i += kST) cnt[i] = 0;
         __syncthreads();
         int dg[KPT], drank[KPT];   // digit, rank among equal digits of the wave
 #pragma unroll
         for (int c = 0; c < KPT; ++c) {
             const bool valid = tid + c * kST < nn;
-            const int d = 15 - ((key_len(x[c]) >> sh) & 15);
+            const int d = (kBins - 1) - ((key_len(x[c]) >> sh) & (kBins - 1));
             uint64_t m = __ballot(valid);
 #pragma unroll
-            for (int bt = 0; bt < 4; ++bt) {
+            for (int bt = 0; bt < kDig; ++bt) {
                 const bool on = (d >> bt) & 1;
                 const uint64_t bb = __ballot(valid && on);
                 m &= on ? bb : ~bb;

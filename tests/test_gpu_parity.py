@@ -71,6 +71,10 @@ def adversarial_windows():
     add("narrow_tile_edges", [rng.integers(3, 10, 3000), [], rng.integers(3, 10, 1500), rng.integers(1, 4, 700)], 24)
     add("narrow_tile_edges_nonjoin", [rng.integers(3, 10, 3000), rng.integers(3, 10, 1501)], 31, mode="nonjoin",
         quota=2500)
+    # more ranks than the LDS rank table (1024) and than a block's threads, some empty
+    add("many_ranks_w1500", [rng.integers(1, 2000, int(rng.integers(0, 12))) for _ in range(1500)], 8192)
+    per = [rng.integers(1, 2000, int(rng.integers(1, 9))) for _ in range(700)]
+    add("many_ranks_w700_nonjoin", per, 6000, mode="nonjoin", quota=sum(len(x) for x in per) // 2)
     return out
 
 

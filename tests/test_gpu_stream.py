@@ -94,6 +94,8 @@ def edge_cases():
     # one rank with 600,000 views: its emitted-view bits exceed the LDS budget and are set
     # in global memory
     add("long_rank", rng.integers(1, 12, 600000), 1, 64, 1024, 1024, [1024])
+    # more ranks than a round block has threads (the round decision loops over them)
+    add("many_ranks", rng.integers(1, 300, 4000), 600, 2000, 4, 4, [2] * 600)
     n = 2003
     for q in (1, 500, n + 1):
         add(f"nonjoin_q{q}", rng.integers(1, 2000, n), 4, 6000, 100, 150, [150, 90, 40, 150], mode="nonjoin",

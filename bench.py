@@ -13,7 +13,9 @@ schedule (one stream, plan then collate) is timed too.  Prints one JSON line:
                its average duration from HIP events on the launch stream, vs 8 TB/s;
                traffic = HBM bytes per call from the committed rocprofv3 counters
                (profiles/), reported only while the collate source is unchanged;
-               copy_ceiling_gbs = a plain 4 GiB device copy, as a practical ceiling
+               copy_ceiling_gbs = a plain 4 GiB device copy, as a practical ceiling;
+               mix_copy_gbs = a torch broadcast copy (1 GiB read, 4 GiB written) with the
+               collate's 1 : 4 read : write bytes
   cpu_baseline the CPU oracle on a bounded sample of the same workload (consecutive
                4-rank groups of the window, at least 10 s), single-threaded on this host
 """
@@ -126,6 +128,29 @@ def host_cpu():
     except OSError:
         pass
     return model, len(os.sched_getaffinity(0))
+
+
+def mix_copy(dev, gib=1.0, reps=5):
+    """torch broadcast copy of a `gib` GiB int32 array into a [4, n] output: 4 bytes read
+    for every 16 written, the collate's mix, through a library elementwise kernel."""
+    import numpy as np
+    import torch
+
+    m = int(gib * (1 << 30)) // 4
+    src = torch.ones(m, dtype=torch.int32, device=dev)
+    dst = torch.empty((4, m), dtype=torch.int32, device=dev)
+    view = src.unsqueeze(0).expand(4, m)
+    dst.copy_(view)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in ev:
+        a.record()
+        dst.copy_(view)
+        b.record()
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    del src, dst, view
+    torch.cuda.empty_cache()
+    return 20 * m / (ms * 1e-3) / 1e9
 
 
 def copy_ceiling(dev, gib=4.0, reps=5):
@@ -375,7 +400,9 @@ def main():
             f"collate {stream['collate_ms']:.1f} ms; two streams {stream['two_stream_ms_per_iteration']:.1f} ms "
             f"per iteration")
     copy_gbs = copy_ceiling(dev)
-    log(f"[bench] plain 4 GiB device copy: {copy_gbs:.0f} GB/s")
+    mix_gbs = mix_copy(dev)
+    log(f"[bench] plain 4 GiB device copy: {copy_gbs:.0f} GB/s; broadcast copy at the collate's 1:4 mix: "
+        f"{mix_gbs:.0f} GB/s")
 
     n = w.n
     K = pipe.num_slots
@@ -431,6 +458,7 @@ def main():
             "avg_launch_ms": collate_ms,
             "median_launch_ms": float(np.median(collate_all)),
             "copy_ceiling_gbs": copy_gbs,
+            "mix_copy_gbs": mix_gbs,
         },
     }
     if not args.no_cpu_baseline:

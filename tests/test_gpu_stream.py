@@ -210,6 +210,33 @@ def test_stream_window_workload():
     run_case("mm_stream", lens, perm, 8, w.budget, 1024, 1024, rate, full_collate=False)
 
 
+@pytest.mark.parametrize("quota_div", [1, 3])
+def test_stream_bimodal_nonjoin(quota_div):
+    # the bimodal 16-rank window's 1.05M samples streamed in non-join mode with two worker
+    # rates and a depth of 2048 (four sort keys per thread): quota N stops when the fast
+    # ranks finish, quota N/3 at the quota; plan, trace and weights exact, the collate on
+    # sampled elements
+    import torch
+    import paper_2606_19989_amd as odb
+
+    from _parity import compare_collate_sampled
+
+    w = synth.WORKLOADS["bimodal_w16x65536"].window()
+    lens = np.diff(w.tok_off)
+    perm = np.random.default_rng(79).permutation(len(lens)).astype(np.int32)
+    toks = synth.fill_tokens_torch(int(w.tok_off[-1]), "cuda")
+    sp, ref = run_case(f"bimodal_nonjoin_q{quota_div}", lens, perm, 16, 32768, 1024, 2048,
+                       np.array([1024, 512] * 8, np.int32), mode="nonjoin", quota=len(lens) // quota_div,
+                       full_collate=False, tokens=toks)
+    assert ref.sinfo["stop_reason"] == (oracle.STOP_RANK_FINISHED if quota_div == 1 else oracle.STOP_QUOTA)
+    outs = sp.collate()
+    torch.cuda.synchronize()
+    odb.odb_collate_status(sp.ws)
+    compare_collate_sampled(w, outs, ref)
+    del sp, outs, toks
+    torch.cuda.empty_cache()
+
+
 def test_stream_full_size():
     # the largest window's 16.7M samples streamed by 64 ranks with the paper's buffer
     # of 1024 and a budget in its L_max range; the benchmark times this configuration.

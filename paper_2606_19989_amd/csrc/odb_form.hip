@@ -53,9 +53,8 @@ __global__ void __launch_bounds__(kBlock) lengths_kernel(const int64_t* __restri
     uint32_t lmin = 0xFFFFFFFFu, lmax = 0;
     int64_t bad = LLONG_MAX;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
-        const int64_t a = tok_off[p];
-        int64_t l = tok_off[p + 1] - a;
+    auto one = [&](int64_t p, int64_t a, int64_t b) {
+        int64_t l = b - a;
         if (l < 1 || l > INT_MAX || a < 0) {
             bad = bad < p ? bad : p;
             l = 1;
@@ -63,7 +62,21 @@ __global__ void __launch_bounds__(kBlock) lengths_kernel(const int64_t* __restri
         len[p] = (int32_t)l;
         lmin = (uint32_t)l < lmin ? (uint32_t)l : lmin;
         lmax = (uint32_t)l > lmax ? (uint32_t)l : lmax;
+    };
+    // four grid-stride iterations at a time, their loads issued together: with the grid at
+    // full occupancy, one load in flight per lane leaves the kernel latency bound
+    int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (; p + 3 * stride < n; p += 4 * stride) {
+        int64_t a[4], b[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            a[k] = tok_off[p + k * stride];
+            b[k] = tok_off[p + k * stride + 1];
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) one(p + k * stride, a[k], b[k]);
     }
+    for (; p < n; p += stride) one(p, tok_off[p], tok_off[p + 1]);
     // one pair of atomics per block: lanes -> waves (shuffles) -> block (LDS)
     __shared__ uint32_t s_min[kBlock / kWave], s_max[kBlock / kWave];
 #pragma unroll

@@ -7,12 +7,13 @@
 //                    launched when the plan brings these row records itself.
 //   collate_kernel   stationary on the flat output: the four outputs share one element
 //                    index space [0, padded_elems).  The output is cut into steps of
-//                    kBlockStep elements; runs of kRunSteps consecutive steps are dealt
-//                    to the blocks round robin, so the blocks in flight read and write one
-//                    compact region of every array.  In a step every lane owns kGroups
-//                    groups of 4 consecutive elements (a wave's groups are 256 elements
-//                    apart) and stores each group as one aligned 16-byte non-temporal
-//                    store per output.
+//                    kBlockStep elements; a block works through runs of kRunSteps
+//                    consecutive steps, its first run by its index, later ones taken
+//                    from a counter in order, so the blocks in flight read and write one
+//                    compact region of every array and finish together.  In a step every
+//                    lane owns kGroups groups of 4 consecutive elements (a wave's groups
+//                    are 256 elements apart) and stores each group as one aligned 16-byte
+//                    non-temporal store per output.
 //
 // Row edges.  A group whose 4 elements cross from one row into the next (the next row in
 // the same tile, rows of at least 4 elements) takes the first row's part from its own
@@ -48,11 +49,13 @@ constexpr int kGroups = 1;                                           // groups p
 constexpr int64_t kGroupSpan = (int64_t)kWave * kVec;                // 256
 constexpr int64_t kWaveStep = kGroupSpan * kGroups;                  // 256
 constexpr int64_t kBlockStep = kWaveStep * (kCollateBlock / kWave);  // 1024
-constexpr int64_t kRunSteps = 128;                                   // consecutive steps per run
-// Three resident blocks (12 waves) per compute unit stream as fast as the six that the
-// register budget allows (both within 1% at 8 G elements), and they leave four wave slots
-// and half the registers of every SIMD to kernels on other streams: the grouping and
-// alignment of the next window can run beside this kernel instead of after it.
+// consecutive steps per run, a block's unit of work (64 measured best with runs taken from a
+// counter: 32 repositions too often, 128 and 256 leave a longer tail)
+constexpr int64_t kRunSteps = 64;
+// Three resident blocks (12 waves) per compute unit stream as fast as more would (four or
+// six were slower), and they leave four wave slots and half the registers of every SIMD
+// to kernels on other streams: the grouping and alignment of the next window can run
+// beside this kernel instead of after it.
 constexpr int kCollateBlocksPerCU = 3;
 
 typedef int v4i __attribute__((ext_vector_type(4)));
@@ -102,6 +105,7 @@ struct Plan {
                          // padding views); set in the kernel
     int64_t tok_end;     // tokens [0, tok_end) are addressable (tok_off[n], set in the kernel)
     int32_t* err;
+    unsigned long long* runs;   // counter of runs handed out after each block's first
 };
 
 // Position of a group's first element.
@@ -293,10 +297,25 @@ __device__ __forceinline__ v4i load_tokens(const Cursor& c, const RowRec& r, con
 
 // Next step of this block's sequence (runs of kRunSteps steps, run r to block r mod
 // gridDim.x), or -1 past its end.
-__device__ __forceinline__ int64_t next_step(int64_t s, int64_t nsteps, int64_t nruns) {
+// The step after s: the next step of its run, else the first step of the block's next
+// run.  A block's first run is its index; later runs are taken from a counter when a block
+// needs one, so blocks that meet cheaper runs take more of them (dealt statically, the
+// blocks of one launch finished up to 15% of the kernel's time apart).  Thread 0 keeps
+// the block's next run index fetched one run ahead (`pf`), so the atomic's latency is off
+// the pipeline; the waves of a block cross a run boundary at the same step, where the
+// index is handed to them through LDS.
+__device__ __forceinline__ int64_t next_step(int64_t s, int64_t nsteps, int64_t nruns, unsigned long long& pf,
+                                             unsigned long long* runs) {
     const int64_t r = s / kRunSteps;
     if (s + 1 < (r + 1) * kRunSteps && s + 1 < nsteps) return s + 1;
-    const int64_t r2 = r + gridDim.x;
+    __shared__ int64_t s_run;
+    if (threadIdx.x == 0) {
+        s_run = (int64_t)pf;
+        pf = atomicAdd(runs, 1ull) + gridDim.x;
+    }
+    __syncthreads();
+    const int64_t r2 = s_run;
+    __syncthreads();
     return r2 < nruns ? r2 * kRunSteps : -1;
 }
 
@@ -397,6 +416,10 @@ __device__ __forceinline__ void stage_values(const Stage& a, int64_t e, int64_t 
     }
 }
 
+__global__ void clear_runs_kernel(unsigned long long* runs) {
+    if (threadIdx.x == 0) *runs = 0;
+}
+
 __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t pad_id, int64_t capacity,
                                                                 int32_t* __restrict__ o_ids,
                                                                 int32_t* __restrict__ o_lab,
@@ -425,9 +448,11 @@ __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t 
     };
 
     // pipeline: step s0 is stored from stage a, s1's tokens load into b, s2's rows into c
+    unsigned long long pf = 0;
+    if (threadIdx.x == 0) pf = atomicAdd(p.runs, 1ull) + gridDim.x;
     int64_t s0 = (int64_t)blockIdx.x * kRunSteps;
-    int64_t s1 = next_step(s0, nsteps, nruns);
-    int64_t s2 = s1 >= 0 ? next_step(s1, nsteps, nruns) : -1;
+    int64_t s1 = next_step(s0, nsteps, nruns, pf, p.runs);
+    int64_t s2 = s1 >= 0 ? next_step(s1, nsteps, nruns, pf, p.runs) : -1;
     Stage X, Y, Z;
     {
         const int64_t e = elem(s0);
@@ -474,7 +499,7 @@ __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t 
         }                                                                                     \
         s0 = s1;                                                                              \
         s1 = s2;                                                                              \
-        s2 = s2 >= 0 ? next_step(s2, nsteps, nruns) : -1;                                     \
+        s2 = s2 >= 0 ? next_step(s2, nsteps, nruns, pf, p.runs) : -1;                         \
     }
     // unrolled three times so that no stage register is copied while its load is in flight
     for (;;) {
@@ -533,10 +558,13 @@ extern "C" int odb_collate(const odb_window_t* w, int64_t num_slots, const int32
         row_ts = ts;
         row_len = len;
     }
+    unsigned long long* runs = &ws_at<DevStatus>(d_ws, L.status)->collate_runs;
     Plan p{d_slot_tile_off, d_slot_maxlen, d_slot_rows, d_slot_row_off, row_ts, row_len, w->d_tokens,
-           w->d_token_offsets, num_slots, n, max_rows, 0, err};
-    // kCollateBlocksPerCU blocks per compute unit, all resident at once; runs are dealt
-    // round robin over them
+           w->d_token_offsets, num_slots, n, max_rows, 0, err, runs};
+    hipLaunchKernelGGL(clear_runs_kernel, dim3(1), dim3(64), 0, s, runs);
+    ODB_LAUNCHED();
+    // kCollateBlocksPerCU blocks per compute unit, all resident at once; each starts on the
+    // run of its index and then takes runs from the counter
     const unsigned grid = (unsigned)(num_cus() * kCollateBlocksPerCU);
     hipLaunchKernelGGL(collate_kernel, dim3(grid), dim3(kCollateBlock), 0, s, p, pad_id, out_capacity_elems,
                        d_input_ids, d_labels, d_attention_mask, d_position_ids);

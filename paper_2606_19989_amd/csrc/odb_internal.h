@@ -62,6 +62,7 @@ struct DevStatus {
     uint32_t min_len;
     uint32_t max_len;
     int32_t jump_changed[kMaxJumpRounds];
+    unsigned long long collate_runs;   // runs handed out by the collate beyond its first wave
 };
 
 // Per-rank alignment state, kept on the device across rounds.

@@ -311,13 +311,15 @@ __global__ void __launch_bounds__(kBlock) scan_tile_sums(Load load, int64_t n, O
     if (threadIdx.x == 0) partials[blockIdx.x] = s;
 }
 
+// One block of kBlock threads: a 1024-thread block would need a quarter of every SIMD's
+// wave slots on one compute unit, which a resident collate grid never leaves free.
 template <typename Out>
-__global__ void __launch_bounds__(1024) scan_partials(Out* partials, int64_t m) {
-    __shared__ Out wtot[1024 / kWave];
+__global__ void __launch_bounds__(kBlock) scan_partials(Out* partials, int64_t m) {
+    __shared__ Out wtot[kBlock / kWave];
     __shared__ Out carry_s;
     if (threadIdx.x == 0) carry_s = 0;
     __syncthreads();
-    for (int64_t base = 0; base < m; base += 1024) {
+    for (int64_t base = 0; base < m; base += kBlock) {
         int64_t i = base + threadIdx.x;
         Out v = i < m ? partials[i] : Out(0);
         Out inc = wave_incl_sum(v);
@@ -325,7 +327,8 @@ __global__ void __launch_bounds__(1024) scan_partials(Out* partials, int64_t m) 
         if ((threadIdx.x & (kWave - 1)) == kWave - 1) wtot[w] = inc;
         __syncthreads();
         Out pre = 0, tot = 0;
-        for (int k = 0; k < 1024 / kWave; ++k) {
+#pragma unroll
+        for (int k = 0; k < kBlock / kWave; ++k) {
             pre += (k < w) ? wtot[k] : Out(0);
             tot += wtot[k];
         }
@@ -360,7 +363,7 @@ int device_excl_scan(Load load, Store store, int64_t n, Out* partials, hipStream
     hipLaunchKernelGGL((scan_tile_sums<Out, Load>), dim3((unsigned)tiles), dim3(kBlock), 0, s,
                        load, n, partials);
     ODB_LAUNCHED();
-    hipLaunchKernelGGL((scan_partials<Out>), dim3(1), dim3(1024), 0, s, partials, tiles);
+    hipLaunchKernelGGL((scan_partials<Out>), dim3(1), dim3(kBlock), 0, s, partials, tiles);
     ODB_LAUNCHED();
     hipLaunchKernelGGL((scan_tiles<Out, Load, Store>), dim3((unsigned)tiles), dim3(kBlock), 0, s,
                        load, store, n, (const Out*)partials);

@@ -221,10 +221,12 @@ int odb_align_groups(const odb_window_t* w, int64_t budget, const odb_align_para
  *                       kernel, one random 16-byte read per row); with row records
  *                       d_emit_order is not read and may be NULL
  *   out_capacity_elems  length of each output array; elements beyond it are not written
- *   d_ws / ws_bytes     the workspace: a status word, and the gathered row records when
- *                       none are passed
+ *   d_ws / ws_bytes     the workspace: a status word, the counter from which the kernel's
+ *                       blocks take runs of steps, and the gathered row records when none
+ *                       are passed; two collates in flight at once need two workspaces
  *
- * Asynchronous (one kernel with row records, two without).  Accesses are bounds-checked
+ * Asynchronous (a counter clear and one kernel with row records, one kernel more
+ * without).  Accesses are bounds-checked
  * against the window and the plan: a row record outside the token stream or longer
  * than its tile, or an emitted id outside [0, n), sets a device status word that
  * odb_collate_status() reads (such a row is written as padding).

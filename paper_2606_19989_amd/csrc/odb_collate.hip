@@ -20,8 +20,10 @@
 // vector load and the next row's record and first tokens from uniform-address scalar
 // loads, one boundary lane of the wave at a time.  Scalar loads complete on their own
 // counter, so waiting for them does not wait for the stores the wave has in flight,
-// which a late vector load would (see below).  Other edge cases (tile edges, rows
-// shorter than 4) are finished element by element.
+// which a late vector load would (see below).  A group that crosses from the last row of
+// a tile into the next tile takes the same path when the next row holds the group's
+// remaining elements.  Other edge cases (rows shorter than 4, a next row too short) are
+// finished element by element.
 //
 // Software pipeline.  On CDNA the vector-memory counter covers loads and stores alike
 // and retires in order, so waiting for a load also waits for every store issued before
@@ -34,9 +36,8 @@
 // clamped addresses so none is ever skipped.
 //
 // A group's cursor (slot, row, column) advances with the step sequence: inside a tile it
-// moves by arithmetic, across tiles by a galloping search over the tile offsets.  When a
-// group's 4 elements lie in one row (the common case) its tokens arrive in one 16-byte
-// load; a group that straddles a row or tile edge is finished element by element.
+// moves by arithmetic, across tiles by a search over the tile offsets.  When a group's 4
+// elements lie in one row (the common case) its tokens arrive in one 16-byte load.
 #include "odb_internal.h"
 
 namespace odb {
@@ -52,9 +53,9 @@ constexpr int64_t kBlockStep = kWaveStep * (kCollateBlock / kWave);  // 1024
 // consecutive steps per run, a block's unit of work (64 measured best with runs taken from a
 // counter: 32 repositions too often, 128 and 256 leave a longer tail)
 constexpr int64_t kRunSteps = 64;
-// Three resident blocks (12 waves) per compute unit stream as fast as more would (four or
-// six were slower), and they leave four wave slots and half the registers of every SIMD
-// to kernels on other streams: the grouping and alignment of the next window can run
+// Three resident blocks (12 waves) per compute unit stream fastest (two, four, five or
+// six were slower), and they leave five of the eight wave slots and about half the
+// registers of every SIMD to kernels on other streams: the grouping and alignment of the next window can run
 // beside this kernel instead of after it.
 constexpr int kCollateBlocksPerCU = 3;
 
@@ -295,9 +296,7 @@ __device__ __forceinline__ v4i load_tokens(const Cursor& c, const RowRec& r, con
     return *reinterpret_cast<const v4i*>(p.tokens + a);
 }
 
-// Next step of this block's sequence (runs of kRunSteps steps, run r to block r mod
-// gridDim.x), or -1 past its end.
-// The step after s: the next step of its run, else the first step of the block's next
+// Next step of this block's sequence, or -1 past its end.  The step after s: the next step of its run, else the first step of the block's next
 // run.  A block's first run is its index; later runs are taken from a counter when a block
 // needs one, so blocks that meet cheaper runs take more of them (dealt statically, the
 // blocks of one launch finished up to 15% of the kernel's time apart).  Thread 0 keeps

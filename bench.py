@@ -3,9 +3,9 @@
 One step = grouping (odb_form_groups) + alignment with coverage check
 (odb_align_groups) + padded collation (odb_collate) + exact token-level loss-scaling
 weights (odb_loss_weights) of a whole window whose CSR token stream is already resident
-in HBM.  Steps run double-buffered on two HIP streams: the grouping and alignment of
-step i+1 (plan stream) run while the collate of step i (collate stream) streams its
-outputs; each step has its own plan buffers, the outputs are shared.  The serial
+in HBM.  Steps run double-buffered on two HIP streams: the grouping, alignment and loss
+weights of step i+1 (plan stream) run while the collate of step i (collate stream)
+streams its outputs; each step has its own plan buffers, the outputs are shared.  The serial
 schedule (one stream, plan then collate) is timed too.  Prints one JSON line:
 
   value        emitted samples per second (whole job)
@@ -55,11 +55,12 @@ def pipelined_steps(pipes, plan_stream, collate_stream, steps, plan=window_plan,
     """`steps` steps, double-buffered over the two pipelines in `pipes` (shared outputs):
     step i plans into pipes[i % 2] on `plan_stream` (`plan`: odb_form_groups +
     odb_align_groups for a window, odb_stream_plan for a streaming iteration) once that
-    pipeline's previous collate has finished, and collates on `collate_stream` once its
-    plan is done.  The plan calls synchronise only the plan stream, so while the host
-    waits for step i's plan the collate stream is still writing step i-1.  Returns the
-    host seconds of the whole loop (the collate stream drained) and per step the
-    HIP-event milliseconds of odb_collate and of the loss weights."""
+    pipeline's previous collate has finished, computes its loss weights there too (they
+    read only the plan), and collates on `collate_stream` once its plan is done.  The plan
+    calls synchronise only the plan stream, so while the host waits for step i's plan the
+    collate stream is still writing step i-1.  Returns the host seconds of the whole loop
+    (both streams drained) and per step the HIP-event milliseconds of odb_collate and of
+    the loss weights (the latter beside the previous step's collate)."""
     import torch
 
     free = [torch.cuda.Event(), torch.cuda.Event()]
@@ -72,20 +73,19 @@ def pipelined_steps(pipes, plan_stream, collate_stream, steps, plan=window_plan,
         p = pipes[i % 2]
         plan_stream.wait_event(free[i % 2])
         plan(p, plan_stream)
-        planned = torch.cuda.Event()
-        planned.record(plan_stream)
-        collate_stream.wait_event(planned)
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[2].record(plan_stream)
+        weights(p, plan_stream)
+        ev[3].record(plan_stream)
+        collate_stream.wait_event(ev[3])
         ev[0].record(collate_stream)
         p.collate(collate_stream)
         ev[1].record(collate_stream)
-        weights(p, collate_stream)
-        ev[2].record(collate_stream)
         free[i % 2].record(collate_stream)
         marks.append(ev)
     torch.cuda.synchronize()
     sec = time.perf_counter() - t0
-    return sec, [a.elapsed_time(b) for a, b, _ in marks], [b.elapsed_time(c) for _, b, c in marks]
+    return sec, [e[0].elapsed_time(e[1]) for e in marks], [e[2].elapsed_time(e[3]) for e in marks]
 
 
 def serial_steps(pipe, stream, steps):
@@ -215,8 +215,8 @@ def stream_timing(odb, w, tok_off, tokens, dev, plan_stream, collate_stream, ite
     """Logical iterations of the unified streaming loop over the window's samples as a
     dataset (odb_stream_plan: every round's fetch, grouping, alignment and emission), each
     followed by the collate of its plan.  Serial (host clock around each synchronising
-    call, one pipeline) and two-stream (iteration i+1's plan beside iteration i's collate
-    and loss weights, two pipelines sharing the outputs)."""
+    call, one pipeline) and two-stream (iteration i+1's plan and loss weights beside
+    iteration i's collate, two pipelines sharing the outputs)."""
     import numpy as np
     import torch
 
@@ -443,8 +443,8 @@ def main():
             "budget": w.budget,
             "mode": w.mode,
             "pad_fraction": info["pad_fraction"],
-            "schedule": "two HIP streams, double-buffered plans: grouping + alignment of step i+1 run "
-                        "beside the collate of step i",
+            "schedule": "two HIP streams, double-buffered plans: grouping + alignment + loss weights "
+                        "of step i+1 run beside the collate of step i",
         },
         "roofline": {
             "bound": "hbm",

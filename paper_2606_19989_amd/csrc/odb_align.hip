@@ -41,7 +41,7 @@ __device__ __forceinline__ T block_reduce(T v, Op op) {
     __shared__ T buf[kBlock];
     buf[threadIdx.x] = v;
     __syncthreads();
-    for (int s = kBlock / 2; s > 0; s >>= 1) {
+    for (unsigned s = kBlock / 2; s > 0; s >>= 1) {
         if (threadIdx.x < s) buf[threadIdx.x] = op(buf[threadIdx.x], buf[threadIdx.x + s]);
         __syncthreads();
     }
@@ -268,8 +268,6 @@ __global__ void __launch_bounds__(kBlock) group_sizes_kernel(const int32_t* __re
 
 // Per rank (one block each): split position or overflow selection.
 __global__ void __launch_bounds__(kBlock) adjust_kernel(RankState* ranks, const RoundState* __restrict__ rs,
-                                                        const int64_t* __restrict__ off,
-                                                        const int32_t* __restrict__ gstart,
                                                         const int32_t* __restrict__ gsize,
                                                         int32_t* __restrict__ ov_slot, int32_t* __restrict__ kept,
                                                         DevStatus* st) {
@@ -1223,8 +1221,8 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
         hipLaunchKernelGGL(group_sizes_kernel, dim3(gridn), dim3(kBlock), 0, s, (const int32_t*)gstart,
                            (const int64_t*)d_gbase, d_off, (const RankState*)d_ranks, W, gsize);
         ODB_LAUNCHED();
-        hipLaunchKernelGGL(adjust_kernel, dim3(W), dim3(kBlock), 0, s, d_ranks, (const RoundState*)d_rs, d_off,
-                           (const int32_t*)gstart, (const int32_t*)gsize, ov_slot, kept, st);
+        hipLaunchKernelGGL(adjust_kernel, dim3(W), dim3(kBlock), 0, s, d_ranks, (const RoundState*)d_rs,
+                           (const int32_t*)gsize, ov_slot, kept, st);
         ODB_LAUNCHED();
         hipLaunchKernelGGL(fill_i64_kernel, dim3(gridn), dim3(kBlock), 0, s, steps, max_cnt, (int64_t)0);
         ODB_LAUNCHED();

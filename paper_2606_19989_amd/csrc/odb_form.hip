@@ -555,7 +555,6 @@ int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget,
     int32_t* j1 = ws_at<int32_t>(ws, L.jmp1);
     uint8_t* marks = ws_at<uint8_t>(ws, L.marks);
     int32_t* incl = ws_at<int32_t>(ws, L.incl);
-    int32_t* gstart = ws_at<int32_t>(ws, L.gstart);
     DevStatus* st = ws_at<DevStatus>(ws, L.status);
     const unsigned grid = grid_for(n + 1, kBlock, (int64_t)num_cus() * kPlanBlocksPerCU);
     // distinct steps per rank: at most the distinct values of floor(budget / l), i.e. at

@@ -259,6 +259,34 @@ def test_collate_from_emit_order():
             assert torch.equal(a[:P], b)
 
 
+def test_collate_output_capacity():
+    # outputs shorter than the padded size: the first out_capacity elements are the
+    # oracle's and nothing at or past out_capacity is written, with and without row
+    # records, at capacities that end inside a group, a step and a run of steps
+    import torch
+    import paper_2606_19989_amd as odb
+
+    w = synth.WORKLOADS["ln512_w2x2048"].window()
+    ref = oracle.plan_window(w)
+    pipe, outs = run_gpu(w, pad_id=5)
+    compare_collate_full(w, outs, ref, 5)
+    P = int(pipe.info["padded_elems"])
+    assert P > 70000
+    sentinel = -12345
+    for cap in (0, 1, 3, 1023, 1025, 65 * 1024 + 7, P - 1):
+        for records in (True, False):
+            log(f"collate with out_capacity={cap} of {P}, row records={records}")
+            alt = tuple(torch.full((P + 64,), sentinel, dtype=torch.int32, device="cuda") for _ in range(4))
+            rec = dict(row_token_start=pipe.row_token_start, row_len=pipe.row_len) if records else {}
+            odb.odb_collate(pipe.win, pipe.num_slots, pipe.emit_order, pipe.slot_rows, pipe.slot_maxlen,
+                            pipe.slot_row_off, pipe.slot_tile_off, 5, cap, *alt, pipe.ws, **rec)
+            torch.cuda.synchronize()
+            odb.odb_collate_status(pipe.ws)
+            for a, b in zip(alt, outs):
+                assert torch.equal(a[:cap], b[:cap])
+                assert bool((a[cap:] == sentinel).all())
+
+
 def _formed(w):
     import torch
     import paper_2606_19989_amd as odb

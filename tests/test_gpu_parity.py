@@ -287,6 +287,39 @@ def test_collate_output_capacity():
                 assert bool((a[cap:] == sentinel).all())
 
 
+def test_concurrent_collates():
+    # two collates in flight at once on two streams, each with its own workspace (and so
+    # its own run counter) and outputs, repeated: both give the oracle's outputs
+    import torch
+    import paper_2606_19989_amd as odb
+
+    w = synth.WORKLOADS["ln512_w2x2048"].window()
+    ref = oracle.plan_window(w)
+    pipes = []
+    for pad in (2, 9):
+        pipe, outs = run_gpu(w, pad_id=pad)
+        compare_collate_full(w, outs, ref, pad)
+        pipes.append((pipe, outs, pad))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    P = int(pipes[0][0].info["padded_elems"])
+    alts = [tuple(torch.full((P,), -1, dtype=torch.int32, device="cuda") for _ in range(4)) for _ in pipes]
+    torch.cuda.synchronize()
+    for rep in range(3):
+        log(f"two concurrent collates, repetition {rep}")
+        for (pipe, _, pad), alt, st in zip(pipes, alts, streams):
+            odb.odb_collate(pipe.win, pipe.num_slots, pipe.emit_order, pipe.slot_rows, pipe.slot_maxlen,
+                            pipe.slot_row_off, pipe.slot_tile_off, pad, P, *alt, pipe.ws, st,
+                            row_token_start=pipe.row_token_start, row_len=pipe.row_len)
+        torch.cuda.synchronize()
+        for (pipe, outs, _), alt in zip(pipes, alts):
+            odb.odb_collate_status(pipe.ws)
+            for a, b in zip(alt, outs):
+                assert torch.equal(a, b)
+            for a in alt:
+                a.fill_(-1)
+        torch.cuda.synchronize()
+
+
 def _formed(w):
     import torch
     import paper_2606_19989_amd as odb

@@ -13,7 +13,7 @@
  *   odb_length_sketch CV and short-sample fraction of sketched lengths  (Sec. 1, practical
  *                     (return-on-investment screen)                      guidance section)
  *   odb_stream_plan   the unified streaming loop: one logical sampler    (Sec. 2.3, App. C,
- *                     iteration, round by round (fetch, skip, emit,       App. F)
+ *                     iteration, round by round (fetch, skip, emit,       App. E)
  *                     stop), into the same plan layout
  *
  * Conventions shared by every entry point
@@ -225,11 +225,13 @@ int odb_align_groups(const odb_window_t* w, int64_t budget, const odb_align_para
  *                       blocks take runs of steps, and the gathered row records when none
  *                       are passed; two collates in flight at once need two workspaces
  *
- * Asynchronous (a counter clear and one kernel with row records, one kernel more
- * without).  Accesses are bounds-checked
- * against the window and the plan: a row record outside the token stream or longer
- * than its tile, or an emitted id outside [0, n), sets a device status word that
- * odb_collate_status() reads (such a row is written as padding).
+ * Asynchronous (a clear of the counter and the status word, and one kernel with row
+ * records, one kernel more without).  Accesses are bounds-checked against the window
+ * and the plan: a row record outside the token stream or longer than its tile, or an
+ * emitted id outside [0, n), sets the workspace's collate status word (such a row is
+ * written as padding).  Each odb_collate clears that word when it starts; no other
+ * entry point touches it, so odb_collate_status() reports the last collate on the
+ * workspace even after later grouping or alignment calls on it.
  */
 int odb_collate(const odb_window_t* w, int64_t num_slots,
                 const int32_t* d_emit_order, const int64_t* d_row_token_start,
@@ -252,7 +254,7 @@ int odb_check_coverage(const odb_window_t* w, const int32_t* d_emitted, int64_t 
                        const int32_t* d_leftover, int64_t num_leftover,
                        odb_plan_info_t* h_info, void* d_ws, size_t ws_bytes, void* stream);
 
-/* Loss-scaling weight modes (App. B and the loss-scaling ablation of App. I). */
+/* Loss-scaling weight modes (App. B and the loss-scaling ablation of App. N). */
 typedef enum odb_weight_mode {
     ODB_WEIGHT_SAMPLE = 0,         /* n_{r,j} / sum_r n_{r,j}                                  */
     ODB_WEIGHT_TOKEN_APPROX = 1,   /* a_{r,j} / sum_r a_{r,j}, a = d_slot_tokens_approx         */
@@ -377,7 +379,7 @@ size_t odb_stream_workspace_size(const odb_window_t* w, int32_t depth, int64_t s
 
 /*
  * One logical iteration of the unified loop (Sec. 2.3 "Unified loop and termination",
- * App. C state and transition rules, App. F state machine) over the window's samples
+ * App. C state and transition rules, App. E state machine) over the window's samples
  * taken as dataset identities 0..N-1 (rank_offsets of the window are not used; W is
  * num_ranks).
  *

@@ -111,6 +111,8 @@ def _bind(path: str):
     lib.oracle_collate.argtypes = [P, P, P, ctypes.c_int32, P, P, P, P]
     lib.oracle_collate_rank.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int32, P, P, P, P]
     lib.oracle_collate_rank.restype = ctypes.c_int
+    lib.oracle_collate_rank_all.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int32, P, P, P, P]
+    lib.oracle_collate_rank_all.restype = ctypes.c_int
     lib.oracle_round_targets.argtypes = [P, P]
     lib.oracle_slots_approx.argtypes = [P, P]
     lib.oracle_loss_weights.argtypes = [P, ctypes.c_int32, P, P, P]
@@ -212,10 +214,13 @@ class Plan:
             raise OracleError(f"unknown loss-weight mode {mode}")
         return wt, st, ss
 
-    def collate_rank(self, r: int, tok_off: np.ndarray, rank_tokens: np.ndarray, pad_id: int = 0):
+    def collate_rank(self, r: int, tok_off: np.ndarray, rank_tokens: np.ndarray, pad_id: int = 0,
+                     whole_stream: bool = False):
         """Rank r's tiles only: four int32 arrays covering output positions
         [slot_tile_off[r * steps], slot_tile_off[(r + 1) * steps]).  ``rank_tokens`` holds
-        the CSR positions owned by rank r's samples (from its first sample's offset)."""
+        the CSR positions owned by rank r's samples (from its first sample's offset), or,
+        with ``whole_stream``, the whole token stream (streaming plans, whose rows are
+        identities from anywhere in the dataset)."""
         lib = _load()
         if not 0 <= r < self.W:
             raise OracleError(f"rank {r} out of range")
@@ -224,8 +229,9 @@ class Plan:
         outs = [np.empty(P, dtype=np.int32) for _ in range(4)]
         tok_off = np.ascontiguousarray(tok_off, dtype=np.int64)
         rank_tokens = np.ascontiguousarray(rank_tokens, dtype=np.int32)
-        if lib.oracle_collate_rank(ctypes.c_void_p(self._handle), int(r), _ptr(tok_off), _ptr(rank_tokens),
-                                   int(pad_id), *[_ptr(o) for o in outs]) != 0:
+        fn = lib.oracle_collate_rank_all if whole_stream else lib.oracle_collate_rank
+        if fn(ctypes.c_void_p(self._handle), int(r), _ptr(tok_off), _ptr(rank_tokens), int(pad_id),
+              *[_ptr(o) for o in outs]) != 0:
             raise OracleError(f"rank {r} out of range")
         return tuple(outs)
 
@@ -394,6 +400,16 @@ class StreamPlan(Plan):
         self._handle = self._stream_handle
         try:
             return super().collate(tok_off, tokens, pad_id)
+        finally:
+            self._handle = 0
+
+    def collate_rank(self, r: int, tok_off, tokens, pad_id: int = 0, whole_stream: bool = True):
+        """Rank r's tiles; ``tokens`` is the whole token stream."""
+        if not whole_stream:
+            raise OracleError("a streaming plan's rows need the whole token stream")
+        self._handle = self._stream_handle
+        try:
+            return super().collate_rank(r, tok_off, tokens, pad_id, whole_stream=True)
         finally:
             self._handle = 0
 

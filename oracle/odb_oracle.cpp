@@ -18,7 +18,7 @@
 //   * padding fraction                          throughput-decomposition definition (App. I)
 //   * identity coverage                         App. C (terminal identity coverage)
 //   * loss-scaling weights (sample, approximate  Eq. 2 (Sec. 2.3 "Loss scaling"), App. B,
-//     and exact token level), second-gather      and the loss-scaling ablation (App. I)
+//     and exact token level), second-gather      and the loss-scaling ablation (App. N)
 //     predicate
 // Where the paper is silent the oracle takes the readings documented in the
 // repository's design notes (tie order, list order, trailing group, canonical
@@ -392,7 +392,7 @@ bool run(Result& R, int32_t W, int64_t n, const int64_t* rank_off, const int64_t
 }
 
 // ------------------------------------------------------------------ unified loop
-// The streaming protocol of Sec. 2.3 ("Unified loop and termination") and App. C/F,
+// The streaming protocol of Sec. 2.3 ("Unified loop and termination") and App. C/E,
 // with the per-rank state of App. C: sampler-pending views R_r, the collate buffer B_r
 // (the worker queue is folded into it: a fetched view lands in the buffer in the same
 // round), and emitted views E_r.
@@ -875,6 +875,18 @@ int oracle_collate_rank(void* h, int32_t r, const int64_t* tok_off, const int32_
     if (r < 0 || r >= R.W) return -1;
     const int64_t base = tok_off[R.rank_off[(size_t)r]];
     collate_ranks(R, r, r + 1, tok_off, tokens, base, pad_id, input_ids, labels, attention_mask, position_ids);
+    return 0;
+}
+
+// One rank's tiles as oracle_collate_rank, with `tokens` the whole token stream (CSR
+// position k at tokens[k]): for streaming plans, whose rows carry identities from anywhere
+// in the dataset.  Returns 0, or -1 for a rank out of range.
+int oracle_collate_rank_all(void* h, int32_t r, const int64_t* tok_off, const int32_t* tokens, int32_t pad_id,
+                            int32_t* input_ids, int32_t* labels, int32_t* attention_mask,
+                            int32_t* position_ids) {
+    const Result& R = *static_cast<Result*>(h);
+    if (r < 0 || r >= R.W) return -1;
+    collate_ranks(R, r, r + 1, tok_off, tokens, 0, pad_id, input_ids, labels, attention_mask, position_ids);
     return 0;
 }
 

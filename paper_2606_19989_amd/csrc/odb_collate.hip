@@ -416,8 +416,12 @@ __device__ __forceinline__ void stage_values(const Stage& a, int64_t e, int64_t 
     }
 }
 
-__global__ void clear_runs_kernel(unsigned long long* runs) {
-    if (threadIdx.x == 0) *runs = 0;
+// Start of a collate: the run counter and the error word of this call.
+__global__ void clear_collate_kernel(unsigned long long* runs, int32_t* err) {
+    if (threadIdx.x == 0) {
+        *runs = 0;
+        *err = 0;
+    }
 }
 
 __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t pad_id, int64_t capacity,
@@ -510,6 +514,70 @@ __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t 
 #undef ODB_COLLATE_STEP
 }
 
+
+// Host checks shared by the collate entry points.  Sets *empty when there is nothing to
+// write (no slots, no capacity or no samples).
+int check_collate_args(const odb_window_t* w, int64_t num_slots, const int32_t* d_emit_order,
+                       const int64_t* d_row_token_start, const int32_t* d_row_len, const int32_t* d_slot_rows,
+                       const int32_t* d_slot_maxlen, const int64_t* d_slot_row_off, const int64_t* d_slot_tile_off,
+                       int64_t out_capacity_elems, int32_t* d_input_ids, int32_t* d_labels,
+                       int32_t* d_attention_mask, int32_t* d_position_ids, bool* empty) {
+    if (num_slots < 0 || num_slots >= 0x7FFFFFFFll)
+        return set_error(ODB_E_INVALID_ARG, "num_slots must be in [0, 2^31 - 1)");
+    if (out_capacity_elems < 0) return set_error(ODB_E_INVALID_ARG, "out_capacity_elems must be >= 0");
+    if ((d_row_token_start == nullptr) != (d_row_len == nullptr))
+        return set_error(ODB_E_INVALID_ARG, "d_row_token_start and d_row_len are given together or not at all");
+    *empty = num_slots == 0 || out_capacity_elems == 0 || w->num_samples == 0;
+    if (*empty) return ODB_OK;
+    if (!d_slot_rows || !d_slot_maxlen || !d_slot_row_off || !d_slot_tile_off)
+        return set_error(ODB_E_INVALID_ARG, "plan arrays must not be NULL");
+    if (!d_input_ids || !d_labels || !d_attention_mask || !d_position_ids)
+        return set_error(ODB_E_INVALID_ARG, "output arrays must not be NULL");
+    if (((reinterpret_cast<uintptr_t>(d_input_ids) | reinterpret_cast<uintptr_t>(d_labels) |
+          reinterpret_cast<uintptr_t>(d_attention_mask) | reinterpret_cast<uintptr_t>(d_position_ids)) &
+         15) != 0)
+        return set_error(ODB_E_INVALID_ARG, "output arrays must be 16-byte aligned");
+    if (!d_row_token_start && !d_emit_order) return set_error(ODB_E_INVALID_ARG, "d_emit_order is NULL");
+    return ODB_OK;
+}
+
+// The launches of one collate: clear the run counter and the error word, gather the row
+// records into (row_ts, row_len) when the plan brings none (capacity n + W - 1 rows),
+// then the collate kernel.  `err` and `runs` are device words of the caller's choosing.
+int launch_collate(const odb_window_t* w, int64_t num_slots, const int32_t* d_emit_order,
+                   const int64_t* d_row_token_start, const int32_t* d_row_len, const int32_t* d_slot_rows,
+                   const int32_t* d_slot_maxlen, const int64_t* d_slot_row_off, const int64_t* d_slot_tile_off,
+                   int32_t pad_id, int64_t out_capacity_elems, int32_t* d_input_ids, int32_t* d_labels,
+                   int32_t* d_attention_mask, int32_t* d_position_ids, bool empty, int32_t* err,
+                   unsigned long long* runs, int64_t* row_ts, int32_t* row_len, hipStream_t s) {
+    hipLaunchKernelGGL(clear_collate_kernel, dim3(1), dim3(64), 0, s, runs, err);
+    ODB_LAUNCHED();
+    if (empty) return ODB_OK;
+    const int64_t n = w->num_samples;
+    // a plan may list a sample more than once only through sampler padding: at most
+    // W - 1 extra rows (streaming plans)
+    const int64_t max_rows = n + w->num_ranks - 1;
+    const int64_t* rts = d_row_token_start;
+    const int32_t* rlen = d_row_len;
+    if (!rts) {
+        hipLaunchKernelGGL(row_info_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * kPlanBlocksPerCU)),
+                           dim3(kBlock), 0, s, w->d_token_offsets, n, max_rows, d_emit_order, d_slot_row_off,
+                           num_slots, row_ts, row_len, err);
+        ODB_LAUNCHED();
+        rts = row_ts;
+        rlen = row_len;
+    }
+    Plan p{d_slot_tile_off, d_slot_maxlen, d_slot_rows, d_slot_row_off, rts, rlen, w->d_tokens,
+           w->d_token_offsets, num_slots, n, max_rows, 0, err, runs};
+    // kCollateBlocksPerCU blocks per compute unit, all resident at once; each starts on the
+    // run of its index and then takes runs from the counter
+    const unsigned grid = (unsigned)(num_cus() * kCollateBlocksPerCU);
+    hipLaunchKernelGGL(collate_kernel, dim3(grid), dim3(kCollateBlock), 0, s, p, pad_id, out_capacity_elems,
+                       d_input_ids, d_labels, d_attention_mask, d_position_ids);
+    ODB_LAUNCHED();
+    return ODB_OK;
+}
+
 }  // namespace
 
 }  // namespace odb
@@ -524,52 +592,16 @@ extern "C" int odb_collate(const odb_window_t* w, int64_t num_slots, const int32
                            int32_t* d_position_ids, void* d_ws, size_t ws_bytes, void* stream) {
     Layout L;
     ODB_TRY(check_workspace(w, d_ws, ws_bytes, &L));
-    if (num_slots < 0 || num_slots >= 0x7FFFFFFFll)
-        return set_error(ODB_E_INVALID_ARG, "num_slots must be in [0, 2^31 - 1)");
-    if (out_capacity_elems < 0) return set_error(ODB_E_INVALID_ARG, "out_capacity_elems must be >= 0");
-    if ((d_row_token_start == nullptr) != (d_row_len == nullptr))
-        return set_error(ODB_E_INVALID_ARG, "d_row_token_start and d_row_len are given together or not at all");
-    if (num_slots == 0 || out_capacity_elems == 0) return ODB_OK;
-    if (!d_slot_rows || !d_slot_maxlen || !d_slot_row_off || !d_slot_tile_off)
-        return set_error(ODB_E_INVALID_ARG, "plan arrays must not be NULL");
-    if (!d_input_ids || !d_labels || !d_attention_mask || !d_position_ids)
-        return set_error(ODB_E_INVALID_ARG, "output arrays must not be NULL");
-    if (((reinterpret_cast<uintptr_t>(d_input_ids) | reinterpret_cast<uintptr_t>(d_labels) |
-          reinterpret_cast<uintptr_t>(d_attention_mask) | reinterpret_cast<uintptr_t>(d_position_ids)) &
-         15) != 0)
-        return set_error(ODB_E_INVALID_ARG, "output arrays must be 16-byte aligned");
-    const int64_t n = w->num_samples;
-    if (n == 0) return ODB_OK;  // no rows: every tile is empty
-    const bool have_rows = d_row_token_start != nullptr;
-    if (!have_rows && !d_emit_order) return set_error(ODB_E_INVALID_ARG, "d_emit_order is NULL");
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    // a plan may list a sample more than once only through sampler padding: at most
-    // W - 1 extra rows (streaming plans)
-    const int64_t max_rows = n + w->num_ranks - 1;
-    int32_t* err = &ws_at<DevStatus>(d_ws, L.status)->collate_err;
-    const int64_t* row_ts = d_row_token_start;
-    const int32_t* row_len = d_row_len;
-    if (!have_rows) {
-        int64_t* ts = ws_at<int64_t>(d_ws, L.row_ts);
-        int32_t* len = ws_at<int32_t>(d_ws, L.row_len);
-        hipLaunchKernelGGL(row_info_kernel, dim3(grid_for(n, kBlock, (int64_t)num_cus() * kPlanBlocksPerCU)), dim3(kBlock), 0, s,
-                           w->d_token_offsets, n, max_rows, d_emit_order, d_slot_row_off, num_slots, ts, len, err);
-        ODB_LAUNCHED();
-        row_ts = ts;
-        row_len = len;
-    }
-    unsigned long long* runs = &ws_at<DevStatus>(d_ws, L.status)->collate_runs;
-    Plan p{d_slot_tile_off, d_slot_maxlen, d_slot_rows, d_slot_row_off, row_ts, row_len, w->d_tokens,
-           w->d_token_offsets, num_slots, n, max_rows, 0, err, runs};
-    hipLaunchKernelGGL(clear_runs_kernel, dim3(1), dim3(64), 0, s, runs);
-    ODB_LAUNCHED();
-    // kCollateBlocksPerCU blocks per compute unit, all resident at once; each starts on the
-    // run of its index and then takes runs from the counter
-    const unsigned grid = (unsigned)(num_cus() * kCollateBlocksPerCU);
-    hipLaunchKernelGGL(collate_kernel, dim3(grid), dim3(kCollateBlock), 0, s, p, pad_id, out_capacity_elems,
-                       d_input_ids, d_labels, d_attention_mask, d_position_ids);
-    ODB_LAUNCHED();
-    return ODB_OK;
+    bool empty = false;
+    ODB_TRY(check_collate_args(w, num_slots, d_emit_order, d_row_token_start, d_row_len, d_slot_rows, d_slot_maxlen,
+                               d_slot_row_off, d_slot_tile_off, out_capacity_elems, d_input_ids, d_labels,
+                               d_attention_mask, d_position_ids, &empty));
+    DevStatus* st = ws_at<DevStatus>(d_ws, L.status);
+    return launch_collate(w, num_slots, d_emit_order, d_row_token_start, d_row_len, d_slot_rows, d_slot_maxlen,
+                          d_slot_row_off, d_slot_tile_off, pad_id, out_capacity_elems, d_input_ids, d_labels,
+                          d_attention_mask, d_position_ids, empty, &st->collate_err, &st->collate_runs,
+                          ws_at<int64_t>(d_ws, L.row_ts), ws_at<int32_t>(d_ws, L.row_len),
+                          static_cast<hipStream_t>(stream));
 }
 
 __global__ void clear_collate_status_kernel(DevStatus* st) {

@@ -128,10 +128,12 @@ int check_workspace(const odb_window_t* w, void* d_ws, size_t ws_bytes, Layout* 
     return ODB_OK;
 }
 
+// The collate's error word is left alone: odb_collate clears it when it starts and
+// odb_collate_status when it has read it, so a plan call made on the same workspace in
+// between does not erase a collate error.
 __global__ void init_status_kernel(DevStatus* st) {
     if (threadIdx.x == 0) {
         st->err = 0;
-        st->collate_err = 0;
         st->first_bad = 0x7FFFFFFFFFFFFFFFll;
         st->min_len = 0xFFFFFFFFu;
         st->max_len = 0;

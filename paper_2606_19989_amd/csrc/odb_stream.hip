@@ -1,4 +1,4 @@
-// The unified streaming loop (Sec. 2.3 "Unified loop and termination"; App. C, App. F):
+// The unified streaming loop (Sec. 2.3 "Unified loop and termination"; App. C, App. E):
 // one logical sampler iteration of W ranks, round by round, on the device.
 //
 // Per-rank state (App. C): sampler-pending views R_r (a cursor into the rank's view

@@ -1,5 +1,5 @@
 // Loss-scaling weights of an aligned plan (Sec. 2.3 "Loss scaling", Eq. 2, App. B, and
-// the three scaling modes of the loss-scaling ablation in App. I).
+// the three scaling modes of the loss-scaling ablation in App. N).
 //
 // At step j every rank r trains on its slot (r, j).  DDP averages the ranks' per-token
 // mean losses, so rank r pre-scales its mean by W * w_{r,j}; the exact token-level weight

@@ -166,3 +166,29 @@ def collate_properties(outs, ref, pad_id=0, chunk=1 << 30):
         del m, pad
     assert real == ref.info["real_tokens"]
     return real
+
+
+def compare_collate_by_rank_whole_stream(tok_off, outs, ref, tokens_dev, pad_id=0, check_tokens=1_000_000, seed=0):
+    """Every element of the four outputs of a plan whose rows come from anywhere in the
+    token stream (streaming plans: a rank's views are identities spread over the whole
+    dataset).  The device token stream (written by the seeded generator) is copied back
+    once and a sample of it checked against the generator; then, rank by rank, the
+    oracle collates that rank's tiles from it and the GPU slice is compared."""
+    rng = np.random.default_rng(seed)
+    toks = tokens_dev.cpu().numpy()
+    if len(toks):
+        k = np.unique(np.concatenate([rng.integers(0, len(toks), size=min(check_tokens, len(toks))),
+                                      [0, len(toks) - 1]]))
+        assert np.array_equal(toks[k], synth.token_ids(k).astype(np.int32)), "token stream"
+    S = ref.steps
+    for r in range(ref.W):
+        want = ref.collate_rank(r, tok_off, toks, pad_id, whole_stream=True)
+        lo, hi = int(ref.slot_tile_off[r * S]), int(ref.slot_tile_off[(r + 1) * S])
+        for name, g, e in zip(["input_ids", "labels", "attention_mask", "position_ids"], outs, want):
+            got = g[lo:hi].cpu().numpy()
+            if not np.array_equal(got, e):
+                bad = np.nonzero(got != e)[0]
+                raise AssertionError(f"{name}: rank {r}: {len(bad)} mismatches, first at {lo + bad[0]}: "
+                                     f"{got[bad[0]]} vs {e[bad[0]]}")
+        del want
+    del toks

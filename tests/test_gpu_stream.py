@@ -207,19 +207,32 @@ def test_stream_window_workload():
     rng = np.random.default_rng(73)
     perm = rng.permutation(len(lens)).astype(np.int32)
     rate = np.array([1024, 512, 1024, 256, 1024, 1024, 768, 1024], dtype=np.int32)
-    run_case("mm_stream", lens, perm, 8, w.budget, 1024, 1024, rate, full_collate=False)
+    import torch
+    import paper_2606_19989_amd as odb
+
+    from _parity import compare_collate_by_rank_whole_stream
+
+    toks = synth.fill_tokens_torch(int(w.tok_off[-1]), "cuda")
+    sp, ref = run_case("mm_stream", lens, perm, 8, w.budget, 1024, 1024, rate, full_collate=False, tokens=toks)
+    outs = sp.collate()
+    torch.cuda.synchronize()
+    odb.odb_collate_status(sp.ws)
+    compare_collate_by_rank_whole_stream(w.tok_off, outs, ref, toks)
+    log("  every stream collate element equal")
+    del sp, outs, toks
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("quota_div", [1, 3])
 def test_stream_bimodal_nonjoin(quota_div):
     # the bimodal 16-rank window's 1.05M samples streamed in non-join mode with two worker
     # rates and a depth of 2048 (four sort keys per thread): quota N stops when the fast
-    # ranks finish, quota N/3 at the quota; plan, trace and weights exact, the collate on
-    # sampled elements
+    # ranks finish, quota N/3 at the quota; plan, trace, weights and every collate element
+    # exact
     import torch
     import paper_2606_19989_amd as odb
 
-    from _parity import compare_collate_sampled
+    from _parity import compare_collate_by_rank_whole_stream, compare_collate_sampled
 
     w = synth.WORKLOADS["bimodal_w16x65536"].window()
     lens = np.diff(w.tok_off)
@@ -233,6 +246,8 @@ def test_stream_bimodal_nonjoin(quota_div):
     torch.cuda.synchronize()
     odb.odb_collate_status(sp.ws)
     compare_collate_sampled(w, outs, ref)
+    compare_collate_by_rank_whole_stream(w.tok_off, outs, ref, toks)
+    log("  every stream collate element equal")
     del sp, outs, toks
     torch.cuda.empty_cache()
 
@@ -240,11 +255,11 @@ def test_stream_bimodal_nonjoin(quota_div):
 def test_stream_full_size():
     # the largest window's 16.7M samples streamed by 64 ranks with the paper's buffer
     # of 1024 and a budget in its L_max range; the benchmark times this configuration.
-    # Plan, trace and weights are compared exactly; collate on sampled elements plus
-    # whole-output properties
+    # Plan, trace, weights and every collate element (8.5 G per output) are compared
+    # exactly
     import torch
 
-    from _parity import collate_properties, compare_collate_sampled
+    from _parity import collate_properties, compare_collate_by_rank_whole_stream, compare_collate_sampled
 
     w = synth.WORKLOADS["ln480_w64x262144"].window()
     lens = np.diff(w.tok_off)
@@ -259,6 +274,8 @@ def test_stream_full_size():
     compare_collate_sampled(w, outs, ref)
     collate_properties(outs, ref)
     log("  stream collate sampled and properties equal")
+    compare_collate_by_rank_whole_stream(w.tok_off, outs, ref, toks)
+    log("  every stream collate element equal")
     del sp, outs, toks
     torch.cuda.empty_cache()
 

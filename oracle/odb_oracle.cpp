@@ -27,6 +27,7 @@
 // Build: g++ -O2 -std=c++17 -ffp-contract=off -shared -fPIC odb_oracle.cpp -o libodb_oracle.so
 
 #include <algorithm>
+#include <cstddef>
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
@@ -118,48 +119,57 @@ GroupList form_groups(const std::vector<int32_t>& buffer, const std::vector<int6
     return formed;
 }
 
-// The worked example (App. D) lists the finished groups "from short to long" with each
-// group's members in ascending length.  reading: that list is the exact reverse of the
-// formation order, group by group and member by member.
-GroupList paper_list_order(const GroupList& formed) {
-    GroupList list(formed.rbegin(), formed.rend());
-    for (Group& g : list) std::reverse(g.begin(), g.end());
-    return list;
-}
-
-// Algorithm 1, split branch: while the rank has fewer than T groups and some group has
-// at least two samples, scan the list from its last group backwards, take the first
-// group with >= 2 samples and move its last sample into a new singleton group.
-// reading: the new singleton is appended at the end of the list.
-int64_t split_to(GroupList& list, int64_t T) {
-    int64_t splits = 0;
-    while ((int64_t)list.size() < T) {
-        bool found = false;
-        for (int64_t i = (int64_t)list.size() - 1; i >= 0; --i) {
-            if (list[i].size() >= 2) {
-                int32_t x = list[i].back();
-                list[i].pop_back();
-                list.push_back(Group{x});
-                ++splits;
-                found = true;
-                break;
-            }
+// Algorithm 1, split branch (reading R4).  A rank with fewer than T groups makes up the
+// difference with singletons peeled off multi-sample groups.  Read against the App. D
+// list (short groups first, members ascending), the group it peels from is the one
+// holding the longest samples among those with two or more members, and the sample it
+// peels is that group's longest.  Over the formation-order list (longest group first,
+// members longest first) this means: the first group in formation order that still has
+// two or more members gives up its first member, one peel at a time, until the rank has
+// T groups or every group is a singleton.  A group that is down to one member is passed
+// and the next one gives.  The peeled singleton goes in front of its donor (where in the
+// list is immaterial: the emission order is canonical).  Returns the number of peels.
+int64_t split_to(GroupList& formed, int64_t T) {
+    int64_t need = T - (int64_t)formed.size();
+    int64_t peels = 0;
+    GroupList out;
+    for (Group& g : formed) {
+        size_t first = 0;
+        while (need > 0 && g.size() - first >= 2) {
+            out.push_back(Group{g[first]});
+            ++first;
+            --need;
+            ++peels;
         }
-        if (!found) break;
+        out.push_back(Group(g.begin() + (std::ptrdiff_t)first, g.end()));
     }
-    return splits;
+    formed.swap(out);
+    return peels;
 }
 
-// Algorithm 1, overflow branch: sort the groups by size (descending), keep the first T
-// and return the samples of the rest to the buffer (overflow recirculation).
-// reading: the sort is stable over the short-to-long list, so among equal sizes the
-// group nearer the short end is kept.
-void overflow_to(GroupList& list, int64_t T, std::vector<int32_t>& returned) {
-    std::stable_sort(list.begin(), list.end(),
-                     [](const Group& a, const Group& b) { return a.size() > b.size(); });
-    for (size_t i = (size_t)T; i < list.size(); ++i)
-        for (int32_t x : list[i]) returned.push_back(x);
-    list.resize((size_t)T);
+// Algorithm 1, overflow branch (reading R6).  A rank with more than T groups keeps the T
+// largest and sends the samples of the others back to its buffer.  Equal sizes are
+// decided in favour of the group formed later (shorter samples): the App. D list puts
+// later-formed groups first and the paper's sort by size keeps their relative order.
+// Works on the formation-order list; the kept groups stay in formation order.
+void overflow_to(GroupList& formed, int64_t T, std::vector<int32_t>& returned) {
+    std::vector<size_t> rank_of_group(formed.size());
+    for (size_t g = 0; g < formed.size(); ++g) rank_of_group[g] = g;
+    std::sort(rank_of_group.begin(), rank_of_group.end(), [&](size_t a, size_t b) {
+        if (formed[a].size() != formed[b].size()) return formed[a].size() > formed[b].size();
+        return a > b;
+    });
+    std::vector<char> keep(formed.size(), 0);
+    for (size_t i = 0; i < (size_t)T && i < rank_of_group.size(); ++i) keep[rank_of_group[i]] = 1;
+    GroupList kept;
+    for (size_t g = 0; g < formed.size(); ++g) {
+        if (keep[g]) {
+            kept.push_back(formed[g]);
+        } else {
+            for (int32_t x : formed[g]) returned.push_back(x);
+        }
+    }
+    formed.swap(kept);
 }
 
 // reading (emission order): a rank's aligned groups are emitted short to long and each
@@ -249,11 +259,11 @@ bool run(Result& R, int32_t W, int64_t n, const int64_t* rank_off, const int64_t
         if (mode == MODE_NONJOIN && nonempty < W) { stop = STOP_RANK_FINISHED; break; }
         I.rounds += 1;
 
-        // Grouping of every buffer (Sec. 2.2), as the paper's short-to-long list.
+        // Grouping of every buffer (Sec. 2.2), groups in formation order.
         std::vector<GroupList> list((size_t)W);
         for (int32_t r = 0; r < W; ++r) {
             std::vector<int32_t> visit;
-            list[(size_t)r] = paper_list_order(form_groups(buf[(size_t)r], R.len, L_max, &visit));
+            list[(size_t)r] = form_groups(buf[(size_t)r], R.len, L_max, &visit);
             for (size_t p = 0; p < visit.size(); ++p) pos[(size_t)visit[p]] = (int64_t)p;
         }
 
@@ -535,13 +545,13 @@ bool run_stream(StreamResult& SR, int32_t W, int64_t N, const int64_t* tok_off, 
             continue;
         }
         I.emit_rounds += 1;
-        // group every ready buffer (Sec. 2.2) into the paper's short-to-long list
+        // group every ready buffer (Sec. 2.2), groups in formation order
         std::vector<GroupList> list((size_t)W);
         std::vector<double> mean_len((size_t)W, 0.0);
         for (int32_t r = 0; r < W; ++r) {
             if (!ready[(size_t)r]) continue;
             std::vector<int32_t> visit;
-            list[(size_t)r] = paper_list_order(form_groups(buf[(size_t)r], vlen, L_max, &visit));
+            list[(size_t)r] = form_groups(buf[(size_t)r], vlen, L_max, &visit);
             for (size_t p = 0; p < visit.size(); ++p) pos[(size_t)visit[p]] = (int64_t)p;
             int64_t tok = 0;
             for (int32_t v : buf[(size_t)r]) tok += vlen[(size_t)v];

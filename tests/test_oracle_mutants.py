@@ -23,11 +23,13 @@ MUTANTS = [
     ("trailing_group_dropped", "if (!cur.empty()) formed.push_back(cur);", "if (false) formed.push_back(cur);"),
     ("eq3_min_of_groups", "maxG = std::max(maxG, G);", "maxG = maxG == 0 ? G : std::min(maxG, G);"),
     ("eq3_buffer_bound_dropped", "if (minS > 0) T = std::min(T, minS);", "(void)minS;"),
-    ("split_scans_from_front", "for (int64_t i = (int64_t)list.size() - 1; i >= 0; --i)",
-     "for (int64_t i = 0; i < (int64_t)list.size(); ++i)"),
-    ("split_takes_first_member", "int32_t x = list[i].back();\n                list[i].pop_back();",
-     "int32_t x = list[i].front();\n                list[i].erase(list[i].begin());"),
-    ("overflow_keeps_smallest", "return a.size() > b.size();", "return a.size() < b.size();"),
+    ("split_peels_from_last_formed", "    GroupList out;\n    for (Group& g : formed) {\n",
+     "    GroupList out;\n    std::reverse(formed.begin(), formed.end());\n    for (Group& g : formed) {\n"),
+    ("split_peels_shortest_member", "        size_t first = 0;\n",
+     "        size_t first = 0;\n        std::reverse(g.begin(), g.end());\n"),
+    ("overflow_keeps_smallest", "return formed[a].size() > formed[b].size();",
+     "return formed[a].size() < formed[b].size();"),
+    ("overflow_ties_keep_earlier_formed", "        return a > b;\n    });", "        return a < b;\n    });"),
     ("quota_strict", "emitted >= quota", "emitted > quota"),
     ("pad_fraction_inverted", "I.pad_fraction = I.padded_elems > 0 ? 1.0 - ",
      "I.pad_fraction = I.padded_elems > 0 ? 0.0 + "),

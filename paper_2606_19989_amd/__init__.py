@@ -226,6 +226,13 @@ def _stream(stream) -> Optional[int]:
     return s.cuda_stream
 
 
+def _sync_current(device):
+    """Waits for the current stream of a GPU device (no-op elsewhere)."""
+    import torch
+    if torch.device(device).type == "cuda":
+        torch.cuda.current_stream(device).synchronize()
+
+
 class DeviceWindow:
     """A window resident in device memory, with its C descriptor.
 
@@ -374,6 +381,8 @@ class Pipeline:
         self.slot_tokens_approx = torch.empty(cap, dtype=torch.float64, device=self.device)
         self.slot_row_off = torch.empty(cap + 1, dtype=torch.int64, device=self.device)
         self.slot_tile_off = torch.empty(cap + 1, dtype=torch.int64, device=self.device)
+        # buffers may be used on another stream than the one they were allocated on
+        _sync_current(self.device)
 
     def form(self, stream=None):
         odb_form_groups(self.win, self.budget, self.order, self.sorted_len, self.group_index,
@@ -384,12 +393,14 @@ class Pipeline:
                         self.group_index, self.groups_per_rank, self.slot_capacity, self.emit_order,
                         self.slot_rows, self.slot_maxlen, self.slot_row_off, self.slot_tile_off, self.slot_tokens,
                         self.leftover, self.leftover_off, self.ws, stream)
-        rec = dict(slot_tokens_approx=self.slot_tokens_approx, row_token_start=self.row_token_start,
-                   row_len=self.row_len)
-        st, info = odb_align_groups(*args(), raise_on_capacity=False, **rec)
+        # both argument sets are read when the call is made: a retry after ODB_E_CAPACITY
+        # must pass the reallocated slot arrays, every one of them
+        rec = lambda: dict(slot_tokens_approx=self.slot_tokens_approx, row_token_start=self.row_token_start,
+                           row_len=self.row_len)
+        st, info = odb_align_groups(*args(), raise_on_capacity=False, **rec())
         if st == ODB_E_CAPACITY:
             self._alloc_slots(int(info["required_slot_capacity"]))
-            st, info = odb_align_groups(*args(), **rec)
+            st, info = odb_align_groups(*args(), **rec())
         self.info = info
         return info
 
@@ -402,6 +413,9 @@ class Pipeline:
         elems = max(int(elems), 1)
         if self.outputs is None or self.outputs[0].numel() < elems:
             self.outputs = tuple(torch.empty(elems, dtype=torch.int32, device=self.device) for _ in range(4))
+            # the allocator may hand out memory freed by work still queued on the current
+            # stream; the library may write it on another stream
+            _sync_current(self.device)
         return self.outputs
 
     def collate(self, stream=None):
@@ -499,6 +513,8 @@ class StreamPipeline:
         if size == 0:
             _check(ODB_E_INVALID_ARG)
         self.ws = torch.empty(size, dtype=torch.uint8, device=d)
+        # buffers may be used on another stream than the one they were allocated on
+        _sync_current(d)
 
     def _call(self, stream):
         info = StreamInfo()
@@ -535,6 +551,7 @@ class StreamPipeline:
         P = int(self.info["padded_elems"])
         if self.outputs is None or self.outputs[0].numel() < max(P, 1):
             self.outputs = tuple(torch.empty(max(P, 1), dtype=torch.int32, device=self.device) for _ in range(4))
+            _sync_current(self.device)
         odb_collate(self.win, self.num_slots, self.emit_order, self.slot_rows, self.slot_maxlen, self.slot_row_off,
                     self.slot_tile_off, self.pad_id, P, *self.outputs, self.ws, stream,
                     row_token_start=self.row_token_start, row_len=self.row_len)

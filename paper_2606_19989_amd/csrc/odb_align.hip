@@ -1251,6 +1251,18 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
         ODB_TRY_HIP(hipStreamSynchronize(s));
         if (hst.err & kErrInternal)
             return set_error(ODB_E_INTERNAL, "alignment round %d: group sizes inconsistent", rounds);
+        // every round empties part of some buffer (T >= 1 steps of >= 1 sample for each
+        // active rank) and never grows one; anything else is device state this call did
+        // not write, and the loop stops rather than run on it
+        int64_t left_before = 0, left_after = 0;
+        for (int r = 0; r < W; ++r) {
+            if (hranks[r].cnt < 0 || hranks[r].cnt > cnt[r])
+                return set_error(ODB_E_INTERNAL, "alignment round %d: rank %d's buffer grew", rounds, r);
+            left_before += cnt[r];
+            left_after += hranks[r].cnt;
+        }
+        if (left_after == left_before && !(nonjoin && hrs.quota_hit))
+            return set_error(ODB_E_INTERNAL, "alignment round %d emitted nothing", rounds);
         S += hrs.cut;
         for (int r = 0; r < W; ++r) cnt[r] = hranks[r].cnt;
         cur = RoundBuffers{bids[flip], blen[flip], nullptr};

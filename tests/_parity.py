@@ -191,4 +191,6 @@ def compare_collate_by_rank_whole_stream(tok_off, outs, ref, tokens_dev, pad_id=
                 raise AssertionError(f"{name}: rank {r}: {len(bad)} mismatches, first at {lo + bad[0]}: "
                                      f"{got[bad[0]]} vs {e[bad[0]]}")
         del want
+        if r % 8 == 7 or r == ref.W - 1:
+            log(f"  ranks 0-{r}: every collate element equal")
     del toks

@@ -20,7 +20,8 @@
  *   - Pointers named d_* are device pointers (HIP global memory on the current device);
  *     all other pointers are host pointers.  The caller owns every buffer; the library
  *     allocates no device memory (scratch comes from the caller's workspace), keeps no
- *     pointer after returning and holds no state except a thread-local error message.
+ *     pointer after returning and holds no state except a thread-local error message and
+ *     the fixed per-device scratch array of odb_collate_static.
  *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Work is enqueued
  *     on it in order.  odb_form_groups and odb_align_groups synchronise `stream` because
  *     their output sizes are data dependent; odb_collate does not synchronise.
@@ -240,6 +241,34 @@ int odb_collate(const odb_window_t* w, int64_t num_slots,
                 const int64_t* d_slot_tile_off, int32_t pad_id, int64_t out_capacity_elems,
                 int32_t* d_input_ids, int32_t* d_labels, int32_t* d_attention_mask,
                 int32_t* d_position_ids, void* d_ws, size_t ws_bytes, void* stream);
+
+/* Rows of gathered row records the static scratch of odb_collate_static holds. */
+#define ODB_COLLATE_STATIC_MAX_ROWS 2097152
+
+/*
+ * odb_collate without a workspace, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid allocation).  Same
+ * arguments, checks and outputs as odb_collate; it allocates nothing and synchronises
+ * nothing.  Its scratch (the kernel's run counter and, when the plan brings no row
+ * records, the gathered records) is a fixed array inside the library: 25,166,080 bytes per
+ * device, held from the first call on that device until the process ends.
+ *
+ *   d_status   [1] device out: set to 0 when the call starts, nonzero if the plan is
+ *              inconsistent (the cases odb_collate reports through odb_collate_status)
+ *
+ * Without row records the window may hold at most ODB_COLLATE_STATIC_MAX_ROWS - W + 1
+ * samples (n + W - 1 rows); a larger window returns ODB_E_INVALID_ARG before anything
+ * is launched (pass the plan's row records, or use odb_collate).  Every call on a device
+ * shares that device's scratch: calls that overlap on one device race, so keep them on
+ * one stream or order them with events.
+ */
+int odb_collate_static(const odb_window_t* w, int64_t num_slots,
+                       const int32_t* d_emit_order, const int64_t* d_row_token_start,
+                       const int32_t* d_row_len, const int32_t* d_slot_rows,
+                       const int32_t* d_slot_maxlen, const int64_t* d_slot_row_off,
+                       const int64_t* d_slot_tile_off, int32_t pad_id, int64_t out_capacity_elems,
+                       int32_t* d_input_ids, int32_t* d_labels, int32_t* d_attention_mask,
+                       int32_t* d_position_ids, int32_t* d_status, void* stream);
 
 /* Synchronises `stream` and returns ODB_OK, or ODB_E_INVALID_DATA if the last
  * odb_collate on this workspace met an inconsistent plan (and clears the word). */

@@ -38,8 +38,9 @@ ODB_WEIGHT_SAMPLE, ODB_WEIGHT_TOKEN_APPROX, ODB_WEIGHT_TOKEN_EXACT = 0, 1, 2
 EXPORTED = [
     "odb_status_string", "odb_last_error_message", "odb_workspace_size", "odb_form_groups",
     "odb_align_groups", "odb_collate", "odb_collate_status", "odb_check_coverage", "odb_loss_weights",
-    "odb_length_sketch", "odb_stream_workspace_size", "odb_stream_plan",
+    "odb_length_sketch", "odb_stream_workspace_size", "odb_stream_plan", "odb_collate_static",
 ]
+ODB_COLLATE_STATIC_MAX_ROWS = 2097152
 
 
 class OdbError(RuntimeError):
@@ -185,6 +186,8 @@ def load():
                                          P, P, P, P, P, P, P, P, P, P, P, ctypes.POINTER(PlanInfo), P, SZ, P]
         lib.odb_collate.restype = ctypes.c_int
         lib.odb_collate.argtypes = [W, I64, P, P, P, P, P, P, P, I32, I64, P, P, P, P, P, SZ, P]
+        lib.odb_collate_static.restype = ctypes.c_int
+        lib.odb_collate_static.argtypes = [W, I64, P, P, P, P, P, P, P, I32, I64, P, P, P, P, P, P]
         lib.odb_collate_status.restype = ctypes.c_int
         lib.odb_collate_status.argtypes = [P, SZ, P]
         lib.odb_check_coverage.restype = ctypes.c_int
@@ -299,6 +302,18 @@ def odb_collate(win, num_slots, emit_order, slot_rows, slot_maxlen, slot_row_off
                               _dptr(slot_row_off), _dptr(slot_tile_off), int(pad_id), int(out_capacity),
                               _dptr(input_ids), _dptr(labels), _dptr(attention_mask), _dptr(position_ids),
                               _dptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def odb_collate_static(win, num_slots, emit_order, slot_rows, slot_maxlen, slot_row_off, slot_tile_off, pad_id,
+                       out_capacity, input_ids, labels, attention_mask, position_ids, status, stream=None,
+                       row_token_start=None, row_len=None):
+    """odb_collate without a workspace (the library's fixed scratch); ``status`` is a
+    device int32 tensor of one element that receives 0 or the plan-error flag."""
+    _check(load().odb_collate_static(win.ref, int(num_slots), _dptr(emit_order), _dptr(row_token_start),
+                                     _dptr(row_len), _dptr(slot_rows), _dptr(slot_maxlen), _dptr(slot_row_off),
+                                     _dptr(slot_tile_off), int(pad_id), int(out_capacity), _dptr(input_ids),
+                                     _dptr(labels), _dptr(attention_mask), _dptr(position_ids), _dptr(status),
+                                     _stream(stream)))
 
 
 def odb_collate_status(ws, stream=None):

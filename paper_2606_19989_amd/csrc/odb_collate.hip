@@ -38,6 +38,8 @@
 // A group's cursor (slot, row, column) advances with the step sequence: inside a tile it
 // moves by arithmetic, across tiles by a search over the tile offsets.  When a group's 4
 // elements lie in one row (the common case) its tokens arrive in one 16-byte load.
+#include <mutex>
+
 #include "odb_internal.h"
 
 namespace odb {
@@ -601,6 +603,78 @@ extern "C" int odb_collate(const odb_window_t* w, int64_t num_slots, const int32
                           d_slot_row_off, d_slot_tile_off, pad_id, out_capacity_elems, d_input_ids, d_labels,
                           d_attention_mask, d_position_ids, empty, &st->collate_err, &st->collate_runs,
                           ws_at<int64_t>(d_ws, L.row_ts), ws_at<int32_t>(d_ws, L.row_len),
+                          static_cast<hipStream_t>(stream));
+}
+
+// ---------------------------------------------------------------- allocation-free variant
+// odb_collate_static keeps the collate's scratch in this file-scope device array instead
+// of a caller workspace: the run counter in the first 256 bytes, then, when the plan
+// brings no row records, the gathered records (token starts, then lengths).  Each device
+// holds its own copy until the process ends.  Host code never passes the array's name to
+// a kernel (on the host it is only a stand-in for the symbol): it passes the device
+// address that hipGetSymbolAddress returns, looked up once per device.
+namespace odb {
+namespace {
+
+constexpr int64_t kStaticRows = ODB_COLLATE_STATIC_MAX_ROWS;
+constexpr size_t kStaticHeader = 256;
+constexpr size_t kStaticBytes = kStaticHeader + 12 * (size_t)kStaticRows;
+constexpr int kMaxDevices = 64;
+
+static __device__ __align__(256) unsigned char scratch[kStaticBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's scratch array (looked up on the first call per device).
+int static_scratch(void** out) {
+    int dev = -1;
+    ODB_TRY_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return set_error(ODB_E_INTERNAL, "device index %d out of range", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || p == nullptr)
+            return set_error(ODB_E_HIP, "hipGetSymbolAddress of the collate scratch failed on device %d: %s", dev,
+                             hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return ODB_OK;
+}
+
+}  // namespace
+}  // namespace odb
+
+extern "C" int odb_collate_static(const odb_window_t* w, int64_t num_slots, const int32_t* d_emit_order,
+                                  const int64_t* d_row_token_start, const int32_t* d_row_len,
+                                  const int32_t* d_slot_rows, const int32_t* d_slot_maxlen,
+                                  const int64_t* d_slot_row_off, const int64_t* d_slot_tile_off, int32_t pad_id,
+                                  int64_t out_capacity_elems, int32_t* d_input_ids, int32_t* d_labels,
+                                  int32_t* d_attention_mask, int32_t* d_position_ids, int32_t* d_status,
+                                  void* stream) {
+    ODB_TRY(check_window(w));
+    if (!d_status) return set_error(ODB_E_INVALID_ARG, "d_status is NULL");
+    bool empty = false;
+    ODB_TRY(check_collate_args(w, num_slots, d_emit_order, d_row_token_start, d_row_len, d_slot_rows, d_slot_maxlen,
+                               d_slot_row_off, d_slot_tile_off, out_capacity_elems, d_input_ids, d_labels,
+                               d_attention_mask, d_position_ids, &empty));
+    const int64_t max_rows = w->num_samples + w->num_ranks - 1;
+    if (!empty && !d_row_token_start && max_rows > kStaticRows)
+        return set_error(ODB_E_INVALID_ARG,
+                         "without row records the plan may hold %lld rows, more than the %lld the static scratch "
+                         "holds: pass the plan's row records or use odb_collate with a workspace",
+                         (long long)max_rows, (long long)kStaticRows);
+    void* base = nullptr;
+    ODB_TRY(static_scratch(&base));
+    char* b = static_cast<char*>(base);
+    return launch_collate(w, num_slots, d_emit_order, d_row_token_start, d_row_len, d_slot_rows, d_slot_maxlen,
+                          d_slot_row_off, d_slot_tile_off, pad_id, out_capacity_elems, d_input_ids, d_labels,
+                          d_attention_mask, d_position_ids, empty, d_status,
+                          reinterpret_cast<unsigned long long*>(b),
+                          reinterpret_cast<int64_t*>(b + kStaticHeader),
+                          reinterpret_cast<int32_t*>(b + kStaticHeader + 8 * (size_t)kStaticRows),
                           static_cast<hipStream_t>(stream));
 }
 

@@ -16,8 +16,9 @@ schedule (one stream, plan then collate) is timed too.  Prints one JSON line:
                copy_ceiling_gbs = a plain 4 GiB device copy, as a practical ceiling;
                mix_copy_gbs = a torch broadcast copy (1 GiB read, 4 GiB written) with the
                collate's 1 : 4 read : write bytes
-  cpu_baseline the CPU oracle on a bounded sample of the same workload (consecutive
-               4-rank groups of the window, at least 10 s), single-threaded on this host
+  cpu_baseline the CPU oracle on the same window, single-threaded on this host: the plan
+               of the whole window and the collate of its first ranks until about 20 s,
+               extrapolated to the whole window per rank
 """
 import argparse
 import json
@@ -269,45 +270,71 @@ def stream_timing(odb, w, tok_off, tokens, dev, plan_stream, collate_stream, ite
     return out
 
 
-def cpu_baseline(workload, tokens_dev, group=4, min_seconds=10.0, pad_id=0):
-    """The oracle (plan + full collate), single-threaded, on consecutive groups of
-    `group` ranks of the same window until at least `min_seconds` of CPU work."""
-    import numpy as np
-
+def cpu_baseline(w, tokens_dev, min_seconds=20.0, pad_id=0):
+    """The oracle, single-threaded, on the same window: its plan of the whole window (every
+    rank, the alignment over all W ranks), then its collate rank by rank (each rank's
+    token range copied back from the device, not timed) until at least `min_seconds` of
+    oracle time; the whole window's time is the plan plus the collated ranks' average
+    collate time times W (every rank when the bound allows)."""
     import oracle
-    import synth
 
-    wl = synth.WORKLOADS[workload]
-    per_rank = wl.draw(wl.seed)
-    done = samples = toks = 0
-    elapsed = 0.0
-    tok_base = 0
-    while done < wl.W and elapsed < min_seconds:
-        part = per_rank[done:done + group]
-        w = synth.window_from_ranks(f"{workload}_ranks{done}", part, wl.budget, mode=wl.mode,
-                                    quota=sum(len(x) for x in part) if wl.mode == "nonjoin" else 0)
-        # the same token values the GPU read for these ranks
-        tokens = tokens_dev[tok_base:tok_base + w.total_tokens].cpu().numpy()
+    t0 = time.perf_counter()
+    p = oracle.plan_window(w)
+    t_plan = time.perf_counter() - t0
+    t_coll = 0.0
+    done = 0
+    while done < w.W and t_plan + t_coll < min_seconds:
+        r = done
+        a, b = int(w.tok_off[w.rank_off[r]]), int(w.tok_off[w.rank_off[r + 1]])
+        toks = tokens_dev[a:b].cpu().numpy()
         t0 = time.perf_counter()
-        p = oracle.plan_window(w)
-        p.collate(w.tok_off, tokens, pad_id)
-        elapsed += time.perf_counter() - t0
-        samples += p.info["emitted_samples"]
-        toks += p.info["real_tokens"]
-        tok_base += w.total_tokens
-        done += len(part)
-        del tokens, p
+        out = p.collate_rank(r, w.tok_off, toks, pad_id)
+        t_coll += time.perf_counter() - t0
+        done += 1
+        del toks, out
+    est = t_plan + (t_coll / done * w.W if done else 0.0)
+    samples = int(p.info["emitted_samples"])
+    toks = int(p.info["real_tokens"])
     model, nproc = host_cpu()
     return {
-        "value": samples / elapsed,
+        "value": samples / est,
         "unit": "samples/s",
         "cores": 1,
         "host": f"{model}, {nproc} cores available",
         "kind": "oracle",
-        "sample": f"ranks 0-{done - 1} of {wl.W} of the same window, {group} ranks per oracle window "
-                  f"({samples} samples, {toks} tokens), plan + full collate, {elapsed:.1f} s single-threaded",
-        "tokens_per_s": toks / elapsed,
+        "sample": f"the oracle's plan of the whole window ({w.W} ranks, {w.n} samples, alignment over all ranks: "
+                  f"{t_plan:.1f} s) and its collate of ranks 0-{done - 1} ({t_coll:.1f} s); whole-window time = plan "
+                  f"+ average rank collate x {w.W} = {est:.1f} s, single-threaded",
+        "tokens_per_s": toks / est,
+        "plan_seconds": t_plan,
+        "collated_ranks": done,
+        "collate_seconds": t_coll,
+        "whole_window_seconds": est,
     }
+
+
+def plan_only(odb, w, win, stream, steps, warmup):
+    """Grouping + alignment alone, serial on one stream (host clock around both calls, the
+    alignment ending in its synchronisation): the plan's latency per window."""
+    import numpy as np
+
+    pipe = odb.Pipeline(win, w.budget, mode=w.mode, quota=w.quota, pad_id=0)
+    for _ in range(max(warmup, 1)):
+        pipe.form(stream)
+        pipe.align(stream)
+    t = []
+    for _ in range(steps):
+        t0 = time.perf_counter()
+        pipe.form(stream)
+        pipe.align(stream)
+        t.append(time.perf_counter() - t0)
+    ms = float(np.median(t)) * 1e3
+    return {"metric": "plan latency (grouping + alignment) on 1 MI355X", "value": w.n / (ms * 1e-3),
+            "unit": "samples/s", "ms_per_plan": ms, "ms_min": float(np.min(t)) * 1e3, "steps": steps,
+            "warmup": warmup, "n_gpus": 1, "higher_is_better": True, "dtype": "i32", "data": "synthetic",
+            "config": {"workload": w.name, "samples": w.n, "simulated_ranks": w.W, "budget": w.budget,
+                       "mode": w.mode, "steps_aligned": int(pipe.info["steps"]),
+                       "rounds": int(pipe.info["rounds"]), "groups": int(pipe.groups_per_rank.sum())}}
 
 
 def main():
@@ -316,13 +343,20 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--workload", default="ln480_w64x262144")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum CPU time of the oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="oracle time after which the CPU baseline stops collating ranks (the plan of the whole "
+                         "window is always timed)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stream", dest="stream", action="store_false",
                     help="skip the unified-streaming-loop measurement")
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="GIB",
                     help="before the steps, run one plain device copy of GIB GiB (int32 -> int32) as a "
                          "known-size reference for hardware byte counters")
+    ap.add_argument("--budget", type=int, default=0,
+                    help="padded-token budget in place of the workload's (with --plan-only: e.g. 67108864 takes the "
+                         "pointer-jumping path on the largest window)")
+    ap.add_argument("--plan-only", action="store_true",
+                    help="time grouping + alignment alone (serial, one stream), no collate; prints a plan line")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the simulated ranks of a window are "
@@ -338,7 +372,10 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     t = time.time()
     w = wl.window()
-    log(f"[bench] {wl.name}: W={w.W} n={w.n} tokens={w.total_tokens} (drawn in {time.time() - t:.1f} s)")
+    if args.budget > 0:
+        w.budget = args.budget
+    log(f"[bench] {wl.name}: W={w.W} n={w.n} tokens={w.total_tokens} budget={w.budget} "
+        f"(drawn in {time.time() - t:.1f} s)")
     dev = torch.device("cuda:0")
     torch.cuda.init()
     # the two streams are created before any other stream is used, so the runtime puts
@@ -348,6 +385,9 @@ def main():
     tok_off, tokens, ident = synth.device_tensors(w, dev)
     torch.cuda.synchronize()
     win = odb.DeviceWindow(w.rank_off, tok_off, tokens, ident, w.num_identities)
+    if args.plan_only:
+        print(json.dumps(plan_only(odb, w, win, plan_stream, args.steps, args.warmup)), flush=True)
+        return
     pipes = [odb.Pipeline(win, w.budget, mode=w.mode, quota=w.quota, pad_id=0) for _ in range(2)]
     pipe = pipes[0]
     log(f"[bench] inputs resident: {(tok_off.numel() * 8 + tokens.numel() * 4) / 1e9:.1f} GB")
@@ -463,7 +503,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log(f"[bench] CPU oracle on groups of ranks for >= {args.cpu_seconds:.0f} s ...")
-        result["cpu_baseline"] = cpu_baseline(wl.name, tokens, min_seconds=args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(w, tokens, min_seconds=args.cpu_seconds)
         log("[bench] CPU oracle done")
     print(json.dumps(result), flush=True)
 

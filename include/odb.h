@@ -23,8 +23,9 @@
  *     pointer after returning and holds no state except a thread-local error message and
  *     the fixed per-device scratch array of odb_collate_static.
  *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Work is enqueued
- *     on it in order.  odb_form_groups and odb_align_groups synchronise `stream` because
- *     their output sizes are data dependent; odb_collate does not synchronise.
+ *     on it in order.  odb_align_groups synchronises `stream` because its output sizes
+ *     are data dependent; odb_form_groups does so only on its multi-block path (ranks of
+ *     more than 16,384 samples, or budgets of millions); odb_collate does not.
  *   - Every call returns an odb_status_t.  Argument errors are detected on the host
  *     before anything is launched.  Data errors found on the device are reported at the
  *     call's synchronisation point.  On any error the outputs are unspecified.  No C++
@@ -107,8 +108,17 @@ size_t odb_workspace_size(const odb_window_t* w);
  *   d_groups_per_rank   [W] out: G_r, groups formed by rank r
  *   d_ws / ws_bytes     workspace of at least odb_workspace_size(w) bytes, 256-B aligned
  *
- * Synchronises `stream` once (to validate lengths).  Returns ODB_E_INVALID_DATA if some
- * l_i < 1 or l_i >= 2^31 (message names the first such sample).
+ * Two paths, equal results:
+ *   - every rank holds at most 16,384 samples and its distinct batch sizes fit a
+ *     3,840-entry table (budget < 3,682,561, or ranks of at most 3,840 samples): one block
+ *     per rank sorts and walks its samples; two kernels, asynchronous.  A sample whose
+ *     length lies outside [1, 2^31), or whose token offset is negative, is grouped as if
+ *     its length were 1, and odb_align_groups on these outputs returns ODB_E_INVALID_DATA
+ *     naming the first such sample.
+ *   - otherwise a multi-block radix sort and run walk (or pointer jumping for budgets
+ *     whose batch sizes may exceed the table); this path synchronises `stream` once, to
+ *     size its radix passes from the window's length range, and returns
+ *     ODB_E_INVALID_DATA itself for such a sample (message names the first one).
  */
 int odb_form_groups(const odb_window_t* w, int64_t budget,
                     int32_t* d_order, int32_t* d_sorted_len, int32_t* d_group_index,
@@ -184,9 +194,14 @@ typedef struct odb_plan_info {
  *   d_leftover_off    [W+1] out: rank r's leftovers are [off[r], off[r+1])
  *   h_info            host out: plan summary (always filled when the plan was built)
  *
- * Synchronises `stream` once per alignment round and once at the end.  Returns
+ * Synchronises `stream` once per alignment round and once at the end: twice for windows
+ * that align in one round (every rank buffering the same number of samples, no capacity
+ * limit, as in all of the benchmark windows), each time with one device-to-host copy.
+ * Returns
  * ODB_E_CAPACITY (with h_info->required_slot_capacity) if slot_capacity < W * S,
- * ODB_E_INVALID_DATA if the stage-1 arrays are inconsistent (an order that is not each
+ * ODB_E_INVALID_DATA if a sample's CSR length lies outside [1, 2^31) or its token offset
+ * is negative (the message names the first such sample), or if the stage-1 arrays are
+ * inconsistent (an order that is not each
  * rank's ids by (length desc, id asc), a group index that does not step by 0 or 1, a
  * sorted length < 1 or different from the sample's CSR length; the last is checked
  * once the plan is built, against every emitted and left-over sample), and

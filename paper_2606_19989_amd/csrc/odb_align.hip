@@ -3,13 +3,13 @@
 //
 // Every rank's buffer is a contiguous run of formation positions; a group is a range
 // of them.  One alignment round is:
-//   target_kernel      the simulated all_gather of (G_r, S_r, C_r) and Eq. 3's T
 //   group_sizes        size of every group
-//   adjust_kernel      per rank: split (closed form, below) or overflow (size threshold)
+//   adjust_kernel      per rank: the simulated all_gather of (G_r, S_r, C_r) and Eq. 3's T,
+//                      then split (closed form, below) or overflow (size threshold)
 //   slot_records       rows / max length / real tokens of every aligned step, and the
 //                      global sample count of every step
-//   cut_kernel         join: all T steps; non-join: up to the first step reaching Q
-//   finalize_kernel    per rank: which positions are emitted, where they go
+//   finalize_kernel    per rank: the round's cut (join: all T steps; non-join: up to the
+//                      first step reaching Q), which positions are emitted, where they go
 //   emit_kernel        writes emitted ids (rows short to long) and the next buffer
 // and rounds repeat on the returned samples until the termination rule fires.
 //
@@ -33,6 +33,29 @@
 #include "odb_internal.h"
 
 namespace odb {
+
+// A pair of int64 sums, scanned together by the generic scan (its shuffles are found by
+// argument-dependent lookup, next to the scalar ones).  Trivially default-constructible, so
+// it can live in LDS.
+struct I64Pair {
+    int64_t a, b;
+    I64Pair() = default;
+    __host__ __device__ constexpr I64Pair(int z) : a(z), b(z) {}
+    __host__ __device__ constexpr I64Pair(int64_t x, int64_t y) : a(x), b(y) {}
+};
+__device__ __forceinline__ I64Pair operator+(I64Pair x, I64Pair y) { return I64Pair{x.a + y.a, x.b + y.b}; }
+__device__ __forceinline__ I64Pair operator-(I64Pair x, I64Pair y) { return I64Pair{x.a - y.a, x.b - y.b}; }
+__device__ __forceinline__ I64Pair& operator+=(I64Pair& x, I64Pair y) {
+    x.a += y.a;
+    x.b += y.b;
+    return x;
+}
+__device__ __forceinline__ I64Pair __shfl_up(I64Pair v, unsigned int d, int width) {
+    return I64Pair{::__shfl_up(v.a, d, width), ::__shfl_up(v.b, d, width)};
+}
+__device__ __forceinline__ I64Pair __shfl_xor(I64Pair v, int m, int width) {
+    return I64Pair{::__shfl_xor(v.a, m, width), ::__shfl_xor(v.b, m, width)};
+}
 
 namespace {
 
@@ -82,10 +105,6 @@ __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
 }
 
-__global__ void fill_i64_kernel(int64_t* p, int64_t n, int64_t v) {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
-}
 
 // ---------------------------------------------------------------- round 0 inputs
 // Rank state from the stage-1 group counts; G_r must be 0 exactly for empty ranks and
@@ -93,9 +112,13 @@ __global__ void fill_i64_kernel(int64_t* p, int64_t n, int64_t v) {
 __global__ void __launch_bounds__(kBlock) round0_ranks_kernel(const int64_t* __restrict__ off,
                                                               const int32_t* __restrict__ groups, int W,
                                                               RankState* ranks, int64_t* __restrict__ gbase,
-                                                              DevStatus* st) {
+                                                              DevStatus* st, RoundState* rs, DevInfo* info) {
     __shared__ int64_t carry;
-    if (threadIdx.x == 0) carry = 0;
+    if (threadIdx.x == 0) {
+        carry = 0;
+        *rs = RoundState{};
+        *info = DevInfo{};
+    }
     __syncthreads();
     for (int b = 0; b < W; b += kBlock) {
         const int r = b + threadIdx.x;
@@ -190,73 +213,24 @@ struct LiveLenIncl {
     __device__ void operator()(int64_t i, int64_t ex) const { cs[i] = ex + ld(i); }
 };
 
-// Eq. 3 over the active ranks, then the action of every rank.  One block.
-__global__ void __launch_bounds__(kBlock) target_kernel(RankState* ranks, const int64_t* __restrict__ cap,
-                                                        int has_cap, int W, RoundState* rs) {
-    int64_t maxG = 0, minC = LLONG_MAX, minS = LLONG_MAX, active = 0, totalG = 0;
-    for (int r = threadIdx.x; r < W; r += kBlock) {
-        const int64_t G = ranks[r].G;
-        totalG += G;
-        if (G <= 0) continue;
-        active += 1;
-        maxG = G > maxG ? G : maxG;
-        const int64_t S = ranks[r].cnt;
-        if (S > 0 && S < minS) minS = S;
-        if (has_cap && cap[r] > 0 && cap[r] < minC) minC = cap[r];
-    }
-    maxG = block_reduce(maxG, MaxOp{});
-    minC = block_reduce(minC, MinOp{});
-    minS = block_reduce(minS, MinOp{});
-    active = block_reduce(active, SumOp{});
-    totalG = block_reduce(totalG, SumOp{});
-    int64_t T = maxG;
-    if (minC != LLONG_MAX && minC < T) T = minC;
-    if (minS != LLONG_MAX && minS < T) T = minS;
-    if (T < 1) T = 1;
-    int64_t splits = 0, over = 0, changed = 0;
-    for (int r = threadIdx.x; r < W; r += kBlock) {
-        RankState& R = ranks[r];
-        const int64_t G = R.G;
-        R.X = 0;
-        R.jstar = 0;
-        R.qcut = 0;
-        if (G <= 0) {
-            R.action = kActInactive;
-        } else if (G < T) {
-            R.action = kActSplit;
-            splits += T - G;
-            changed += 1;
-        } else if (G > T) {
-            R.action = kActOverflow;
-            over += G - T;
-            changed += 1;
-        } else {
-            R.action = kActKeep;
-        }
-    }
-    splits = block_reduce(splits, SumOp{});
-    over = block_reduce(over, SumOp{});
-    changed = block_reduce(changed, SumOp{});
-    if (threadIdx.x == 0) {
-        // App. B: the pre-alignment counts of the first exchange are exact only if no
-        // active rank's groups changed; otherwise exact token weights need a second one
-        rs->second_gather += changed > 0 ? 1 : 0;
-        rs->T = T;
-        rs->active = active;
-        rs->total_groups = totalG;
-        rs->splits += splits;
-        rs->overflow += over;
-        rs->cut = 0;
-    }
+// Stage-1 arrays that round0_check_kernel found inconsistent: the round's kernels that
+// index through group starts do nothing (the host reports the error at the round's
+// synchronisation).
+__device__ __forceinline__ bool stage1_bad(const DevStatus* st) {
+    return (*(volatile const int32_t*)&st->err & (kErrOrder | kErrGroupIndex)) != 0;
 }
 
 __global__ void __launch_bounds__(kBlock) group_sizes_kernel(const int32_t* __restrict__ gstart,
                                                              const int64_t* __restrict__ gbase,
                                                              const int64_t* __restrict__ off,
                                                              const RankState* __restrict__ ranks, int W,
-                                                             int32_t* __restrict__ gsize) {
+                                                             int32_t* __restrict__ gsize, int64_t* __restrict__ steps,
+                                                             int64_t nsteps, const DevStatus* st) {
+    if (stage1_bad(st)) return;
     const int64_t total = gbase[W];
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    // the round's per-step sample counts, summed by slot_records_kernel
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < nsteps; j += stride) steps[j] = 0;
     for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < total; g += stride) {
         const int r = rank_of(gbase, W, g);
         const int64_t lg = g - gbase[r];
@@ -266,16 +240,73 @@ __global__ void __launch_bounds__(kBlock) group_sizes_kernel(const int32_t* __re
     }
 }
 
-// Per rank (one block each): split position or overflow selection.
-__global__ void __launch_bounds__(kBlock) adjust_kernel(RankState* ranks, const RoundState* __restrict__ rs,
+// Per rank (one block each): the simulated all_gather of (G_r, S_r, C_r) and Eq. 3's
+// target T over the active ranks (every block computes it; block 0 also records the round's
+// statistics), then this rank's action: split position or overflow selection.
+__global__ void __launch_bounds__(kBlock) adjust_kernel(RankState* ranks, const int64_t* __restrict__ cap,
+                                                        int has_cap, int W, RoundState* rs,
                                                         const int32_t* __restrict__ gsize,
                                                         int32_t* __restrict__ ov_slot, int32_t* __restrict__ kept,
                                                         DevStatus* st) {
+    if (stage1_bad(st)) return;
+    int64_t maxG = 0, minC = LLONG_MAX, minS = LLONG_MAX;
+    for (int q = threadIdx.x; q < W; q += kBlock) {
+        const int64_t Gq = ranks[q].G;
+        if (Gq <= 0) continue;
+        maxG = Gq > maxG ? Gq : maxG;
+        const int64_t S = ranks[q].cnt;
+        if (S > 0 && S < minS) minS = S;
+        if (has_cap && cap[q] > 0 && cap[q] < minC) minC = cap[q];
+    }
+    maxG = block_reduce(maxG, MaxOp{});
+    minC = block_reduce(minC, MinOp{});
+    minS = block_reduce(minS, MinOp{});
+    int64_t T = maxG;
+    if (minC != LLONG_MAX && minC < T) T = minC;
+    if (minS != LLONG_MAX && minS < T) T = minS;
+    if (T < 1) T = 1;
+    if (blockIdx.x == 0) {
+        int64_t active = 0, totalG = 0, splits = 0, over = 0, changed = 0;
+        for (int q = threadIdx.x; q < W; q += kBlock) {
+            const int64_t Gq = ranks[q].G;
+            totalG += Gq;
+            if (Gq <= 0) continue;
+            active += 1;
+            if (Gq < T) {
+                splits += T - Gq;
+                changed += 1;
+            } else if (Gq > T) {
+                over += Gq - T;
+                changed += 1;
+            }
+        }
+        active = block_reduce(active, SumOp{});
+        totalG = block_reduce(totalG, SumOp{});
+        splits = block_reduce(splits, SumOp{});
+        over = block_reduce(over, SumOp{});
+        changed = block_reduce(changed, SumOp{});
+        if (threadIdx.x == 0) {
+            // App. B: the pre-alignment counts of the first exchange are exact only if no
+            // active rank's groups changed; otherwise exact token weights need a second one
+            rs->second_gather += changed > 0 ? 1 : 0;
+            rs->T = T;
+            rs->active = active;
+            rs->total_groups = totalG;
+            rs->splits += splits;
+            rs->overflow += over;
+            rs->cut = 0;
+        }
+    }
     const int r = blockIdx.x;
-    const int32_t action = ranks[r].action;
-    if (action != kActSplit && action != kActOverflow) return;
-    const int64_t T = rs->T;
     const int64_t G = ranks[r].G;
+    const int32_t action = G <= 0 ? kActInactive : (G < T ? kActSplit : (G > T ? kActOverflow : kActKeep));
+    if (threadIdx.x == 0) {
+        ranks[r].X = 0;
+        ranks[r].jstar = 0;
+        ranks[r].qcut = 0;
+        ranks[r].action = action;
+    }
+    if (action != kActSplit && action != kActOverflow) return;
     const int64_t gb = ranks[r].gbase;
     __shared__ int64_t s_found;
     if (action == kActSplit) {
@@ -381,8 +412,9 @@ __global__ void __launch_bounds__(kBlock) slot_records_kernel(
     const int32_t* __restrict__ gstart, const int32_t* __restrict__ gsize, const int32_t* __restrict__ kept,
     const int32_t* __restrict__ cur_len, const int64_t* __restrict__ cs, int32_t* __restrict__ srows,
     int32_t* __restrict__ smax, int64_t* __restrict__ stok, double* __restrict__ sadj,
-    int64_t* __restrict__ steps) {
+    int64_t* __restrict__ steps, const DevStatus* st) {
 #pragma clang fp contract(off)
+    if (stage1_bad(st)) return;
     const int64_t T = rs->T;
     const int64_t total = (int64_t)W * T;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -413,12 +445,11 @@ __global__ void __launch_bounds__(kBlock) slot_records_kernel(
     }
 }
 
-// Join: every step is emitted.  Non-join: steps up to the first one at which the
-// cumulative global emitted count reaches the quota (Theorem 2).  One block.
-__global__ void __launch_bounds__(kBlock) cut_kernel(RoundState* rs, const int64_t* __restrict__ steps,
-                                                     int nonjoin, int64_t quota) {
-    const int64_t T = rs->T;
-    const int64_t before = rs->emitted_total;
+// Steps of this round that are emitted: join, all T; non-join, up to the first step at
+// which the cumulative global emitted count reaches the quota (Theorem 2).  Block-uniform;
+// *sum and *mx receive the emitted steps' sample total and largest step.
+__device__ int64_t round_cut(const int64_t* __restrict__ steps, int64_t T, int64_t before, int nonjoin,
+                             int64_t quota, int64_t* sum_out, int64_t* mx_out) {
     __shared__ int64_t s_cut;
     if (threadIdx.x == 0) s_cut = T;
     __syncthreads();
@@ -442,27 +473,35 @@ __global__ void __launch_bounds__(kBlock) cut_kernel(RoundState* rs, const int64
         sum += v;
         mx = v > mx ? v : mx;
     }
-    sum = block_reduce(sum, SumOp{});
-    mx = block_reduce(mx, MaxOp{});
-    if (threadIdx.x == 0) {
-        rs->cut = cut;
-        rs->emitted_total = before + sum;
-        if (mx > rs->step_max) rs->step_max = mx;
-        if (nonjoin && before + sum >= quota) rs->quota_hit = 1;
-    }
+    *sum_out = block_reduce(sum, SumOp{});
+    *mx_out = block_reduce(mx, MaxOp{});
+    return cut;
 }
 
-// Per rank (one block each): emitted positions and the layout of the next buffer.
-__global__ void __launch_bounds__(kBlock) finalize_kernel(RankState* ranks, const RoundState* __restrict__ rs,
-                                                          const int64_t* __restrict__ off,
+// Per rank (one block each): the round's cut (every block computes it; block 0 records it
+// and the running totals, which advance_kernel makes current), then the rank's emitted
+// positions and the layout of its next buffer.
+__global__ void __launch_bounds__(kBlock) finalize_kernel(RankState* ranks, RoundState* rs,
+                                                          const int64_t* __restrict__ steps, int nonjoin,
+                                                          int64_t quota, const int64_t* __restrict__ off,
                                                           const int32_t* __restrict__ gstart,
                                                           const int32_t* __restrict__ gsize,
                                                           const int32_t* __restrict__ ov_slot,
                                                           const int32_t* __restrict__ kept,
-                                                          int32_t* __restrict__ ov_lo) {
+                                                          int32_t* __restrict__ ov_lo, const DevStatus* st) {
+    if (stage1_bad(st)) return;
     const int r = blockIdx.x;
     RankState& R = ranks[r];
-    const int64_t T = rs->T, cut = rs->cut;
+    const int64_t T = rs->T;
+    const int64_t before = rs->emitted_total;
+    int64_t step_sum, step_mx;
+    const int64_t cut = round_cut(steps, T, before, nonjoin, quota, &step_sum, &step_mx);
+    if (r == 0 && threadIdx.x == 0) {
+        rs->cut = cut;
+        rs->emitted_next = before + step_sum;
+        if (step_mx > rs->step_max) rs->step_max = step_mx;
+        if (nonjoin && before + step_sum >= quota) rs->quota_hit = 1;
+    }
     if (threadIdx.x == 0) R.ebase = R.emitted;
     if (R.action == kActInactive) {
         if (threadIdx.x == 0) R.next_cnt = 0;
@@ -521,7 +560,9 @@ __global__ void __launch_bounds__(kBlock) emit_kernel(
     int64_t n, const int32_t* __restrict__ cur_ids, const int32_t* __restrict__ cur_len,
     const int32_t* __restrict__ gidx, const int32_t* __restrict__ gstart, const int32_t* __restrict__ gsize,
     const int32_t* __restrict__ ov_slot, const int32_t* __restrict__ ov_lo, int32_t* __restrict__ dst,
-    int32_t* __restrict__ dst_len, int32_t* __restrict__ next_ids, int32_t* __restrict__ next_len) {
+    int32_t* __restrict__ dst_len, int32_t* __restrict__ next_ids, int32_t* __restrict__ next_len,
+    const DevStatus* st) {
+    if (stage1_bad(st)) return;
     __shared__ int64_t s_off[kLdsRanks + 1];
     off = stage_ranks(off, W, s_off);
     const int64_t cut = rs->cut;
@@ -560,9 +601,11 @@ __global__ void __launch_bounds__(kBlock) emit_kernel(
     }
 }
 
-__global__ void advance_kernel(RankState* ranks, int W) {
-    for (int r = blockIdx.x * blockDim.x + threadIdx.x; r < W; r += gridDim.x * blockDim.x)
-        ranks[r].cnt = ranks[r].next_cnt;
+// End of a round: the next buffers' counts and the running emitted total become current.
+__global__ void advance_kernel(RankState* ranks, int W, RoundState* rs) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i == 0) rs->emitted_total = rs->emitted_next;
+    for (int r = i; r < W; r += gridDim.x * blockDim.x) ranks[r].cnt = ranks[r].next_cnt;
 }
 
 // ---------------------------------------------------------------- final plan
@@ -573,9 +616,11 @@ __global__ void __launch_bounds__(kBlock) plan_slots_kernel(const RankState* __r
                                                             const int64_t* __restrict__ stok,
                                                             const double* __restrict__ sadj,
                                                             int32_t* __restrict__ rows, int32_t* __restrict__ maxlen,
-                                                            int64_t* __restrict__ tokens, double* __restrict__ approx) {
+                                                            int64_t* __restrict__ tokens, double* __restrict__ approx,
+                                                            DevInfo* info) {
     const int64_t K = (int64_t)W * S;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t real = 0;
     for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < K; k += stride) {
         const int r = (int)(k / S);
         const int64_t j = k - (int64_t)r * S;
@@ -584,6 +629,7 @@ __global__ void __launch_bounds__(kBlock) plan_slots_kernel(const RankState* __r
             rows[k] = srows[src];
             maxlen[k] = smax[src];
             tokens[k] = stok[src];
+            real += stok[src];
             if (approx) approx[k] = sadj[src];
         } else {
             rows[k] = 0;
@@ -592,22 +638,28 @@ __global__ void __launch_bounds__(kBlock) plan_slots_kernel(const RankState* __r
             if (approx) approx[k] = 0.0;
         }
     }
+    // the plan's real tokens (Sec. 2.1 / App. I padding fraction)
+    real = block_sum(real);
+    if (threadIdx.x == 0 && real) atomicAdd((unsigned long long*)&info->real_tokens, (unsigned long long)real);
 }
 
-struct RowsLoad {
-    const int32_t* rows;
-    int64_t K;
-    __device__ int64_t operator()(int64_t i) const { return i < K ? (int64_t)rows[i] : 0; }
-};
-struct TileLoad {
+// The row and tile offsets of the slots in one scan: a slot contributes (rows, rows *
+// maxlen).
+struct RowsTilesLoad {
     const int32_t* rows;
     const int32_t* mx;
     int64_t K;
-    __device__ int64_t operator()(int64_t i) const { return i < K ? (int64_t)rows[i] * mx[i] : 0; }
+    __device__ I64Pair operator()(int64_t i) const {
+        return i < K ? I64Pair{(int64_t)rows[i], (int64_t)rows[i] * mx[i]} : I64Pair{0, 0};
+    }
 };
-struct Store64 {
-    int64_t* out;
-    __device__ void operator()(int64_t i, int64_t v) const { out[i] = v; }
+struct RowsTilesStore {
+    int64_t* row_off;
+    int64_t* tile_off;
+    __device__ void operator()(int64_t i, I64Pair v) const {
+        row_off[i] = v.a;
+        tile_off[i] = v.b;
+    }
 };
 
 __global__ void __launch_bounds__(kBlock) compact_emit_kernel(const int32_t* __restrict__ stage,
@@ -643,6 +695,20 @@ __global__ void __launch_bounds__(kBlock) compact_emit_kernel(const int32_t* __r
 // L2 and are read from HBM about once.
 constexpr int kXcds = 8;
 
+// The CSR length of sample s against the length its plan row carries: a length outside
+// [1, 2^31) or a negative offset is invalid data (grouping took such a sample as length
+// 1); any other difference means the stage-1 arrays are not this window's.
+__device__ __forceinline__ void check_csr_length(int32_t s, int64_t a, int64_t b, int32_t carried, DevStatus* st) {
+    const int64_t l = b - a;
+    if (l < 1 || l > INT_MAX || a < 0) {
+        atomicOr(&st->err, kErrLength);
+        atomicMin((unsigned long long*)&st->first_bad_len, (unsigned long long)s);
+    } else if (l != (int64_t)carried) {
+        atomicOr(&st->err, kErrSortedLen);
+        atomicMin((unsigned long long*)&st->first_bad, (unsigned long long)s);
+    }
+}
+
 __global__ void __launch_bounds__(kBlock) row_check_kernel(const int64_t* __restrict__ tok_off,
                                                            const int32_t* __restrict__ emit,
                                                            const int32_t* __restrict__ len,
@@ -660,10 +726,7 @@ __global__ void __launch_bounds__(kBlock) row_check_kernel(const int64_t* __rest
         for (int64_t k = lo + gb * blockDim.x + threadIdx.x; k < hi; k += stride) {
             const int32_t s = emit[k];
             const int64_t a = tok_off[s];
-            if (tok_off[s + 1] - a != (int64_t)len[k]) {
-                atomicOr(&st->err, kErrSortedLen);
-                atomicMin((unsigned long long*)&st->first_bad, (unsigned long long)s);
-            }
+            check_csr_length(s, a, tok_off[s + 1], len[k], st);
             if (ts) ts[k] = a;
         }
         if (!xcd_ranks) break;
@@ -706,30 +769,8 @@ __global__ void __launch_bounds__(kBlock) leftover_kernel(const int32_t* __restr
         if (q < ranks[r].cnt) {
             const int32_t s = cur_ids[p];
             left[loff[r] + q] = s;
-            if (tok_off[s + 1] - tok_off[s] != (int64_t)cur_len[p]) {
-                atomicOr(&st->err, kErrSortedLen);
-                atomicMin((unsigned long long*)&st->first_bad, (unsigned long long)s);
-            }
+            check_csr_length(s, tok_off[s], tok_off[s + 1], cur_len[p], st);
         }
-    }
-}
-
-__global__ void __launch_bounds__(kBlock) tokens_sum_kernel(const int64_t* __restrict__ tokens, int64_t K,
-                                                            DevInfo* info) {
-    int64_t s = 0;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < K; k += stride) s += tokens[k];
-    s = block_sum(s);
-    if (threadIdx.x == 0 && s) atomicAdd((unsigned long long*)&info->real_tokens, (unsigned long long)s);
-}
-
-__global__ void finish_info_kernel(const int64_t* __restrict__ row_off, const int64_t* __restrict__ tile_off,
-                                   int64_t K, DevInfo* info) {
-    if (threadIdx.x == 0) {
-        info->padded_elems = K > 0 ? tile_off[K] : 0;
-        info->emitted = K > 0 ? row_off[K] : 0;
-        info->pad_fraction =
-            info->padded_elems > 0 ? 1.0 - (double)info->real_tokens / (double)info->padded_elems : 0.0;
     }
 }
 
@@ -993,11 +1034,20 @@ __global__ void __launch_bounds__(kCovBlock) coverage_lds_kernel(
     }
 }
 
+// The plan's totals (padded elements, emitted rows, pad fraction) and the coverage chunks:
 // chunk_first[r] = sum_{r' < r} ceil(n_r' / C).  One block.
-__global__ void __launch_bounds__(kBlock) chunks_kernel(const int64_t* __restrict__ off, int W, int64_t C,
-                                                        int64_t* __restrict__ chunk_first) {
+__global__ void __launch_bounds__(kBlock) finish_plan_kernel(const int64_t* __restrict__ row_off,
+                                                             const int64_t* __restrict__ tile_off, int64_t K,
+                                                             DevInfo* info, const int64_t* __restrict__ off, int W,
+                                                             int64_t C, int64_t* __restrict__ chunk_first) {
     __shared__ int64_t carry;
-    if (threadIdx.x == 0) carry = 0;
+    if (threadIdx.x == 0) {
+        carry = 0;
+        info->padded_elems = K > 0 ? tile_off[K] : 0;
+        info->emitted = K > 0 ? row_off[K] : 0;
+        info->pad_fraction =
+            info->padded_elems > 0 ? 1.0 - (double)info->real_tokens / (double)info->padded_elems : 0.0;
+    }
     __syncthreads();
     for (int b = 0; b < W; b += kBlock) {
         const int r = b + threadIdx.x;
@@ -1016,11 +1066,10 @@ __global__ void __launch_bounds__(kBlock) chunks_kernel(const int64_t* __restric
 // Coverage of an aligned plan: per-rank LDS bitsets for the views, global counters for
 // the identities of an identity map.
 int run_plan_coverage(const odb_window_t* w, const Layout& L, void* ws, const int32_t* emit,
-                      const int64_t* row_off, int64_t S, const int32_t* left, const int64_t* loff, int64_t ne,
-                      int64_t nl, hipStream_t s) {
+                      const int64_t* row_off, const int64_t* tile_off, int64_t S, const int32_t* left,
+                      const int64_t* loff, int64_t ne, int64_t nl, hipStream_t s) {
     const int W = w->num_ranks;
     const int64_t n = w->num_samples;
-    if (n == 0) return ODB_OK;
     int64_t max_nr = 0, chunks = 0;
     for (int r = 0; r < W; ++r) {
         const int64_t nr = w->rank_offsets[r + 1] - w->rank_offsets[r];
@@ -1032,8 +1081,10 @@ int run_plan_coverage(const odb_window_t* w, const Layout& L, void* ws, const in
     for (int r = 0; r < W; ++r) chunks += (w->rank_offsets[r + 1] - w->rank_offsets[r] + C - 1) / C;
     int64_t* chunk_first = ws_at<int64_t>(ws, L.tile_first);
     const int64_t* d_off = ws_at<int64_t>(ws, L.rank_off);
-    hipLaunchKernelGGL(chunks_kernel, dim3(1), dim3(kBlock), 0, s, d_off, W, C, chunk_first);
+    hipLaunchKernelGGL(finish_plan_kernel, dim3(1), dim3(kBlock), 0, s, row_off, tile_off, (int64_t)W * S,
+                       ws_at<DevInfo>(ws, L.info), d_off, W, C, chunk_first);
     ODB_LAUNCHED();
+    if (n == 0) return ODB_OK;
     hipLaunchKernelGGL(coverage_lds_kernel, dim3((unsigned)chunks), dim3(kCovBlock), (size_t)(C / 4), s, d_off, W,
                        (const int64_t*)chunk_first, C, emit, row_off, S, left, loff, w->d_identity ? 0 : 1,
                        ws_at<DevInfo>(ws, L.info), ws_at<DevStatus>(ws, L.status));
@@ -1161,24 +1212,13 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     const int64_t gcap = (int64_t)num_cus() * kPlanBlocksPerCU;
     const unsigned gridn = grid_for(n, kBlock, gcap);
 
-    hipLaunchKernelGGL(init_align_kernel, dim3(1), dim3(64), 0, s, d_rs, d_info);
-    ODB_LAUNCHED();
     hipLaunchKernelGGL(round0_ranks_kernel, dim3(1), dim3(kBlock), 0, s, d_off, d_groups_per_rank, W, d_ranks,
-                       d_gbase, st);
+                       d_gbase, st, d_rs, d_info);
     ODB_LAUNCHED();
     if (n > 0) {
         hipLaunchKernelGGL(round0_check_kernel, dim3(gridn), dim3(kBlock), 0, s, d_off, (const RankState*)d_ranks, W,
                            n, d_order, d_sorted_len, d_group_index, gstart, st);
         ODB_LAUNCHED();
-    }
-    {
-        DevStatus hs;
-        ODB_TRY_HIP(hipMemcpyAsync(&hs, st, sizeof(hs), hipMemcpyDeviceToHost, s));
-        ODB_TRY_HIP(hipStreamSynchronize(s));
-        if (hs.err & (kErrOrder | kErrGroupIndex))
-            return set_error(ODB_E_INVALID_DATA,
-                             "stage-1 arrays do not describe this window (first inconsistent position %lld)",
-                             (long long)hs.first_bad);
     }
 
     std::vector<int64_t> cnt(W);
@@ -1189,7 +1229,7 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     int32_t rounds = 0;
     int32_t stop = ODB_STOP_DRAINED;
     RoundState hrs{};
-    std::vector<RankState> hranks(W);
+    HostState hstate;
     for (;;) {
         int nonempty = 0;
         int64_t max_cnt = 0;
@@ -1216,39 +1256,38 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
         ODB_TRY((device_excl_scan<int64_t>(LiveLen{cur.len, d_off, d_ranks, W, rounds > 1 ? 1 : 0},
                                            LiveLenIncl{LiveLen{cur.len, d_off, d_ranks, W, rounds > 1 ? 1 : 0}, cs},
                                            n, ws_at<int64_t>(d_ws, L.partials), s)));
-        hipLaunchKernelGGL(target_kernel, dim3(1), dim3(kBlock), 0, s, d_ranks, d_cap, cap ? 1 : 0, W, d_rs);
-        ODB_LAUNCHED();
         hipLaunchKernelGGL(group_sizes_kernel, dim3(gridn), dim3(kBlock), 0, s, (const int32_t*)gstart,
-                           (const int64_t*)d_gbase, d_off, (const RankState*)d_ranks, W, gsize);
+                           (const int64_t*)d_gbase, d_off, (const RankState*)d_ranks, W, gsize, steps, max_cnt,
+                           (const DevStatus*)st);
         ODB_LAUNCHED();
-        hipLaunchKernelGGL(adjust_kernel, dim3(W), dim3(kBlock), 0, s, d_ranks, (const RoundState*)d_rs,
+        hipLaunchKernelGGL(adjust_kernel, dim3(W), dim3(kBlock), 0, s, d_ranks, d_cap, cap ? 1 : 0, W, d_rs,
                            (const int32_t*)gsize, ov_slot, kept, st);
-        ODB_LAUNCHED();
-        hipLaunchKernelGGL(fill_i64_kernel, dim3(gridn), dim3(kBlock), 0, s, steps, max_cnt, (int64_t)0);
         ODB_LAUNCHED();
         hipLaunchKernelGGL(slot_records_kernel, dim3(gridn), dim3(kBlock), 0, s, (const RankState*)d_ranks,
                            (const RoundState*)d_rs, d_off, W, (const int32_t*)gstart, (const int32_t*)gsize,
-                           (const int32_t*)kept, cur.len, (const int64_t*)cs, srows, smax, stok, sadj, steps);
+                           (const int32_t*)kept, cur.len, (const int64_t*)cs, srows, smax, stok, sadj, steps,
+                           (const DevStatus*)st);
         ODB_LAUNCHED();
-        hipLaunchKernelGGL(cut_kernel, dim3(1), dim3(kBlock), 0, s, d_rs, (const int64_t*)steps, nonjoin ? 1 : 0,
-                           params->quota);
-        ODB_LAUNCHED();
-        hipLaunchKernelGGL(finalize_kernel, dim3(W), dim3(kBlock), 0, s, d_ranks, (const RoundState*)d_rs, d_off,
+        hipLaunchKernelGGL(finalize_kernel, dim3(W), dim3(kBlock), 0, s, d_ranks, d_rs, (const int64_t*)steps,
+                           nonjoin ? 1 : 0, params->quota, d_off,
                            (const int32_t*)gstart, (const int32_t*)gsize, (const int32_t*)ov_slot,
-                           (const int32_t*)kept, ov_lo);
+                           (const int32_t*)kept, ov_lo, (const DevStatus*)st);
         ODB_LAUNCHED();
         hipLaunchKernelGGL(emit_kernel, dim3(gridn), dim3(kBlock), 0, s, (const RankState*)d_ranks,
                            (const RoundState*)d_rs, d_off, W, n, cur.ids, cur.len, cur.gidx, (const int32_t*)gstart,
                            (const int32_t*)gsize, (const int32_t*)ov_slot, (const int32_t*)ov_lo, dst, dst_len,
-                           bids[flip], blen[flip]);
+                           bids[flip], blen[flip], (const DevStatus*)st);
         ODB_LAUNCHED();
-        hipLaunchKernelGGL(advance_kernel, dim3(grid_for(W, kBlock)), dim3(kBlock), 0, s, d_ranks, W);
+        hipLaunchKernelGGL(advance_kernel, dim3(grid_for(W, kBlock)), dim3(kBlock), 0, s, d_ranks, W, d_rs);
         ODB_LAUNCHED();
-        ODB_TRY_HIP(hipMemcpyAsync(&hrs, d_rs, sizeof(hrs), hipMemcpyDeviceToHost, s));
-        ODB_TRY_HIP(hipMemcpyAsync(hranks.data(), d_ranks, sizeof(RankState) * W, hipMemcpyDeviceToHost, s));
-        DevStatus hst;
-        ODB_TRY_HIP(hipMemcpyAsync(&hst, st, sizeof(hst), hipMemcpyDeviceToHost, s));
-        ODB_TRY_HIP(hipStreamSynchronize(s));
+        ODB_TRY(read_state(L, d_ws, W, &hstate, s));
+        hrs = hstate.rs;
+        const DevStatus& hst = hstate.st;
+        const std::vector<RankState>& hranks = hstate.ranks;
+        if (hst.err & (kErrOrder | kErrGroupIndex))
+            return set_error(ODB_E_INVALID_DATA,
+                             "stage-1 arrays do not describe this window (first inconsistent position %lld)",
+                             (long long)hst.first_bad);
         if (hst.err & kErrInternal)
             return set_error(ODB_E_INTERNAL, "alignment round %d: group sizes inconsistent", rounds);
         // every round empties part of some buffer (T >= 1 steps of >= 1 sample for each
@@ -1290,13 +1329,12 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
         hipLaunchKernelGGL(plan_slots_kernel, dim3(grid_for(K, kBlock, gcap)), dim3(kBlock), 0, s,
                            (const RankState*)d_ranks, d_off, W, S, (const int32_t*)srows, (const int32_t*)smax,
                            (const int64_t*)stok, (const double*)sadj, d_slot_rows, d_slot_maxlen, d_slot_tokens,
-                           d_slot_tokens_approx);
+                           d_slot_tokens_approx, d_info);
         ODB_LAUNCHED();
     }
-    ODB_TRY((device_excl_scan<int64_t>(RowsLoad{d_slot_rows, K}, Store64{d_slot_row_off}, K + 1,
-                                       ws_at<int64_t>(d_ws, L.partials), s)));
-    ODB_TRY((device_excl_scan<int64_t>(TileLoad{d_slot_rows, d_slot_maxlen, K}, Store64{d_slot_tile_off}, K + 1,
-                                       ws_at<int64_t>(d_ws, L.partials), s)));
+    ODB_TRY((device_excl_scan<I64Pair>(RowsTilesLoad{d_slot_rows, d_slot_maxlen, K},
+                                       RowsTilesStore{d_slot_row_off, d_slot_tile_off}, K + 1,
+                                       ws_at<I64Pair>(d_ws, L.partials), s)));
     if (nonjoin && n > 0) {
         hipLaunchKernelGGL(compact_emit_kernel, dim3(gridn), dim3(kBlock), 0, s, (const int32_t*)dst,
                            (const int32_t*)dst_len, d_off, (const RankState*)d_ranks, W, n,
@@ -1329,22 +1367,12 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
         ODB_LAUNCHED();
     }
     // stats (Sec. 2.1 / App. I padding fraction) and coverage (App. C)
-    if (K > 0) {
-        hipLaunchKernelGGL(tokens_sum_kernel, dim3(grid_for(K, kBlock, gcap)), dim3(kBlock), 0, s,
-                           (const int64_t*)d_slot_tokens, K, d_info);
-        ODB_LAUNCHED();
-    }
-    hipLaunchKernelGGL(finish_info_kernel, dim3(1), dim3(64), 0, s, (const int64_t*)d_slot_row_off,
-                       (const int64_t*)d_slot_tile_off, K, d_info);
-    ODB_LAUNCHED();
-    ODB_TRY(run_plan_coverage(w, L, d_ws, d_emit_order, d_slot_row_off, S, d_leftover, d_leftover_off, nemit, nleft,
-                              s));
+    ODB_TRY(run_plan_coverage(w, L, d_ws, d_emit_order, d_slot_row_off, d_slot_tile_off, S, d_leftover,
+                              d_leftover_off, nemit, nleft, s));
 
-    DevInfo hi;
-    DevStatus hs;
-    ODB_TRY_HIP(hipMemcpyAsync(&hi, d_info, sizeof(hi), hipMemcpyDeviceToHost, s));
-    ODB_TRY_HIP(hipMemcpyAsync(&hs, st, sizeof(hs), hipMemcpyDeviceToHost, s));
-    ODB_TRY_HIP(hipStreamSynchronize(s));
+    ODB_TRY(read_state(L, d_ws, W, &hstate, s));
+    const DevInfo& hi = hstate.info;
+    const DevStatus& hs = hstate.st;
     h_info->emitted_samples = hi.emitted;
     h_info->leftover_samples = nleft;
     h_info->real_tokens = hi.real_tokens;
@@ -1353,6 +1381,10 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
     h_info->duplicate_ids = hi.duplicate_ids;
     h_info->bad_views = hi.bad_views;
     h_info->pad_fraction = hi.pad_fraction;
+    if (hs.err & kErrLength)
+        return set_error(ODB_E_INVALID_DATA,
+                         "sample %lld has a length outside [1, 2^31) or a negative token offset",
+                         (long long)hs.first_bad_len);
     if (hs.err & kErrSortedLen)
         return set_error(ODB_E_INVALID_DATA,
                          "stage-1 arrays do not describe this window (sorted length of sample %lld is not its CSR "

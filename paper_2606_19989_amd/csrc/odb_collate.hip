@@ -52,9 +52,14 @@ constexpr int kGroups = 1;                                           // groups p
 constexpr int64_t kGroupSpan = (int64_t)kWave * kVec;                // 256
 constexpr int64_t kWaveStep = kGroupSpan * kGroups;                  // 256
 constexpr int64_t kBlockStep = kWaveStep * (kCollateBlock / kWave);  // 1024
-// consecutive steps per run, a block's unit of work (64 measured best with runs taken from a
-// counter: 32 repositions too often, 128 and 256 leave a longer tail)
-constexpr int64_t kRunSteps = 64;
+// Consecutive steps per run, a block's unit of work: 64 on large outputs (measured best with
+// runs taken from a counter: 32 repositions too often, 128 and 256 leave a longer tail),
+// shorter when the output gives a block fewer than kRunsPerBlock runs of 64 (down to
+// kMinRunSteps), so the blocks' finishing times stay within a small fraction of the kernel.
+constexpr int64_t kRunSteps = 64;       // 2^6
+constexpr int64_t kMinRunSteps = 16;    // 2^4
+constexpr int64_t kRunsPerBlock = 32;
+static_assert(kRunSteps == 64 && kMinRunSteps == 16, "the run length is 2^4 .. 2^6 steps");
 // Three resident blocks (12 waves) per compute unit stream fastest (two, four, five or
 // six were slower), and they leave five of the eight wave slots and about half the
 // registers of every SIMD to kernels on other streams: the grouping and alignment of the next window can run
@@ -306,10 +311,11 @@ __device__ __forceinline__ v4i load_tokens(const Cursor& c, const RowRec& r, con
 // ahead (`pf`), so the atomic's latency is off the pipeline; the waves of a block cross a
 // run boundary at the same step, where the index is handed to them through LDS.  Smaller
 // runs for the last stretch (8 to 32 steps) trimmed the finishing tail by under 0.1%.
-__device__ __forceinline__ int64_t next_step(int64_t s, int64_t nsteps, int64_t nruns, unsigned long long& pf,
+__device__ __forceinline__ int64_t next_step(int64_t s, int64_t nsteps, int64_t nruns, int run_shift,
+                                             unsigned long long& pf,
                                              unsigned long long* runs) {
-    const int64_t r = s / kRunSteps;
-    if (s + 1 < (r + 1) * kRunSteps && s + 1 < nsteps) return s + 1;
+    const int64_t r = s >> run_shift;
+    if (s + 1 < ((r + 1) << run_shift) && s + 1 < nsteps) return s + 1;
     __shared__ int64_t s_run;
     if (threadIdx.x == 0) {
         s_run = (int64_t)pf;
@@ -318,7 +324,7 @@ __device__ __forceinline__ int64_t next_step(int64_t s, int64_t nsteps, int64_t 
     __syncthreads();
     const int64_t r2 = s_run;
     __syncthreads();
-    return r2 < nruns ? r2 * kRunSteps : -1;
+    return r2 < nruns ? r2 << run_shift : -1;
 }
 
 // One pipeline stage of a lane: where its 4 elements are, their row, their tokens.
@@ -441,7 +447,11 @@ __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t 
     const int64_t total = total_plan < capacity ? total_plan : capacity;
     if (total <= 0) return;
     const int64_t nsteps = (total + kBlockStep - 1) / kBlockStep;
-    const int64_t nruns = (nsteps + kRunSteps - 1) / kRunSteps;
+    // runs of 2^run_shift steps: the largest power of two from kMinRunSteps to kRunSteps that
+    // still gives every block kRunsPerBlock runs
+    int run_shift = 4;
+    while (run_shift < 6 && ((int64_t)gridDim.x * kRunsPerBlock << (run_shift + 1)) <= nsteps) ++run_shift;
+    const int64_t nruns = (nsteps + (1ll << run_shift) - 1) >> run_shift;
     if ((int64_t)blockIdx.x >= nruns) return;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
@@ -456,9 +466,9 @@ __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t 
     // pipeline: step s0 is stored from stage a, s1's tokens load into b, s2's rows into c
     unsigned long long pf = 0;
     if (threadIdx.x == 0) pf = atomicAdd(p.runs, 1ull) + gridDim.x;
-    int64_t s0 = (int64_t)blockIdx.x * kRunSteps;
-    int64_t s1 = next_step(s0, nsteps, nruns, pf, p.runs);
-    int64_t s2 = s1 >= 0 ? next_step(s1, nsteps, nruns, pf, p.runs) : -1;
+    int64_t s0 = (int64_t)blockIdx.x << run_shift;
+    int64_t s1 = next_step(s0, nsteps, nruns, run_shift, pf, p.runs);
+    int64_t s2 = s1 >= 0 ? next_step(s1, nsteps, nruns, run_shift, pf, p.runs) : -1;
     Stage X, Y, Z;
     {
         const int64_t e = elem(s0);
@@ -505,7 +515,7 @@ __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t 
         }                                                                                     \
         s0 = s1;                                                                              \
         s1 = s2;                                                                              \
-        s2 = s2 >= 0 ? next_step(s2, nsteps, nruns, pf, p.runs) : -1;                         \
+        s2 = s2 >= 0 ? next_step(s2, nsteps, nruns, run_shift, pf, p.runs) : -1;                         \
     }
     // unrolled three times so that no stage register is copied while its load is in flight
     for (;;) {

@@ -69,11 +69,12 @@ bool make_layout(const odb_window_t* w, Layout* L) {
         o = align_up(o + (bytes ? bytes : 1));
         return at;
     };
+    // status, round, info and ranks first and in this order: one copy reads them all
     L->status = take(sizeof(DevStatus));
     L->round = take(sizeof(RoundState));
     L->info = take(sizeof(DevInfo));
-    L->sketch = take(256);
     L->ranks = take(sizeof(RankState) * W);
+    L->sketch = take(256);
     L->rank_off = take(8 * (W + 1));
     L->cap = take(8 * W);
     L->gbase = take(8 * (W + 1));
@@ -84,7 +85,7 @@ bool make_layout(const odb_window_t* w, Layout* L) {
     L->vals0 = take(4 * n1);
     L->vals1 = take(4 * n1);
     L->counts = take(4 * (256 * nb + 1));
-    L->partials = take(8 * partials);
+    L->partials = take(16 * partials);   // room for pairs of int64 sums
     L->jmp0 = take(4 * n1);
     L->jmp1 = take(4 * n1);
     L->marks = take(n1);
@@ -128,27 +129,66 @@ int check_workspace(const odb_window_t* w, void* d_ws, size_t ws_bytes, Layout* 
     return ODB_OK;
 }
 
-// The collate's error word is left alone: odb_collate clears it when it starts and
-// odb_collate_status when it has read it, so a plan call made on the same workspace in
-// between does not erase a collate error.
-__global__ void init_status_kernel(DevStatus* st) {
-    if (threadIdx.x == 0) {
-        st->err = 0;
-        st->first_bad = 0x7FFFFFFFFFFFFFFFll;
-        st->min_len = 0xFFFFFFFFu;
-        st->max_len = 0;
+// Small host arrays reach the device as kernel arguments, kValuesPerLaunch values per
+// launch: no host-to-device copy (which, from pageable memory, may wait for the stream)
+// and nothing a graph capture could not record.
+constexpr int kValuesPerLaunch = 64;
+struct Values64 {
+    int64_t v[kValuesPerLaunch];
+};
+
+// Stores values [first, first + count) of an array; the first launch of a call also
+// resets the status word.  The collate's error word is left alone: odb_collate clears it
+// when it starts and odb_collate_status when it has read it, so a plan call made on the
+// same workspace in between does not erase a collate error.
+__global__ void store_values_kernel(Values64 vals, int64_t* dst, int count, DevStatus* st) {
+    const int t = threadIdx.x;
+    if (t < count) dst[t] = vals.v[t];
+    if (st) {
+        if (t == 0) {
+            st->err = 0;
+            st->first_bad = 0x7FFFFFFFFFFFFFFFll;
+            st->first_bad_len = 0x7FFFFFFFFFFFFFFFll;
+            st->min_len = 0xFFFFFFFFu;
+            st->max_len = 0;
+        }
+        if (t < kMaxJumpRounds) st->jump_changed[t] = 0;
     }
-    if (threadIdx.x < kMaxJumpRounds) st->jump_changed[threadIdx.x] = 0;
+}
+
+static int store_values(const int64_t* src, int64_t count, int64_t* dst, DevStatus* st, hipStream_t s) {
+    int64_t a = 0;
+    do {
+        Values64 v{};
+        const int64_t left = count - a;
+        const int c = (int)(left < kValuesPerLaunch ? (left > 0 ? left : 0) : kValuesPerLaunch);
+        for (int i = 0; i < c; ++i) v.v[i] = src[a + i];
+        hipLaunchKernelGGL(store_values_kernel, dim3(1), dim3(kValuesPerLaunch), 0, s, v, dst + a, c,
+                           a == 0 ? st : (DevStatus*)nullptr);
+        ODB_LAUNCHED();
+        a += kValuesPerLaunch;
+    } while (a < count);
+    return ODB_OK;
 }
 
 int upload_small(const odb_window_t* w, const Layout& L, void* ws, const int64_t* cap, hipStream_t s) {
     const int W = w->num_ranks;
-    ODB_TRY_HIP(hipMemcpyAsync(ws_at<int64_t>(ws, L.rank_off), w->rank_offsets, 8 * (size_t)(W + 1),
-                               hipMemcpyHostToDevice, s));
-    if (cap)
-        ODB_TRY_HIP(hipMemcpyAsync(ws_at<int64_t>(ws, L.cap), cap, 8 * (size_t)W, hipMemcpyHostToDevice, s));
-    hipLaunchKernelGGL(init_status_kernel, dim3(1), dim3(64), 0, s, ws_at<DevStatus>(ws, L.status));
-    ODB_LAUNCHED();
+    ODB_TRY(store_values(w->rank_offsets, W + 1, ws_at<int64_t>(ws, L.rank_off), ws_at<DevStatus>(ws, L.status), s));
+    if (cap) ODB_TRY(store_values(cap, W, ws_at<int64_t>(ws, L.cap), nullptr, s));
+    return ODB_OK;
+}
+
+int read_state(const Layout& L, void* ws, int W, HostState* h, hipStream_t s) {
+    const size_t bytes = L.ranks + sizeof(RankState) * (size_t)W - L.status;
+    h->buf.resize(bytes);
+    ODB_TRY_HIP(hipMemcpyAsync(h->buf.data(), ws_at<char>(ws, L.status), bytes, hipMemcpyDeviceToHost, s));
+    ODB_TRY_HIP(hipStreamSynchronize(s));
+    const char* b = h->buf.data();
+    memcpy(&h->st, b, sizeof(DevStatus));
+    memcpy(&h->rs, b + (L.round - L.status), sizeof(RoundState));
+    memcpy(&h->info, b + (L.info - L.status), sizeof(DevInfo));
+    h->ranks.resize((size_t)W);
+    memcpy(h->ranks.data(), b + (L.ranks - L.status), sizeof(RankState) * (size_t)W);
     return ODB_OK;
 }
 

@@ -165,9 +165,15 @@ __global__ void __launch_bounds__(kBlock) radix_hist_kernel(const int64_t* __res
     const SortTile b = sort_tile(off, tile_first, W, blockIdx.x);
     const int radix = 1 << dbits;
     const uint32_t mask = (uint32_t)radix - 1;
-    __shared__ uint32_t h[256];
-    for (int d = threadIdx.x; d < radix; d += kBlock) h[d] = 0;
+    // one count table per wave: each distinct digit of a wave has one leader lane, the only
+    // writer of its entry, so no atomics; the leaders write in up to four steps by the
+    // digit's top two bits (digits d and d + 64 share an LDS bank), so no bank conflicts
+    constexpr int kWaves = kBlock / kWave;
+    __shared__ uint32_t h[kWaves][256];
+    const int w = threadIdx.x / kWave;
+    for (int i = threadIdx.x; i < kWaves * 256; i += kBlock) (&h[0][0])[i] = 0;
     __syncthreads();
+    const uint32_t quarters = ((uint32_t)radix + 63u) >> 6;
     for (int it = 0; it < kSortItems; ++it) {
         const int li = it * kBlock + threadIdx.x;
         const bool valid = li < b.count;
@@ -176,12 +182,20 @@ __global__ void __launch_bounds__(kBlock) radix_hist_kernel(const int64_t* __res
         if (valid) key = kFirst ? maxl - (uint32_t)len_in[p] : keys_in[p];
         const uint32_t d = (key >> shift) & mask;
         const uint64_t peers = match_digit(d, valid, dbits);
-        if (valid && lanes_below(peers) == 0) atomicAdd(&h[d], (uint32_t)__popcll(peers));
+        const bool lead = valid && lanes_below(peers) == 0;
+        const uint32_t c = (uint32_t)__popcll(peers);
+#pragma nounroll
+        for (uint32_t q = 0; q < quarters; ++q)
+            if (lead && (d >> 6) == q) h[w][d] += c;
     }
     __syncthreads();
     const int64_t col = (int64_t)b.first << dbits;
-    for (int d = threadIdx.x; d < radix; d += kBlock)
-        counts[col + (int64_t)d * b.seg_tiles + b.j] = h[d];
+    for (int d = threadIdx.x; d < radix; d += kBlock) {
+        uint32_t sum = 0;
+#pragma unroll
+        for (int k = 0; k < kWaves; ++k) sum += h[k][d];
+        counts[col + (int64_t)d * b.seg_tiles + b.j] = sum;
+    }
 }
 
 // Scatter one tile.  Items are taken in position order (round `it` covers positions
@@ -234,6 +248,7 @@ __global__ void __launch_bounds__(kBlock) radix_scatter_kernel(
     }
     __syncthreads();
     const int w = threadIdx.x / kWave;
+    const uint32_t quarters = ((uint32_t)radix + 63u) >> 6;
     for (int it = 0; it < kSortItems; ++it) {
         const int li = it * kBlock + threadIdx.x;
         const bool valid = li < b.count;
@@ -247,12 +262,24 @@ __global__ void __launch_bounds__(kBlock) radix_scatter_kernel(
         const uint32_t d = (key >> shift) & mask;
         const uint64_t peers = match_digit(d, valid, dbits);
         const uint32_t below = lanes_below(peers);
-        if (valid && below == 0) s_w[w][d] = (uint32_t)__popcll(peers);
+        const bool lead = valid && below == 0;
+        const uint32_t c = (uint32_t)__popcll(peers);
+        // digit-indexed LDS accesses go in steps by the digit's top two bits (digits d and
+        // d + 64 share a bank), so the distinct digits of one step never collide
+#pragma nounroll
+        for (uint32_t h = 0; h < quarters; ++h)
+            if (lead && (d >> 6) == h) s_w[w][d] = c;
         __syncthreads();
+        uint32_t q = 0;
+#pragma nounroll
+        for (uint32_t h = 0; h < quarters; ++h) {
+            if (valid && (d >> 6) == h) {
+                uint32_t pre = s_run[d] + s_local[d];
+                for (int k = 0; k < w; ++k) pre += s_w[k][d];
+                q = pre + below;
+            }
+        }
         if (valid) {
-            uint32_t pre = s_run[d];
-            for (int k = 0; k < w; ++k) pre += s_w[k][d];
-            const uint32_t q = s_local[d] + pre + below;
             s_key[q] = key;
             s_val[q] = val;
         }
@@ -528,7 +555,465 @@ __global__ void groups_kernel(const int32_t* __restrict__ incl, const int64_t* _
     }
 }
 
+// ---- one block per rank
+// When every rank holds at most kRankBlockMax samples, each rank is grouped by one
+// 1024-thread block in two launches, with no host synchronisation: rank_sort_kernel (lengths, validity, stable LSD
+// radix sort on byte digits of the length) and rank_walk_kernel (the group chain over the
+// runs of equal batch size, and the group index of every position in closed form).
+constexpr int kRankThreads = 1024;
+constexpr int kRankWaves = kRankThreads / kWave;
+constexpr int kRankItems = 4;                     // lengths a thread loads at once in the first pass
+constexpr int kRankGroup = 4;                     // rounds of a pass whose items are loaded together
+constexpr int kRankRunCap = 3840;                 // runs of equal batch size a rank may have
+// Samples of the largest rank grouped this way.  A block's pass over its rank is bound by
+// the issue rate of its one compute unit (every round of 1024 items costs each of its 16
+// waves a few hundred instructions: ~2.7 us per round on MI355X), so larger ranks go to the
+// multi-block path, whose launches and one synchronisation cost less than a block's
+// rounds from about this size on.
+constexpr int64_t kRankBlockMax = 16384;
+
+// Exclusive scan of v over the first 256 threads of a kRankThreads block (4 waves), every
+// thread of the block taking part in the barriers; *total receives the sum.
+__device__ __forceinline__ uint32_t scan256(uint32_t v, uint32_t* total) {
+    __shared__ uint32_t s_w[4];
+    const int t = threadIdx.x;
+    uint32_t inc = 0;
+    if (t < 256) {
+        inc = wave_scan_dpp<OpAdd>(v);
+        if ((t & (kWave - 1)) == kWave - 1) s_w[t / kWave] = inc;
+    }
+    __syncthreads();
+    uint32_t pre = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t x = s_w[i];
+        pre += (t < 256 && i < t / kWave) ? x : 0u;
+        tot += x;
+    }
+    __syncthreads();
+    *total = tot;
+    return pre + inc - v;
+}
+
+// LDS has 64 banks of 4 bytes and a table row holds 256 digit values, so digits d and
+// d + 64 share a bank.  Accesses indexed by a lane's digit therefore go in four steps, one
+// per value of the digit's top two bits: within a step the lanes' distinct digits sit in
+// distinct banks (lanes with equal digits share an address, a broadcast), so no step has
+// a bank conflict.  The loop is kept rolled so the four masked accesses stay four.
+#define ODB_BY_DIGIT_QUARTER(d, stmt)                     \
+    _Pragma("nounroll") for (uint32_t h_ = 0; h_ < 4u; ++h_) \
+        if (((d) >> 6) == h_) { stmt; }
+
+// Per-wave digit counts: for each distinct digit of the wave's valid lanes, the lowest such
+// lane adds the number of lanes holding it to row w of `tbl` (one writer per address).
+__device__ __forceinline__ void count_digits(uint32_t (*tbl)[256], int w, uint32_t d, bool valid) {
+    const uint64_t peers = match_digit(d, valid, 8);
+    const bool lead = valid && lanes_below(peers) == 0;
+    const uint32_t c = (uint32_t)__popcll(peers);
+    ODB_BY_DIGIT_QUARTER(d, if (lead) tbl[w][d] += c)
+}
+
+// One stable scatter pass of rank_sort_kernel over digit bits [shift, shift + 8): round i
+// places items i*1024 .. i*1024+1023 of the pass's input (keys sk, ids sv; the first
+// pass's ids are the positions themselves).  A round's rank of an item among equal digits
+// is: items of that digit placed in earlier rounds (s_run), in lower waves of this round
+// (s_cnt prefix) and in lower lanes of its wave (ballot match).  The two barriers of a
+// round order LDS only: nothing in the block reads the round's global stores before the
+// pass ends.  Loads run a group of kRankGroup rounds ahead, into the register set (A or B)
+// of the group after next, at clamped positions (unconditional loads: a load under a branch
+// makes the compiler wait for it where the paths join).
+template <bool kFirst>
+__device__ __forceinline__ void scatter_pass(const int32_t* __restrict__ sk, const int32_t* __restrict__ sv,
+                                             int32_t* __restrict__ dk, int32_t* __restrict__ dv, int64_t base,
+                                             int cnt, int rounds, int shift, uint32_t (*s_cnt)[256],
+                                             uint32_t (*s_pre)[256], uint32_t* s_run) {
+    const int t = threadIdx.x, w = t / kWave;
+    auto load_group = [&](int g, uint32_t (&kk)[kRankGroup], int32_t (&vv)[kRankGroup]) {
+#pragma unroll
+        for (int j = 0; j < kRankGroup; ++j) {
+            const int q = (g * kRankGroup + j) * kRankThreads + t;
+            const int qc = q < cnt ? q : cnt - 1;
+            kk[j] = (uint32_t)sk[base + qc];
+            vv[j] = kFirst ? (int32_t)(base + q) : sv[base + qc];
+        }
+    };
+    auto place_group = [&](int g, const uint32_t (&kk)[kRankGroup], const int32_t (&vv)[kRankGroup]) {
+#pragma unroll
+        for (int j = 0; j < kRankGroup; ++j) {
+            const int i = g * kRankGroup + j;
+            if (i >= rounds) break;   // uniform
+            const int q = i * kRankThreads + t;
+            const bool valid = q < cnt;
+            const uint32_t key = kk[j];
+            const uint32_t d = (key >> shift) & 255u;
+            const uint64_t peers = match_digit(d, valid, 8);
+            const uint32_t below = lanes_below(peers);
+            const bool lead = valid && below == 0;
+            const uint32_t c_lead = (uint32_t)__popcll(peers);
+            ODB_BY_DIGIT_QUARTER(d, if (lead) s_cnt[w][d] = c_lead)
+            lds_barrier();
+            if (t < 256) {
+                // s_pre: where this round's first item of digit t from each wave goes
+                // (s_run holds the bucket's start plus the items placed so far)
+                uint32_t run = s_run[t];
+#pragma unroll
+                for (int k2 = 0; k2 < kRankWaves; ++k2) {
+                    const uint32_t c = s_cnt[k2][t];
+                    s_pre[k2][t] = run;
+                    run += c;
+                    s_cnt[k2][t] = 0;
+                }
+                s_run[t] = run;
+            }
+            lds_barrier();
+            uint32_t at = 0;
+            ODB_BY_DIGIT_QUARTER(d, if (valid) at = s_pre[w][d])
+            if (valid) {
+                dk[base + at + below] = (int32_t)key;
+                dv[base + at + below] = vv[j];
+            }
+        }
+    };
+    const int groups = (rounds + kRankGroup - 1) / kRankGroup;
+    uint32_t ka_[kRankGroup], kb_[kRankGroup];
+    int32_t va_[kRankGroup], vb_[kRankGroup];
+    load_group(0, ka_, va_);
+    for (int g = 0; g < groups; g += 2) {
+        load_group(g + 1, kb_, vb_);
+        place_group(g, ka_, va_);
+        if (g + 1 >= groups) break;   // uniform
+        load_group(g + 2, ka_, va_);
+        place_group(g + 1, kb_, vb_);
+    }
+}
+
+// Sorts rank r's samples by (length desc, id asc): writes len (every sample's length,
+// invalid ones as 1), order and sorted_len.  Digits are the bytes of the length, low to
+// high; a digit whose value is the same for every sample of the rank is skipped; each pass
+// places the buckets from the highest digit value down and keeps the order within a
+// bucket, so the result is by length descending, ties in sample-id order.
+__global__ void __launch_bounds__(kRankThreads) rank_sort_kernel(
+    const int64_t* __restrict__ tok_off, const int64_t* __restrict__ off, int32_t* __restrict__ len,
+    int32_t* __restrict__ ka, int32_t* __restrict__ va, int32_t* __restrict__ kb, int32_t* __restrict__ vb,
+    int32_t* __restrict__ order, int32_t* __restrict__ slen, DevStatus* st) {
+    __shared__ uint32_t s_cnt[kRankWaves][256];   // first pass: digit-0 counts; passes: counts of a round
+    __shared__ uint32_t s_pre[kRankWaves][256];   // first pass: digit-1 counts; passes: prefixes of a round
+    __shared__ uint32_t s_hist[4][256];
+    __shared__ uint32_t s_run[256];
+    __shared__ uint32_t s_max;
+    __shared__ unsigned long long s_bad;
+    __shared__ int s_active[4];
+    const int r = blockIdx.x;
+    const int64_t base = off[r];
+    const int cnt = (int)(off[r + 1] - base);
+    if (cnt <= 0) return;
+    const int t = threadIdx.x, w = t / kWave;
+    for (int i = t; i < kRankWaves * 256; i += kRankThreads) {
+        (&s_cnt[0][0])[i] = 0;
+        (&s_pre[0][0])[i] = 0;
+    }
+    if (t == 0) {
+        s_max = 0;
+        s_bad = ~0ull;
+    }
+    __syncthreads();
+
+    // lengths, validity, histograms of digits 0 and 1
+    uint32_t lmax = 0;
+    unsigned long long bad = ~0ull;
+    for (int q0 = 0; q0 < cnt; q0 += kRankThreads * kRankItems) {
+        int64_t a[kRankItems], b[kRankItems];
+#pragma unroll
+        for (int j = 0; j < kRankItems; ++j) {
+            const int q = q0 + j * kRankThreads + t;
+            const int qc = q < cnt ? q : cnt - 1;
+            a[j] = tok_off[base + qc];
+            b[j] = tok_off[base + qc + 1];
+        }
+#pragma unroll
+        for (int j = 0; j < kRankItems; ++j) {
+            const int q = q0 + j * kRankThreads + t;
+            const bool valid = q < cnt;
+            uint32_t l = 0;
+            if (valid) {
+                int64_t ll = b[j] - a[j];
+                if (ll < 1 || ll > INT_MAX || a[j] < 0) {
+                    const unsigned long long id = (unsigned long long)(base + q);
+                    bad = id < bad ? id : bad;
+                    ll = 1;
+                }
+                l = (uint32_t)ll;
+                len[base + q] = (int32_t)l;
+                lmax = l > lmax ? l : lmax;
+            }
+            count_digits(s_cnt, w, l & 255u, valid);
+            count_digits(s_pre, w, (l >> 8) & 255u, valid);
+        }
+    }
+    lmax = wave_scan_dpp<OpMax>(lmax);
+    if ((t & (kWave - 1)) == kWave - 1) atomicMax(&s_max, lmax);
+    if (bad != ~0ull) atomicMin(&s_bad, bad);
+    __syncthreads();
+    if (t < 512) {
+        const int d = t & 255;
+        uint32_t (*tbl)[256] = t < 256 ? s_cnt : s_pre;
+        uint32_t sum = 0;
+#pragma unroll
+        for (int k = 0; k < kRankWaves; ++k) {
+            sum += tbl[k][d];
+            tbl[k][d] = 0;
+        }
+        s_hist[t / 256][d] = sum;
+    }
+    if (t == 0 && s_bad != ~0ull) {
+        atomicOr(&st->err, kErrLength);
+        atomicMin((unsigned long long*)&st->first_bad, s_bad);
+    }
+    __syncthreads();
+    const uint32_t maxl = s_max;
+    if (maxl >= (1u << 16)) {
+        // lengths of 2^16 or more: histograms of digits 2 and 3
+        for (int q0 = 0; q0 < cnt; q0 += kRankThreads) {
+            const int q = q0 + t;
+            const bool valid = q < cnt;
+            const uint32_t l = valid ? (uint32_t)len[base + q] : 0u;
+            count_digits(s_cnt, w, (l >> 16) & 255u, valid);
+            count_digits(s_pre, w, l >> 24, valid);
+        }
+        __syncthreads();
+        if (t < 512) {
+            const int d = t & 255;
+            uint32_t (*tbl)[256] = t < 256 ? s_cnt : s_pre;
+            uint32_t sum = 0;
+#pragma unroll
+            for (int k = 0; k < kRankWaves; ++k) {
+                sum += tbl[k][d];
+                tbl[k][d] = 0;
+            }
+            s_hist[2 + t / 256][d] = sum;
+        }
+    } else if (t < 512) {
+        s_hist[2 + t / 256][t & 255] = (t & 255) == 0 ? (uint32_t)cnt : 0u;
+    }
+    __syncthreads();
+    // a digit takes part if more than one of its values occurs
+    if (t < 4 * kWave) {
+        const int k = t / kWave, lane = t & (kWave - 1);
+        int nz = 0;
+        for (int d = lane; d < 256; d += kWave) nz += s_hist[k][d] != 0;
+        nz = wave_sum(nz);
+        if (lane == 0) s_active[k] = nz > 1;
+    }
+    __syncthreads();
+    int passes = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) passes += s_active[k];
+
+    if (passes == 0) {   // every length equal: formation order is id order
+        for (int q = t; q < cnt; q += kRankThreads) {
+            order[base + q] = (int32_t)(base + q);
+            slen[base + q] = len[base + q];
+        }
+        return;
+    }
+    int pass = 0;
+    const int rounds = (cnt + kRankThreads - 1) / kRankThreads;
+    for (int k = 0; k < 4; ++k) {
+        if (!s_active[k]) continue;
+        const bool first = pass == 0, last = pass == passes - 1;
+        const int32_t* sk = first ? len : ((pass & 1) ? ka : kb);
+        const int32_t* sv = (pass & 1) ? va : vb;
+        int32_t* dk = last ? slen : ((pass & 1) ? kb : ka);
+        int32_t* dv = last ? order : ((pass & 1) ? vb : va);
+        // bucket of digit value d starts after every higher value's samples
+        {
+            uint32_t tot;
+            const uint32_t v = t < 256 ? s_hist[k][255 - t] : 0u;
+            const uint32_t ex = scan256(v, &tot);
+            if (t < 256) s_run[255 - t] = ex;
+        }
+        __syncthreads();
+        if (first)
+            scatter_pass<true>(sk, sk, dk, dv, base, cnt, rounds, 8 * k, s_cnt, s_pre, s_run);
+        else
+            scatter_pass<false>(sk, sv, dk, dv, base, cnt, rounds, 8 * k, s_cnt, s_pre, s_run);
+        __syncthreads();
+        ++pass;
+    }
+}
+
+// Batch size B(l) (Eq. 1), clipped to 2^31 - 1 (any larger step leaves the rank).
+__device__ __forceinline__ uint32_t step_of(int32_t l, int64_t budget) {
+    const int64_t b = batch_size(budget, l);
+    return (uint32_t)(b < INT32_MAX ? b : INT32_MAX);
+}
+
+// Calls f(q, step) for every run start q in [lo, hi) (1 <= lo < hi <= cnt), in order: q = 1,
+// and every q whose step B(l[q-1]) differs from the previous position's B(l[q-2]).  Loads
+// eight lengths at a time, at clamped positions, so the loads of a batch are in flight
+// together; equal neighbouring lengths skip the divisions.
+template <typename F>
+__device__ __forceinline__ void chunk_run_starts(const int32_t* __restrict__ slen, int64_t base, int lo, int hi,
+                                                 int64_t budget, F f) {
+    int32_t lp = lo >= 2 ? slen[base + lo - 2] : 0;
+    uint32_t bp = lo >= 2 ? step_of(lp, budget) : 0u;
+    for (int q0 = lo; q0 < hi; q0 += 8) {
+        int32_t l8[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int qq = q0 + j < hi ? q0 + j : hi - 1;
+            l8[j] = slen[base + qq - 1];
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int q = q0 + j;
+            if (q >= hi) break;
+            const int32_t l = l8[j];
+            if (q == 1) {
+                bp = step_of(l, budget);
+                f(q, bp);
+            } else if (l != lp) {
+                const uint32_t b = step_of(l, budget);
+                if (b != bp) f(q, b);
+                bp = b;
+            }
+            lp = l;
+        }
+    }
+}
+
+// Group chain of rank r from its sorted lengths.  Positions q >= 1 fall into runs of equal
+// step B(l[q-1]) (the lengths are sorted, so the step never decreases along the rank).
+// Inside a run of step b the chain advances by b, so one thread walks the runs and records
+// each run's first chain position c; then every position's group index follows in closed
+// form: the chain positions before its run, plus those of its run up to it.
+__global__ void __launch_bounds__(kRankThreads) rank_walk_kernel(const int64_t* __restrict__ off,
+                                                                 const int32_t* __restrict__ slen, int64_t budget,
+                                                                 int32_t* __restrict__ gidx,
+                                                                 int32_t* __restrict__ groups_out, DevStatus* st) {
+    __shared__ uint32_t s_start[kRankRunCap + 1], s_b[kRankRunCap], s_c[kRankRunCap], s_gb[kRankRunCap];
+    const int r = blockIdx.x;
+    const int64_t base = off[r];
+    const int cnt = (int)(off[r + 1] - base);
+    const int t = threadIdx.x;
+    if (cnt <= 1) {
+        if (t == 0) {
+            if (cnt == 1) gidx[base] = 0;
+            groups_out[r] = cnt;
+        }
+        return;
+    }
+    // run starts: every thread checks a chunk of positions [1, cnt); the step is monotone, so
+    // a chunk whose first position and last position have the step of the position before
+    // it holds no run start
+    const int span = cnt - 1;
+    const int per = (span + kRankThreads - 1) / kRankThreads;
+    const int lo = 1 + t * per;
+    const int hi = lo + per < cnt ? lo + per : cnt;
+    const bool busy = lo < hi && (lo == 1 || step_of(slen[base + lo - 2], budget) !=
+                                                 step_of(slen[base + hi - 2], budget));
+    uint32_t mine = 0;
+    if (busy) chunk_run_starts(slen, base, lo, hi, budget, [&](int, uint32_t) { ++mine; });
+    // exclusive scan of the per-thread counts over the block
+    __shared__ uint32_t s_wsum[kRankWaves];
+    __shared__ uint32_t s_total;
+    uint32_t inc = wave_scan_dpp<OpAdd>(mine);
+    if ((t & (kWave - 1)) == kWave - 1) s_wsum[t / kWave] = inc;
+    __syncthreads();
+    uint32_t pre = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kRankWaves; ++i) {
+        pre += i < t / kWave ? s_wsum[i] : 0u;
+        tot += s_wsum[i];
+    }
+    const uint32_t at0 = pre + inc - mine;
+    if (tot > (uint32_t)kRankRunCap) {
+        // more runs than the table holds (the host picks this path only when that cannot
+        // happen): report, and leave the rank without groups
+        if (t == 0) {
+            atomicOr(&st->err, kErrInternal);
+            groups_out[r] = 0;
+        }
+        return;
+    }
+    if (mine) {
+        uint32_t at = at0;
+        chunk_run_starts(slen, base, lo, hi, budget, [&](int q, uint32_t b) {
+            s_start[at] = (uint32_t)q;
+            s_b[at] = b;
+            ++at;
+        });
+    }
+    const int R = (int)tot;
+    if (t == 0) s_start[R] = (uint32_t)cnt;
+    __syncthreads();
+    if (t == 0) {
+        // positions, steps and their sums stay below 2^32 (positions < 2^31, steps <= 2^31 - 1),
+        // so the walk runs on 32-bit division
+        uint32_t cur = 1;   // next(0) = 1: the second group starts at position 1
+        for (int i = 0; i < R; ++i) {
+            const uint32_t e = s_start[i + 1], b = s_b[i];
+            const bool hit = cur < e;
+            s_c[i] = hit ? cur : 0xFFFFFFFFu;
+            const uint32_t k = hit ? (e - cur + b - 1) / b : 0u;
+            cur += k * b;
+        }
+    }
+    __syncthreads();
+    // chain positions per run and their exclusive prefix (runs dealt round robin over threads)
+    {
+        uint32_t carry = 0;
+        for (int i0 = 0; i0 < R; i0 += kRankThreads) {
+            const int i = i0 + t;
+            uint32_t ng = 0;
+            if (i < R) {
+                const uint32_t c = s_c[i], e = s_start[i + 1], b = s_b[i];
+                ng = c < e ? (e - c + b - 1) / b : 0u;
+            }
+            const uint32_t inc2 = wave_scan_dpp<OpAdd>(ng);
+            __syncthreads();
+            if ((t & (kWave - 1)) == kWave - 1) s_wsum[t / kWave] = inc2;
+            __syncthreads();
+            uint32_t pre2 = 0, tot2 = 0;
+#pragma unroll
+            for (int w2 = 0; w2 < kRankWaves; ++w2) {
+                pre2 += w2 < t / kWave ? s_wsum[w2] : 0u;
+                tot2 += s_wsum[w2];
+            }
+            if (i < R) s_gb[i] = carry + pre2 + inc2 - ng;
+            carry += tot2;
+        }
+        if (t == 0) s_total = carry;
+    }
+    __syncthreads();
+    // group index of every position: chain positions up to it, minus one
+    for (int q = t; q < cnt; q += kRankThreads) {
+        int32_t g = 0;
+        if (q > 0) {
+            int a = 0, z = R;   // last run with start <= q: s_start[a] <= q < s_start[z]
+            while (z - a > 1) {
+                const int m = (a + z) >> 1;
+                if (s_start[m] <= (uint32_t)q) a = m; else z = m;
+            }
+            const uint32_t c = s_c[a];
+            g = (int32_t)(s_gb[a] + ((uint32_t)q >= c ? ((uint32_t)q - c) / s_b[a] + 1u : 0u));
+        }
+        gidx[base + q] = g;
+    }
+    if (t == 0) groups_out[r] = (int32_t)(1 + s_total);
+}
+
 }  // namespace
+
+// Distinct steps a rank's sorted sequence can hold: at most the distinct values of
+// floor(budget / l), i.e. at most 2 sqrt(budget) + 1, at most the number of distinct
+// lengths (len_range, if known, else 0) and at most the rank's positions.
+static int64_t runs_bound(int64_t budget, int64_t max_cnt, int64_t len_range) {
+    int64_t b = 2 * ((int64_t)std::sqrt((double)budget) + 1) + 1;
+    if (len_range > 0 && len_range < b) b = len_range;
+    if (max_cnt < b) b = max_cnt;
+    return b;
+}
 
 // Mark scan, group index of every position, global group starts, G_r.
 static int finish_groups(const Layout& L, void* ws, int W, int64_t n, const int64_t* d_off, int32_t* d_gidx,
@@ -557,12 +1042,7 @@ int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget,
     int32_t* incl = ws_at<int32_t>(ws, L.incl);
     DevStatus* st = ws_at<DevStatus>(ws, L.status);
     const unsigned grid = grid_for(n + 1, kBlock, (int64_t)num_cus() * kPlanBlocksPerCU);
-    // distinct steps per rank: at most the distinct values of floor(budget / l), i.e. at
-    // most 2 sqrt(budget) + 1, and at most the number of distinct lengths
-    int64_t runs_bound = 2 * ((int64_t)std::sqrt((double)budget) + 1) + 1;
-    if (len_range > 0 && len_range < runs_bound) runs_bound = len_range;
-    if (max_cnt < runs_bound) runs_bound = max_cnt;
-    if (runs_bound <= kRunCap && n < INT32_MAX) {
+    if (runs_bound(budget, max_cnt, len_range) <= kRunCap && n < INT32_MAX) {
         int32_t* run_start = j0;
         int32_t* run_b = j1;
         int32_t* run_c = ws_at<int32_t>(ws, L.gsize);
@@ -619,6 +1099,24 @@ extern "C" int odb_form_groups(const odb_window_t* w, int64_t budget, int32_t* d
     RankState* d_ranks = ws_at<RankState>(d_ws, L.ranks);
     DevStatus* st = ws_at<DevStatus>(d_ws, L.status);
     int32_t* len = ws_at<int32_t>(d_ws, L.len);
+    int64_t max_cnt = 0;
+    for (int r = 0; r < W; ++r) {
+        const int64_t c = w->rank_offsets[r + 1] - w->rank_offsets[r];
+        if (c > max_cnt) max_cnt = c;
+    }
+
+    // one block per rank: two launches, no synchronisation (invalid lengths are grouped as
+    // length 1 and reported by odb_align_groups)
+    if (max_cnt <= kRankBlockMax && runs_bound(budget, max_cnt, 0) <= kRankRunCap) {
+        hipLaunchKernelGGL(rank_sort_kernel, dim3(W), dim3(kRankThreads), 0, s, w->d_token_offsets, d_off, len,
+                           ws_at<int32_t>(d_ws, L.keys0), ws_at<int32_t>(d_ws, L.vals0), ws_at<int32_t>(d_ws, L.keys1),
+                           ws_at<int32_t>(d_ws, L.vals1), d_order, d_sorted_len, st);
+        ODB_LAUNCHED();
+        hipLaunchKernelGGL(rank_walk_kernel, dim3(W), dim3(kRankThreads), 0, s, d_off, (const int32_t*)d_sorted_len,
+                           budget, d_group_index, d_groups_per_rank, st);
+        ODB_LAUNCHED();
+        return ODB_OK;
+    }
     hipLaunchKernelGGL(rank_counts_kernel, dim3(grid_for(W, kBlock)), dim3(kBlock), 0, s, d_off, W, d_ranks);
     ODB_LAUNCHED();
 
@@ -689,12 +1187,10 @@ extern "C" int odb_form_groups(const odb_window_t* w, int64_t budget, int32_t* d
         }
     }
 
-    // (a3, a4) links, pointer jumping, group indices, G_r
-    int64_t max_cnt = 0;
-    for (int r = 0; r < W; ++r) {
-        const int64_t c = w->rank_offsets[r + 1] - w->rank_offsets[r];
-        if (c > max_cnt) max_cnt = c;
-    }
+    // (a3, a4) the group chain: the multi-kernel run walk or pointer jumping.  (A large
+    // rank's chain walked by one block per rank takes ~0.4 ms alone but tens of ms beside a
+    // running collate, which stalls the two-stream schedule; these grid-wide kernels
+    // share the GPU with it.)
     return group_sequences(L, d_ws, W, n, budget, d_off, max_cnt, n > 0 ? (int64_t)hs.max_len - hs.min_len + 1 : 0,
                            d_sorted_len, d_group_index, d_groups_per_rank, d_ranks, s);
 }

@@ -5,6 +5,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <vector>
 
 #include "odb.h"
 
@@ -59,6 +60,7 @@ struct DevStatus {
     int32_t err;
     int32_t collate_err;
     int64_t first_bad;            // smallest offending sample index (atomicMin)
+    int64_t first_bad_len;        // smallest sample with an invalid CSR length found by alignment
     uint32_t min_len;
     uint32_t max_len;
     int32_t jump_changed[kMaxJumpRounds];
@@ -87,6 +89,7 @@ struct RoundState {
     int64_t T;               // alignment target of the current round
     int64_t cut;             // steps of this round that are emitted
     int64_t emitted_total;   // cumulative emitted samples before this round
+    int64_t emitted_next;    // the same after this round (current once the round ends)
     int64_t step_max;        // largest global step count so far
     int64_t splits;          // all rounds
     int64_t overflow;        // all rounds
@@ -139,6 +142,18 @@ int check_workspace(const odb_window_t* w, void* d_ws, size_t ws_bytes, Layout* 
 int upload_small(const odb_window_t* w, const Layout& L, void* d_ws, const int64_t* cap,
                  hipStream_t s);
 
+// Host copy of the status word, round state, summary and per-rank state, read with one
+// device-to-host copy (the workspace keeps them next to each other) and one
+// synchronisation of the stream.
+struct HostState {
+    DevStatus st;
+    RoundState rs;
+    DevInfo info;
+    std::vector<RankState> ranks;
+    std::vector<char> buf;
+};
+int read_state(const Layout& L, void* ws, int W, HostState* h, hipStream_t s);
+
 int num_cus();
 
 inline unsigned grid_for(int64_t n, int per_block, int64_t cap = 1 << 20) {
@@ -179,6 +194,15 @@ __device__ __forceinline__ const int64_t* stage_ranks(const int64_t* off, int W,
     for (int i = threadIdx.x; i <= W; i += blockDim.x) s_off[i] = off[i];
     __syncthreads();
     return s_off;
+}
+
+// Workgroup barrier ordering LDS only: unlike __syncthreads() it does not wait for the
+// wave's outstanding global loads and stores, for loops whose barriers guard LDS tables
+// while their global stores are read by nobody in the block before a full barrier.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 template <typename T>
@@ -356,10 +380,52 @@ __global__ void __launch_bounds__(kBlock) scan_tiles(Load load, Store store, int
     }
 }
 
+// Scans of at most kSmallScan elements run as one launch of one block: 16 consecutive
+// elements per thread, one block scan of the thread sums.  The total goes to *total.
+constexpr int kSmallScanThreads = 1024;
+constexpr int kSmallScanItems = 16;
+constexpr int64_t kSmallScan = (int64_t)kSmallScanThreads * kSmallScanItems;
+
+template <typename Out, typename Load, typename Store>
+__global__ void __launch_bounds__(kSmallScanThreads) scan_small(Load load, Store store, int64_t n, Out* total) {
+    __shared__ Out wtot[kSmallScanThreads / kWave];
+    const int t = threadIdx.x, w = t / kWave;
+    const int64_t base = (int64_t)t * kSmallScanItems;
+    Out v[kSmallScanItems];
+    Out sum = 0;
+#pragma unroll
+    for (int j = 0; j < kSmallScanItems; ++j) {
+        v[j] = base + j < n ? load(base + j) : Out(0);
+        sum += v[j];
+    }
+    const Out inc = wave_incl_sum(sum);
+    if ((t & (kWave - 1)) == kWave - 1) wtot[w] = inc;
+    __syncthreads();
+    Out pre = 0, tot = 0;
+#pragma unroll
+    for (int k = 0; k < kSmallScanThreads / kWave; ++k) {
+        pre += k < w ? wtot[k] : Out(0);
+        tot += wtot[k];
+    }
+    Out run = pre + inc - sum;
+#pragma unroll
+    for (int j = 0; j < kSmallScanItems; ++j) {
+        if (base + j < n) store(base + j, run);
+        run += v[j];
+    }
+    if (t == 0) *total = tot;
+}
+
 template <typename Out, typename Load, typename Store>
 int device_excl_scan(Load load, Store store, int64_t n, Out* partials, hipStream_t s) {
     if (n <= 0) return ODB_OK;
     int64_t tiles = (n + kScanTile - 1) / kScanTile;
+    if (n <= kSmallScan) {
+        hipLaunchKernelGGL((scan_small<Out, Load, Store>), dim3(1), dim3(kSmallScanThreads), 0, s, load, store, n,
+                           partials + tiles);
+        ODB_LAUNCHED();
+        return ODB_OK;
+    }
     hipLaunchKernelGGL((scan_tile_sums<Out, Load>), dim3((unsigned)tiles), dim3(kBlock), 0, s,
                        load, n, partials);
     ODB_LAUNCHED();

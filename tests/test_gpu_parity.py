@@ -144,6 +144,41 @@ def test_workload_full_size(name):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("case", ["at_block_limit", "past_block_limit", "wide_lengths", "one_length_per_rank"])
+def test_grouping_paths(case):
+    # The two grouping paths (one block per rank up to 16,384 samples per rank, the
+    # multi-block sort and run walk beyond) at the limit; lengths up to 2^25 (all four
+    # byte digits of the one-block sort in use) with the collate left out (the token
+    # stream of such lengths would not fit); equal lengths within each rank (no digit varies)
+    import torch
+
+    rng = np.random.default_rng(61)
+    if case == "at_block_limit":
+        per = [rng.integers(1, 5000, 16384), rng.integers(1, 5000, 100), rng.integers(1, 5000, 16384)]
+        w = win(per, 20000)
+    elif case == "past_block_limit":
+        per = [rng.integers(1, 5000, 16385), rng.integers(1, 5000, 5)]
+        w = win(per, 20000)
+    elif case == "wide_lengths":
+        per = [np.concatenate([rng.integers(1, 1 << 25, 3000), rng.integers(1, 300, 1000)]) for _ in range(3)]
+        w = win(per, 1 << 21)
+    else:
+        per = [np.full(3000, 77), np.full(10, 5000), np.full(1, 1)]
+        w = win(per, 9000)
+    w.name = f"paths_{case}"
+    log(f"case {w.name}: W={w.W} n={w.n} budget={w.budget}")
+    ref = oracle.plan_window(w)
+    if case == "wide_lengths":
+        pipe, _ = run_gpu(w, tokens=torch.zeros(64, dtype=torch.int32, device="cuda"), collate=False)
+        compare_plan(w, pipe, ref)
+        compare_loss_weights(pipe, ref)
+    else:
+        pipe, outs = run_gpu(w)
+        compare_plan(w, pipe, ref)
+        compare_collate_full(w, outs, ref)
+        compare_loss_weights(pipe, ref)
+
+
 def _numpy_coverage(ids, n, identity=None, nid=0):
     cnt = np.bincount(ids, minlength=n)
     bad = int((cnt != 1).sum())

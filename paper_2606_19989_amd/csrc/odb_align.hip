@@ -1247,7 +1247,7 @@ extern "C" int odb_align_groups(const odb_window_t* w, int64_t budget, const odb
             break;
         }
         if (rounds > 0) {
-            ODB_TRY(group_sequences(L, d_ws, W, n, budget, d_off, max_cnt, 0, cur.len, wgidx, nullptr, d_ranks,
+            ODB_TRY(group_sequences(L, d_ws, W, n, budget, d_off, max_cnt, 0, false, cur.len, wgidx, nullptr, d_ranks,
                                     s));
             cur.gidx = wgidx;
         }

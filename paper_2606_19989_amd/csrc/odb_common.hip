@@ -79,6 +79,7 @@ bool make_layout(const odb_window_t* w, Layout* L) {
     L->cap = take(8 * W);
     L->gbase = take(8 * (W + 1));
     L->tile_first = take(8 * (W + 1));
+    L->rank_runs = take(4 * (W + 1));
     L->len = take(4 * n1);
     L->keys0 = take(4 * n1);
     L->keys1 = take(4 * n1);

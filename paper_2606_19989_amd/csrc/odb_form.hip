@@ -374,131 +374,236 @@ __global__ void __launch_bounds__(kBlock) jump_kernel(const int32_t* __restrict_
     if (__ballot(changed) && (threadIdx.x & (kWave - 1)) == 0) st->jump_changed[round] = 1;
 }
 
-// ---- run-based chain walk
+// ---- run-table chain walk
+// Positions q >= 1 of a rank (q < cnt_r) fall into runs of equal step: q starts a run when
+// q = 1 or its step B(l[q - 1]) differs from the step of q - 1.  The chain's group starts
+// are q = 0 and, in run k, the positions c_k, c_k + b_k, ... of the run, where b_k is the
+// run's step and c_k its first chain position (none if the chain jumps over the run).  The
+// group index of a position is the number of group starts at or before it, minus one.
+// Rank r's run table (run k: start, step, first chain position, group starts before the
+// run) sits at positions off[r] + k of four position-indexed arrays (a rank has fewer runs
+// than positions).  Work is split into the sort's tiles (at most kSortTile positions of
+// one rank).
 constexpr int kRunCap = 4096;   // runs per rank held in LDS by run_chase_kernel
 
-// Run-start flags: position q >= 1 of a rank starts a run when q = 1 or its step differs
-// from the previous position's.
-__global__ void __launch_bounds__(kBlock) run_flags_kernel(const int32_t* __restrict__ slen,
-                                                           const int64_t* __restrict__ off,
-                                                           const RankState* __restrict__ ranks, int W, int64_t n,
-                                                           int64_t budget, uint8_t* __restrict__ flags) {
-    __shared__ int64_t s_off[kLdsRanks + 1];
-    off = stage_ranks(off, W, s_off);
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
-        const int r = rank_of(off, W, p);
-        const int64_t q = p - off[r];
-        uint8_t f = 0;
-        if (q >= 1 && q < ranks[r].cnt)
-            f = q == 1 || batch_size(budget, slen[p - 1]) != batch_size(budget, slen[p - 2]);
-        flags[p] = f;
+// Whether rank-local position q (global p) starts a run.
+__device__ __forceinline__ bool run_start_at(const int32_t* __restrict__ slen, int64_t p, int64_t q, int64_t cnt,
+                                             int64_t budget) {
+    if (q < 1 || q >= cnt) return false;
+    return q == 1 || batch_size(budget, slen[p - 1]) != batch_size(budget, slen[p - 2]);
+}
+
+struct RunTile {
+    int r;
+    int64_t base;    // off[r]
+    int64_t start;   // first position of the tile
+    int32_t count;   // positions of the tile
+    int64_t cnt;     // live positions of the rank
+};
+
+__device__ __forceinline__ RunTile run_tile(const int64_t* __restrict__ off, const int64_t* __restrict__ tile_first,
+                                            int W, const RankState* __restrict__ ranks, int64_t b) {
+    RunTile t;
+    t.r = rank_of(tile_first, W, b);
+    t.base = off[t.r];
+    t.start = t.base + (b - tile_first[t.r]) * kSortTile;
+    const int64_t left = off[t.r + 1] - t.start;
+    t.count = (int32_t)(left < kSortTile ? left : kSortTile);
+    t.cnt = ranks[t.r].cnt;
+    return t;
+}
+
+// Run starts per tile.
+__global__ void __launch_bounds__(kBlock) run_count_kernel(const int64_t* __restrict__ off,
+                                                           const int64_t* __restrict__ tile_first, int W,
+                                                           const RankState* __restrict__ ranks,
+                                                           const int32_t* __restrict__ slen, int64_t budget,
+                                                           uint32_t* __restrict__ tile_runs) {
+    const RunTile t = run_tile(off, tile_first, W, ranks, blockIdx.x);
+    uint32_t c = 0;
+    for (int i = threadIdx.x; i < t.count; i += kBlock)
+        c += run_start_at(slen, t.start + i, t.start + i - t.base, t.cnt, budget);
+    c = block_sum(c);
+    if (threadIdx.x == 0) tile_runs[blockIdx.x] = c;
+}
+
+// One block per rank: the rank's tile counts become the index of each tile's first run
+// (in place), and rank_runs[r] the rank's number of runs.
+__global__ void __launch_bounds__(kBlock) run_tile_scan_kernel(const int64_t* __restrict__ tile_first,
+                                                               uint32_t* __restrict__ tile_runs,
+                                                               uint32_t* __restrict__ rank_runs) {
+    const int r = blockIdx.x;
+    const int64_t t0 = tile_first[r], t1 = tile_first[r + 1];
+    uint32_t carry = 0;
+    for (int64_t b = t0; b < t1; b += kBlock) {
+        const int64_t t = b + threadIdx.x;
+        const uint32_t v = t < t1 ? tile_runs[t] : 0u;
+        uint32_t tot;
+        const uint32_t ex = block_excl_sum(v, &tot);
+        if (t < t1) tile_runs[t] = carry + ex;
+        carry += tot;
+    }
+    if (threadIdx.x == 0) rank_runs[r] = carry;
+}
+
+// The run table's starts and steps, written by the tile holding each run start.  A tile's
+// positions are taken in rounds of kBlock consecutive positions, so a block scan of the
+// round's flags numbers its run starts in position order.
+__global__ void __launch_bounds__(kBlock) run_write_kernel(const int64_t* __restrict__ off,
+                                                           const int64_t* __restrict__ tile_first, int W,
+                                                           const RankState* __restrict__ ranks,
+                                                           const int32_t* __restrict__ slen, int64_t budget,
+                                                           const uint32_t* __restrict__ tile_runs,
+                                                           int32_t* __restrict__ run_start,
+                                                           int32_t* __restrict__ run_b) {
+    const RunTile t = run_tile(off, tile_first, W, ranks, blockIdx.x);
+    uint32_t k0 = tile_runs[blockIdx.x];
+    for (int i0 = 0; i0 < t.count; i0 += kBlock) {
+        const int i = i0 + threadIdx.x;
+        const int64_t p = t.start + i;
+        const bool f = i < t.count && run_start_at(slen, p, p - t.base, t.cnt, budget);
+        uint32_t tot;
+        const uint32_t ex = block_excl_sum((uint32_t)f, &tot);
+        if (f) {
+            const int64_t k = t.base + k0 + ex;
+            const int64_t b = batch_size(budget, slen[p - 1]);
+            run_start[k] = (int32_t)(p - t.base);
+            run_b[k] = (int32_t)(b < INT32_MAX ? b : INT32_MAX);   // any step >= 2^31 leaves the rank
+        }
+        k0 += tot;
     }
 }
 
-// Scan store of the run-start flags: the inclusive count of every position (its run id
-// + 1) and, at each run start, the run table entry: run k (global numbering, rank by
-// rank) starts at rank-local position run_start[k] with step run_b[k].
-struct RunStore {
-    const uint8_t* flags;
-    const int32_t* slen;
-    const int64_t* off;
-    int W;
-    int64_t budget;
-    int32_t* incl;
-    int32_t* run_start;
-    int32_t* run_b;
-    __device__ void operator()(int64_t p, uint32_t ex) const {
-        const uint32_t f = flags[p];
-        incl[p] = (int32_t)(ex + f);
-        if (!f) return;
-        const int r = rank_of(off, W, p);
-        run_start[ex] = (int32_t)(p - off[r]);
-        const int64_t b = batch_size(budget, slen[p - 1]);
-        run_b[ex] = (int32_t)(b < INT32_MAX ? b : INT32_MAX);   // any step >= 2^31 leaves the rank
-    }
-};
-
-// One block per rank: thread 0 walks the chain run by run and records the first chain
-// position of every run (INT32_MAX if the chain skips the run).  Positions and steps stay
-// below 2^31 (larger steps are stored as INT32_MAX), so the walk runs in 32-bit integers;
-// the table and its results sit in LDS when they fit.
-__global__ void __launch_bounds__(kBlock) run_chase_kernel(const int32_t* __restrict__ incl,
-                                                           const int64_t* __restrict__ off,
-                                                           const RankState* __restrict__ ranks,
+// One block per rank: thread 0 walks the chain run by run and records for every run the
+// first chain position (INT32_MAX if the chain skips the run) and the group starts before
+// the run; G_r is the rank's number of group starts.  Positions and steps stay below 2^31
+// (larger steps are stored as INT32_MAX), so the walk runs in 32-bit integers; the table
+// and its results sit in LDS when they fit.
+__global__ void __launch_bounds__(kBlock) run_chase_kernel(const int64_t* __restrict__ off, RankState* ranks,
+                                                           const uint32_t* __restrict__ rank_runs,
                                                            const int32_t* __restrict__ run_start,
                                                            const int32_t* __restrict__ run_b,
-                                                           int32_t* __restrict__ run_c) {
-    __shared__ uint32_t ls[kRunCap + 1], lb[kRunCap], lc[kRunCap];
+                                                           int32_t* __restrict__ run_c, int32_t* __restrict__ run_g) {
+    __shared__ uint32_t ls[kRunCap + 1], lb[kRunCap], lc[kRunCap], lg[kRunCap];
     const int r = blockIdx.x;
     const int64_t base = off[r];
     const int64_t c = ranks[r].cnt;
-    if (c < 2) return;   // no position >= 1, no run
-    const int64_t rb = base > 0 ? incl[base - 1] : 0;
-    const int64_t R = incl[base + c - 1] - rb;
+    if (c < 2) {   // no position >= 1, no run: position 0 (if any) is the only group start
+        if (threadIdx.x == 0) ranks[r].G = c;
+        return;
+    }
+    const int64_t R = rank_runs[r];
     if (R <= kRunCap) {
         for (int64_t i = threadIdx.x; i < R; i += blockDim.x) {
-            ls[i] = (uint32_t)run_start[rb + i];
-            lb[i] = (uint32_t)run_b[rb + i];
+            ls[i] = (uint32_t)run_start[base + i];
+            lb[i] = (uint32_t)run_b[base + i];
         }
         __syncthreads();
         if (threadIdx.x == 0) {
             ls[R] = (uint32_t)c;
-            uint32_t cur = 1;   // next(0) = 1: the second group starts at position 1
+            uint32_t cur = 1;     // next(0) = 1: the second group starts at position 1
+            uint32_t marks = 1;   // position 0
 #pragma unroll 4
             for (int i = 0; i < (int)R; ++i) {
                 const uint32_t e = ls[i + 1], b = lb[i];
                 const bool hit = cur < e;
                 lc[i] = hit ? cur : (uint32_t)INT32_MAX;
+                lg[i] = marks;
                 // chain positions cur, cur + b, ... below e; the next one is >= e
                 const uint32_t k = hit ? (e - cur + b - 1) / b : 0u;
                 cur += k * b;
+                marks += k;
             }
+            ranks[r].G = marks;
         }
         __syncthreads();
-        for (int64_t i = threadIdx.x; i < R; i += blockDim.x) run_c[rb + i] = (int32_t)lc[i];
+        for (int64_t i = threadIdx.x; i < R; i += blockDim.x) {
+            run_c[base + i] = (int32_t)lc[i];
+            run_g[base + i] = (int32_t)lg[i];
+        }
         return;
     }
     if (threadIdx.x != 0) return;
-    uint32_t cur = 1;
+    uint32_t cur = 1, marks = 1;
     for (int64_t i = 0; i < R; ++i) {
-        const uint32_t e = (uint32_t)(i + 1 < R ? run_start[rb + i + 1] : c);
-        const uint32_t b = (uint32_t)run_b[rb + i];
+        const uint32_t e = (uint32_t)(i + 1 < R ? run_start[base + i + 1] : c);
+        const uint32_t b = (uint32_t)run_b[base + i];
         const bool hit = cur < e;
-        run_c[rb + i] = hit ? (int32_t)cur : INT32_MAX;
+        run_c[base + i] = hit ? (int32_t)cur : INT32_MAX;
+        run_g[base + i] = (int32_t)marks;
         const uint32_t k = hit ? (e - cur + b - 1) / b : 0u;
         cur += k * b;
+        marks += k;
     }
+    ranks[r].G = marks;
 }
 
-// Group-start marks from the run table: q = 0, and q >= 1 at its run's first chain
-// position plus a multiple of the run's step.
-__global__ void __launch_bounds__(kBlock) run_marks_kernel(const int32_t* __restrict__ incl,
-                                                           const int64_t* __restrict__ off,
-                                                           const RankState* __restrict__ ranks, int W, int64_t n,
-                                                           const int32_t* __restrict__ run_b,
-                                                           const int32_t* __restrict__ run_c,
-                                                           uint8_t* __restrict__ marks) {
-    __shared__ int64_t s_off[kLdsRanks + 1];
-    off = stage_ranks(off, W, s_off);
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p <= n; p += stride) {
-        if (p == n) {
-            marks[n] = 0;
-            continue;
+// One block: every rank's first global group id (exclusive sum of G_r), the group count
+// per rank for the caller, and the total in gbase[W].
+__global__ void __launch_bounds__(kBlock) rank_groups_kernel(RankState* ranks, int W, int64_t* __restrict__ gbase,
+                                                             int32_t* __restrict__ groups_out) {
+    int64_t carry = 0;
+    for (int b = 0; b < W; b += kBlock) {
+        const int r = b + threadIdx.x;
+        const int64_t G = r < W ? ranks[r].G : 0;
+        int64_t tot;
+        const int64_t ex = block_excl_sum(G, &tot);
+        if (r < W) {
+            ranks[r].gbase = carry + ex;
+            gbase[r] = carry + ex;
+            if (groups_out) groups_out[r] = (int32_t)G;
         }
-        const int r = rank_of(off, W, p);
-        const int64_t q = p - off[r];
-        uint8_t m = 0;
-        if (q == 0) {
-            m = ranks[r].cnt > 0;
-        } else if (q < ranks[r].cnt) {
-            const int64_t k = incl[p] - 1;
-            const int64_t c0 = run_c[k];
-            const uint32_t b = (uint32_t)run_b[k];
-            m = q >= c0 && (uint32_t)(q - c0) % b == 0;
+        carry += tot;
+    }
+    if (threadIdx.x == 0) gbase[W] = carry;
+}
+
+// Group index of every live position and the global position of every group start, from
+// the run table: position q of run k is in the group that starts at the last chain
+// position of the run at or before q, or, before c_k, in the last group started before
+// the run.
+__global__ void __launch_bounds__(kBlock) run_gidx_kernel(const int64_t* __restrict__ off,
+                                                          const int64_t* __restrict__ tile_first, int W,
+                                                          const RankState* __restrict__ ranks,
+                                                          const int32_t* __restrict__ slen, int64_t budget,
+                                                          const uint32_t* __restrict__ tile_runs,
+                                                          const int32_t* __restrict__ run_b,
+                                                          const int32_t* __restrict__ run_c,
+                                                          const int32_t* __restrict__ run_g,
+                                                          int32_t* __restrict__ gidx, int32_t* __restrict__ gstart) {
+    const RunTile t = run_tile(off, tile_first, W, ranks, blockIdx.x);
+    const int64_t gb = ranks[t.r].gbase;
+    // run starts before the current position in this rank, the current position included
+    uint32_t k0 = tile_runs[blockIdx.x];
+    for (int i0 = 0; i0 < t.count; i0 += kBlock) {
+        const int i = i0 + threadIdx.x;
+        const int64_t p = t.start + i;
+        const int64_t q = p - t.base;
+        const bool live = i < t.count && q < t.cnt;
+        const bool f = live && run_start_at(slen, p, q, t.cnt, budget);
+        uint32_t tot;
+        const uint32_t ex = block_excl_sum((uint32_t)f, &tot);
+        if (live) {
+            int64_t g = 0;
+            bool mark = true;
+            if (q > 0) {
+                const int64_t k = t.base + k0 + ex + (f ? 1 : 0) - 1;   // q's run
+                const uint32_t c = (uint32_t)run_c[k], b = (uint32_t)run_b[k];
+                const int64_t G = run_g[k];
+                if ((uint32_t)q >= c) {
+                    const uint32_t d = (uint32_t)q - c;
+                    const uint32_t m = d / b;
+                    g = G + m;
+                    mark = d - m * b == 0;
+                } else {
+                    g = G - 1;
+                    mark = false;
+                }
+            }
+            gidx[p] = (int32_t)g;
+            if (mark) gstart[gb + g] = (int32_t)p;
         }
-        marks[p] = m;
+        k0 += tot;
     }
 }
 
@@ -1029,7 +1134,7 @@ static int finish_groups(const Layout& L, void* ws, int W, int64_t n, const int6
 }
 
 int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget, const int64_t* d_off,
-                    int64_t max_cnt, int64_t len_range, const int32_t* d_slen, int32_t* d_gidx,
+                    int64_t max_cnt, int64_t len_range, bool tiles_ready, const int32_t* d_slen, int32_t* d_gidx,
                     int32_t* d_groups_out, RankState* d_ranks, hipStream_t s) {
     int32_t* j0 = ws_at<int32_t>(ws, L.jmp0);
     int32_t* j1 = ws_at<int32_t>(ws, L.jmp1);
@@ -1038,22 +1143,46 @@ int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget,
     DevStatus* st = ws_at<DevStatus>(ws, L.status);
     const unsigned grid = grid_for(n + 1, kBlock, (int64_t)num_cus() * kPlanBlocksPerCU);
     if (runs_bound(budget, max_cnt, len_range) <= kRunCap && n < INT32_MAX) {
+        // run-table walk over the sort's tiles
+        int64_t* d_tile_first = ws_at<int64_t>(ws, L.tile_first);
+        if (!tiles_ready) {
+            hipLaunchKernelGGL(sort_tiles_kernel, dim3(1), dim3(kBlock), 0, s, d_off, W, d_tile_first);
+            ODB_LAUNCHED();
+        }
+        const unsigned tiles = (unsigned)L.num_sort_blocks;
+        uint32_t* tile_runs = ws_at<uint32_t>(ws, L.counts);
+        uint32_t* rank_runs = ws_at<uint32_t>(ws, L.rank_runs);
         int32_t* run_start = j0;
         int32_t* run_b = j1;
         int32_t* run_c = ws_at<int32_t>(ws, L.gsize);
-        hipLaunchKernelGGL(run_flags_kernel, dim3(grid), dim3(kBlock), 0, s, d_slen, d_off, (const RankState*)d_ranks,
-                           W, n, budget, marks);
+        int32_t* run_g = incl;
+        const RankState* cr = d_ranks;
+        if (tiles > 0) {
+            hipLaunchKernelGGL(run_count_kernel, dim3(tiles), dim3(kBlock), 0, s, d_off, (const int64_t*)d_tile_first,
+                               W, cr, d_slen, budget, tile_runs);
+            ODB_LAUNCHED();
+        }
+        hipLaunchKernelGGL(run_tile_scan_kernel, dim3(W), dim3(kBlock), 0, s, (const int64_t*)d_tile_first, tile_runs,
+                           rank_runs);
         ODB_LAUNCHED();
-        ODB_TRY((device_excl_scan<uint32_t>(MarkLoad{marks},
-                                            RunStore{marks, d_slen, d_off, W, budget, incl, run_start, run_b}, n,
-                                            ws_at<uint32_t>(ws, L.partials), s)));
-        hipLaunchKernelGGL(run_chase_kernel, dim3(W), dim3(kBlock), 0, s, (const int32_t*)incl, d_off,
-                           (const RankState*)d_ranks, (const int32_t*)run_start, (const int32_t*)run_b, run_c);
+        if (tiles > 0) {
+            hipLaunchKernelGGL(run_write_kernel, dim3(tiles), dim3(kBlock), 0, s, d_off, (const int64_t*)d_tile_first,
+                               W, cr, d_slen, budget, (const uint32_t*)tile_runs, run_start, run_b);
+            ODB_LAUNCHED();
+        }
+        hipLaunchKernelGGL(run_chase_kernel, dim3(W), dim3(kBlock), 0, s, d_off, d_ranks, (const uint32_t*)rank_runs,
+                           (const int32_t*)run_start, (const int32_t*)run_b, run_c, run_g);
         ODB_LAUNCHED();
-        hipLaunchKernelGGL(run_marks_kernel, dim3(grid), dim3(kBlock), 0, s, (const int32_t*)incl, d_off,
-                           (const RankState*)d_ranks, W, n, (const int32_t*)run_b, (const int32_t*)run_c, marks);
+        hipLaunchKernelGGL(rank_groups_kernel, dim3(1), dim3(kBlock), 0, s, d_ranks, W, ws_at<int64_t>(ws, L.gbase),
+                           d_groups_out);
         ODB_LAUNCHED();
-        return finish_groups(L, ws, W, n, d_off, d_gidx, d_groups_out, d_ranks, s);
+        if (tiles > 0) {
+            hipLaunchKernelGGL(run_gidx_kernel, dim3(tiles), dim3(kBlock), 0, s, d_off, (const int64_t*)d_tile_first,
+                               W, cr, d_slen, budget, (const uint32_t*)tile_runs, (const int32_t*)run_b,
+                               (const int32_t*)run_c, (const int32_t*)run_g, d_gidx, ws_at<int32_t>(ws, L.gstart));
+            ODB_LAUNCHED();
+        }
+        return ODB_OK;
     }
     hipLaunchKernelGGL(links_kernel, dim3(grid), dim3(kBlock), 0, s, d_slen, d_off,
                        (const RankState*)d_ranks, W, n, budget, j0, marks);
@@ -1187,5 +1316,5 @@ extern "C" int odb_form_groups(const odb_window_t* w, int64_t budget, int32_t* d
     // running collate, which stalls the two-stream schedule; these grid-wide kernels
     // share the GPU with it.)
     return group_sequences(L, d_ws, W, n, budget, d_off, max_cnt, n > 0 ? (int64_t)hs.max_len - hs.min_len + 1 : 0,
-                           d_sorted_len, d_group_index, d_groups_per_rank, d_ranks, s);
+                           passes > 0, d_sorted_len, d_group_index, d_groups_per_rank, d_ranks, s);
 }

@@ -115,7 +115,7 @@ struct DevInfo {
 
 // ------------------------------------------------------------------ workspace layout
 struct Layout {
-    size_t status, round, ranks, rank_off, cap, gbase, tile_first;
+    size_t status, round, ranks, rank_off, cap, gbase, tile_first, rank_runs;
     size_t len, keys0, keys1, vals0, vals1, counts, partials;
     size_t jmp0, jmp1, marks, incl;
     size_t gstart, gsize, gmax, sadj, cs, ov_slot, ov_lo, kept;
@@ -439,15 +439,17 @@ int device_excl_scan(Load load, Store store, int64_t n, Out* partials, hipStream
 
 // ------------------------------------------------------------------ cross-file launchers
 // Grouping of the per-rank sequences held in `slen` (positions [off[r], off[r] + cnt_r)
-// of every rank r, cnt_r = d_ranks[r].cnt): marks the group starts with pointer jumping
-// over the next-group-start links, then writes the formation group index of every
-// position (d_gidx), the global position of every group start (workspace gstart, group
-// ids numbered rank by rank), G_r and the first group id of every rank (d_ranks[r].G,
-// .gbase and workspace gbase[W+1]), and optionally G_r to d_groups_out.
+// of every rank r, cnt_r = d_ranks[r].cnt): finds the group starts (a walk over the runs of
+// equal step, or pointer jumping over the next-group-start links when a rank may hold
+// too many runs), then writes the formation group index of every position (d_gidx), the
+// global position of every group start (workspace gstart, group ids numbered rank by
+// rank), G_r and the first group id of every rank (d_ranks[r].G, .gbase and workspace
+// gbase[W+1]), and optionally G_r to d_groups_out.
 // len_range = max_len - min_len + 1 of the sequences if known (0 otherwise); it only
-// selects between two equivalent ways of finding the chain (see odb_form.hip).
+// selects between the two equivalent ways of finding the chain (see odb_form.hip).
+// tiles_ready: workspace tile_first already holds the sort tiles of d_rank_off.
 int group_sequences(const Layout& L, void* ws, int W, int64_t n, int64_t budget,
-                    const int64_t* d_rank_off, int64_t max_cnt, int64_t len_range,
+                    const int64_t* d_rank_off, int64_t max_cnt, int64_t len_range, bool tiles_ready,
                     const int32_t* d_slen, int32_t* d_gidx, int32_t* d_groups_out,
                     RankState* d_ranks, hipStream_t s);
 

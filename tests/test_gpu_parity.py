@@ -144,12 +144,16 @@ def test_workload_full_size(name):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("case", ["at_block_limit", "past_block_limit", "wide_lengths", "one_length_per_rank"])
+@pytest.mark.parametrize("case", ["at_block_limit", "past_block_limit", "wide_lengths", "one_length_per_rank",
+                                  "long_rank", "tile_edges"])
 def test_grouping_paths(case):
     # The two grouping paths (one block per rank up to 16,384 samples per rank, the
-    # multi-block sort and run walk beyond) at the limit; lengths up to 2^25 (all four
-    # byte digits of the one-block sort in use) with the collate left out (the token
-    # stream of such lengths would not fit); equal lengths within each rank (no digit varies)
+    # multi-block sort and run-table walk beyond) at the limit; lengths up to 2^25 (all
+    # four byte digits of the one-block sort in use) with the collate left out (the token
+    # stream of such lengths would not fit); equal lengths within each rank (no digit
+    # varies); a rank of 700,000 samples (342 sort tiles: the per-rank scan of the tiles'
+    # run counts takes two passes of its block) beside one of 3; ranks one position past,
+    # at and one short of a tile edge, with empty and one-sample ranks
     import torch
 
     rng = np.random.default_rng(61)
@@ -162,13 +166,21 @@ def test_grouping_paths(case):
     elif case == "wide_lengths":
         per = [np.concatenate([rng.integers(1, 1 << 25, 3000), rng.integers(1, 300, 1000)]) for _ in range(3)]
         w = win(per, 1 << 21)
+    elif case == "long_rank":
+        per = [rng.integers(1, 3000, 700000), rng.integers(1, 3000, 3)]
+        w = win(per, 20000)
+    elif case == "tile_edges":
+        per = [rng.integers(1, 5000, 10 * 2048 + 1), rng.integers(1, 5000, 10 * 2048),
+               np.zeros(0, np.int64), rng.integers(1, 5000, 10 * 2048 - 1), rng.integers(1, 5000, 1),
+               rng.integers(1, 5000, 2)]
+        w = win(per, 20000)
     else:
         per = [np.full(3000, 77), np.full(10, 5000), np.full(1, 1)]
         w = win(per, 9000)
     w.name = f"paths_{case}"
     log(f"case {w.name}: W={w.W} n={w.n} budget={w.budget}")
     ref = oracle.plan_window(w)
-    if case == "wide_lengths":
+    if case in ("wide_lengths", "long_rank"):
         pipe, _ = run_gpu(w, tokens=torch.zeros(64, dtype=torch.int32, device="cuda"), collate=False)
         compare_plan(w, pipe, ref)
         compare_loss_weights(pipe, ref)

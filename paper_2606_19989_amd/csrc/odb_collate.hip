@@ -52,14 +52,16 @@ constexpr int kGroups = 1;                                           // groups p
 constexpr int64_t kGroupSpan = (int64_t)kWave * kVec;                // 256
 constexpr int64_t kWaveStep = kGroupSpan * kGroups;                  // 256
 constexpr int64_t kBlockStep = kWaveStep * (kCollateBlock / kWave);  // 1024
-// Consecutive steps per run, a block's unit of work: 64 on large outputs (measured best with
-// runs taken from a counter: 32 repositions too often, 128 and 256 leave a longer tail),
-// shorter when the output gives a block fewer than kRunsPerBlock runs of 64 (down to
-// kMinRunSteps), so the blocks' finishing times stay within a small fraction of the kernel.
-constexpr int64_t kRunSteps = 64;       // 2^6
-constexpr int64_t kMinRunSteps = 16;    // 2^4
-constexpr int64_t kRunsPerBlock = 32;
-static_assert(kRunSteps == 64 && kMinRunSteps == 16, "the run length is 2^4 .. 2^6 steps");
+// Consecutive steps per run, a block's unit of work: the longest of 8, 16, 32 and 64 steps
+// that still gives every block kRunsPerBlock runs.  Measured per run length (8/16/32/64
+// steps, ms per call): 64 x 262,144 samples 26.88/26.74/26.68/26.64; 8 x 262,144 multimodal
+// 15.72/15.71/15.72/15.75; 16 x 65,536 bimodal 3.91/4.00/4.05/4.09; 8 x 65,536 text
+// 1.42/1.45/1.47/1.51; 2 x 2,048 0.024/0.033/0.052/0.090.  Long runs reposition less often;
+// on smaller outputs short runs keep the blocks' finishing times close.
+constexpr int64_t kRunSteps = 64;      // 2^6
+constexpr int64_t kMinRunSteps = 8;    // 2^3
+constexpr int64_t kRunsPerBlock = 128;
+static_assert(kRunSteps == 64 && kMinRunSteps == 8, "the run length is 2^3 .. 2^6 steps");
 // Three resident blocks (12 waves) per compute unit stream fastest (two, four, five or
 // six were slower), and they leave five of the eight wave slots and about half the
 // registers of every SIMD to kernels on other streams: the grouping and alignment of the next window can run
@@ -449,7 +451,7 @@ __global__ void __launch_bounds__(kCollateBlock) collate_kernel(Plan p, int32_t 
     const int64_t nsteps = (total + kBlockStep - 1) / kBlockStep;
     // runs of 2^run_shift steps: the largest power of two from kMinRunSteps to kRunSteps that
     // still gives every block kRunsPerBlock runs
-    int run_shift = 4;
+    int run_shift = 3;
     while (run_shift < 6 && ((int64_t)gridDim.x * kRunsPerBlock << (run_shift + 1)) <= nsteps) ++run_shift;
     const int64_t nruns = (nsteps + (1ll << run_shift) - 1) >> run_shift;
     if ((int64_t)blockIdx.x >= nruns) return;

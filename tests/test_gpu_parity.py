@@ -107,6 +107,47 @@ def test_random_small_windows():
         check_full(w, pad_id=int(rng.integers(0, 5)))
 
 
+def test_random_medium_windows():
+    # windows past the one-block-per-rank limit (ranks of up to 60,000 samples) in random
+    # shapes: 1-24 ranks of unequal sizes, uniform, lognormal and bimodal lengths, budgets
+    # from below the longest sample to 2^23 (where a wide length range sends group
+    # discovery to pointer jumping), join and non-join modes, per-rank slot capacities
+    import torch
+
+    rng = np.random.default_rng(2025)
+    for t in range(14):
+        W = int(rng.integers(1, 25))
+        big = int(rng.integers(0, W))
+        kind = t % 3
+        per = []
+        for r in range(W):
+            m = int(rng.integers(16385, 60000)) if r == big else int(rng.integers(0, 9000))
+            if kind == 0:
+                x = rng.integers(1, int(rng.integers(2, 3000)), size=m)
+            elif kind == 1:
+                x = np.clip(np.rint(synth.lognormal(rng, 200, 1.5, m)), 1, 8000).astype(np.int64)
+            else:
+                x = np.where(rng.random(m) < 0.9, rng.integers(8, 300, size=m), rng.integers(2000, 8000, size=m))
+            per.append(x)
+        jump = t % 5 == 4
+        if jump:   # lengths 1 and 8000 in the window: more distinct steps than the run table holds
+            per[big] = np.concatenate([per[big], [1, 8000]])
+        n = sum(len(x) for x in per)
+        budget = 1 << 23 if jump else int(rng.integers(2000, 300000))
+        mode = "nonjoin" if t % 4 == 3 else "join"
+        cap = rng.integers(0, 40, size=W) if t % 6 == 1 else None
+        w = win(per, budget, mode=mode, quota=int(rng.integers(1, n + 2)), capacity=cap)
+        w.name = f"random_medium_{t}"
+        if jump:
+            log(f"case {w.name}: W={w.W} n={w.n} budget={w.budget} mode={w.mode} (plan only)")
+            ref = oracle.plan_window(w)
+            pipe, _ = run_gpu(w, tokens=torch.zeros(64, dtype=torch.int32, device="cuda"), collate=False)
+            compare_plan(w, pipe, ref)
+            compare_loss_weights(pipe, ref)
+        else:
+            check_full(w, pad_id=int(rng.integers(0, 5)))
+
+
 def test_sampler_padding_identity_coverage():
     # identity-coverage audit arithmetic: N = 57,284 over 8 ranks leaves P = 4 padding views
     views, q, P = synth.sampler_views(57284, 8, seed=3)

@@ -186,7 +186,7 @@ def test_workload_full_size(name):
 
 
 @pytest.mark.parametrize("case", ["at_block_limit", "past_block_limit", "wide_lengths", "one_length_per_rank",
-                                  "long_rank", "tile_edges"])
+                                  "long_rank", "tile_edges", "many_ranks", "many_ranks_jump"])
 def test_grouping_paths(case):
     # The two grouping paths (one block per rank up to 16,384 samples per rank, the
     # multi-block sort and run-table walk beyond) at the limit; lengths up to 2^25 (all
@@ -194,7 +194,9 @@ def test_grouping_paths(case):
     # stream of such lengths would not fit); equal lengths within each rank (no digit
     # varies); a rank of 700,000 samples (342 sort tiles: the per-rank scan of the tiles'
     # run counts takes two passes of its block) beside one of 3; ranks one position past,
-    # at and one short of a tile edge, with empty and one-sample ranks
+    # at and one short of a tile edge, with empty and one-sample ranks; 1,100 ranks (more
+    # than the rank table kernels stage in LDS) with one past the one-block limit, grouped
+    # by the run-table walk and, at budget 2^23 with lengths 1..8000, by pointer jumping
     import torch
 
     rng = np.random.default_rng(61)
@@ -215,13 +217,18 @@ def test_grouping_paths(case):
                np.zeros(0, np.int64), rng.integers(1, 5000, 10 * 2048 - 1), rng.integers(1, 5000, 1),
                rng.integers(1, 5000, 2)]
         w = win(per, 20000)
+    elif case in ("many_ranks", "many_ranks_jump"):
+        per = [rng.integers(1, 3000, 20000)] + [rng.integers(1, 3000, int(rng.integers(0, 21))) for _ in range(1099)]
+        if case == "many_ranks_jump":
+            per[0] = np.concatenate([per[0], [1, 8000]])
+        w = win(per, (1 << 23) if case == "many_ranks_jump" else 20000)
     else:
         per = [np.full(3000, 77), np.full(10, 5000), np.full(1, 1)]
         w = win(per, 9000)
     w.name = f"paths_{case}"
     log(f"case {w.name}: W={w.W} n={w.n} budget={w.budget}")
     ref = oracle.plan_window(w)
-    if case in ("wide_lengths", "long_rank"):
+    if case in ("wide_lengths", "long_rank", "many_ranks_jump"):
         pipe, _ = run_gpu(w, tokens=torch.zeros(64, dtype=torch.int32, device="cuda"), collate=False)
         compare_plan(w, pipe, ref)
         compare_loss_weights(pipe, ref)

@@ -502,7 +502,7 @@ def main():
         },
     }
     if not args.no_cpu_baseline:
-        log(f"[bench] CPU oracle on groups of ranks for >= {args.cpu_seconds:.0f} s ...")
+        log(f"[bench] CPU oracle: plan of the whole window, then its collate rank by rank for >= {args.cpu_seconds:.0f} s ...")
         result["cpu_baseline"] = cpu_baseline(w, tokens, min_seconds=args.cpu_seconds)
         log("[bench] CPU oracle done")
     print(json.dumps(result), flush=True)

@@ -10,7 +10,9 @@ schedule (one stream, plan then collate) is timed too.  Prints one JSON line:
 
   value        emitted samples per second (whole job)
   roofline     the collate stage (dominant): algorithmic bytes per odb_collate call /
-               its average duration from HIP events on the launch stream, vs 8 TB/s;
+               its average duration from HIP events on the launch stream, vs 8 TB/s, in
+               the two-stream schedule (frac) and in the serial one, where nothing runs
+               beside it (alone_frac);
                traffic = HBM bytes per call from the committed rocprofv3 counters
                (profiles/), reported only while the collate source is unchanged;
                copy_ceiling_gbs = a plain 4 GiB device copy, as a practical ceiling;
@@ -90,18 +92,25 @@ def pipelined_steps(pipes, plan_stream, collate_stream, steps, plan=window_plan,
 
 
 def serial_steps(pipe, stream, steps):
-    """`steps` window steps on one stream, each planned and then collated."""
+    """`steps` window steps on one stream, each planned and then collated.  Returns the host
+    seconds of the loop and per step the HIP-event milliseconds of odb_collate, which here
+    runs with nothing beside it."""
     import torch
 
+    marks = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
         pipe.form(stream)
         pipe.align(stream)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record(stream)
         pipe.collate(stream)
+        ev[1].record(stream)
         pipe.loss_weights(stream=stream)
+        marks.append(ev)
     torch.cuda.synchronize()
-    return time.perf_counter() - t0
+    return time.perf_counter() - t0, [e[0].elapsed_time(e[1]) for e in marks]
 
 
 def measured_traffic(workload):
@@ -423,8 +432,11 @@ def main():
     collate_ms = float(np.mean(collate_all))
     weights_ms = float(np.mean(weights_all))
     serial_n = min(max(3, args.steps // 2), 20)
-    serial_sec_per_step = serial_steps(pipe, plan_stream, serial_n) / serial_n
-    log(f"[bench] serial schedule: {serial_sec_per_step * 1e3:.2f} ms/step")
+    serial_sec, collate_alone = serial_steps(pipe, plan_stream, serial_n)
+    serial_sec_per_step = serial_sec / serial_n
+    collate_alone_ms = float(np.mean(collate_alone))
+    log(f"[bench] serial schedule: {serial_sec_per_step * 1e3:.2f} ms/step, odb_collate alone "
+        f"{collate_alone_ms:.3f} ms (beside the next plan {collate_ms:.3f} ms)")
 
     sketch = length_sketch_timing(odb, win, pipe.ws, w, dev)
     log(f"[bench] length sketch: cv={sketch['cv']:.3f} f_s={sketch['short_fraction']:.3f} "
@@ -497,6 +509,8 @@ def main():
             "alg_bytes_per_launch": alg,
             "avg_launch_ms": collate_ms,
             "median_launch_ms": float(np.median(collate_all)),
+            "alone_avg_launch_ms": collate_alone_ms,
+            "alone_frac": alg / (collate_alone_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "copy_ceiling_gbs": copy_gbs,
             "mix_copy_gbs": mix_gbs,
         },

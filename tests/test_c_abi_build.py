@@ -1,0 +1,22 @@
+"""include/odb.h as plain C (no GPU): the C driver of the window pipeline compiles as
+strict C11 with warnings as errors, links against libodb.so and the HIP runtime, and
+starts (its shared libraries resolve) with a usage error when given no arguments."""
+import importlib.util
+import os
+import subprocess
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def _builder():
+    spec = importlib.util.spec_from_file_location("odb_c_abi_build", os.path.join(HERE, "c_abi", "build_program.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_c_driver_compiles_links_and_starts(tmp_path):
+    exe = _builder().build(str(tmp_path / "window_pipeline"))
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 2, (r.returncode, r.stderr)
+    assert "usage:" in r.stderr

@@ -66,7 +66,6 @@ struct StreamGlobal {
     int32_t done;
     int32_t stop;
     int32_t err;
-    int32_t cap_overflow;
 };
 
 // A rank's committed state, written by the emit phase of every round that runs.
@@ -570,7 +569,10 @@ __device__ int64_t emit_rank(const StreamArgs& a, int64_t k, int64_t base, const
     const int64_t E = cum[T];
     const double mean = (double)tok / (double)n;
     int64_t* stepsum = a.stepsum + (k % 3) * a.D;
-    // slot records: step j of the round is adjusted group T-1-j (short to long)
+    // slot records: step j of the round is adjusted group T-1-j (short to long).  Steps at
+    // or past the capacity are not staged: when the iteration's final step count S fits
+    // the capacity they all lie past S (a non-join quota cut can drop the round's last
+    // steps), and otherwise the call reports ODB_E_CAPACITY from S
     for (int64_t t = threadIdx.x; t < T; t += kST) {
         const int64_t j = T - 1 - t;
         const int64_t x = base + j;
@@ -581,8 +583,6 @@ __device__ int64_t emit_rank(const StreamArgs& a, int64_t k, int64_t base, const
             a.smax[o] = rows > 0 ? key_len(kl[as[t]]) : 0;
             a.stok[o] = (int64_t)gtok[t];
             a.sadj[o] = (double)rows * mean;
-        } else {
-            a.g->cap_overflow = 1;
         }
         atomicAdd((unsigned long long*)&stepsum[j], (unsigned long long)rows);
     }
@@ -741,14 +741,12 @@ __global__ void __launch_bounds__(kST) stream_round_kernel(StreamArgs a, int64_t
         if (v.kind == 0 && fr.status < 0) {   // finished rank in join mode: IDLE slots
             for (int64_t t = tid; t < v.T; t += kST) {
                 const int64_t x = base + t;
-                if (x < a.scap) {
+                if (x < a.scap) {   // steps past the capacity are not staged (see the slot records)
                     const int64_t o = (int64_t)r * a.scap + x;
                     a.srows[o] = 0;
                     a.smax[o] = 0;
                     a.stok[o] = 0;
                     a.sadj[o] = 0.0;
-                } else {
-                    a.g->cap_overflow = 1;
                 }
             }
         } else if (v.kind == 0) {
@@ -1343,7 +1341,7 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     h_info->second_gather_rounds = hg.second_gather;
     h_info->max_outstanding = (int64_t)hg.max_outstanding;
     h_info->required_slot_capacity = K;
-    if (hg.cap_overflow || S > scap)
+    if (S > scap)
         return set_error(ODB_E_CAPACITY, "plan needs %lld slots, capacity is %lld", (long long)K,
                          (long long)slot_capacity);
 

@@ -21,7 +21,7 @@ def offsets(lens):
 
 
 def run_case(name, lens, perm, W, budget, buffer_size, depth, rate, mode="join", quota=0, cap=None, pad_id=0,
-             full_collate=True, tokens=None, max_rounds=None, device_perm=None):
+             full_collate=True, tokens=None, max_rounds=None, device_perm=None, slot_capacity=None):
     import torch
     import paper_2606_19989_amd as odb
 
@@ -39,7 +39,7 @@ def run_case(name, lens, perm, W, budget, buffer_size, depth, rate, mode="join",
     dperm = perm if device_perm is None else device_perm
     sp = odb.StreamPipeline(win, torch.from_numpy(np.asarray(dperm, dtype=np.int32)).cuda(), budget,
                             buffer_size=buffer_size, depth=depth, rate=rate, mode=mode, quota=quota, capacity=cap,
-                            pad_id=pad_id, max_rounds=max_rounds)
+                            pad_id=pad_id, max_rounds=max_rounds, slot_capacity=slot_capacity)
     info = sp.plan()
     torch.cuda.synchronize()
     for f in STREAM_INFO_EXACT:
@@ -324,3 +324,17 @@ def test_stream_two_stream_schedule():
     wt, st, ss = sps[0].loss_weights(oracle.WEIGHT_TOKEN_EXACT)
     ewt, est, ess = ref.loss_weights(oracle.WEIGHT_TOKEN_EXACT)
     assert np.array_equal(wt.cpu().numpy().view(np.int64), ewt.view(np.int64))
+
+
+def test_stream_quota_cut_retry_at_the_reported_capacity():
+    # room for one step per rank first: the call reports W * S and the retry at exactly
+    # that capacity must succeed even though the round that reaches the quota stages more
+    # steps than the cut keeps
+    rng = np.random.default_rng(79)
+    N, W = 6007, 5
+    lens = np.clip(np.rint(synth.lognormal(rng, 300.0, 1.0, N)), 1, 4000).astype(np.int64)
+    perm = rng.permutation(N).astype(np.int32)
+    rate = rng.integers(8, 40, W).astype(np.int32)
+    sp, ref = run_case("quota_cut_retry", lens, perm, W, 8192, 64, 96, rate, mode="nonjoin", quota=N // 3,
+                       slot_capacity=W)
+    assert sp.slot_capacity == W * ref.steps

@@ -1,6 +1,7 @@
-"""include/odb.h as plain C (no GPU): the C driver of the window pipeline compiles as
-strict C11 with warnings as errors, links against libodb.so and the HIP runtime, and
-starts (its shared libraries resolve) with a usage error when given no arguments."""
+"""include/odb.h as plain C (no GPU): the C drivers of the window pipeline and of the
+streaming iteration compile as strict C11 with warnings as errors, link against libodb.so
+and the HIP runtime, and start (their shared libraries resolve) with a usage error when
+given no arguments."""
 import importlib.util
 import os
 import subprocess
@@ -15,8 +16,10 @@ def _builder():
     return mod
 
 
-def test_c_driver_compiles_links_and_starts(tmp_path):
-    exe = _builder().build(str(tmp_path / "window_pipeline"))
-    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
-    assert r.returncode == 2, (r.returncode, r.stderr)
-    assert "usage:" in r.stderr
+def test_c_drivers_compile_link_and_start(tmp_path):
+    exes = _builder().build(str(tmp_path))
+    assert len(exes) == 2
+    for exe in exes:
+        r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+        assert r.returncode == 2, (exe, r.returncode, r.stderr)
+        assert "usage:" in r.stderr, exe

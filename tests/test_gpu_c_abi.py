@@ -1,7 +1,8 @@
-"""The window pipeline driven from plain C (tests/c_abi/window_pipeline.c: hipMalloc'd
-buffers, include/odb.h, no Python in the loop), compared with the oracle: grouping,
-alignment (after the one retry with the slot capacity the first call reports), the
-collated tiles and the exact token-level loss weights."""
+"""The pipeline driven from plain C (tests/c_abi/*.c: hipMalloc'd buffers, include/odb.h,
+no Python in the loop), compared with the oracle.  Window: grouping, alignment (after the
+one retry with the slot capacity the first call reports), the collated tiles and the
+exact token-level loss weights.  Streaming: one logical iteration (round trace, plan,
+row records, leftovers, after the same retry), its collated tiles and weights."""
 import os
 import subprocess
 
@@ -16,7 +17,12 @@ pytestmark = pytest.mark.gpu
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 BIN = os.path.join(HERE, "c_abi", "window_pipeline")
+STREAM_BIN = os.path.join(HERE, "c_abi", "stream_pipeline")
 INFO_FIELDS = INFO_EXACT[:13] + ["second_gather_rounds", "required_slot_capacity"]
+STREAM_FIELDS = ["steps", "rounds", "emit_rounds", "skip_rounds", "stop_reason", "views", "emitted_views",
+                 "undelivered_views", "pending_views", "real_tokens", "padded_elems", "max_step_samples", "splits",
+                 "overflow_groups", "missing_ids", "duplicate_ids", "bad_views", "second_gather_rounds",
+                 "max_outstanding", "required_slot_capacity"]
 
 
 def _window(case):
@@ -87,6 +93,67 @@ def test_window_pipeline_from_c(case, tmp_path):
     P = ref.padded_elems
     for name, want in zip(["input_ids", "labels", "attention_mask", "position_ids"],
                           ref.collate(w.tok_off, tokens, 0)):
+        got = rd.take(np.int32, P)
+        assert np.array_equal(got, want), (name, int(np.count_nonzero(got != want)))
+    wt = rd.take(np.float64, K)
+    ewt, _, _ = ref.loss_weights(oracle.WEIGHT_TOKEN_EXACT)
+    assert np.array_equal(wt.view(np.int64), ewt.view(np.int64)), "loss weights"
+    assert rd.at == len(rd.raw), "trailing output"
+
+
+@pytest.mark.parametrize("case", ["join", "nonjoin"])
+def test_stream_iteration_from_c(case, tmp_path):
+    assert os.path.exists(STREAM_BIN), "tests/c_abi/stream_pipeline is missing: run __graft_entry__.build()"
+    rng = np.random.default_rng(79)
+    N, W, budget, buffer_size, depth = 6007, 5, 8192, 64, 96
+    lens = np.clip(np.rint(synth.lognormal(rng, 300.0, 1.0, N)), 1, 4000).astype(np.int64)
+    tok_off = np.zeros(N + 1, np.int64)
+    np.cumsum(lens, out=tok_off[1:])
+    tokens = synth.tokens_numpy(0, int(tok_off[-1]))
+    perm = rng.permutation(N).astype(np.int32)
+    rate = rng.integers(8, 40, W).astype(np.int32)
+    mode, quota = (0, 0) if case == "join" else (1, N // 3)
+    q = -(-N // W)
+    max_rounds = q + (q + 1) * -(-buffer_size // int(rate.min())) + 2
+    src, dst = tmp_path / "in.bin", tmp_path / "out.bin"
+    with open(src, "wb") as f:
+        np.array([W, N, len(tokens)], np.int64).tofile(f)
+        tok_off.tofile(f)
+        tokens.astype(np.int32).tofile(f)
+        perm.tofile(f)
+        rate.tofile(f)
+    log(f"stream case c_{case}: N={N} W={W} budget={budget} buffer={buffer_size} depth={depth} quota={quota}")
+    r = subprocess.run([STREAM_BIN, str(src), str(dst), str(budget), str(mode), str(quota), str(buffer_size),
+                        str(depth), str(max_rounds)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+
+    ref = oracle.stream(tok_off, perm, W, budget, mode=oracle.MODE_NONJOIN if mode else oracle.MODE_JOIN,
+                        quota=quota, buffer_size=buffer_size, depth=depth, rate=rate)
+    rd = _Reader(open(dst, "rb").read())
+    info = dict(zip(STREAM_FIELDS, rd.take(np.int64, 20).tolist()))
+    pad_fraction = float(rd.take(np.float64, 1)[0])
+    retries = int(rd.take(np.int64, 1)[0])
+    for f in STREAM_FIELDS[:-1]:
+        assert info[f] == ref.sinfo[f], (f, info[f], ref.sinfo[f])
+    S, M, E = ref.steps, ref.sinfo["views"], ref.sinfo["emitted_views"]
+    K = W * S
+    assert info["required_slot_capacity"] == K
+    rf = ref.sinfo["pad_fraction"]
+    assert abs(pad_fraction - rf) <= PAD_FRACTION_RTOL * max(abs(rf), 1e-300) or pad_fraction == rf
+    assert retries == (1 if S > 1 else 0), retries
+    assert np.array_equal(rd.take(np.int64, 4 * info["rounds"]).reshape(-1, 4), ref.trace), "trace"
+    ids = np.asarray(ref.emit_order, dtype=np.int64)
+    for name, dtype, count, want in [
+        ("emit_views", np.int32, E, ref.emit_views), ("emit_order", np.int32, E, ref.emit_order),
+        ("row_token_start", np.int64, E, tok_off[ids]), ("row_len", np.int32, E, lens[ids]),
+        ("slot_rows", np.int32, K, ref.slot_rows), ("slot_maxlen", np.int32, K, ref.slot_maxlen),
+        ("slot_row_off", np.int64, K + 1, ref.slot_row_off), ("slot_tile_off", np.int64, K + 1, ref.slot_tile_off),
+        ("slot_tokens", np.int64, K, ref.slot_tokens), ("left_views", np.int32, M - E, ref.left_views),
+        ("left_off", np.int64, W + 1, ref.left_off),
+    ]:
+        assert np.array_equal(rd.take(dtype, count), want), name
+    P = int(ref.sinfo["padded_elems"])
+    for name, want in zip(["input_ids", "labels", "attention_mask", "position_ids"], ref.collate(tok_off, tokens, 0)):
         got = rd.take(np.int32, P)
         assert np.array_equal(got, want), (name, int(np.count_nonzero(got != want)))
     wt = rd.take(np.float64, K)

@@ -2,8 +2,9 @@
  * The window pipeline driven from plain C through include/odb.h, with no Python and no
  * torch: device memory from the HIP runtime API, then odb_form_groups ->
  * odb_align_groups (retried once with the slot capacity the plan reports) ->
- * odb_collate -> odb_loss_weights, and every output written to a file for the test to
- * compare with the oracle.
+ * odb_collate and odb_collate_static (into a second set of outputs) -> odb_loss_weights,
+ * and odb_length_sketch over every sample; every output is written to a file for the
+ * test to compare with the oracle.
  *
  *   window_pipeline IN OUT BUDGET MODE QUOTA
  *
@@ -16,8 +17,10 @@
  * groups_per_rank[W]; int32 emit_order[emitted]; int32 slot_rows[K], slot_maxlen[K];
  * int64 slot_row_off[K+1], slot_tile_off[K+1], slot_tokens[K]; int32 leftover[leftover];
  * int64 leftover_off[W+1]; int32 input_ids[P], labels[P], attention_mask[P],
- * position_ids[P]; double weight[K] (exact token-level mode), with K = W * steps and
- * P = padded_elems.
+ * position_ids[P]; the same four arrays from odb_collate_static and its int32 status;
+ * double weight[K] (exact token-level mode); int64 sketch[7] (samples, short_samples,
+ * sum_len, sum_sq_hi, sum_sq_lo, min_len, max_len), double sketch[3] (mean, cv,
+ * short_fraction), int64 high_roi; with K = W * steps and P = padded_elems.
  *
  * Exit status 0 on success; otherwise the failing call and its message go to stderr.
  */
@@ -180,6 +183,14 @@ int main(int argc, char** argv) {
     if (st != ODB_OK) return fail("odb_collate", st);
     st = odb_collate_status(d_ws, ws_bytes, stream);
     if (st != ODB_OK) return fail("odb_collate_status", st);
+    /* the allocation-free variant, same plan, its own outputs and status word */
+    int32_t* d_static_out[4];
+    for (int i = 0; i < 4; ++i) d_static_out[i] = dev_alloc(sizeof(int32_t) * (size_t)P);
+    int32_t* d_static_status = dev_alloc(sizeof(int32_t));
+    st = odb_collate_static(&w, K, d_emit, d_row_ts, d_row_len, d_rows, d_maxlen, d_row_off, d_tile_off, 0, P,
+                            d_static_out[0], d_static_out[1], d_static_out[2], d_static_out[3], d_static_status,
+                            stream);
+    if (st != ODB_OK) return fail("odb_collate_static", st);
 
     /* exact token-level loss-scaling weights (Eq. 2) */
     double* d_weight = dev_alloc(sizeof(double) * (size_t)K);
@@ -187,6 +198,10 @@ int main(int argc, char** argv) {
                           NULL, stream);
     if (st != ODB_OK) return fail("odb_loss_weights", st);
     HIP_CHECK(hipStreamSynchronize(stream));
+    /* the return-on-investment screen over every sample of the window */
+    odb_length_sketch_t sk;
+    st = odb_length_sketch(&w, NULL, n, budget, &sk, d_ws, ws_bytes, stream);
+    if (st != ODB_OK) return fail("odb_length_sketch", st);
 
     FILE* out = fopen(argv[2], "wb");
     if (!out) {
@@ -216,12 +231,24 @@ int main(int argc, char** argv) {
     dump(out, d_leftover, sizeof(int32_t) * (size_t)info.leftover_samples);
     dump(out, d_leftover_off, sizeof(int64_t) * (size_t)(W + 1));
     for (int i = 0; i < 4; ++i) dump(out, d_out[i], sizeof(int32_t) * (size_t)P);
+    for (int i = 0; i < 4; ++i) dump(out, d_static_out[i], sizeof(int32_t) * (size_t)P);
+    dump(out, d_static_status, sizeof(int32_t));
     dump(out, d_weight, sizeof(double) * (size_t)K);
+    const int64_t sk_int[7] = {sk.samples, sk.short_samples, sk.sum_len, (int64_t)sk.sum_sq_hi, (int64_t)sk.sum_sq_lo,
+                               sk.min_len, sk.max_len};
+    const double sk_real[3] = {sk.mean, sk.cv, sk.short_fraction};
+    const int64_t sk_roi = sk.high_roi;
+    if (fwrite(sk_int, sizeof sk_int, 1, out) != 1 || fwrite(sk_real, sizeof sk_real, 1, out) != 1 ||
+        fwrite(&sk_roi, sizeof sk_roi, 1, out) != 1) {
+        fprintf(stderr, "short write\n");
+        return 2;
+    }
     fclose(out);
 
     void* bufs[] = {d_tok_off, d_tokens, d_ws, d_order, d_sorted_len, d_group_index, d_groups, d_emit, d_row_ts,
                     d_row_len, d_leftover, d_leftover_off, d_rows, d_maxlen, d_row_off, d_tile_off, d_slot_tok,
-                    d_out[0], d_out[1], d_out[2], d_out[3], d_weight};
+                    d_out[0], d_out[1], d_out[2], d_out[3], d_weight, d_static_out[0], d_static_out[1],
+                    d_static_out[2], d_static_out[3], d_static_status};
     for (size_t i = 0; i < sizeof bufs / sizeof bufs[0]; ++i) HIP_CHECK(hipFree(bufs[i]));
     HIP_CHECK(hipStreamDestroy(stream));
     free(rank_off);

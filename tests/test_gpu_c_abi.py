@@ -1,7 +1,8 @@
 """The pipeline driven from plain C (tests/c_abi/*.c: hipMalloc'd buffers, include/odb.h,
 no Python in the loop), compared with the oracle.  Window: grouping, alignment (after the
-one retry with the slot capacity the first call reports), the collated tiles and the
-exact token-level loss weights.  Streaming: one logical iteration (round trace, plan,
+one retry with the slot capacity the first call reports), the collated tiles (from
+odb_collate and from odb_collate_static), the exact token-level loss weights and the
+length sketch of the whole window.  Streaming: one logical iteration (round trace, plan,
 row records, leftovers, after the same retry), its collated tiles and weights."""
 import os
 import subprocess
@@ -91,13 +92,25 @@ def test_window_pipeline_from_c(case, tmp_path):
     ]:
         assert np.array_equal(rd.take(dtype, count), want), name
     P = ref.padded_elems
-    for name, want in zip(["input_ids", "labels", "attention_mask", "position_ids"],
-                          ref.collate(w.tok_off, tokens, 0)):
-        got = rd.take(np.int32, P)
-        assert np.array_equal(got, want), (name, int(np.count_nonzero(got != want)))
+    want = ref.collate(w.tok_off, tokens, 0)
+    for entry in ("odb_collate", "odb_collate_static"):
+        for name, e in zip(["input_ids", "labels", "attention_mask", "position_ids"], want):
+            got = rd.take(np.int32, P)
+            assert np.array_equal(got, e), (entry, name, int(np.count_nonzero(got != e)))
+    assert int(rd.take(np.int32, 1)[0]) == 0, "odb_collate_static status"
     wt = rd.take(np.float64, K)
     ewt, _, _ = ref.loss_weights(oracle.WEIGHT_TOKEN_EXACT)
     assert np.array_equal(wt.view(np.int64), ewt.view(np.int64)), "loss weights"
+    samples, short, sum_len, sq_hi, sq_lo, min_len, max_len = rd.take(np.int64, 7).tolist()
+    mean, cv, short_fraction = rd.take(np.float64, 3).tolist()
+    high_roi = int(rd.take(np.int64, 1)[0])
+    sk = oracle.length_sketch(w.tok_off, None, w.budget)
+    assert (samples, short, sum_len, (sq_hi << 32) + (sq_lo & 0xFFFFFFFFFFFFFFFF), min_len, max_len, high_roi) == \
+        (sk["samples"], sk["short_samples"], sk["sum_len"], sk["sum_sq"], sk["min_len"], sk["max_len"],
+         sk["high_roi"])
+    assert short_fraction == sk["short_fraction"]
+    assert abs(mean - sk["mean"]) <= 2.0 ** -52 * sk["mean"]
+    assert abs(cv - sk["cv"]) <= 1e-15 * max(sk["cv"], 1e-300), (cv, sk["cv"])
     assert rd.at == len(rd.raw), "trailing output"
 
 

@@ -3,8 +3,9 @@
  * torch: device memory from the HIP runtime API, then odb_form_groups ->
  * odb_align_groups (retried once with the slot capacity the plan reports) ->
  * odb_collate and odb_collate_static (into a second set of outputs) -> odb_loss_weights,
- * and odb_length_sketch over every sample; every output is written to a file for the
- * test to compare with the oracle.
+ * odb_check_coverage over the plan's emitted and left-over ids, and odb_length_sketch
+ * over every sample; every output is written to a file for the test to compare with the
+ * oracle.
  *
  *   window_pipeline IN OUT BUDGET MODE QUOTA
  *
@@ -20,7 +21,8 @@
  * position_ids[P]; the same four arrays from odb_collate_static and its int32 status;
  * double weight[K] (exact token-level mode); int64 sketch[7] (samples, short_samples,
  * sum_len, sum_sq_hi, sum_sq_lo, min_len, max_len), double sketch[3] (mean, cv,
- * short_fraction), int64 high_roi; with K = W * steps and P = padded_elems.
+ * short_fraction), int64 high_roi; int64 coverage[3] (bad_views, missing_ids,
+ * duplicate_ids); with K = W * steps and P = padded_elems.
  *
  * Exit status 0 on success; otherwise the failing call and its message go to stderr.
  */
@@ -202,6 +204,12 @@ int main(int argc, char** argv) {
     odb_length_sketch_t sk;
     st = odb_length_sketch(&w, NULL, n, budget, &sk, d_ws, ws_bytes, stream);
     if (st != ODB_OK) return fail("odb_length_sketch", st);
+    /* the identity-coverage self-check on its own, over the plan's emitted and left-over ids */
+    odb_plan_info_t cov;
+    memset(&cov, 0, sizeof cov);
+    st = odb_check_coverage(&w, d_emit, info.emitted_samples, d_leftover, info.leftover_samples, &cov, d_ws, ws_bytes,
+                            stream);
+    if (st != ODB_OK) return fail("odb_check_coverage", st);
 
     FILE* out = fopen(argv[2], "wb");
     if (!out) {
@@ -240,6 +248,11 @@ int main(int argc, char** argv) {
     const int64_t sk_roi = sk.high_roi;
     if (fwrite(sk_int, sizeof sk_int, 1, out) != 1 || fwrite(sk_real, sizeof sk_real, 1, out) != 1 ||
         fwrite(&sk_roi, sizeof sk_roi, 1, out) != 1) {
+        fprintf(stderr, "short write\n");
+        return 2;
+    }
+    const int64_t cov_out[3] = {cov.bad_views, cov.missing_ids, cov.duplicate_ids};
+    if (fwrite(cov_out, sizeof cov_out, 1, out) != 1) {
         fprintf(stderr, "short write\n");
         return 2;
     }

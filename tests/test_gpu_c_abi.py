@@ -1,8 +1,9 @@
 """The pipeline driven from plain C (tests/c_abi/*.c: hipMalloc'd buffers, include/odb.h,
 no Python in the loop), compared with the oracle.  Window: grouping, alignment (after the
 one retry with the slot capacity the first call reports), the collated tiles (from
-odb_collate and from odb_collate_static), the exact token-level loss weights and the
-length sketch of the whole window.  Streaming: one logical iteration (round trace, plan,
+odb_collate and from odb_collate_static), the exact token-level loss weights, the
+coverage check of the emitted and left-over ids and the length sketch of the whole
+window.  Streaming: one logical iteration (round trace, plan,
 row records, leftovers, after the same retry), its collated tiles and weights."""
 import os
 import subprocess
@@ -111,6 +112,8 @@ def test_window_pipeline_from_c(case, tmp_path):
     assert short_fraction == sk["short_fraction"]
     assert abs(mean - sk["mean"]) <= 2.0 ** -52 * sk["mean"]
     assert abs(cv - sk["cv"]) <= 1e-15 * max(sk["cv"], 1e-300), (cv, sk["cv"])
+    # every sample emitted or left over exactly once
+    assert rd.take(np.int64, 3).tolist() == [0, 0, 0], "coverage"
     assert rd.at == len(rd.raw), "trailing output"
 
 

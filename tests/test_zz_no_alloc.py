@@ -1,7 +1,7 @@
 """odb_collate_static (the collate without a workspace, for callers that cannot allocate)
 against odb_collate on the same plans, through the C ABI: two calls in a row, the second
 on a smaller window, with and without the plan's row records; the status output; the
-host-side size limit."""
+host-side size limit, and a window at that limit."""
 import numpy as np
 import pytest
 
@@ -103,3 +103,24 @@ def test_static_collate_rejects_windows_beyond_the_scratch():
                            row_token_start=one, row_len=i32)
     torch.cuda.synchronize()
     assert int(status.item()) == 0
+
+
+def test_static_collate_at_the_scratch_limit():
+    # without row records, a window of exactly ODB_COLLATE_STATIC_MAX_ROWS - W + 1
+    # samples (n + W - 1 rows, the scratch's last row included) is accepted and collates
+    # like odb_collate
+    import torch
+    import paper_2606_19989_amd as odb
+
+    W = 2
+    n = odb.ODB_COLLATE_STATIC_MAX_ROWS - W + 1
+    rng = np.random.default_rng(59)
+    w = synth.window_from_ranks("at_limit", [rng.integers(1, 4, n // 2), rng.integers(1, 4, n - n // 2)], 4096)
+    log(f"static collate at the scratch limit: n={w.n} W={w.W}")
+    pipe, want = _planned(w)
+    status = torch.full((1,), 77, dtype=torch.int32, device="cuda")
+    got = _static(pipe, False, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    for name, g, e in zip(["input_ids", "labels", "attention_mask", "position_ids"], got, want):
+        assert torch.equal(g, e), name

@@ -186,7 +186,8 @@ def test_workload_full_size(name):
 
 
 @pytest.mark.parametrize("case", ["at_block_limit", "past_block_limit", "wide_lengths", "one_length_per_rank",
-                                  "long_rank", "tile_edges", "many_ranks", "many_ranks_jump"])
+                                  "long_rank", "tile_edges", "many_ranks", "many_ranks_jump", "max_lengths",
+                                  "max_lengths_one_block"])
 def test_grouping_paths(case):
     # The two grouping paths (one block per rank up to 16,384 samples per rank, the
     # multi-block sort and run-table walk beyond) at the limit; lengths up to 2^25 (all
@@ -196,7 +197,10 @@ def test_grouping_paths(case):
     # run counts takes two passes of its block) beside one of 3; ranks one position past,
     # at and one short of a tile edge, with empty and one-sample ranks; 1,100 ranks (more
     # than the rank table kernels stage in LDS) with one past the one-block limit, grouped
-    # by the run-table walk and, at budget 2^23 with lengths 1..8000, by pointer jumping
+    # by the run-table walk and, at budget 2^23 with lengths 1..8000, by pointer jumping;
+    # lengths over the whole valid range [1, 2^31 - 1] (31-bit keys: four radix passes of
+    # 8-bit digits; with ranks of at most 16,384 samples, the one-block sort's top byte)
+    # at a budget of 2^40 (64-bit batch sizes), plan only
     import torch
 
     rng = np.random.default_rng(61)
@@ -222,13 +226,22 @@ def test_grouping_paths(case):
         if case == "many_ranks_jump":
             per[0] = np.concatenate([per[0], [1, 8000]])
         w = win(per, (1 << 23) if case == "many_ranks_jump" else 20000)
+    elif case == "max_lengths":
+        top = (1 << 31) - 1
+        per = [np.concatenate([rng.integers(1, top, 17000), [top, 1, top]]), rng.integers(1, top, 3),
+               np.zeros(0, np.int64), np.concatenate([rng.integers(1, top, 2000), [top, top, 1]])]
+        w = win(per, 1 << 40)
+    elif case == "max_lengths_one_block":
+        top = (1 << 31) - 1
+        per = [np.concatenate([rng.integers(1, top, 2000), [top, 1, top]]), rng.integers(1, top, 3)]
+        w = win(per, 1 << 40)
     else:
         per = [np.full(3000, 77), np.full(10, 5000), np.full(1, 1)]
         w = win(per, 9000)
     w.name = f"paths_{case}"
     log(f"case {w.name}: W={w.W} n={w.n} budget={w.budget}")
     ref = oracle.plan_window(w)
-    if case in ("wide_lengths", "long_rank", "many_ranks_jump"):
+    if case in ("wide_lengths", "long_rank", "many_ranks_jump", "max_lengths", "max_lengths_one_block"):
         pipe, _ = run_gpu(w, tokens=torch.zeros(64, dtype=torch.int32, device="cuda"), collate=False)
         compare_plan(w, pipe, ref)
         compare_loss_weights(pipe, ref)

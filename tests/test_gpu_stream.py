@@ -338,3 +338,19 @@ def test_stream_quota_cut_retry_at_the_reported_capacity():
     sp, ref = run_case("quota_cut_retry", lens, perm, W, 8192, 64, 96, rate, mode="nonjoin", quota=N // 3,
                        slot_capacity=W)
     assert sp.slot_capacity == W * ref.steps
+
+
+@pytest.mark.parametrize("mode", ["join", "nonjoin"])
+def test_stream_max_lengths(mode):
+    # lengths over the whole valid range [1, 2^31 - 1] (31-bit sort keys: seven 5-bit
+    # digit passes) at a budget of 2^40 (64-bit batch sizes); plan and weights only, the
+    # token stream would not fit
+    import torch
+
+    rng = np.random.default_rng(78)
+    top = (1 << 31) - 1
+    lens = np.concatenate([rng.integers(1, top, 600), [top, 1, top], rng.integers(1, 50, 300)])
+    perm = rng.permutation(len(lens)).astype(np.int32)
+    run_case(f"max_lengths_{mode}", lens, perm, 3, 1 << 40, 64, 96, [64, 30, 64], mode=mode,
+             quota=len(lens) // 2 if mode == "nonjoin" else 0, full_collate=False,
+             tokens=torch.zeros(64, dtype=torch.int32, device="cuda"))

@@ -346,6 +346,31 @@ def test_length_sketch_whole_window_and_edge_cases():
     assert e.value.status == odb.ODB_E_INVALID_DATA
 
 
+def test_length_sketch_sums_past_64_bits():
+    # lengths near 2^31: the sum of squares passes 2^64 (the 128-bit accumulation), at a
+    # budget of 2^40 (the short-sample test 4 l < L_max in 64 bits)
+    import torch
+    import paper_2606_19989_amd as odb
+
+    rng = np.random.default_rng(53)
+    n = 6000
+    lens = np.concatenate([rng.integers(1 << 30, 1 << 31, n - 4), [(1 << 31) - 1, 1, (1 << 31) - 1, 7]])
+    off = np.zeros(n + 1, np.int64)
+    np.cumsum(lens, out=off[1:])
+    tok_off = torch.from_numpy(off).cuda()
+    win = odb.DeviceWindow(np.array([0, n], np.int64), tok_off, torch.zeros(4, dtype=torch.int32, device="cuda"),
+                           None, 0)
+    ws = torch.empty(odb.odb_workspace_size(win), dtype=torch.uint8, device="cuda")
+    want = oracle.length_sketch(off, None, 1 << 40)
+    assert want["sum_sq"] >= 1 << 64
+    log("sketch past 64 bits")
+    _compare_sketch(odb.odb_length_sketch(win, None, n, 1 << 40, ws), want)
+    ids = rng.integers(0, n, 5000).astype(np.int32)   # with repeats
+    for budget in (1 << 40, 1 << 33, 7):
+        got = odb.odb_length_sketch(win, torch.from_numpy(ids).cuda(), len(ids), budget, ws)
+        _compare_sketch(got, oracle.length_sketch(off, ids, budget))
+
+
 def test_collate_from_emit_order():
     # odb_collate without row records gathers them from the emitted ids itself; both
     # routes give the oracle's outputs

@@ -350,7 +350,9 @@ __device__ __forceinline__ void stage_values(const Stage& a, int64_t e, int64_t 
     // first row of the next non-empty tile, which starts right after row A.  Its width is
     // not at hand then, so that case needs row B to hold the group's remaining elements.
     const bool same_tile = c.ri + 1 < c.ri_end;
-    bool edge = vec_ok && c.ml >= kVec && c.col + kVec > c.ml && c.ri >= 0 && c.ri < c.ri_end &&
+    // column + 4 in 32-bit unsigned: a tile may be 2^31 - 1 wide, and 0 <= col < ml
+    const uint32_t col4 = (uint32_t)c.col + kVec;
+    bool edge = vec_ok && c.ml >= kVec && col4 > (uint32_t)c.ml && c.ri >= 0 && c.ri < c.ri_end &&
                 c.ri + 1 < p.max_rows && r.ts + c.col + kVec <= p.tok_end;
     int32_t bl = 0;
     v4i bt = {0, 0, 0, 0};
@@ -389,7 +391,7 @@ __device__ __forceinline__ void stage_values(const Stage& a, int64_t e, int64_t 
             vmsk[i] = real ? 1 : 0;
             vpos[i] = real ? col : 0;
         }
-    } else if (vec_ok && c.col + (kVec - 1) < c.ml && (nreal <= 0 || r.ts + c.col + kVec <= p.tok_end)) {
+    } else if (vec_ok && col4 <= (uint32_t)c.ml && (nreal <= 0 || r.ts + c.col + kVec <= p.tok_end)) {
         // the 4 elements sit in one row and the vector load covered them
 #pragma unroll
         for (int i = 0; i < kVec; ++i) {

@@ -371,6 +371,40 @@ def test_length_sketch_sums_past_64_bits():
         _compare_sketch(got, oracle.length_sketch(off, ids, budget))
 
 
+def test_collate_tile_width_at_the_length_limit():
+    # tiles 2^31 - 1 and 2^31 - 2 elements wide (the longest valid samples): a 4-element
+    # group that starts 1 to 3 columns before a row's end must still take the row-edge
+    # path there (column + 4 is past 2^31); every element around each row edge and a
+    # random sample are checked against the oracle's per-element rule
+    import torch
+
+    top = (1 << 31) - 1
+    for lens, name in (([top, top, top - 1], "width_2p31m1"), ([top - 1, top - 1, 5, top - 2], "width_2p31m2")):
+        w = win([np.array(lens, np.int64)], 1 << 40)
+        w.name = name
+        log(f"collate at the length limit: {name}, {int(w.tok_off[-1])} tokens")
+        ref = oracle.plan_window(w)
+        pipe, outs = run_gpu(w)
+        compare_plan(w, pipe, ref)
+        P = ref.padded_elems
+        edges = []
+        for k in range(len(ref.slot_rows)):
+            t0, ml, rows = int(ref.slot_tile_off[k]), int(ref.slot_maxlen[k]), int(ref.slot_rows[k])
+            for r in range(1, rows + 1):
+                edges.append(np.arange(t0 + r * ml - 24, t0 + r * ml + 24))
+        idx = np.concatenate(edges + [np.random.default_rng(5).integers(0, P, 20000), [0, P - 1]])
+        idx = np.unique(idx[(idx >= 0) & (idx < P)])
+        want = oracle.collate_elements(ref, w.tok_off, synth.token_ids, idx, 0)
+        ti = torch.from_numpy(idx).cuda()
+        for label, g, e in zip(["input_ids", "labels", "attention_mask", "position_ids"], outs, want):
+            got = g[ti].cpu().numpy()
+            bad = np.nonzero(got != e)[0]
+            assert len(bad) == 0, f"{name} {label}: {len(bad)} mismatches, first at {idx[bad[0]]}"
+        del pipe, outs, ti
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
+
 def test_collate_from_emit_order():
     # odb_collate without row records gathers them from the emitted ids itself; both
     # routes give the oracle's outputs

@@ -164,13 +164,16 @@ inline unsigned grid_for(int64_t n, int per_block, int64_t cap = 1 << 20) {
 }
 
 // ------------------------------------------------------------------ device helpers
-// Eq. 1: B(l) = max(floor(L_max / l), 1), integer division.
+// Eq. 1: B(l) = max(floor(L_max / l), 1), integer division, clipped to 2^31 - 1.  A rank
+// holds fewer than 2^31 - 1 samples, so a group of B >= 2^31 - 1 takes the rest of its rank
+// either way; the clip keeps position + B inside int64 for budgets up to 2^63 - 1.
 __device__ __forceinline__ int64_t batch_size(int64_t budget, int32_t l) {
     int64_t b;
     if (budget <= 0xFFFFFFFFll)
         b = (int64_t)((uint32_t)budget / (uint32_t)l);
     else
         b = budget / (int64_t)l;
+    b = b < INT32_MAX ? b : INT32_MAX;
     return b > 1 ? b : 1;
 }
 

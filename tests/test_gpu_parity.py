@@ -187,7 +187,7 @@ def test_workload_full_size(name):
 
 @pytest.mark.parametrize("case", ["at_block_limit", "past_block_limit", "wide_lengths", "one_length_per_rank",
                                   "long_rank", "tile_edges", "many_ranks", "many_ranks_jump", "max_lengths",
-                                  "max_lengths_one_block"])
+                                  "max_lengths_one_block", "budget_int64_max", "budget_int64_max_jump"])
 def test_grouping_paths(case):
     # The two grouping paths (one block per rank up to 16,384 samples per rank, the
     # multi-block sort and run-table walk beyond) at the limit; lengths up to 2^25 (all
@@ -200,7 +200,9 @@ def test_grouping_paths(case):
     # by the run-table walk and, at budget 2^23 with lengths 1..8000, by pointer jumping;
     # lengths over the whole valid range [1, 2^31 - 1] (31-bit keys: four radix passes of
     # 8-bit digits; with ranks of at most 16,384 samples, the one-block sort's top byte)
-    # at a budget of 2^40 (64-bit batch sizes), plan only
+    # at a budget of 2^40 (64-bit batch sizes), plan only; a budget of 2^63 - 1 (batch
+    # sizes past any rank: every group after the first takes the rest of its rank), on the
+    # one-block path and on pointer jumping (plan only there)
     import torch
 
     rng = np.random.default_rng(61)
@@ -231,6 +233,12 @@ def test_grouping_paths(case):
         per = [np.concatenate([rng.integers(1, top, 17000), [top, 1, top]]), rng.integers(1, top, 3),
                np.zeros(0, np.int64), np.concatenate([rng.integers(1, top, 2000), [top, top, 1]])]
         w = win(per, 1 << 40)
+    elif case == "budget_int64_max":
+        per = [rng.integers(1, 3000, 2000), rng.integers(1, 3000, 500), np.array([1, 1, 2])]
+        w = win(per, (1 << 63) - 1)
+    elif case == "budget_int64_max_jump":
+        per = [rng.integers(1, 20000, 17000), rng.integers(1, 100, 5)]
+        w = win(per, (1 << 63) - 1)
     elif case == "max_lengths_one_block":
         top = (1 << 31) - 1
         per = [np.concatenate([rng.integers(1, top, 2000), [top, 1, top]]), rng.integers(1, top, 3)]
@@ -241,7 +249,8 @@ def test_grouping_paths(case):
     w.name = f"paths_{case}"
     log(f"case {w.name}: W={w.W} n={w.n} budget={w.budget}")
     ref = oracle.plan_window(w)
-    if case in ("wide_lengths", "long_rank", "many_ranks_jump", "max_lengths", "max_lengths_one_block"):
+    if case in ("wide_lengths", "long_rank", "many_ranks_jump", "max_lengths", "max_lengths_one_block",
+                "budget_int64_max_jump"):
         pipe, _ = run_gpu(w, tokens=torch.zeros(64, dtype=torch.int32, device="cuda"), collate=False)
         compare_plan(w, pipe, ref)
         compare_loss_weights(pipe, ref)

@@ -354,3 +354,11 @@ def test_stream_max_lengths(mode):
     run_case(f"max_lengths_{mode}", lens, perm, 3, 1 << 40, 64, 96, [64, 30, 64], mode=mode,
              quota=len(lens) // 2 if mode == "nonjoin" else 0, full_collate=False,
              tokens=torch.zeros(64, dtype=torch.int32, device="cuda"))
+
+
+def test_stream_budget_int64_max():
+    # a budget of 2^63 - 1: every group after a round's first takes the rest of the buffer
+    rng = np.random.default_rng(80)
+    lens = rng.integers(1, 3000, 2500)
+    perm = rng.permutation(len(lens)).astype(np.int32)
+    run_case("budget_int64_max", lens, perm, 3, (1 << 63) - 1, 128, 200, [128, 50, 128])

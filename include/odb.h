@@ -416,8 +416,9 @@ typedef struct odb_stream_info {
     int64_t required_slot_capacity;/* W * S; set on ODB_E_CAPACITY and on success            */
 } odb_stream_info_t;
 
-/* Bytes of device workspace odb_stream_plan needs (0 for invalid arguments).  The
- * workspace starts with the window workspace, so odb_collate can reuse it. */
+/* Bytes of device workspace odb_stream_plan needs (0 for invalid arguments, and for a
+ * slot_capacity or max_rounds that would ask for more than 2^50 bytes).  The workspace
+ * starts with the window workspace, so odb_collate can reuse it. */
 size_t odb_stream_workspace_size(const odb_window_t* w, int32_t depth, int64_t slot_capacity,
                                  int64_t max_rounds);
 

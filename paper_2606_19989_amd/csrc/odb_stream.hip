@@ -1107,9 +1107,16 @@ struct StreamLayout {
         totals, partials, rate, cap, total;
 };
 
+// Workspace layout of a streaming iteration after the window workspace (`at` bytes).
+// Returns false when the slot capacity or the round limit asks for more than kMaxStreamBytes
+// of workspace (every size is checked before it is multiplied, so none wraps).
+constexpr int64_t kMaxStreamBytes = int64_t(1) << 50;
+
 bool stream_layout(size_t at, int64_t W, int64_t N, int64_t D, int64_t scap, int64_t rounds, StreamLayout* L) {
     const int64_t q = N > 0 ? (N + W - 1) / W : 0;
     const int64_t M = q * W;
+    // per-rank staging slots and round records, bounded before any product is formed
+    if (scap < 0 || rounds < 1 || scap > kMaxStreamBytes / 8 / W || rounds > kMaxStreamBytes / 64) return false;
     const int64_t K1 = W * scap + 1;
     const int64_t scan_n = (K1 > M + 1 ? K1 : M + 1);
     size_t o = at;
@@ -1140,7 +1147,7 @@ bool stream_layout(size_t at, int64_t W, int64_t N, int64_t D, int64_t scap, int
     L->rate = take(4 * W);
     L->cap = take(8 * W);
     L->total = o;
-    return true;
+    return o - at <= (size_t)kMaxStreamBytes;
 }
 
 // A lower bound on the rounds still to run after the committed state `hr`: a rank fetches
@@ -1198,7 +1205,8 @@ extern "C" size_t odb_stream_workspace_size(const odb_window_t* w, int32_t depth
     if (!make_layout(w, &L)) return 0;
     if (depth < 1 || depth > kMaxDepth || slot_capacity < 0 || max_rounds < 1) return 0;
     StreamLayout S;
-    stream_layout(L.total, w->num_ranks, w->num_samples, depth, slot_capacity / w->num_ranks, max_rounds, &S);
+    if (!stream_layout(L.total, w->num_ranks, w->num_samples, depth, slot_capacity / w->num_ranks, max_rounds, &S))
+        return 0;
     return S.total;
 }
 
@@ -1230,7 +1238,9 @@ extern "C" int odb_stream_plan(const odb_window_t* w, const int32_t* d_perm, int
     if (scap > 0 && (!d_slot_rows || !d_slot_maxlen || !d_slot_tokens))
         return set_error(ODB_E_INVALID_ARG, "slot arrays must not be NULL");
     StreamLayout SL;
-    stream_layout(L.total, W, N, params->depth, scap, params->max_rounds, &SL);
+    if (!stream_layout(L.total, W, N, params->depth, scap, params->max_rounds, &SL))
+        return set_error(ODB_E_INVALID_ARG, "slot_capacity (%lld) or max_rounds (%lld) asks for more than 2^50 bytes of "
+                         "workspace", (long long)slot_capacity, (long long)params->max_rounds);
     if (!d_ws) return set_error(ODB_E_INVALID_ARG, "workspace is NULL");
     if (reinterpret_cast<uintptr_t>(d_ws) & 255) return set_error(ODB_E_INVALID_ARG, "workspace must be 256-byte aligned");
     if (ws_bytes < SL.total)

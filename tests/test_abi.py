@@ -137,6 +137,10 @@ def test_stream_arguments_checked_on_host():
     assert lib.odb_stream_workspace_size(ctypes.byref(w), 4097, 100, 50) == 0     # deeper than the LDS sort
     assert lib.odb_stream_workspace_size(ctypes.byref(w), 64, -1, 50) == 0
     assert lib.odb_stream_workspace_size(ctypes.byref(w), 64, 100, 0) == 0
+    # capacities and round limits whose workspace would pass 2^50 bytes (sizes that would
+    # wrap if multiplied unchecked) are refused, not wrapped
+    for cap, rounds in ((1 << 62, 50), ((1 << 63) - 1, 50), (100, 1 << 62), (100, (1 << 63) - 1)):
+        assert lib.odb_stream_workspace_size(ctypes.byref(w), 64, cap, rounds) == 0, (cap, rounds)
     fake_ws = 0x100000  # never dereferenced: every call below fails its host checks first
     rate = np.array([4, 4], dtype=np.int32)
     bad_rate = np.array([4, 0], dtype=np.int32)
@@ -157,6 +161,10 @@ def test_stream_arguments_checked_on_host():
     p = odb.StreamParams(**good)
     assert call(ctypes.byref(p), budget=0) == odb.ODB_E_INVALID_ARG
     assert call(ctypes.byref(p), cap=-1) == odb.ODB_E_INVALID_ARG
+    assert call(ctypes.byref(p), cap=(1 << 63) - 1) == odb.ODB_E_INVALID_ARG
+    p_rounds = odb.StreamParams(**{**good, "max_rounds": (1 << 63) - 1})
+    assert call(ctypes.byref(p_rounds)) == odb.ODB_E_INVALID_ARG
+    assert b"2^50 bytes" in lib.odb_last_error_message()
     assert call(ctypes.byref(p), ts=1) == odb.ODB_E_INVALID_ARG
     assert call(ctypes.byref(p), ln=1) == odb.ODB_E_INVALID_ARG
 

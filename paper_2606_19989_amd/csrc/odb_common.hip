@@ -1,5 +1,6 @@
 // Host-side plumbing shared by every entry point: error strings, workspace layout,
 // window validation and small uploads.
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -194,16 +195,17 @@ int read_state(const Layout& L, void* ws, int W, HostState* h, hipStream_t s) {
 }
 
 int num_cus() {
-    static int cached[64] = {0};
+    // per device, looked up once; threads that race on the first lookup store the same value
+    static std::atomic<int> cached[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (!cached[dev]) {
-        int v = 0;
+    int v = cached[dev].load(std::memory_order_relaxed);
+    if (!v) {
         if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
             v = 256;
-        cached[dev] = v;
+        cached[dev].store(v, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return v;
 }
 
 }  // namespace odb
